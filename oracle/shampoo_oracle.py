@@ -1,0 +1,334 @@
+"""CPU fp64 oracle for the scalable-Shampoo hot path.
+
+TEST INFRASTRUCTURE ONLY.  Nothing in the product path (the HIP library and
+its Python binding) imports, links or calls this module; only the tests,
+``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of ``bench.py`` do.
+It shares no code with the GPU path.
+
+Everything is computed in float64 with numpy/scipy.  Inputs are the exact
+values the GPU sees (fp32 arrays, or bf16 values decoded exactly), up-cast to
+float64 before any arithmetic.
+
+Paper: Anil, Gupta, Koren, Regan, Singer, "Scalable Second Order Optimization
+for Deep Learning" (arXiv 2002.09018).  Passages are cited by section,
+algorithm, equation or table.
+
+Functions and what pins them (tests under ``tests/test_oracle_*.py``):
+
+* ``stats_update``      -- Preliminaries, "The Shampoo algorithm" (definition
+  of L_t, R_t) and Algorithm 2 (beta2 EMA branch).  Pinned by the rank-1
+  closed form of the K-FAC comparison appendix, the trace identity, integer
+  inputs, the one-hot embedding identity (appendix "Shampoo for embedding
+  layers") and Lemmas 1 and 2 as PSD checks.
+* ``inv_root``          -- matrix power defined through the eigendecomposition
+  (Preliminaries, notation paragraph), with damping (Algorithm 1 and the
+  "Scaled damping" item of the coupled-Newton appendix).  Pinned by closed
+  forms (diagonal, c*I, p=1 inverse, p=2 squares to the inverse), 50-digit
+  mpmath brute force on 4x4, scipy's Schur-Pade fractional power, the
+  Kronecker identity (A (x) B)^a = A^a (x) B^a and X^p (A+eps I) = I.
+* ``max_sv``            -- Algorithm 1, procedure MaxSV.  Pinned by the
+  largest eigenvalue from eigh on matrices with a spectral gap.
+* ``coupled_newton``    -- Algorithm 1, procedure CoupledIteration, fp64.
+  Pinned against ``inv_root`` (<= 1e-9) and against the scalar recurrence
+  for iteration counts on diagonal inputs.
+* ``precondition``      -- Preliminaries (Shampoo update) and Lemma 1's
+  one-sided forms.  Pinned by brute force with the Kronecker product of the
+  full-matrix AdaGrad preconditioner on tiny shapes.
+* ``graft_update``      -- Algorithm 2 (momentum on both directions) and the
+  appendix "Further details on experiments", paragraph "Layer wise learning
+  rates" (AdaGrad magnitude, Shampoo direction).  Pinned by the step-norm
+  identity ||dW||_F = eta0 ||D^{-1/2} o G||_F and the t=1 closed form
+  eta0 * sqrt(nnz(G)).
+
+Readings of the paper where it is silent or ambiguous (each is listed in the
+design notes of the repository as well):
+
+R1  ||M - I||_inf in Algorithm 1 is the largest absolute entry.
+R2  Algorithm 1 uses one symbol for the stopping tolerance and the damping
+    scale; the damping is eps_d, the stop tolerance is ``tol``.
+R3  Stopping rules: CONVERGED when r <= tol; DIVERGED when r is not finite or
+    exceeds 1e6; STAGNATED when the previous residual was already below
+    STAG_GATE (quadratic phase) and the new one did not decrease; MAXITER
+    after ``max_iters`` iterations.
+R4  MaxSV starts from v = ones(n) and stops on a relative change
+    |lambda - lambda_old| <= maxsv_tol * lambda.
+R5  The Frobenius norm that sets z is taken after damping.
+R6  The cold start is X0 = z^{1/p} I, M0 = z (A + eps_eff I) (Algorithm 1).
+R7  The ridge epsilon*I is added exactly once, at the root; statistics
+    accumulate from zero.
+R8  D^{-1/2} o G is 0 where D is 0 (then G is 0 as well).
+R9  When ||P||_F = 0 the step size is 0.
+R10 The input to a root is symmetrised, A_s = (A + A^T)/2, before use.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+# Per-matrix outcome codes of an inverse-root computation.  The GPU library
+# uses the same numbering.
+CONVERGED, STAGNATED, MAXITER, DIVERGED, NOT_PD = 0, 1, 2, 3, 4
+
+STAG_GATE = 1e-3      # R3: stagnation is only tested once r fell below this
+DIVERGE_AT = 1e6      # R3: a residual above this (or non-finite) diverged
+
+
+def _f64(a):
+    return np.asarray(a, dtype=np.float64)
+
+
+def bf16_bits_to_f64(bits):
+    """Decode raw bfloat16 bit patterns (uint16) exactly into float64."""
+    bits = np.asarray(bits, dtype=np.uint16).astype(np.uint32) << 16
+    return bits.view(np.float32).astype(np.float64)
+
+
+# --------------------------------------------------------------------------
+# Statistics (Preliminaries "The Shampoo algorithm"; Algorithm 2)
+# --------------------------------------------------------------------------
+def stats_update(L, R, G, beta2=1.0):
+    """One statistics step for a block with gradient G (m x n).
+
+    beta2 == 1: L + G G^T and R + G^T G (plain sums, as in the definition of
+    L_t, R_t in Preliminaries).  beta2 < 1: beta2 L + (1 - beta2) G G^T, and
+    the same for R (Algorithm 2).  Either side may be None (not tracked).
+    The ridge is not added here (R7).  Returns (L_new, R_new) in float64.
+    """
+    G = _f64(G)
+    c = 1.0 if beta2 == 1.0 else 1.0 - beta2
+    Ln = None if L is None else beta2 * _f64(L) + c * (G @ G.T)
+    Rn = None if R is None else beta2 * _f64(R) + c * (G.T @ G)
+    return Ln, Rn
+
+
+# --------------------------------------------------------------------------
+# Inverse p-th roots
+# --------------------------------------------------------------------------
+def max_sv(A, n_step=100, tol=1e-6):
+    """Largest eigenvalue of a symmetric PSD matrix: Algorithm 1, MaxSV.
+
+    Power iteration with the Rayleigh quotient lambda = v_hat^T A v_hat,
+    starting from v = ones (R4) and stopping after n_step steps or once the
+    relative change is at most tol.  Returns (lambda, steps_taken).
+    """
+    A = _f64(A)
+    n = A.shape[0]
+    v = np.ones(n)
+    lam, i = 0.0, 0
+    while i < n_step:
+        vh = v / np.linalg.norm(v)
+        v = A @ vh
+        lam_old, lam = lam, float(vh @ v)
+        i += 1
+        if abs(lam - lam_old) <= tol * abs(lam):
+            break
+    return lam, i
+
+
+def damping(A, eps, eps_relative=False, lam_max=None, maxsv_steps=100,
+            maxsv_tol=1e-6):
+    """Effective damping eps_eff: eps (absolute) or eps * lambda_max(A).
+
+    The scaled variant follows the "Scaled damping" item of the coupled
+    Newton appendix and Algorithm 1.  ``lam_max`` may be supplied (e.g. the
+    value the GPU reported) to isolate the root error from the estimate.
+    Returns (eps_eff, lam_max_used).
+    """
+    if not eps_relative:
+        return float(eps), None
+    if lam_max is None:
+        lam_max, _ = max_sv(A, maxsv_steps, maxsv_tol)
+    return float(eps) * float(lam_max), float(lam_max)
+
+
+def inv_root(A, p, eps=0.0, eps_relative=False, lam_max=None):
+    """(A_s + eps_eff I)^(-1/p) by symmetric eigendecomposition.
+
+    Definition of A^alpha through A = U D U^T (Preliminaries, notation
+    paragraph): A^alpha = U D^alpha U^T, defined for alpha < 0 only when
+    every eigenvalue is positive.  Returns (X, status, eps_eff) with status
+    CONVERGED (root defined) or NOT_PD (X is None).
+    """
+    A = _f64(A)
+    As = 0.5 * (A + A.T)                                   # R10
+    eps_eff, _ = damping(As, eps, eps_relative, lam_max)
+    w, Q = np.linalg.eigh(As)
+    w = w + eps_eff
+    if not np.all(w > 0.0):
+        return None, NOT_PD, eps_eff
+    X = (Q * w ** (-1.0 / p)) @ Q.T
+    return 0.5 * (X + X.T), CONVERGED, eps_eff
+
+
+def cond_damped(A, eps=0.0, eps_relative=False, lam_max=None):
+    """Condition number of the damped matrix A_s + eps_eff I (eigh)."""
+    A = _f64(A)
+    As = 0.5 * (A + A.T)
+    eps_eff, _ = damping(As, eps, eps_relative, lam_max)
+    w = np.linalg.eigvalsh(As) + eps_eff
+    return float(w.max() / w.min()) if w.min() > 0 else np.inf
+
+
+def coupled_newton(A, p, eps=0.0, tol=1e-10, max_iters=100,
+                   eps_relative=False, lam_max=None, X0=None):
+    """Algorithm 1, CoupledIteration, in float64.
+
+    Steps in the paper's order: optional MaxSV and scaled damping; cold start
+    z = (1+p) / (2 ||A_d||_F), X = z^{1/p} I, M = z A_d (R5, R6), or the warm
+    start M = X^p A_d; then while ||M - I|| > tol:
+        M1 = (1 - alpha) I + alpha M   with alpha = -1/p
+        X  = X M1
+        M  = M1^p M
+    with the stopping rules of R1 and R3.  Returns a dict with X, iters,
+    resid (last ||M - I||, R1), status, eps_eff and z.
+    """
+    A = _f64(A)
+    n = A.shape[0]
+    As = 0.5 * (A + A.T)
+    eps_eff, lam = damping(As, eps, eps_relative, lam_max)
+    Ad = As + eps_eff * np.eye(n)
+    alpha = -1.0 / p
+    I = np.eye(n)
+    if X0 is not None:
+        X = _f64(X0)
+        M = np.linalg.matrix_power(X, p) @ Ad
+        z = None
+    else:
+        z = (1.0 + p) / (2.0 * np.linalg.norm(Ad, 'fro'))
+        X = z ** (1.0 / p) * I
+        M = z * Ad
+    r = float(np.max(np.abs(M - I)))
+    k = 0
+    status = CONVERGED
+    while not (r <= tol):
+        if not np.isfinite(r) or r > DIVERGE_AT:
+            status = DIVERGED
+            break
+        if k >= max_iters:
+            status = MAXITER
+            break
+        M1 = (1.0 - alpha) * I + alpha * M
+        X = X @ M1
+        M = np.linalg.matrix_power(M1, p) @ M
+        k += 1
+        r_new = float(np.max(np.abs(M - I)))
+        if not np.isfinite(r_new) or r_new > DIVERGE_AT:
+            r = r_new
+            status = DIVERGED
+            break
+        if r < STAG_GATE and r_new >= r and r_new > tol:
+            r = r_new
+            status = STAGNATED
+            break
+        r = r_new
+    return dict(X=X, iters=k, resid=r, status=status, eps_eff=eps_eff, z=z,
+                lam_max=lam)
+
+
+def scalar_newton_iters(m0, p, tol, max_iters=1000):
+    """Iterations the scalar recurrence m <- ((p+1-m)/p)^p m needs to reach
+    |m - 1| <= tol from m0: Algorithm 1 applied to a 1x1 matrix after
+    scaling.  Used to pin iteration counts on diagonal inputs."""
+    m, k = float(m0), 0
+    while abs(m - 1.0) > tol and k < max_iters:
+        m = ((p + 1.0 - m) / p) ** p * m
+        k += 1
+    return k
+
+
+# --------------------------------------------------------------------------
+# Preconditioned gradient (Preliminaries; Lemma 1 one-sided forms)
+# --------------------------------------------------------------------------
+def precondition(G, Lr=None, Rr=None):
+    """P = Lr G Rr; a missing root acts as the identity on its side."""
+    P = _f64(G)
+    if Lr is not None:
+        P = _f64(Lr) @ P
+    if Rr is not None:
+        P = P @ _f64(Rr)
+    return P
+
+
+# --------------------------------------------------------------------------
+# Grafting and the parameter update (Algorithm 2; "Layer wise learning rates")
+# --------------------------------------------------------------------------
+def adagrad_direction(D, G):
+    """D^{-1/2} o G with the convention 0 where D == 0 (R8)."""
+    D = _f64(D)
+    G = _f64(G)
+    out = np.zeros_like(G)
+    nz = D > 0
+    out[nz] = G[nz] / np.sqrt(D[nz])
+    return out
+
+
+def graft_update(W, D, G, P=None, eta0=1.0, beta1=0.0, Mg=None, Ps=None,
+                 use_shampoo=True):
+    """One parameter update of a block, Algorithm 2 with grafting.
+
+        D  <- D + G o G
+        Mg <- beta1 Mg + (1 - beta1) D^{-1/2} o G
+        if use_shampoo:
+            Ps  <- beta1 Ps + (1 - beta1) P
+            eta <- eta0 ||Mg||_F / ||Ps||_F      (0 when ||Ps||_F = 0, R9)
+            W   <- W - eta Ps
+        else:
+            eta <- eta0;  W <- W - eta Mg       (before the first roots)
+
+    At beta1 = 0 this is exactly the appendix graft: step magnitude
+    eta0 ||D^{-1/2} o G||_F along the unit Shampoo direction.  Mg and Ps may
+    be None when beta1 == 0 (they are then not carried).  Returns a dict
+    with W, D, Mg, Ps, eta and the two norms.
+    """
+    W = _f64(W)
+    D = _f64(D) + _f64(G) ** 2
+    g = adagrad_direction(D, G)
+    Mg_new = g if beta1 == 0.0 or Mg is None else beta1 * _f64(Mg) + (1.0 - beta1) * g
+    Ps_new = None if Ps is None else _f64(Ps)
+    if use_shampoo:
+        Pf = _f64(P)
+        Ps_new = Pf if beta1 == 0.0 or Ps is None else beta1 * _f64(Ps) + (1.0 - beta1) * Pf
+        nm = float(np.linalg.norm(Mg_new))
+        nps = float(np.linalg.norm(Ps_new))
+        eta = 0.0 if nps == 0.0 else eta0 * nm / nps
+        W_new = W - eta * Ps_new
+    else:
+        nm = float(np.linalg.norm(Mg_new))
+        nps = 0.0 if Ps_new is None else float(np.linalg.norm(Ps_new))
+        eta = float(eta0)
+        W_new = W - eta * Mg_new
+    return dict(W=W_new, D=D, Mg=Mg_new, Ps=Ps_new, eta=eta, norm_mg=nm,
+                norm_ps=nps)
+
+
+# --------------------------------------------------------------------------
+# Whole step of one block (Algorithm 2 with tau1 = tau2 = 1 unless given)
+# --------------------------------------------------------------------------
+def shampoo_step(state, G, p=4, eps=1e-6, eta0=1e-2, beta1=0.0, beta2=1.0,
+                 refresh_roots=True, use_shampoo=True, left=True, right=True,
+                 eps_relative=False):
+    """Stats, optional root refresh (eigh definition), precondition, graft.
+
+    ``state`` holds W, D and optionally L, R, Lr, Rr, Mg, Ps (float64).
+    Returns the new state dict.
+    """
+    s = dict(state)
+    L, R = stats_update(s.get('L') if left else None,
+                        s.get('R') if right else None, G, beta2)
+    if left:
+        s['L'] = L
+    if right:
+        s['R'] = R
+    if refresh_roots:
+        if left:
+            s['Lr'], st, _ = inv_root(L, p, eps, eps_relative)
+            assert st == CONVERGED
+        if right:
+            s['Rr'], st, _ = inv_root(R, p, eps, eps_relative)
+            assert st == CONVERGED
+    P = precondition(G, s.get('Lr') if left else None,
+                     s.get('Rr') if right else None) if use_shampoo else None
+    out = graft_update(s['W'], s['D'], G, P, eta0, beta1, s.get('Mg'),
+                       s.get('Ps'), use_shampoo)
+    s.update(W=out['W'], D=out['D'], Mg=out['Mg'], Ps=out['Ps'],
+             eta=out['eta'], P=P)
+    return s

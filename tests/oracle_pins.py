@@ -1,0 +1,408 @@
+"""Pins for the CPU oracle: checks against facts the paper and mathematics fix.
+
+Each ``pin_*`` takes a namespace ``o`` exposing the oracle's functions (the
+real module, or a deliberately broken copy in the mutation tests) and raises
+AssertionError when the oracle disagrees with the pinned fact.  None of the
+pins re-types the oracle's own formula: each compares against an
+independent route (closed form, brute force, another library algorithm, or a
+lemma of the paper).
+"""
+from __future__ import annotations
+
+import numpy as np
+
+rng = np.random.default_rng
+
+
+def _spd(n, cond, seed):
+    r = rng(seed)
+    Q, _ = np.linalg.qr(r.standard_normal((n, n)))
+    lam = np.logspace(0, np.log10(cond), n)
+    return (Q * lam) @ Q.T
+
+
+def _relf(a, b):
+    return np.linalg.norm(a - b) / np.linalg.norm(b)
+
+
+# ------------------------------------------------------------------ stats
+def pin_stats_rank1(o):
+    """G = u v^T gives G G^T = |v|^2 u u^T and G^T G = |u|^2 v v^T
+    (rank-one gradients, appendix comparing with K-FAC)."""
+    r = rng(1)
+    u, v = r.standard_normal(7), r.standard_normal(5)
+    L, R = o.stats_update(np.zeros((7, 7)), np.zeros((5, 5)), np.outer(u, v))
+    assert _relf(L, (v @ v) * np.outer(u, u)) < 1e-14
+    assert _relf(R, (u @ u) * np.outer(v, v)) < 1e-14
+
+
+def pin_stats_trace(o):
+    """tr L_t = tr R_t = sum_s ||G_s||_F^2 (both sides from zero)."""
+    r = rng(2)
+    L, R = np.zeros((6, 6)), np.zeros((9, 9))
+    tot = 0.0
+    for _ in range(4):
+        G = r.standard_normal((6, 9))
+        tot += float(np.sum(G * G))
+        L, R = o.stats_update(L, R, G)
+    assert abs(np.trace(L) - tot) < 1e-12 * tot
+    assert abs(np.trace(R) - tot) < 1e-12 * tot
+
+
+def pin_stats_integer_bruteforce(o):
+    """Integer gradients: the sums are exact; compare with a pure-Python
+    triple loop over the definition of L_t and R_t."""
+    r = rng(3)
+    m, n, T = 4, 3, 3
+    Gs = [r.integers(-5, 6, size=(m, n)) for _ in range(T)]
+    L, R = np.zeros((m, m)), np.zeros((n, n))
+    for G in Gs:
+        L, R = o.stats_update(L, R, G)
+    Lb = [[sum(int(G[i, k]) * int(G[j, k]) for G in Gs for k in range(n))
+           for j in range(m)] for i in range(m)]
+    Rb = [[sum(int(G[k, i]) * int(G[k, j]) for G in Gs for k in range(m))
+           for j in range(n)] for i in range(n)]
+    assert np.array_equal(L, np.array(Lb, dtype=float))
+    assert np.array_equal(R, np.array(Rb, dtype=float))
+
+
+def pin_stats_onehot_embedding(o):
+    """Embedding layer with one-hot inputs: G = dy x^T and x^T x = I give
+    G G^T = dy dy^T; with multi-hot columns x^T x is diagonal (appendix
+    "Shampoo for embedding layers")."""
+    r = rng(4)
+    d, N, m = 5, 40, 6
+    dy = r.standard_normal((d, m))
+    x = np.zeros((N, m))
+    x[r.choice(N, m, replace=False), np.arange(m)] = 1.0
+    L, _ = o.stats_update(np.zeros((d, d)), None, dy @ x.T)
+    assert _relf(L, dy @ dy.T) < 1e-13
+    # multi-hot: column j has c_j ones in rows no other column uses
+    x = np.zeros((N, m))
+    rows = r.permutation(N)
+    counts = [1, 2, 3, 1, 2, 4]
+    s = 0
+    for j, c in enumerate(counts):
+        x[rows[s:s + c], j] = 1.0
+        s += c
+    L, _ = o.stats_update(np.zeros((d, d)), None, dy @ x.T)
+    assert _relf(L, dy @ np.diag(counts) @ dy.T) < 1e-13
+
+
+def pin_stats_ema(o):
+    """beta2 < 1 with a constant gradient: L_t = (1 - beta2^t) G G^T
+    (geometric series of Algorithm 2's EMA from L_0 = 0)."""
+    r = rng(5)
+    G = r.standard_normal((4, 6))
+    b2, t = 0.9, 7
+    L, R = np.zeros((4, 4)), np.zeros((6, 6))
+    for _ in range(t):
+        L, R = o.stats_update(L, R, G, beta2=b2)
+    f = 1.0 - b2 ** t
+    assert _relf(L, f * G @ G.T) < 1e-13
+    assert _relf(R, f * G.T @ G) < 1e-13
+
+
+def pin_lemma1(o):
+    """Lemma 1: with rank <= r gradients, H_hat <= r L^{1/p} (x) R^{1/q}
+    for 1/p + 1/q = 1 (Loewner order); vec is row stacking."""
+    r = rng(6)
+    m, n, rank, eps = 3, 4, 2, 1e-3
+    L, R = np.zeros((m, m)), np.zeros((n, n))
+    H = eps * np.eye(m * n)
+    for _ in range(3):
+        G = r.standard_normal((m, rank)) @ r.standard_normal((rank, n))
+        L, R = o.stats_update(L, R, G)
+        g = G.reshape(-1)
+        H += np.outer(g, g)
+    L += eps * np.eye(m)
+    R += eps * np.eye(n)
+    for p in (2.0, 3.0, 1.5):
+        q = p / (p - 1.0)
+        Lp, _, _ = o.inv_root(L, -p)       # L^{1/p}
+        Rq, _, _ = o.inv_root(R, -q)
+        gap = rank * np.kron(Lp, Rq) - H
+        assert np.linalg.eigvalsh(0.5 * (gap + gap.T)).min() > -1e-9
+
+
+def pin_lemma2(o):
+    """Lemma 2: H_hat <= k B_t with B_t block diagonal over k sub-vectors."""
+    r = rng(7)
+    m, k, eps = 3, 4, 1e-3
+    H = eps * np.eye(m * k)
+    blocks = [eps * np.eye(m) for _ in range(k)]
+    for _ in range(5):
+        g = r.standard_normal(m * k)
+        H += np.outer(g, g)
+        for j in range(k):
+            gj = g[j * m:(j + 1) * m].reshape(m, 1)
+            blocks[j], _ = o.stats_update(blocks[j], None, gj)
+    B = np.zeros((m * k, m * k))
+    for j in range(k):
+        B[j * m:(j + 1) * m, j * m:(j + 1) * m] = blocks[j]
+    gap = k * B - H
+    assert np.linalg.eigvalsh(gap).min() > -1e-9
+
+
+# ------------------------------------------------------------------ roots
+def pin_root_diagonal(o):
+    """diag(d) + eps I -> diag((d + eps)^(-1/p))."""
+    d = np.array([0.5, 2.0, 7.0, 1e-3, 30.0])
+    for p in (1, 2, 4, 8):
+        X, st, _ = o.inv_root(np.diag(d), p, eps=1e-4)
+        assert st == o.CONVERGED
+        assert np.max(np.abs(X - np.diag((d + 1e-4) ** (-1.0 / p)))) < 1e-12 * np.max(X)
+
+
+def pin_root_scaled_identity(o):
+    """c I -> (c + eps)^(-1/p) I, also with eps relative to lambda_max = c."""
+    n, c = 6, 3.7
+    for p in (2, 4):
+        X, _, _ = o.inv_root(c * np.eye(n), p, eps=0.1)
+        assert np.allclose(X, (c + 0.1) ** (-1.0 / p) * np.eye(n), rtol=1e-13, atol=0)
+        X, _, e = o.inv_root(c * np.eye(n), p, eps=0.1, eps_relative=True)
+        assert abs(e - 0.1 * c) < 1e-12
+        assert np.allclose(X, (c * 1.1) ** (-1.0 / p) * np.eye(n), rtol=1e-12, atol=0)
+
+
+def pin_root_p1_inverse(o):
+    """p = 1 is the ordinary inverse (LU-based numpy.linalg.inv)."""
+    A = _spd(12, 1e3, 8)
+    X, _, _ = o.inv_root(A, 1, eps=1e-3)
+    assert _relf(X, np.linalg.inv(A + 1e-3 * np.eye(12))) < 1e-11
+
+
+def pin_root_p2_square(o):
+    """p = 2: X^2 (A + eps I) = I."""
+    A = _spd(10, 1e4, 9)
+    X, _, _ = o.inv_root(A, 2, eps=1e-2)
+    assert np.linalg.norm(X @ X @ (A + 1e-2 * np.eye(10)) - np.eye(10)) < 1e-10
+
+
+def pin_root_invariant(o):
+    """||X^p (A + eps I) - I||_F <= 1e-6 at condition numbers up to 1e6."""
+    for n, cond, p in ((64, 1e3, 4), (96, 1e6, 4), (80, 1e6, 2), (48, 1e5, 8)):
+        A = _spd(n, cond, 10 + n)
+        X, _, _ = o.inv_root(A, p, eps=1e-6)
+        res = np.linalg.matrix_power(X, p) @ (A + 1e-6 * np.eye(n)) - np.eye(n)
+        assert np.linalg.norm(res) <= 1e-6
+
+
+def pin_root_mpmath_4x4(o):
+    """4 x 4 brute force at 50 digits: mpmath powm(A + eps I, -1/p)."""
+    import mpmath as mp
+    mp.mp.dps = 50
+    r = rng(11)
+    B = r.standard_normal((4, 4))
+    A = B @ B.T + 0.1 * np.eye(4)
+    for p in (2, 4):
+        X, _, _ = o.inv_root(A, p, eps=1e-3)
+        Am = mp.matrix([[mp.mpf(float(A[i, j])) + (mp.mpf('1e-3') if i == j else 0)
+                         for j in range(4)] for i in range(4)])
+        Xm = mp.powm(Am, mp.mpf(-1) / p)
+        Xb = np.array([[float(mp.re(Xm[i, j])) for j in range(4)] for i in range(4)])
+        assert _relf(X, Xb) < 1e-13
+
+
+def pin_root_2x2_closed_form(o):
+    """2 x 2 SPD square root: sqrt(A) = (A + s I) / t, s = sqrt(det A),
+    t = sqrt(tr A + 2 s); A^{-1/4} is the inverse of sqrt(sqrt(A))."""
+    A = np.array([[3.0, 1.2], [1.2, 2.0]])
+
+    def sqrt2(M):
+        s = np.sqrt(np.linalg.det(M))
+        return (M + s * np.eye(2)) / np.sqrt(np.trace(M) + 2 * s)
+    X, _, _ = o.inv_root(A, 4)
+    assert _relf(X, np.linalg.inv(sqrt2(sqrt2(A)))) < 1e-14
+    X, _, _ = o.inv_root(A, 2)
+    assert _relf(X, np.linalg.inv(sqrt2(A))) < 1e-14
+
+
+def pin_root_schur_pade(o):
+    """scipy's fractional_matrix_power (Schur-Pade, not eigh) agrees."""
+    from scipy.linalg import fractional_matrix_power
+    A = _spd(40, 1e4, 12)
+    for p in (2, 4, 8):
+        X, _, _ = o.inv_root(A, p, eps=1e-5)
+        Y = np.real(fractional_matrix_power(A + 1e-5 * np.eye(40), -1.0 / p))
+        assert _relf(X, Y) < 1e-10
+
+
+def pin_root_kronecker(o):
+    """(A (x) B)^a = A^a (x) B^a (Preliminaries)."""
+    A, B = _spd(3, 20.0, 13), _spd(4, 50.0, 14)
+    X, _, _ = o.inv_root(np.kron(A, B), 4)
+    XA, _, _ = o.inv_root(A, 4)
+    XB, _, _ = o.inv_root(B, 4)
+    assert _relf(X, np.kron(XA, XB)) < 1e-12
+
+
+def pin_root_not_pd(o):
+    """A^alpha with alpha < 0 is undefined unless positive definite."""
+    A = np.diag([1.0, 2.0, -0.5])
+    X, st, _ = o.inv_root(A, 4, eps=0.1)
+    assert st == o.NOT_PD and X is None
+
+
+def pin_root_asymmetric_input(o):
+    """An input that is symmetric up to a perturbation gives the root of its
+    symmetric part: add a skew matrix and the result must not change."""
+    A = _spd(8, 100.0, 15)
+    S = rng(16).standard_normal((8, 8))
+    X0, _, _ = o.inv_root(A, 4)
+    X1, _, _ = o.inv_root(A + 1e-3 * (S - S.T), 4)
+    assert _relf(X1, X0) < 1e-13
+
+
+# ------------------------------------------------------------------ MaxSV
+def pin_maxsv(o):
+    """Power iteration converges to the top eigenvalue when it is isolated."""
+    r = rng(17)
+    Q, _ = np.linalg.qr(r.standard_normal((30, 30)))
+    lam = np.concatenate([np.linspace(0.1, 1.0, 29), [5.0]])
+    A = (Q * lam) @ Q.T
+    l, steps = o.max_sv(A, n_step=500, tol=1e-12)
+    assert abs(l - 5.0) < 1e-9 and steps < 500
+
+
+# ------------------------------------------------------------------ coupled Newton (Algorithm 1)
+def pin_newton_vs_eigh(o):
+    """The fp64 coupled iteration reaches the eigh-defined root to 1e-9."""
+    for n, cond, p in ((64, 1e2, 4), (64, 1e6, 4), (48, 1e6, 2), (32, 1e4, 8), (40, 1e3, 1)):
+        A = _spd(n, cond, 20 + n + p)
+        res = o.coupled_newton(A, p, eps=1e-6, tol=1e-12)
+        X, _, _ = o.inv_root(A, p, eps=1e-6)
+        assert res['status'] in (o.CONVERGED, o.STAGNATED)
+        assert _relf(res['X'], X) < 1e-9
+
+
+def pin_newton_scalar_iters(o):
+    """On a diagonal input every eigenvalue follows the scalar recurrence
+    m <- ((p+1-m)/p)^p m from m0 = z lambda_i, so the iteration count is
+    the largest count over the diagonal, and the iterate stays diagonal."""
+    d = np.array([1e-3, 0.1, 1.0, 3.0, 50.0])
+    for p in (2, 4):
+        res = o.coupled_newton(np.diag(d), p, eps=0.0, tol=1e-12)
+        z = (1.0 + p) / (2.0 * np.linalg.norm(d))
+        want = max(o.scalar_newton_iters(z * x, p, 1e-12) for x in d)
+        assert abs(res['iters'] - want) <= 1
+        assert np.count_nonzero(res['X'] - np.diag(np.diag(res['X']))) == 0
+        assert _relf(np.diag(res['X']), d ** (-1.0 / p)) < 1e-10
+    # heavy damping: z is set by the damped matrix (Frobenius norm taken
+    # after the ridge), which fixes the count through the same recurrence
+    d2, eps = np.array([1e-3, 1.0, 3.0]), 100.0
+    for p in (2, 4):
+        res = o.coupled_newton(np.diag(d2), p, eps=eps, tol=1e-12)
+        z = (1.0 + p) / (2.0 * np.linalg.norm(d2 + eps))
+        want = max(o.scalar_newton_iters(z * (x + eps), p, 1e-12) for x in d2)
+        assert res['status'] == o.CONVERGED and abs(res['iters'] - want) <= 1
+        assert _relf(np.diag(res['X']), (d2 + eps) ** (-1.0 / p)) < 1e-12
+
+
+def pin_newton_status_rules(o):
+    """MAXITER at a tiny cap, DIVERGED on an indefinite matrix, STAGNATED
+    when the tolerance is below what fp64 can reach, MaxSV damping used."""
+    A = _spd(16, 1e3, 30)
+    assert o.coupled_newton(A, 4, eps=0.0, tol=1e-12, max_iters=1)['status'] == o.MAXITER
+    assert o.coupled_newton(np.diag([1.0, 2.0, -1.0]), 4, tol=1e-10)['status'] == o.DIVERGED
+    res = o.coupled_newton(A, 4, tol=0.0)
+    assert res['status'] == o.STAGNATED and res['resid'] < 1e-12
+    res = o.coupled_newton(A, 4, eps=1e-3, eps_relative=True, tol=1e-12)
+    lmax = np.linalg.eigvalsh(A).max()
+    assert abs(res['eps_eff'] - 1e-3 * lmax) < 1e-6 * lmax
+
+
+# ------------------------------------------------------------------ precondition
+def pin_precondition_kronecker(o):
+    """vec(Lr G Rr) = (Lr (x) Rr^T) vec(G) with row-stacking vec, on
+    non-symmetric factors so a transposed operand would show."""
+    r = rng(40)
+    Lr, Rr, G = r.standard_normal((6, 6)), r.standard_normal((5, 5)), r.standard_normal((6, 5))
+    P = o.precondition(G, Lr, Rr)
+    assert _relf(P.reshape(-1), np.kron(Lr, Rr.T) @ G.reshape(-1)) < 1e-13
+    assert _relf(o.precondition(G, None, Rr), G @ Rr) < 1e-14
+    assert _relf(o.precondition(G, Lr, None), Lr @ G) < 1e-14
+    assert np.array_equal(o.precondition(G, None, None), G)
+
+
+def pin_precondition_full_matrix_link(o):
+    """With H = (L (x) R)^{1/2} formed and rooted as one mn x mn matrix,
+    H^{-1/2} vec(G) equals vec(L^{-1/4} G R^{-1/4}) (Shampoo update from
+    the full-matrix AdaGrad rule)."""
+    r = rng(41)
+    m, n = 4, 3
+    L, R = np.zeros((m, m)), np.zeros((n, n))
+    for _ in range(6):
+        L, R = o.stats_update(L, R, r.standard_normal((m, n)))
+    L += 1e-2 * np.eye(m)
+    R += 1e-2 * np.eye(n)
+    G = r.standard_normal((m, n))
+    w, Q = np.linalg.eigh(np.kron(L, R))
+    Hm12 = (Q * w ** -0.25) @ Q.T              # ((L (x) R)^{1/2})^{-1/2}
+    Lr, _, _ = o.inv_root(L, 4)
+    Rr, _, _ = o.inv_root(R, 4)
+    assert _relf(o.precondition(G, Lr, Rr).reshape(-1), Hm12 @ G.reshape(-1)) < 1e-11
+
+
+# ------------------------------------------------------------------ graft
+def pin_graft_norm_identity(o):
+    """beta1 = 0: ||dW||_F = eta0 ||D^{-1/2} o G||_F whatever the direction."""
+    r = rng(50)
+    W, D0 = r.standard_normal((7, 5)), r.random((7, 5))
+    G, P = r.standard_normal((7, 5)), r.standard_normal((7, 5))
+    out = o.graft_update(W, D0, G, P, eta0=0.3)
+    want = 0.3 * np.linalg.norm(G / np.sqrt(D0 + G * G))
+    assert abs(np.linalg.norm(out['W'] - W) - want) < 1e-13 * want
+    assert _relf(out['D'], D0 + G * G) < 1e-15
+
+
+def pin_graft_first_step(o):
+    """t = 1 (D_0 = 0): D^{-1/2} o G = sign(G), so ||dW||_F = eta0 sqrt(nnz);
+    zero entries of G stay zero (no 0/0)."""
+    r = rng(51)
+    G = r.standard_normal((6, 6))
+    G[r.random((6, 6)) < 0.3] = 0.0
+    P = r.standard_normal((6, 6))
+    out = o.graft_update(np.zeros((6, 6)), np.zeros((6, 6)), G, P, eta0=0.5)
+    nnz = np.count_nonzero(G)
+    assert abs(np.linalg.norm(out['W']) - 0.5 * np.sqrt(nnz)) < 1e-13
+    assert np.array_equal(out['Mg'], np.sign(G))
+
+
+def pin_graft_identity_roots(o):
+    """Roots proportional to I: the direction is G / ||G||_F."""
+    r = rng(52)
+    G, D0 = r.standard_normal((5, 4)), r.random((5, 4))
+    P = o.precondition(G, 2.0 * np.eye(5), 0.5 * np.eye(4))
+    out = o.graft_update(np.zeros((5, 4)), D0, G, P, eta0=1.0)
+    mag = np.linalg.norm(G / np.sqrt(D0 + G * G))
+    assert _relf(-out['W'], mag * G / np.linalg.norm(G)) < 1e-14
+
+
+def pin_graft_adagrad_fallback(o):
+    """Before the first roots (t <= tau1) the step is eta0 * M_t."""
+    r = rng(53)
+    W, D0, G = r.standard_normal((3, 3)), r.random((3, 3)), r.standard_normal((3, 3))
+    out = o.graft_update(W, D0, G, None, eta0=0.1, use_shampoo=False)
+    assert _relf(out['W'], W - 0.1 * G / np.sqrt(D0 + G * G)) < 1e-15
+
+
+def pin_graft_momentum_1x1(o):
+    """Two steps of Algorithm 2 on a 1 x 1 block, worked by hand:
+    beta1 = 1/2, eta0 = 1, G = 3 then 4, P = 2 then 2.
+      t=1: D=9,  D^-1/2 G = 1,   M = 1/2,  P_1 = 1,   eta = 1/2,  W -= 1/2
+      t=2: D=25, D^-1/2 G = 4/5, M = 13/20, P_2 = 3/2, eta = 13/30, W -= 13/20
+    so W ends at W0 - 23/20; a third step with P = -3/2 makes P_3 = 0 and
+    then eta = 0 (no update)."""
+    s = dict(W=np.array([[1.0]]), D=np.zeros((1, 1)), Mg=np.zeros((1, 1)), Ps=np.zeros((1, 1)))
+    o1 = o.graft_update(s['W'], s['D'], np.array([[3.0]]), np.array([[2.0]]), 1.0, 0.5, s['Mg'], s['Ps'])
+    assert abs(o1['eta'] - 0.5) < 1e-15 and abs(o1['W'][0, 0] - 0.5) < 1e-15
+    o2 = o.graft_update(o1['W'], o1['D'], np.array([[4.0]]), np.array([[2.0]]), 1.0, 0.5, o1['Mg'], o1['Ps'])
+    assert abs(o2['Mg'][0, 0] - 0.65) < 1e-15 and abs(o2['Ps'][0, 0] - 1.5) < 1e-15
+    assert abs(o2['eta'] - 13.0 / 30.0) < 1e-15
+    assert abs(o2['W'][0, 0] - (1.0 - 23.0 / 20.0)) < 1e-14
+    o3 = o.graft_update(o2['W'], o2['D'], np.array([[1.0]]), np.array([[-1.5]]), 1.0, 0.5, o2['Mg'], o2['Ps'])
+    assert o3['eta'] == 0.0 and o3['W'][0, 0] == o2['W'][0, 0]
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith('pin_')]

@@ -1,0 +1,74 @@
+"""Planted mistakes in the oracle must be caught by its pins.
+
+Each case rewrites one snippet of one oracle function (a dropped term, a
+wrong sign or exponent, a transposed operand, a swapped ratio), installs the
+broken function in place of the real one for the duration of the test, and
+checks that at least one of the named pins now fails.  This is the evidence
+that the pins constrain every part of the oracle and are not tautologies.
+"""
+import inspect
+import textwrap
+
+import pytest
+
+import oracle.shampoo_oracle as O
+from tests import oracle_pins as P
+
+MUTATIONS = [
+    # (function, original snippet, planted mistake, pins that must notice)
+    ("inv_root", "w ** (-1.0 / p)", "w ** (1.0 / p)", [P.pin_root_diagonal]),
+    ("inv_root", "w = w + eps_eff", "w = w + 0.0 * eps_eff", [P.pin_root_diagonal]),
+    ("inv_root", "(Q * w ** (-1.0 / p)) @ Q.T", "(Q * w ** (-1.0 / p)) @ Q", [P.pin_root_mpmath_4x4]),
+    ("inv_root", "As = 0.5 * (A + A.T)", "As = np.triu(A) + np.triu(A, 1).T",
+     [P.pin_root_asymmetric_input]),
+    ("damping", "return float(eps) * float(lam_max), float(lam_max)",
+     "return float(eps), float(lam_max)", [P.pin_root_scaled_identity]),
+    ("stats_update", "c * (G @ G.T)", "c * (G.T @ G) if G.shape[0] == G.shape[1] else c * (G @ G.T)",
+     [P.pin_stats_integer_bruteforce, P.pin_lemma1]),
+    ("stats_update", "c = 1.0 if beta2 == 1.0 else 1.0 - beta2", "c = 1.0", [P.pin_stats_ema]),
+    ("stats_update", "beta2 * _f64(R)", "_f64(R)", [P.pin_stats_ema]),
+    ("max_sv", "lam_old, lam = lam, float(vh @ v)", "lam_old, lam = lam, float(v @ v)", [P.pin_maxsv]),
+    ("coupled_newton", "M1 = (1.0 - alpha) * I + alpha * M", "M1 = (1.0 + alpha) * I - alpha * M",
+     [P.pin_newton_vs_eigh]),
+    ("coupled_newton", "X = z ** (1.0 / p) * I", "X = z ** (-1.0 / p) * I", [P.pin_newton_vs_eigh]),
+    ("coupled_newton", "M = np.linalg.matrix_power(M1, p) @ M", "M = np.linalg.matrix_power(M1, p - 1) @ M",
+     [P.pin_newton_vs_eigh]),
+    ("coupled_newton", "z = (1.0 + p) / (2.0 * np.linalg.norm(Ad, 'fro'))",
+     "z = (1.0 + p) / (2.0 * np.linalg.norm(As, 'fro'))", [P.pin_newton_scalar_iters]),
+    ("precondition", "P = _f64(Lr) @ P", "P = _f64(Lr).T @ P", [P.pin_precondition_kronecker]),
+    ("precondition", "P = P @ _f64(Rr)", "P = P @ _f64(Rr).T",
+     [P.pin_precondition_kronecker]),
+    ("adagrad_direction", "G[nz] / np.sqrt(D[nz])", "G[nz] / D[nz]", [P.pin_graft_norm_identity]),
+    ("graft_update", "D = _f64(D) + _f64(G) ** 2", "D = _f64(D) + _f64(G)", [P.pin_graft_norm_identity]),
+    ("graft_update", "eta = 0.0 if nps == 0.0 else eta0 * nm / nps", "eta = 0.0 if nm == 0.0 else eta0 * nps / nm",
+     [P.pin_graft_norm_identity, P.pin_graft_identity_roots]),
+    ("graft_update", "beta1 * _f64(Ps) + (1.0 - beta1) * Pf", "beta1 * _f64(Ps) + Pf", [P.pin_graft_momentum_1x1]),
+    ("graft_update", "W_new = W - eta * Mg_new", "W_new = W - eta * G", [P.pin_graft_adagrad_fallback]),
+]
+
+
+def _mutant(fname, old, new):
+    src = textwrap.dedent(inspect.getsource(getattr(O, fname)))
+    assert old in src, f"snippet not found in {fname}: {old}"
+    ns = {}
+    exec(compile(src.replace(old, new), f"<mutant {fname}>", "exec"), O.__dict__, ns)
+    return ns[fname]
+
+
+@pytest.mark.parametrize("fname,old,new,pins", MUTATIONS,
+                         ids=[f"{m[0]}:{i}" for i, m in enumerate(MUTATIONS)])
+def test_planted_mistake_is_caught(monkeypatch, fname, old, new, pins):
+    monkeypatch.setattr(O, fname, _mutant(fname, old, new))
+    caught = []
+    for pin in pins:
+        try:
+            pin(O)
+        except (AssertionError, ValueError, FloatingPointError, ZeroDivisionError, TypeError):
+            caught.append(pin.__name__)
+    assert caught, f"mutation of {fname} ({new!r}) slipped past {[p.__name__ for p in pins]}"
+
+
+def test_real_oracle_passes_all_pins_used_here():
+    for _, _, _, pins in MUTATIONS:
+        for pin in pins:
+            pin(O)
