@@ -1,0 +1,237 @@
+/*
+ * shampoo.h -- C ABI of the MI355X (gfx950) scalable-Shampoo hot path.
+ *
+ * Paper: Anil, Gupta, Koren, Regan, Singer, "Scalable Second Order
+ * Optimization for Deep Learning" (arXiv 2002.09018).  The three steps the
+ * paper lists as Shampoo's extra cost (Section 3, "Scaling-up Second Order
+ * Optimization": statistics, inverse p-th roots, preconditioned gradient) map
+ * onto shampoo_update_stats, shampoo_inv_root_batched and shampoo_precondition;
+ * the layer-wise grafted update of Algorithm 2 and of the appendix "Further
+ * details on experiments" (paragraph "Layer wise learning rates") is
+ * shampoo_graft.
+ *
+ * Conventions shared by every call
+ *  - Matrices are row-major.  A block is a strided view of a larger tensor:
+ *    element (i, j) of the view lives at ptr[i * ld + j].
+ *  - Every tensor pointer is a DEVICE pointer on the handle's device, owned
+ *    by the caller.  The library never frees caller memory.
+ *  - Every call is ordered on `stream` (a hipStream_t passed as void*; NULL
+ *    is the null stream).  Host arrays passed in (blocks, jobs, params) are
+ *    copied before the call returns and may be reused at once.
+ *  - Return codes cover argument and launch errors only.  Numeric outcomes of
+ *    root computations are per-matrix status codes written to device memory.
+ *  - One handle per host thread/stream pair; handles share no state.
+ *  - The library owns only what hangs off its handle: device copies of the
+ *    block/job tables, a grow-on-demand scratch area for the intermediate
+ *    G*Rr of two-sided preconditioning, and a few bytes of pinned host memory
+ *    used to poll convergence.
+ */
+#ifndef SHAMPOO_MI355X_H
+#define SHAMPOO_MI355X_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum shampoo_status {
+  SHAMPOO_OK = 0,
+  SHAMPOO_EINVAL = -1,       /* bad argument: NULL where required, size out of range, ... */
+  SHAMPOO_EUNSUPPORTED = -2, /* valid but not implemented (e.g. p not in {1,2,4,8}) */
+  SHAMPOO_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
+  SHAMPOO_ENOMEM = -4        /* workspace too small, or a library allocation failed */
+} shampoo_status;
+
+/* Element type of the gradient views G. */
+typedef enum shampoo_dtype {
+  SHAMPOO_F32 = 0,
+  SHAMPOO_BF16 = 1 /* raw bfloat16 bit patterns; up-cast exactly to fp32 on load */
+} shampoo_dtype;
+
+/* Per-matrix outcome of shampoo_inv_root_batched (shampoo_root_info.status). */
+enum {
+  SHAMPOO_ROOT_CONVERGED = 0, /* max|M - I| <= tol */
+  SHAMPOO_ROOT_STAGNATED = 1, /* residual stopped decreasing below 1e-3: rounding floor reached */
+  SHAMPOO_ROOT_MAXITER = 2,   /* iteration cap reached */
+  SHAMPOO_ROOT_DIVERGED = 3,  /* residual non-finite or above 1e6 */
+  SHAMPOO_ROOT_NOT_PD = 4     /* damped matrix has a non-positive diagonal entry or zero norm */
+};
+
+/* Arithmetic used for roots (shampoo_root_params.precision). */
+enum {
+  SHAMPOO_PRECISION_FP32 = 0, /* fp32 MFMA only */
+  SHAMPOO_PRECISION_AUTO = 1, /* fp32 MFMA; matrices that need more iterations than a matrix
+                                 of condition kappa32 would (or that fail) are redone in fp64 */
+  SHAMPOO_PRECISION_FP64 = 2  /* fp64 MFMA only */
+};
+
+/*
+ * One preconditioned block (Section 3.1, "Preconditioning blocks from large
+ * tensors": each block of a large tensor is treated as a tensor of its own).
+ * rows x cols = m x n, both in [1, 4096].  G, W, D, P, Mg and Ps are m x n
+ * views sharing the row stride `ld` (elements, >= cols).  L is m x m and R is
+ * n x n, contiguous (ld = m and n).  A NULL statistic means that side is not
+ * tracked; a NULL root means the identity on that side (one-sided
+ * preconditioning, Lemma 1).  Mg and Ps are needed only when beta1 > 0.
+ * Element types: G per call (shampoo_dtype), everything else fp32.
+ */
+typedef struct shampoo_block {
+  int32_t rows, cols;
+  int64_t ld;
+  const void* G;
+  float* W;
+  float* D;
+  float* P;
+  float* Mg;
+  float* Ps;
+  float* L;
+  float* R;
+  const float* Lr;
+  const float* Rr;
+} shampoo_block;
+
+/*
+ * One inverse-root job: X = (A_s + eps_eff I)^(-1/p) with A_s the symmetric
+ * part of A.  A and X are contiguous n x n fp32, n in [1, 4096]; A is only
+ * read.  X receives the root; on a status other than CONVERGED/STAGNATED it
+ * holds the last iterate.
+ */
+typedef struct shampoo_root_job {
+  int32_t n;
+  int32_t reserved; /* must be 0 */
+  const float* A;
+  float* X;
+} shampoo_root_job;
+
+/* Parameters of a root call (Algorithm 1).  shampoo_root_params_default()
+ * fills the values used throughout the repository. */
+typedef struct shampoo_root_params {
+  int32_t p;            /* root order: X = A^(-1/p); one of 1, 2, 4, 8 */
+  float eps;            /* damping: eps_eff = eps, or eps * lambda_max when eps_relative */
+  int32_t eps_relative; /* 1: scaled damping with lambda_max from MaxSV power iteration */
+  float tol;            /* stop when max_ij |M - I|_ij <= tol */
+  int32_t max_iters;    /* iteration cap of a precision phase */
+  int32_t precision;    /* SHAMPOO_PRECISION_* */
+  float kappa32;        /* AUTO: largest damped condition number accepted from fp32 */
+  int32_t maxsv_steps;  /* MaxSV cap on power steps */
+  float maxsv_tol;      /* MaxSV stop: |lambda - lambda_old| <= maxsv_tol * lambda */
+  int32_t poll;         /* 1: the host polls a device counter and stops enqueuing
+                           iterations once no matrix is active (the call then waits
+                           for the stream); 0: enqueue max_iters iterations, fully
+                           asynchronous, converged matrices skip their work */
+} shampoo_root_params;
+
+/* Per-matrix result of a root call, written on the stream (device memory). */
+typedef struct shampoo_root_info {
+  int32_t status;     /* SHAMPOO_ROOT_* of the phase that produced X */
+  int32_t iters;      /* iterations of that phase */
+  int32_t precision;  /* 32 or 64: arithmetic that produced X */
+  int32_t iters_fp32; /* iterations spent in fp32 (also when escalated) */
+  float resid;        /* last max|M - I| */
+  float lambda_max;   /* MaxSV estimate (eps_relative), else 0 */
+  float cond_est;     /* condition-number upper estimate from the iteration count */
+  float eps_eff;      /* damping actually added */
+} shampoo_root_info;
+
+/* Create / destroy a handle bound to HIP device `device`. */
+shampoo_status shampoo_create(void** handle, int device);
+shampoo_status shampoo_destroy(void* handle);
+/* Text of the last error on this handle ("" if none).  Valid until the next call. */
+const char* shampoo_last_error(const void* handle);
+/* Library version string. */
+const char* shampoo_version(void);
+
+/* Defaults: p=4, eps=1e-6 absolute, tol=1e-6, max_iters=100, precision AUTO,
+ * kappa32=1e4, maxsv_steps=100, maxsv_tol=1e-6, poll=1. */
+void shampoo_root_params_default(shampoo_root_params* params);
+
+/*
+ * Statistics update, Preliminaries ("The Shampoo algorithm", definition of
+ * L_t and R_t) and Algorithm 2:
+ *   beta2 == 1:  L += G G^T,  R += G^T G
+ *   beta2 <  1:  L = beta2 L + (1 - beta2) G G^T  (same for R)
+ * For every block with non-NULL L (resp. R).  L and R stay exactly symmetric:
+ * the upper triangle is computed and mirrored.  The ridge eps*I is not added
+ * here; shampoo_inv_root_batched adds it once.  G: g_dtype.
+ * Errors: EINVAL for nblocks < 0, NULL blocks with nblocks > 0, a block with
+ * both L and R NULL is skipped, sizes outside [1, 4096], ld < cols, beta2
+ * outside (0, 1].
+ */
+shampoo_status shampoo_update_stats(void* handle, const shampoo_block* blocks, int nblocks,
+                                    int g_dtype, float beta2, void* stream);
+
+/* Device workspace (bytes) that shampoo_inv_root_batched needs for `jobs`
+ * under `precision`; 0 on invalid arguments. */
+size_t shampoo_inv_root_workspace_bytes(const shampoo_root_job* jobs, int njobs, int precision);
+
+/*
+ * Batched inverse p-th roots by the coupled Newton iteration, Algorithm 1
+ * (appendix "A coupled Newton iteration for computation of inverse p-th
+ * roots"), all matrices in one grouped launch per product:
+ *   eps_eff = eps, or eps * MaxSV(A) (scaled damping);
+ *   A_d = A_s + eps_eff I;  z = (1 + p) / (2 ||A_d||_F);
+ *   X = z^(1/p) I;  M = z A_d;
+ *   while max|M - I| > tol:  M1 = ((p + 1) I - M) / p;  X = X M1;  M = M1^p M.
+ * Each matrix leaves the iteration on its own (CONVERGED, STAGNATED, MAXITER,
+ * DIVERGED).  Products of the commuting symmetric iterates are computed on
+ * their upper triangle and mirrored.  `workspace` is device memory of at least
+ * shampoo_inv_root_workspace_bytes(jobs, njobs, params->precision) bytes,
+ * owned by the caller and used exclusively by this call until the stream
+ * reaches its end.  `info` is a device array of njobs entries.
+ * Errors: EINVAL (NULL pointers, n outside [1, 4096], eps < 0, tol < 0,
+ * max_iters < 1), EUNSUPPORTED (p not in {1,2,4,8}), ENOMEM (ws_bytes too small).
+ */
+shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jobs, int njobs,
+                                        const shampoo_root_params* params, void* workspace,
+                                        size_t ws_bytes, shampoo_root_info* info, void* stream);
+
+/*
+ * Preconditioned gradient P = Lr G Rr (Preliminaries, Shampoo update rule;
+ * one-sided forms of Lemma 1 when a root is NULL; P = G when both are).
+ * Lr and Rr must be symmetric (inverse roots are).  G: g_dtype.
+ * Errors: as shampoo_update_stats; P must be non-NULL.
+ */
+shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, int nblocks,
+                                    int g_dtype, void* stream);
+
+/*
+ * Grafted parameter update, Algorithm 2 with the AdaGrad-magnitude /
+ * Shampoo-direction graft ("Layer wise learning rates"):
+ *   D  = D + G o G
+ *   Mg = beta1 Mg + (1 - beta1) D^(-1/2) o G        (D^(-1/2) o G := 0 where D == 0)
+ *   use_shampoo:  Ps  = beta1 Ps + (1 - beta1) P
+ *                 eta = eta0 ||Mg||_F / ||Ps||_F     (0 when ||Ps||_F == 0)
+ *                 W   = W - eta Ps
+ *   otherwise:    W   = W - eta0 Mg                  (before the first roots)
+ * With beta1 == 0, Mg and Ps are not stored (may be NULL) and P is used as Ps.
+ * norms (device, may be NULL): per block {||Mg||_F, ||Ps||_F, eta} as 3 floats.
+ * Errors: EINVAL as above, non-finite eta0, beta1 outside [0, 1), NULL
+ * W/D, P NULL with use_shampoo, Mg/Ps NULL with beta1 > 0.
+ */
+shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                             float eta0, float beta1, int use_shampoo, float* norms, void* stream);
+
+/*
+ * Measurement support.  While enabled, every launch of the timed kernel
+ * classes below is bracketed by HIP events on its stream.
+ * shampoo_timing_read synchronizes those events, returns the summed duration
+ * (ms) and launch count of one class, and clears that class.
+ */
+enum {
+  SHAMPOO_KCLASS_NEWTON_F32 = 0, /* grouped Newton products, fp32 MFMA */
+  SHAMPOO_KCLASS_NEWTON_F64 = 1, /* grouped Newton products, fp64 MFMA */
+  SHAMPOO_KCLASS_STATS = 2,      /* grouped statistics SYRK */
+  SHAMPOO_KCLASS_PRECOND = 3,    /* grouped preconditioning GEMMs */
+  SHAMPOO_KCLASS_GRAFT = 4,      /* graft reduction and update passes */
+  SHAMPOO_KCLASS_ROOT_AUX = 5,   /* root prologue/epilogue/state kernels */
+  SHAMPOO_KCLASS_COUNT = 6
+};
+shampoo_status shampoo_timing_enable(void* handle, int enable);
+shampoo_status shampoo_timing_read(void* handle, int kclass, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SHAMPOO_MI355X_H */

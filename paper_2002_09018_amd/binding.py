@@ -1,0 +1,226 @@
+"""ctypes binding of libshampoo.so (the C ABI in include/shampoo.h).
+
+Argument marshalling only: every step of the computation runs in the HIP
+kernels behind the C entry points.  Functions carry the C names.  Tensors are
+torch tensors on the handle's device (torch is used for device memory and
+streams); the binding passes their data pointers and the current stream.
+There is no CPU fallback: if the library cannot be loaded, importing this
+module raises.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+from dataclasses import dataclass
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.environ.get("SHAMPOO_LIB", os.path.join(HERE, "libshampoo.so"))
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"libshampoo.so not found at {LIB_PATH}: build it with "
+                      f"`python -c 'import __graft_entry__ as g; g.build()'`")
+_lib = C.CDLL(LIB_PATH)
+
+SHAMPOO_OK, SHAMPOO_EINVAL, SHAMPOO_EUNSUPPORTED, SHAMPOO_EHIP, SHAMPOO_ENOMEM = 0, -1, -2, -3, -4
+SHAMPOO_F32, SHAMPOO_BF16 = 0, 1
+ROOT_CONVERGED, ROOT_STAGNATED, ROOT_MAXITER, ROOT_DIVERGED, ROOT_NOT_PD = 0, 1, 2, 3, 4
+PRECISION_FP32, PRECISION_AUTO, PRECISION_FP64 = 0, 1, 2
+KCLASS_NEWTON_F32, KCLASS_NEWTON_F64, KCLASS_STATS, KCLASS_PRECOND, KCLASS_GRAFT, KCLASS_ROOT_AUX = range(6)
+KCLASS_NAMES = ["newton_f32", "newton_f64", "stats", "precond", "graft", "root_aux"]
+
+
+class shampoo_block(C.Structure):
+    _fields_ = [("rows", C.c_int32), ("cols", C.c_int32), ("ld", C.c_int64),
+                ("G", C.c_void_p), ("W", C.c_void_p), ("D", C.c_void_p), ("P", C.c_void_p),
+                ("Mg", C.c_void_p), ("Ps", C.c_void_p), ("L", C.c_void_p), ("R", C.c_void_p),
+                ("Lr", C.c_void_p), ("Rr", C.c_void_p)]
+
+
+class shampoo_root_job(C.Structure):
+    _fields_ = [("n", C.c_int32), ("reserved", C.c_int32), ("A", C.c_void_p), ("X", C.c_void_p)]
+
+
+class shampoo_root_params(C.Structure):
+    _fields_ = [("p", C.c_int32), ("eps", C.c_float), ("eps_relative", C.c_int32), ("tol", C.c_float),
+                ("max_iters", C.c_int32), ("precision", C.c_int32), ("kappa32", C.c_float),
+                ("maxsv_steps", C.c_int32), ("maxsv_tol", C.c_float), ("poll", C.c_int32)]
+
+
+class shampoo_root_info(C.Structure):
+    _fields_ = [("status", C.c_int32), ("iters", C.c_int32), ("precision", C.c_int32),
+                ("iters_fp32", C.c_int32), ("resid", C.c_float), ("lambda_max", C.c_float),
+                ("cond_est", C.c_float), ("eps_eff", C.c_float)]
+
+
+ROOT_INFO_FIELDS = [f for f, _ in shampoo_root_info._fields_]
+
+_vp, _i, _f, _sz = C.c_void_p, C.c_int, C.c_float, C.c_size_t
+_sig = {
+    "shampoo_create": (_i, [C.POINTER(_vp), _i]),
+    "shampoo_destroy": (_i, [_vp]),
+    "shampoo_last_error": (C.c_char_p, [_vp]),
+    "shampoo_version": (C.c_char_p, []),
+    "shampoo_root_params_default": (None, [C.POINTER(shampoo_root_params)]),
+    "shampoo_update_stats": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _vp]),
+    "shampoo_inv_root_workspace_bytes": (_sz, [C.POINTER(shampoo_root_job), _i, _i]),
+    "shampoo_inv_root_batched": (_i, [_vp, C.POINTER(shampoo_root_job), _i, C.POINTER(shampoo_root_params),
+                                      _vp, _sz, _vp, _vp]),
+    "shampoo_precondition": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _vp]),
+    "shampoo_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
+    "shampoo_timing_enable": (_i, [_vp, _i]),
+    "shampoo_timing_read": (_i, [_vp, _i, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
+}
+for _name, (_res, _args) in _sig.items():
+    _fn = getattr(_lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+EXPORTED = tuple(_sig)
+
+
+class ShampooError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"shampoo error {code}: {msg}")
+        self.code = code
+
+
+def _ptr(t):
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream):
+    if stream is not None:
+        return stream if isinstance(stream, int) else stream.cuda_stream
+    import torch
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _check(handle, code):
+    if code != SHAMPOO_OK:
+        msg = _lib.shampoo_last_error(handle)
+        raise ShampooError(code, msg.decode() if msg else "")
+
+
+@dataclass
+class Block:
+    """One block view.  Tensors must share the row stride of G (``ld``)."""
+    G: object
+    W: Optional[object] = None
+    D: Optional[object] = None
+    P: Optional[object] = None
+    Mg: Optional[object] = None
+    Ps: Optional[object] = None
+    L: Optional[object] = None
+    R: Optional[object] = None
+    Lr: Optional[object] = None
+    Rr: Optional[object] = None
+
+
+def _blocks(blocks: Sequence[Block]):
+    arr = (shampoo_block * max(1, len(blocks)))()
+    for i, b in enumerate(blocks):
+        g = b.G
+        arr[i].rows, arr[i].cols = int(g.shape[0]), int(g.shape[1])
+        arr[i].ld = int(g.stride(0))
+        for name in ("G", "W", "D", "P", "Mg", "Ps", "L", "R", "Lr", "Rr"):
+            setattr(arr[i], name, _ptr(getattr(b, name)))
+    return arr
+
+
+def _dtype_code(blocks):
+    if not blocks:
+        return SHAMPOO_F32
+    import torch
+    dt = blocks[0].G.dtype
+    return SHAMPOO_BF16 if dt == torch.bfloat16 else SHAMPOO_F32
+
+
+# ------------------------------------------------------------------ entry points
+def shampoo_version():
+    return _lib.shampoo_version().decode()
+
+
+def shampoo_root_params_default(**overrides):
+    p = shampoo_root_params()
+    _lib.shampoo_root_params_default(C.byref(p))
+    for k, v in overrides.items():
+        setattr(p, k, v)
+    return p
+
+
+def shampoo_create(device=0):
+    h = C.c_void_p()
+    code = _lib.shampoo_create(C.byref(h), int(device))
+    if code != SHAMPOO_OK:
+        raise ShampooError(code, f"shampoo_create(device={device}) failed")
+    return h
+
+
+def shampoo_destroy(handle):
+    _check(handle, _lib.shampoo_destroy(handle))
+
+
+def shampoo_update_stats(handle, blocks, beta2=1.0, stream=None):
+    arr = _blocks(blocks)
+    _check(handle, _lib.shampoo_update_stats(handle, arr, len(blocks), _dtype_code(blocks), float(beta2),
+                                             _stream(stream)))
+
+
+def _jobs(As, Xs):
+    arr = (shampoo_root_job * max(1, len(As)))()
+    for i, (a, x) in enumerate(zip(As, Xs)):
+        arr[i].n = int(a.shape[0])
+        arr[i].reserved = 0
+        arr[i].A = _ptr(a)
+        arr[i].X = _ptr(x)
+    return arr
+
+
+def shampoo_inv_root_workspace_bytes(ns, precision=PRECISION_AUTO):
+    arr = (shampoo_root_job * max(1, len(ns)))()
+    for i, n in enumerate(ns):
+        arr[i].n = int(n)
+    return int(_lib.shampoo_inv_root_workspace_bytes(arr, len(ns), int(precision)))
+
+
+def shampoo_inv_root_batched(handle, As, Xs, params, workspace, info, stream=None):
+    """As, Xs: lists of contiguous n x n fp32 device tensors; workspace: a
+    uint8 device tensor; info: an int32 device tensor of 8 * len(As)."""
+    arr = _jobs(As, Xs)
+    _check(handle, _lib.shampoo_inv_root_batched(handle, arr, len(As), C.byref(params), _ptr(workspace),
+                                                 int(workspace.numel() * workspace.element_size()),
+                                                 _ptr(info), _stream(stream)))
+
+
+def shampoo_precondition(handle, blocks, stream=None):
+    arr = _blocks(blocks)
+    _check(handle, _lib.shampoo_precondition(handle, arr, len(blocks), _dtype_code(blocks), _stream(stream)))
+
+
+def shampoo_graft(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
+    arr = _blocks(blocks)
+    _check(handle, _lib.shampoo_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0), float(beta1),
+                                      int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+
+
+def shampoo_timing_enable(handle, enable=True):
+    _check(handle, _lib.shampoo_timing_enable(handle, int(bool(enable))))
+
+
+def shampoo_timing_read(handle, kclass):
+    ms, n = C.c_double(), C.c_int64()
+    _check(handle, _lib.shampoo_timing_read(handle, int(kclass), C.byref(ms), C.byref(n)))
+    return ms.value, n.value
+
+
+def decode_root_info(info_tensor):
+    """Host view of a root-info device array: list of dicts."""
+    import numpy as np
+    raw = info_tensor.detach().cpu().numpy().astype(np.int32).reshape(-1, 8)
+    fl = raw.view(np.float32)
+    out = []
+    for r, f in zip(raw, fl):
+        out.append(dict(status=int(r[0]), iters=int(r[1]), precision=int(r[2]), iters_fp32=int(r[3]),
+                        resid=float(f[4]), lambda_max=float(f[5]), cond_est=float(f[6]), eps_eff=float(f[7])))
+    return out

@@ -1,0 +1,720 @@
+// Device kernels of the Shampoo hot path (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdint.h>
+
+#include "tile_mfma.hpp"
+
+namespace shp {
+
+// ============================================================================
+// Grouped GEMM for statistics and preconditioning.
+// One "problem" per output matrix; workgroups enumerate the 128 x 128 output
+// tiles of all problems (only the upper-triangular tiles of a symmetric
+// output, whose tiles are mirrored).
+//   C = alpha * opA(A) opB(B) + beta * C      (beta == 0: C is not read)
+// ============================================================================
+struct GemmProblem {
+  const void* A;
+  const void* B;
+  float* C;
+  int64_t lda, ldb, ldc;
+  int a_rows, a_cols;  // A as stored
+  int b_rows, b_cols;  // B as stored
+  int M, N, K;
+  float alpha, beta;
+  int sym;        // symmetric output: compute tiles ti <= tj, mirror into the lower part
+  int tiles_n;    // ceil(N / 128)
+  int tile_begin; // first logical tile of this problem
+  int a_aligned, b_aligned;
+};
+
+__device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int nprob, int t) {
+  int lo = 0, hi = nprob - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (probs[mid].tile_begin <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <typename SA, int LA, typename SB, int LB>
+__global__ __launch_bounds__(kThreads) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
+                                                               int nprob, int total_tiles) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  if (t >= total_tiles) return;
+  const GemmProblem P = probs[find_problem_gemm(probs, nprob, t)];
+  int ti, tj;
+  const int lt = t - P.tile_begin;
+  if (P.sym) unrank_upper(lt, P.tiles_n, ti, tj);
+  else { ti = lt / P.tiles_n; tj = lt % P.tiles_n; }
+  const int m0 = ti * kTile, n0 = tj * kTile;
+
+  Operand<SA> A{reinterpret_cast<const SA*>(P.A), P.lda, P.a_rows, P.a_cols, P.a_aligned != 0, 1.f, 0.f};
+  Operand<SB> B{reinterpret_cast<const SB*>(P.B), P.ldb, P.b_rows, P.b_cols, P.b_aligned != 0, 1.f, 0.f};
+  WaveAcc<float> acc;
+  acc.zero();
+  tile_mma<float, SA, LA, SB, LB>(acc, A, false, B, false, m0, n0, P.K, smem);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
+  const bool diag = P.sym && ti == tj;
+  typedef Mfma<float> F;
+#pragma unroll
+  for (int i = 0; i < WaveAcc<float>::NB; ++i)
+#pragma unroll
+    for (int j = 0; j < WaveAcc<float>::NB; ++j)
+#pragma unroll
+      for (int v = 0; v < F::kAcc; ++v) {
+        const int r = wm0 + i * F::kM + F::row(lane, v);
+        const int c = wn0 + j * F::kM + F::col(lane);
+        if (r >= P.M || c >= P.N) continue;
+        if (diag && r > c) continue;
+        float x = P.alpha * acc.c[i][j][v];
+        if (P.beta != 0.f) x += P.beta * P.C[(int64_t)r * P.ldc + c];
+        P.C[(int64_t)r * P.ldc + c] = x;
+        if (P.sym && r != c) P.C[(int64_t)c * P.ldc + r] = x;
+      }
+}
+
+// ============================================================================
+// Coupled Newton iteration (Algorithm 1), grouped over matrices.
+// ============================================================================
+enum : int { kActive = -1 };
+enum : int { kConverged = 0, kStagnated = 1, kMaxIter = 2, kDiverged = 3, kNotPD = 4 };
+
+constexpr float kStagGate = 1e-3f;  // stagnation is tested only below this residual
+constexpr float kDivergeAt = 1e6f;  // residual above this (or non-finite) diverged
+
+// Per-matrix iteration state (device).
+struct RootState {
+  int status;        // kActive or a final code
+  int iters;         // iterations of the current phase
+  int parity;        // buffer index holding the current X and M
+  int iters_fp32;    // iterations spent in the fp32 phase
+  unsigned resid_bits;  // running max |M - I| of the iteration in flight (float bits)
+  float resid;       // residual after the last iteration
+  int escalate;      // AUTO policy: redo in fp64
+  int precision;     // 32 or 64: phase that produced the result
+  double z;          // Frobenius scaling (1 + p) / (2 ||A_d||_F)
+  double eps_eff;    // damping added
+  double lam_max;    // MaxSV estimate (relative damping)
+  double diag_min;   // smallest diagonal entry of A_d
+};
+
+// Buffers of one matrix in one precision.
+template <typename T>
+struct NewtonJob {
+  T* X[2];
+  T* M[2];
+  T* S[2];
+  const float* A;   // input statistics (fp32, n x n)
+  float* Xout;      // caller's output
+  double* part;     // per-tile partial sums (tiles_n^2 x 2)
+  double* vec;      // MaxSV vectors (2 n)
+  int n;
+  int tiles_n;      // ceil(n / 128)
+  int up_begin;     // first logical upper-triangular tile
+  int full_begin;   // first logical full-grid tile
+};
+
+template <typename T>
+__device__ __forceinline__ int find_job_up(const NewtonJob<T>* jobs, int njobs, int t) {
+  int lo = 0, hi = njobs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (jobs[mid].up_begin <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <typename T>
+__device__ __forceinline__ int find_job_full(const NewtonJob<T>* jobs, int njobs, int t) {
+  int lo = 0, hi = njobs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (jobs[mid].full_begin <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Stage kinds of one Newton iteration (p = 2^e):
+//   kFirst  : X' = X M1  and  S[dst] = M1 M1         (two products per tile)
+//   kFirstP1: X' = X M1  and  M' = M1 M   (+residual) (p = 1)
+//   kSquare : S[dst] = S[src] S[src]
+//   kLast   : M' = S[src] M               (+residual)
+// with M1 = a I + b M formed while loading (a = (p+1)/p, b = -1/p), X, M the
+// buffers of the current parity and X', M' those of the other parity.
+enum : int { kFirst = 0, kFirstP1 = 1, kSquare = 2, kLast = 3 };
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
+                                                               int njobs, RootState* __restrict__ st,
+                                                               int total_up, int kind, int src, int dst,
+                                                               float a, float b) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int two = (kind == kFirst || kind == kFirstP1) ? 2 : 1;
+  const int l = xcd_remap(blockIdx.x, gridDim.x);
+  if (l >= two * total_up) return;
+  const int t = l / two, prod = l % two;
+  const int j = find_job_up(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T> J = jobs[j];
+  const int par = st[j].parity;
+  int ti, tj;
+  unrank_upper(t - J.up_begin, J.tiles_n, ti, tj);
+  const int n = J.n;
+  const int m0 = ti * kTile, n0 = tj * kTile;
+
+  const T* pa;
+  const T* pb;
+  T* pc;
+  bool affA = false, affB = false, resid = false;
+  if (kind == kFirst || kind == kFirstP1) {
+    if (prod == 0) {
+      pa = J.X[par]; pb = J.M[par]; pc = J.X[par ^ 1]; affB = true;
+    } else if (kind == kFirst) {
+      pa = J.M[par]; pb = J.M[par]; pc = J.S[dst]; affA = affB = true;
+    } else {
+      pa = J.M[par]; pb = J.M[par]; pc = J.M[par ^ 1]; affA = true; resid = true;
+    }
+  } else if (kind == kSquare) {
+    pa = J.S[src]; pb = J.S[src]; pc = J.S[dst];
+  } else {
+    pa = J.S[src]; pb = J.M[par]; pc = J.M[par ^ 1]; resid = true;
+  }
+  const bool al = (n % SrcVec<T>::n) == 0;
+  Operand<T> A{pa, n, n, n, al, a, 0.f};
+  Operand<T> B{pb, n, n, n, al, a, 0.f};
+  A.mul = affA ? b : 1.f; A.add = affA ? a : 0.f;
+  B.mul = affB ? b : 1.f; B.add = affB ? a : 0.f;
+
+  WaveAcc<T> acc;
+  acc.zero();
+  // All operands are symmetric, so both are read k-major (storage row = k).
+  tile_mma<T, T, kLayoutK, T, kLayoutK>(acc, A, affA, B, affB, m0, n0, n, smem);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
+  const bool diag = ti == tj;
+  typedef Mfma<T> F;
+  float rmax = 0.f;
+#pragma unroll
+  for (int i = 0; i < WaveAcc<T>::NB; ++i)
+#pragma unroll
+    for (int jj = 0; jj < WaveAcc<T>::NB; ++jj)
+#pragma unroll
+      for (int v = 0; v < F::kAcc; ++v) {
+        const int r = wm0 + i * F::kM + F::row(lane, v);
+        const int c = wn0 + jj * F::kM + F::col(lane);
+        if (r >= n || c >= n) continue;
+        if (diag && r > c) continue;
+        const T x = acc.c[i][jj][v];
+        pc[(int64_t)r * n + c] = x;
+        if (r != c) pc[(int64_t)c * n + r] = x;
+        if (resid) {
+          float d = (float)fabs((double)x - (r == c ? 1.0 : 0.0));
+          if (!(d <= 3.0e38f)) d = INFINITY;  // NaN or overflow
+          rmax = rmax > d ? rmax : d;
+        }
+      }
+  if (resid) {
+    rmax = wave_max(rmax);
+    if (lane == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Prologue.  MaxSV (Algorithm 1): power iteration on A_s = (A + A^T)/2 in
+// fp64 arithmetic, one workgroup per matrix, v0 = ones, Rayleigh quotient,
+// relative stop.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ double block_sum(double v, double* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) s += red[w];
+  return s;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void maxsv_kernel(const NewtonJob<T>* __restrict__ jobs,
+                                                        RootState* __restrict__ st, int n_step,
+                                                        double tol, double eps) {
+  __shared__ double red[kThreads / 64];
+  const NewtonJob<T> J = jobs[blockIdx.x];
+  const int n = J.n;
+  const float* A = J.A;
+  double* v = J.vec;       // current v
+  double* vh = J.vec + n;  // normalised v
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  for (int i = tid; i < n; i += kThreads) v[i] = 1.0;
+  __syncthreads();
+  double lam = 0.0;
+  for (int it = 0; it < n_step; ++it) {
+    double s = 0.0;
+    for (int i = tid; i < n; i += kThreads) s += v[i] * v[i];
+    const double nrm = sqrt(block_sum(s, red));
+    for (int i = tid; i < n; i += kThreads) vh[i] = nrm > 0.0 ? v[i] / nrm : 0.0;
+    __syncthreads();
+    // column form (A^T vh)_c, one thread per column, coalesced row reads
+    for (int c = tid; c < n; c += kThreads) {
+      double y = 0.0;
+      for (int r = 0; r < n; ++r) y += (double)A[(int64_t)r * n + c] * vh[r];
+      v[c] = 0.5 * y;
+    }
+    __syncthreads();
+    // row form (A vh)_r, one wave per row
+    for (int r = wave; r < n; r += kThreads / 64) {
+      double y = 0.0;
+      for (int c = lane; c < n; c += 64) y += (double)A[(int64_t)r * n + c] * vh[c];
+      y = wave_sum(y);
+      if (lane == 0) v[r] += 0.5 * y;
+    }
+    __syncthreads();
+    double q = 0.0;
+    for (int i = tid; i < n; i += kThreads) q += vh[i] * v[i];
+    const double lam_old = lam;
+    lam = block_sum(q, red);
+    if (fabs(lam - lam_old) <= tol * fabs(lam)) break;
+  }
+  if (tid == 0) {
+    st[blockIdx.x].lam_max = lam;
+    st[blockIdx.x].eps_eff = eps * lam;
+  }
+}
+
+// Symmetrised tile pass over the full tile grid: thread sees
+// s = (A[r][c] + A[c][r]) / 2 for its elements of tile (ti, tj); the
+// transposed block is staged through LDS so both reads are coalesced.
+// Computing every tile (not only the upper ones) keeps the result exactly
+// symmetric because fl(x + y) = fl(y + x).
+template <typename F>
+__device__ __forceinline__ void sym_tile_pass(const float* __restrict__ A, int n, int ti, int tj,
+                                              float* lds /* 128 x 33 */, F&& f) {
+  const int r0 = ti * kTile, c0 = tj * kTile;
+  const int tid = threadIdx.x;
+  for (int q = 0; q < kTile; q += 32) {  // 32-row slab of the tile
+    __syncthreads();
+    // lds[c][rr] = A[c0 + c][r0 + q + rr]
+    for (int e = tid; e < kTile * 32; e += kThreads) {
+      const int c = e >> 5, rr = e & 31;
+      const int gr = c0 + c, gc = r0 + q + rr;
+      lds[c * 33 + rr] = (gr < n && gc < n) ? A[(int64_t)gr * n + gc] : 0.f;
+    }
+    __syncthreads();
+    for (int e = tid; e < 32 * kTile; e += kThreads) {
+      const int rr = e >> 7, c = e & 127;
+      const int r = r0 + q + rr, cc = c0 + c;
+      if (r < n && cc < n) {
+        const double s = 0.5 * ((double)A[(int64_t)r * n + cc] + (double)lds[c * 33 + rr]);
+        f(r, cc, s);
+      }
+    }
+  }
+}
+
+// Per full tile: sum of s^2 over the tile, trace and minimum of its diagonal.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void frob_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                       const RootState* __restrict__ st, int total_full) {
+  __shared__ float lds[kTile * 33];
+  __shared__ double red[kThreads / 64];
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T> J = jobs[j];
+  const int lt = t - J.full_begin;
+  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
+  double ss = 0.0, tr = 0.0, dmin = INFINITY;
+  sym_tile_pass(J.A, J.n, ti, tj, lds, [&](int r, int c, double s) {
+    ss += s * s;
+    if (r == c) { tr += s; dmin = dmin < s ? dmin : s; }
+  });
+  ss = block_sum(ss, red);
+  tr = block_sum(tr, red);
+  // min over the block
+  double m = dmin;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) { const double w = __shfl_xor(m, o, 64); m = m < w ? m : w; }
+  __syncthreads();
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double mm = red[0];
+    for (int w = 1; w < kThreads / 64; ++w) mm = mm < red[w] ? mm : red[w];
+    J.part[3 * lt + 0] = ss;
+    J.part[3 * lt + 1] = tr;
+    J.part[3 * lt + 2] = mm;
+  }
+}
+
+// One thread per matrix: ||A_d||_F^2 = sum s^2 + 2 eps tr + n eps^2 from the
+// tile partials (fixed order), z, NOT_PD check.
+template <typename T>
+__global__ void root_prep_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, RootState* __restrict__ st,
+                                 int p, int eps_relative, double eps) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= njobs || st[j].status != kActive) return;
+  const NewtonJob<T> J = jobs[j];
+  const int nt = J.tiles_n * J.tiles_n;
+  double ss = 0.0, tr = 0.0, dmin = INFINITY;
+  for (int q = 0; q < nt; ++q) {
+    ss += J.part[3 * q + 0];
+    tr += J.part[3 * q + 1];
+    const double m = J.part[3 * q + 2];
+    dmin = dmin < m ? dmin : m;
+  }
+  const double e = eps_relative ? st[j].eps_eff : eps;
+  if (!eps_relative) st[j].eps_eff = eps;
+  const double fro2 = ss + 2.0 * e * tr + (double)J.n * e * e;
+  st[j].diag_min = dmin + e;
+  if (!(dmin + e > 0.0) || !(fro2 > 0.0) || !isfinite(fro2)) {
+    st[j].status = kNotPD;
+    st[j].z = 0.0;
+    return;
+  }
+  st[j].z = (1.0 + p) / (2.0 * sqrt(fro2));
+}
+
+// M0 = z (A_s + eps I), X0 = z^(1/p) I (Algorithm 1 cold start); residual of
+// M0 accumulated into resid_bits.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                            RootState* __restrict__ st, int total_full, int p) {
+  __shared__ float lds[kTile * 33];
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T> J = jobs[j];
+  const int lt = t - J.full_begin;
+  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
+  const double z = st[j].z, e = st[j].eps_eff;
+  const T x0 = (T)pow(z, 1.0 / p);
+  const int n = J.n;
+  T* M = J.M[0];
+  T* X = J.X[0];
+  float rmax = 0.f;
+  sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
+    const T m = (T)(z * (s + (r == c ? e : 0.0)));
+    M[(int64_t)r * n + c] = m;
+    X[(int64_t)r * n + c] = r == c ? x0 : (T)0;
+    float d = (float)fabs((double)m - (r == c ? 1.0 : 0.0));
+    if (!(d <= 3.0e38f)) d = INFINITY;
+    rmax = rmax > d ? rmax : d;
+  });
+  rmax = wave_max(rmax);
+  if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+}
+
+// Resets the state of the matrices that take part in a phase.
+//   phase 0: every matrix (fresh call), phase 1: fp64 tail of AUTO, only
+//   matrices flagged `escalate`.
+__global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int phase, int precision) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= njobs) return;
+  RootState& s = st[j];
+  if (phase == 0) {
+    s.status = kActive;
+    s.iters = 0;
+    s.iters_fp32 = 0;
+    s.escalate = 0;
+    s.lam_max = 0.0;
+    s.eps_eff = 0.0;
+    s.diag_min = 0.0;
+    s.z = 0.0;
+  } else if (!s.escalate) {
+    return;
+  } else {
+    s.status = kActive;
+    s.iters = 0;
+  }
+  s.parity = 0;
+  s.resid_bits = 0u;
+  s.resid = INFINITY;
+  s.precision = precision;
+}
+
+// Per-iteration state machine, one workgroup; also counts active matrices.
+//   init != 0: evaluates the residual of M0 only.
+__global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __restrict__ st, int njobs, int init,
+                                                              float tol, int max_iters, int* __restrict__ count) {
+  __shared__ int red[kThreads / 64];
+  int active = 0;
+  for (int j = threadIdx.x; j < njobs; j += kThreads) {
+    RootState& s = st[j];
+    if (s.status != kActive) continue;
+    const float r = __uint_as_float(s.resid_bits);
+    s.resid_bits = 0u;
+    if (init) {
+      s.resid = r;
+      if (!(r <= kDivergeAt)) s.status = kDiverged;
+      else if (r <= tol) s.status = kConverged;
+    } else {
+      s.parity ^= 1;
+      s.iters += 1;
+      const float prev = s.resid;
+      s.resid = r;
+      if (!(r <= kDivergeAt)) s.status = kDiverged;
+      else if (r <= tol) s.status = kConverged;
+      else if (prev < kStagGate && r >= prev) s.status = kStagnated;
+      else if (s.iters >= max_iters) s.status = kMaxIter;
+    }
+    if (s.status == kActive) ++active;
+  }
+  // block reduce
+  int a = active;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int w = 0; w < kThreads / 64; ++w) s += red[w];
+    *count = s;
+  }
+}
+
+// End of the fp32 phase under AUTO: flag matrices whose fp32 result is not
+// accepted; counts them.
+__global__ __launch_bounds__(kThreads) void root_escalate_kernel(RootState* __restrict__ st, int njobs,
+                                                                int* __restrict__ count) {
+  __shared__ int red[kThreads / 64];
+  int e = 0;
+  for (int j = threadIdx.x; j < njobs; j += kThreads) {
+    RootState& s = st[j];
+    s.iters_fp32 = s.iters;
+    const bool ok = s.status == kConverged || s.status == kStagnated || s.status == kNotPD;
+    s.escalate = ok ? 0 : 1;
+    e += s.escalate;
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) e += __shfl_xor(e, o, 64);
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = e;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int s = 0;
+    for (int w = 0; w < kThreads / 64; ++w) s += red[w];
+    *count = s;
+  }
+}
+
+// Copies the final iterate into the caller's fp32 X: for the fp32 phase only
+// when it sits in the workspace buffer (parity 1; X[0] is the caller's X), for
+// the fp64 phase always (with rounding).  Only matrices whose result came
+// from this phase (`want_escalated` selects the fp64 tail of AUTO).
+template <typename T>
+__global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                              const RootState* __restrict__ st, int total_full,
+                                                              int phase_is_tail) {
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  const RootState& s = st[j];
+  if (phase_is_tail && !s.escalate) return;
+  if (!phase_is_tail && s.escalate) return;
+  if (s.status == kNotPD) return;
+  const NewtonJob<T> J = jobs[j];
+  const T* src = J.X[s.parity];
+  if (sizeof(T) == 4 && s.parity == 0) return;  // already in place
+  const int lt = t - J.full_begin;
+  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
+  const int n = J.n;
+  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+    const int r = ti * kTile + (e >> 7), c = tj * kTile + (e & 127);
+    if (r < n && c < n) J.Xout[(int64_t)r * n + c] = (float)src[(int64_t)r * n + c];
+  }
+}
+
+// Largest m0 in (0, 1] the scalar recurrence m <- ((p+1-m)/p)^p m cannot
+// bring to |m - 1| <= tol within k iterations; (1 + p) / (2 m*) bounds the
+// damped condition number of a matrix that needed k iterations.
+__device__ inline int scalar_iters(double m, int p, double tol, int cap) {
+  int k = 0;
+  while (fabs(m - 1.0) > tol && k < cap) {
+    const double f = (p + 1.0 - m) / p;
+    double fp = 1.0;
+    for (int q = 0; q < p; ++q) fp *= f;
+    m = fp * m;
+    ++k;
+  }
+  return k;
+}
+
+template <typename T>
+__global__ void root_info_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, const RootState* __restrict__ st,
+                                 int p, float tol, void* __restrict__ info_out) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= njobs) return;
+  const RootState& s = st[j];
+  // condition estimate from the iteration count
+  double kappa = 0.0;
+  if (s.status == kConverged || s.status == kStagnated) {
+    const double tl = fmax((double)tol, (double)s.resid);
+    double lo = 1e-30, hi = 1.0;  // N(lo) > iters >= N(hi) (N decreasing on (0, 1])
+    if (scalar_iters(lo, p, tl, 400) <= s.iters) {
+      kappa = 1.0;
+    } else {
+      for (int b = 0; b < 100; ++b) {
+        const double mid = sqrt(lo * hi);
+        if (scalar_iters(mid, p, tl, 400) <= s.iters) hi = mid; else lo = mid;
+      }
+      kappa = (1.0 + p) / (2.0 * hi);
+    }
+  }
+  int32_t* io = reinterpret_cast<int32_t*>(info_out) + 8 * j;
+  float* fo = reinterpret_cast<float*>(io);
+  io[0] = s.status;
+  io[1] = s.iters;
+  io[2] = s.precision;
+  io[3] = s.precision == 32 ? s.iters : s.iters_fp32;
+  fo[4] = s.resid;
+  fo[5] = (float)s.lam_max;
+  fo[6] = (float)kappa;
+  fo[7] = (float)s.eps_eff;
+}
+
+// ============================================================================
+// Graft: pass 1 (D update, momentum, per-chunk sums of squares) and pass 2
+// (per-block step size, parameter update).  Work is split into chunks of
+// whole rows of one block.
+// ============================================================================
+struct GraftBlock {
+  const void* G;
+  float* W;
+  float* D;
+  const float* P;
+  float* Mg;
+  float* Ps;
+  int64_t ld;
+  int rows, cols;
+  int chunk_begin;
+  int nchunks;
+  int rows_per_chunk;
+  int vec4;  // cols, ld and pointers allow 4-wide vector access
+};
+
+__device__ __forceinline__ int find_block_graft(const GraftBlock* b, int nb, int t) {
+  int lo = 0, hi = nb - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (b[mid].chunk_begin <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <typename SG>
+__device__ __forceinline__ float load_g(const void* G, int64_t i) {
+  return cvt<float, SG>(reinterpret_cast<const SG*>(G)[i]);
+}
+
+// D^{-1/2} o G with 0 where D == 0.
+__device__ __forceinline__ float ada_dir(float g, float d) { return d > 0.f ? g / sqrtf(d) : 0.f; }
+
+template <typename SG>
+__global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock* __restrict__ blocks, int nb,
+                                                              int total_chunks, float beta1, int use_shampoo,
+                                                              double* __restrict__ partial) {
+  __shared__ double red[kThreads / 64];
+  const int t = blockIdx.x;
+  if (t >= total_chunks) return;
+  const GraftBlock B = blocks[find_block_graft(blocks, nb, t)];
+  const int ch = t - B.chunk_begin;
+  const int r0 = ch * B.rows_per_chunk;
+  const int r1 = min(B.rows, r0 + B.rows_per_chunk);
+  const bool mom = beta1 > 0.f;
+  float smg = 0.f, sps = 0.f;
+  const int64_t cnt = (int64_t)(r1 - r0) * B.cols;
+  for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+    const int r = r0 + (int)(e / B.cols), c = (int)(e % B.cols);
+    const int64_t i = (int64_t)r * B.ld + c;
+    const float g = load_g<SG>(B.G, i);
+    const float d = B.D[i] + g * g;
+    B.D[i] = d;
+    const float u = ada_dir(g, d);
+    float mg = u;
+    if (mom) { mg = beta1 * B.Mg[i] + (1.f - beta1) * u; B.Mg[i] = mg; }
+    smg += mg * mg;
+    if (use_shampoo) {
+      float ps = B.P[i];
+      if (mom) { ps = beta1 * B.Ps[i] + (1.f - beta1) * ps; B.Ps[i] = ps; }
+      sps += ps * ps;
+    }
+  }
+  const double a = block_sum((double)smg, red);
+  const double b = block_sum((double)sps, red);
+  if (threadIdx.x == 0) {
+    partial[2 * t + 0] = a;
+    partial[2 * t + 1] = b;
+  }
+}
+
+template <typename SG>
+__global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock* __restrict__ blocks, int nb,
+                                                              int total_chunks, float eta0, float beta1,
+                                                              int use_shampoo, const double* __restrict__ partial,
+                                                              float* __restrict__ norms) {
+  const int t = blockIdx.x;
+  if (t >= total_chunks) return;
+  const int bi = find_block_graft(blocks, nb, t);
+  const GraftBlock B = blocks[bi];
+  double smg = 0.0, sps = 0.0;
+  for (int q = 0; q < B.nchunks; ++q) {
+    smg += partial[2 * (B.chunk_begin + q) + 0];
+    sps += partial[2 * (B.chunk_begin + q) + 1];
+  }
+  const double nm = sqrt(smg), nps = sqrt(sps);
+  double eta;
+  if (use_shampoo) eta = nps > 0.0 ? (double)eta0 * nm / nps : 0.0;
+  else eta = eta0;
+  const float etaf = (float)eta;
+  const int ch = t - B.chunk_begin;
+  if (ch == 0 && threadIdx.x == 0 && norms) {
+    norms[3 * bi + 0] = (float)nm;
+    norms[3 * bi + 1] = (float)nps;
+    norms[3 * bi + 2] = etaf;
+  }
+  if (etaf == 0.f) return;
+  const int r0 = ch * B.rows_per_chunk;
+  const int r1 = min(B.rows, r0 + B.rows_per_chunk);
+  const bool mom = beta1 > 0.f;
+  const int64_t cnt = (int64_t)(r1 - r0) * B.cols;
+  for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+    const int r = r0 + (int)(e / B.cols), c = (int)(e % B.cols);
+    const int64_t i = (int64_t)r * B.ld + c;
+    float step;
+    if (use_shampoo) step = mom ? B.Ps[i] : B.P[i];
+    else step = mom ? B.Mg[i] : ada_dir(load_g<SG>(B.G, i), B.D[i]);
+    B.W[i] -= etaf * step;
+  }
+}
+
+// P = G (no root on either side), with up-cast.
+template <typename SG>
+__global__ __launch_bounds__(kThreads) void copy_g_kernel(const GraftBlock* __restrict__ blocks, int nb,
+                                                         int total_chunks) {
+  const int t = blockIdx.x;
+  if (t >= total_chunks) return;
+  const GraftBlock B = blocks[find_block_graft(blocks, nb, t)];
+  const int ch = t - B.chunk_begin;
+  const int r0 = ch * B.rows_per_chunk;
+  const int r1 = min(B.rows, r0 + B.rows_per_chunk);
+  const int64_t cnt = (int64_t)(r1 - r0) * B.cols;
+  float* P = const_cast<float*>(B.P);
+  for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
+    const int r = r0 + (int)(e / B.cols), c = (int)(e % B.cols);
+    const int64_t i = (int64_t)r * B.ld + c;
+    P[i] = load_g<SG>(B.G, i);
+  }
+}
+
+}  // namespace shp

@@ -1,0 +1,815 @@
+// Host side of libshampoo: C ABI, argument checking, table upload, launch
+// orchestration of the grouped kernels in kernels.hpp.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "kernels.hpp"
+#include "shampoo.h"
+
+using namespace shp;
+
+namespace {
+
+constexpr int kMaxDim = 4096;
+constexpr int kCountRing = 64;  // device/pinned slots of per-iteration active counts
+
+inline int cdiv(int a, int b) { return (a + b - 1) / b; }
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+uint64_t fnv1a(const void* p, size_t n) {
+  const unsigned char* c = static_cast<const unsigned char*>(p);
+  uint64_t h = 1469598103934665603ull;
+  for (size_t i = 0; i < n; ++i) h = (h ^ c[i]) * 1099511628211ull;
+  return h;
+}
+
+struct TableEntry {
+  uint64_t key = 0;
+  size_t bytes = 0, cap = 0;
+  void* dev = nullptr;
+  void* host = nullptr;
+  hipEvent_t ev = nullptr;
+  uint64_t last = 0;
+  bool used = false;
+};
+
+struct TimedLaunch {
+  int cls;
+  hipEvent_t a, b;
+};
+
+struct Handle {
+  int device = 0;
+  std::string err;
+  std::vector<TableEntry> cache;
+  std::vector<int> pending;  // cache entries referenced by the launches being enqueued
+  uint64_t clock = 0;
+  void* scratch = nullptr;
+  size_t scratch_cap = 0;
+  void* partial = nullptr;
+  size_t partial_cap = 0;
+  int32_t* pinned = nullptr;  // kCountRing + 1 ints
+  hipEvent_t poll_ev[2] = {nullptr, nullptr};
+  bool timing = false;
+  std::vector<TimedLaunch> timed;
+  std::vector<hipEvent_t> spare_events;
+};
+
+struct DeviceGuard {
+  int old = -1;
+  explicit DeviceGuard(int dev) {
+    if (hipGetDevice(&old) != hipSuccess) old = -1;
+    if (old != dev) (void)hipSetDevice(dev);
+  }
+  ~DeviceGuard() {
+    int cur = -1;
+    if (old >= 0 && hipGetDevice(&cur) == hipSuccess && cur != old) (void)hipSetDevice(old);
+  }
+};
+
+shampoo_status fail(Handle* h, shampoo_status code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  if (h) h->err = buf;
+  return code;
+}
+
+#define HIP_TRY(h, expr)                                                                   \
+  do {                                                                                     \
+    hipError_t e_ = (expr);                                                                \
+    if (e_ != hipSuccess) return fail((h), SHAMPOO_EHIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+#define STATUS_TRY(expr)               \
+  do {                                 \
+    shampoo_status s_ = (expr);        \
+    if (s_ != SHAMPOO_OK) return s_;   \
+  } while (0)
+
+// Device copy of a host table, cached by content.  An entry is reused only
+// after every launch that referenced it has completed (event per entry).
+shampoo_status upload_table(Handle* h, const void* data, size_t bytes, hipStream_t s, const void** out) {
+  const uint64_t key = fnv1a(data, bytes) ^ (bytes * 0x9E3779B97F4A7C15ull);
+  for (size_t i = 0; i < h->cache.size(); ++i) {
+    TableEntry& e = h->cache[i];
+    if (e.used && e.key == key && e.bytes == bytes && memcmp(e.host, data, bytes) == 0) {
+      e.last = ++h->clock;
+      h->pending.push_back((int)i);
+      *out = e.dev;
+      return SHAMPOO_OK;
+    }
+  }
+  int slot = -1;
+  if (h->cache.size() < 64) {
+    h->cache.emplace_back();
+    slot = (int)h->cache.size() - 1;
+    HIP_TRY(h, hipEventCreateWithFlags(&h->cache[slot].ev, hipEventDisableTiming));
+  } else {
+    uint64_t best = UINT64_MAX;
+    for (size_t i = 0; i < h->cache.size(); ++i)
+      if (h->cache[i].last < best) { best = h->cache[i].last; slot = (int)i; }
+    HIP_TRY(h, hipEventSynchronize(h->cache[slot].ev));
+  }
+  TableEntry& e = h->cache[slot];
+  if (e.cap < bytes) {
+    if (e.dev) HIP_TRY(h, hipFree(e.dev));
+    if (e.host) HIP_TRY(h, hipHostFree(e.host));
+    e.dev = e.host = nullptr;
+    const size_t cap = std::max<size_t>(align256(bytes), 4096);
+    HIP_TRY(h, hipMalloc(&e.dev, cap));
+    HIP_TRY(h, hipHostMalloc(&e.host, cap, hipHostMallocDefault));
+    e.cap = cap;
+  }
+  memcpy(e.host, data, bytes);
+  HIP_TRY(h, hipMemcpyAsync(e.dev, e.host, bytes, hipMemcpyHostToDevice, s));
+  e.key = key;
+  e.bytes = bytes;
+  e.used = true;
+  e.last = ++h->clock;
+  h->pending.push_back(slot);
+  *out = e.dev;
+  return SHAMPOO_OK;
+}
+
+// Marks every table referenced since the last call as in use up to here.
+shampoo_status tables_done(Handle* h, hipStream_t s) {
+  for (int i : h->pending) HIP_TRY(h, hipEventRecord(h->cache[i].ev, s));
+  h->pending.clear();
+  return SHAMPOO_OK;
+}
+
+shampoo_status grow(Handle* h, void** buf, size_t* cap, size_t bytes) {
+  if (*cap >= bytes) return SHAMPOO_OK;
+  // The old buffer may still be read by queued work of this handle.
+  HIP_TRY(h, hipDeviceSynchronize());
+  if (*buf) HIP_TRY(h, hipFree(*buf));
+  *buf = nullptr;
+  *cap = 0;
+  const size_t c = align256(bytes + bytes / 4);
+  HIP_TRY(h, hipMalloc(buf, c));
+  *cap = c;
+  return SHAMPOO_OK;
+}
+
+hipEvent_t take_event(Handle* h) {
+  if (!h->spare_events.empty()) {
+    hipEvent_t e = h->spare_events.back();
+    h->spare_events.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+template <typename F>
+shampoo_status launch(Handle* h, int cls, hipStream_t s, F&& f) {
+  hipEvent_t a = nullptr, b = nullptr;
+  if (h->timing) {
+    a = take_event(h);
+    b = take_event(h);
+    if (!a || !b) return fail(h, SHAMPOO_EHIP, "hipEventCreate failed");
+    HIP_TRY(h, hipEventRecord(a, s));
+  }
+  f();
+  HIP_TRY(h, hipGetLastError());
+  if (h->timing) {
+    HIP_TRY(h, hipEventRecord(b, s));
+    h->timed.push_back({cls, a, b});
+  }
+  return SHAMPOO_OK;
+}
+
+template <typename K>
+shampoo_status set_lds(Handle* h, K kernel, int bytes) {
+  HIP_TRY(h, hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                 hipFuncAttributeMaxDynamicSharedMemorySize, bytes));
+  return SHAMPOO_OK;
+}
+
+// ---------------------------------------------------------------- GEMM
+template <typename SA, int LA, typename SB, int LB>
+shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t s, int cls) {
+  if (probs.empty()) return SHAMPOO_OK;
+  int total = 0;
+  for (auto& p : probs) {
+    p.tiles_n = cdiv(p.N, kTile);
+    p.tile_begin = total;
+    total += p.sym ? p.tiles_n * (p.tiles_n + 1) / 2 : cdiv(p.M, kTile) * p.tiles_n;
+  }
+  const void* d = nullptr;
+  STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
+  auto k = gemm_grouped_kernel<SA, LA, SB, LB>;
+  const int lds = gemm_lds_bytes<float>();
+  STATUS_TRY(set_lds(h, k, lds));
+  const int np = (int)probs.size();
+  STATUS_TRY(launch(h, cls, s, [&] {
+    hipLaunchKernelGGL(k, dim3(total), dim3(kThreads), lds, s, (const GemmProblem*)d, np, total);
+  }));
+  return SHAMPOO_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+shampoo_status check_blocks(Handle* h, const shampoo_block* blocks, int nblocks, int g_dtype) {
+  if (nblocks < 0) return fail(h, SHAMPOO_EINVAL, "nblocks < 0");
+  if (nblocks > 0 && !blocks) return fail(h, SHAMPOO_EINVAL, "blocks is NULL");
+  if (g_dtype != SHAMPOO_F32 && g_dtype != SHAMPOO_BF16) return fail(h, SHAMPOO_EINVAL, "bad g_dtype %d", g_dtype);
+  for (int i = 0; i < nblocks; ++i) {
+    const shampoo_block& b = blocks[i];
+    if (b.rows < 1 || b.rows > kMaxDim || b.cols < 1 || b.cols > kMaxDim)
+      return fail(h, SHAMPOO_EINVAL, "block %d: size %d x %d outside [1, %d]", i, b.rows, b.cols, kMaxDim);
+    if (b.ld < b.cols) return fail(h, SHAMPOO_EINVAL, "block %d: ld %lld < cols %d", i, (long long)b.ld, b.cols);
+    if (!b.G) return fail(h, SHAMPOO_EINVAL, "block %d: G is NULL", i);
+  }
+  return SHAMPOO_OK;
+}
+
+template <typename SG>
+shampoo_status stats_impl(Handle* h, const shampoo_block* blocks, int nb, float beta2, hipStream_t s) {
+  const float c = beta2 == 1.0f ? 1.0f : 1.0f - beta2;
+  const int ve = 16 / (int)sizeof(SG);
+  std::vector<GemmProblem> left, right;
+  for (int i = 0; i < nb; ++i) {
+    const shampoo_block& b = blocks[i];
+    const bool al = aligned16(b.G) && (b.ld % ve) == 0;
+    if (b.L) {
+      GemmProblem p{};
+      p.A = b.G; p.B = b.G; p.C = b.L;
+      p.lda = p.ldb = b.ld; p.ldc = b.rows;
+      p.a_rows = p.b_rows = b.rows; p.a_cols = p.b_cols = b.cols;
+      p.M = p.N = b.rows; p.K = b.cols;
+      p.alpha = c; p.beta = beta2; p.sym = 1;
+      p.a_aligned = p.b_aligned = al;
+      left.push_back(p);
+    }
+    if (b.R) {
+      GemmProblem p{};
+      p.A = b.G; p.B = b.G; p.C = b.R;
+      p.lda = p.ldb = b.ld; p.ldc = b.cols;
+      p.a_rows = p.b_rows = b.rows; p.a_cols = p.b_cols = b.cols;
+      p.M = p.N = b.cols; p.K = b.rows;
+      p.alpha = c; p.beta = beta2; p.sym = 1;
+      p.a_aligned = p.b_aligned = al;
+      right.push_back(p);
+    }
+  }
+  // L = G G^T: both operands read with k (= column of G) contiguous.
+  STATUS_TRY((run_gemm<SG, kLayoutRow, SG, kLayoutRow>(h, left, s, SHAMPOO_KCLASS_STATS)));
+  // R = G^T G: both operands read row by row of G (k = row of G).
+  STATUS_TRY((run_gemm<SG, kLayoutK, SG, kLayoutK>(h, right, s, SHAMPOO_KCLASS_STATS)));
+  return tables_done(h, s);
+}
+
+// ---------------------------------------------------------------- elementwise block tables
+std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* total) {
+  std::vector<GraftBlock> v;
+  int t = 0;
+  for (int i = 0; i < nb; ++i) {
+    const shampoo_block& b = blocks[i];
+    GraftBlock g{};
+    g.G = b.G; g.W = b.W; g.D = b.D; g.P = b.P; g.Mg = b.Mg; g.Ps = b.Ps;
+    g.ld = b.ld; g.rows = b.rows; g.cols = b.cols;
+    g.rows_per_chunk = std::max(1, 16384 / b.cols);
+    g.nchunks = cdiv(b.rows, g.rows_per_chunk);
+    g.chunk_begin = t;
+    t += g.nchunks;
+    v.push_back(g);
+  }
+  *total = t;
+  return v;
+}
+
+template <typename SG>
+shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipStream_t s) {
+  const int ve = 16 / (int)sizeof(SG);
+  std::vector<GemmProblem> g_rr, lr_z, lr_g;
+  std::vector<shampoo_block> copy;
+  size_t zbytes = 0;
+  for (int i = 0; i < nb; ++i) {
+    const shampoo_block& b = blocks[i];
+    if (b.Lr && b.Rr) zbytes += align256((size_t)b.rows * b.cols * sizeof(float));
+  }
+  if (zbytes) STATUS_TRY(grow(h, &h->scratch, &h->scratch_cap, zbytes));
+  size_t zoff = 0;
+  for (int i = 0; i < nb; ++i) {
+    const shampoo_block& b = blocks[i];
+    const bool gal = aligned16(b.G) && (b.ld % ve) == 0;
+    if (b.Lr && b.Rr) {
+      float* Z = reinterpret_cast<float*>(static_cast<char*>(h->scratch) + zoff);
+      zoff += align256((size_t)b.rows * b.cols * sizeof(float));
+      GemmProblem p{};  // Z = G Rr
+      p.A = b.G; p.lda = b.ld; p.a_rows = b.rows; p.a_cols = b.cols; p.a_aligned = gal;
+      p.B = b.Rr; p.ldb = b.cols; p.b_rows = b.cols; p.b_cols = b.cols;
+      p.b_aligned = aligned16(b.Rr) && (b.cols % 4) == 0;
+      p.C = Z; p.ldc = b.cols; p.M = b.rows; p.N = b.cols; p.K = b.cols;
+      p.alpha = 1.f; p.beta = 0.f;
+      g_rr.push_back(p);
+      GemmProblem q{};  // P = Lr Z, Lr symmetric: read k-major
+      q.A = b.Lr; q.lda = b.rows; q.a_rows = b.rows; q.a_cols = b.rows;
+      q.a_aligned = aligned16(b.Lr) && (b.rows % 4) == 0;
+      q.B = Z; q.ldb = b.cols; q.b_rows = b.rows; q.b_cols = b.cols; q.b_aligned = (b.cols % 4) == 0;
+      q.C = b.P; q.ldc = b.ld; q.M = b.rows; q.N = b.cols; q.K = b.rows;
+      q.alpha = 1.f; q.beta = 0.f;
+      lr_z.push_back(q);
+    } else if (b.Rr) {
+      GemmProblem p{};  // P = G Rr
+      p.A = b.G; p.lda = b.ld; p.a_rows = b.rows; p.a_cols = b.cols; p.a_aligned = gal;
+      p.B = b.Rr; p.ldb = b.cols; p.b_rows = b.cols; p.b_cols = b.cols;
+      p.b_aligned = aligned16(b.Rr) && (b.cols % 4) == 0;
+      p.C = b.P; p.ldc = b.ld; p.M = b.rows; p.N = b.cols; p.K = b.cols;
+      p.alpha = 1.f; p.beta = 0.f;
+      g_rr.push_back(p);
+    } else if (b.Lr) {
+      GemmProblem q{};  // P = Lr G
+      q.A = b.Lr; q.lda = b.rows; q.a_rows = b.rows; q.a_cols = b.rows;
+      q.a_aligned = aligned16(b.Lr) && (b.rows % 4) == 0;
+      q.B = b.G; q.ldb = b.ld; q.b_rows = b.rows; q.b_cols = b.cols; q.b_aligned = gal;
+      q.C = b.P; q.ldc = b.ld; q.M = b.rows; q.N = b.cols; q.K = b.rows;
+      q.alpha = 1.f; q.beta = 0.f;
+      lr_g.push_back(q);
+    } else {
+      copy.push_back(b);
+    }
+  }
+  STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK>(h, g_rr, s, SHAMPOO_KCLASS_PRECOND)));
+  STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
+  STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK>(h, lr_g, s, SHAMPOO_KCLASS_PRECOND)));
+  if (!copy.empty()) {
+    int total = 0;
+    std::vector<GraftBlock> tb = graft_table(copy.data(), (int)copy.size(), &total);
+    const void* d = nullptr;
+    STATUS_TRY(upload_table(h, tb.data(), tb.size() * sizeof(GraftBlock), s, &d));
+    const int n = (int)tb.size();
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_PRECOND, s, [&] {
+      hipLaunchKernelGGL(copy_g_kernel<SG>, dim3(total), dim3(kThreads), 0, s, (const GraftBlock*)d, n, total);
+    }));
+  }
+  return tables_done(h, s);
+}
+
+template <typename SG>
+shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float eta0, float beta1, int use_shampoo,
+                          float* norms, hipStream_t s) {
+  int total = 0;
+  std::vector<GraftBlock> tb = graft_table(blocks, nb, &total);
+  const void* d = nullptr;
+  STATUS_TRY(upload_table(h, tb.data(), tb.size() * sizeof(GraftBlock), s, &d));
+  STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)total * 2 * sizeof(double)));
+  double* part = static_cast<double*>(h->partial);
+  const GraftBlock* db = static_cast<const GraftBlock*>(d);
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
+    hipLaunchKernelGGL(graft_pass1_kernel<SG>, dim3(total), dim3(kThreads), 0, s, db, nb, total, beta1,
+                       use_shampoo, part);
+  }));
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
+    hipLaunchKernelGGL(graft_pass2_kernel<SG>, dim3(total), dim3(kThreads), 0, s, db, nb, total, eta0, beta1,
+                       use_shampoo, (const double*)part, norms);
+  }));
+  return tables_done(h, s);
+}
+
+// ---------------------------------------------------------------- roots
+struct RootLayout {
+  size_t state = 0, counts = 0, total = 0;
+  std::vector<size_t> part, vec, f32, f64;  // per job offsets
+};
+
+RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
+  RootLayout L;
+  size_t off = 0;
+  L.state = off;
+  off += align256((size_t)njobs * sizeof(RootState));
+  L.counts = off;
+  off += align256((kCountRing + 2) * sizeof(int));
+  for (int j = 0; j < njobs; ++j) {
+    const size_t n = (size_t)jobs[j].n;
+    const size_t T = (size_t)cdiv(jobs[j].n, kTile);
+    L.part.push_back(off);
+    off += align256(3 * T * T * sizeof(double));
+    L.vec.push_back(off);
+    off += align256(2 * n * sizeof(double));
+    L.f32.push_back(off);
+    if (precision != SHAMPOO_PRECISION_FP64) off += 5 * align256(n * n * sizeof(float));
+    L.f64.push_back(off);
+    if (precision != SHAMPOO_PRECISION_FP32) off += 6 * align256(n * n * sizeof(double));
+  }
+  L.total = off;
+  return L;
+}
+
+int host_scalar_iters(double m, int p, double tol, int cap) {
+  int k = 0;
+  while (fabs(m - 1.0) > tol && k < cap) {
+    m = pow((p + 1.0 - m) / p, p) * m;
+    ++k;
+  }
+  return k;
+}
+
+// One precision phase of the coupled Newton iteration.
+template <typename T>
+shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
+                            int total_up, int total_full, int p, float tol, int cap, int poll, int cls,
+                            hipStream_t s) {
+  const int lds = gemm_lds_bytes<T>();
+  auto kstage = newton_stage_kernel<T>;
+  STATUS_TRY(set_lds(h, kstage, lds));
+  const float a = (float)(p + 1) / (float)p, b = -1.0f / (float)p;
+  int e = 0;
+  while ((1 << e) < p) ++e;
+  // initial residual of M0
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p);
+  }));
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
+                       dcount + kCountRing);
+  }));
+  for (int it = 0; it < cap; ++it) {
+    if (p == 1) {
+      STATUS_TRY(launch(h, cls, s, [&] {
+        hipLaunchKernelGGL(kstage, dim3(2 * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
+                           (int)kFirstP1, 0, 0, a, b);
+      }));
+    } else {
+      STATUS_TRY(launch(h, cls, s, [&] {
+        hipLaunchKernelGGL(kstage, dim3(2 * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
+                           (int)kFirst, 0, 0, a, b);
+      }));
+      for (int q = 1; q < e; ++q) {
+        const int src = (q - 1) & 1, dst = q & 1;
+        STATUS_TRY(launch(h, cls, s, [&] {
+          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
+                             (int)kSquare, src, dst, a, b);
+        }));
+      }
+      const int src = (e - 1) & 1;
+      STATUS_TRY(launch(h, cls, s, [&] {
+        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
+                           (int)kLast, src, 0, a, b);
+      }));
+    }
+    int* slot = dcount + (it % kCountRing);
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, cap, slot);
+    }));
+    if (poll) {
+      HIP_TRY(h, hipMemcpyAsync(h->pinned + (it % kCountRing), slot, sizeof(int), hipMemcpyDeviceToHost, s));
+      HIP_TRY(h, hipEventRecord(h->poll_ev[it & 1], s));
+      if (it >= 1) {
+        HIP_TRY(h, hipEventSynchronize(h->poll_ev[(it - 1) & 1]));
+        if (h->pinned[(it - 1) % kCountRing] == 0) break;
+      }
+    }
+  }
+  return SHAMPOO_OK;
+}
+
+template <typename T>
+std::vector<NewtonJob<T>> newton_table(const shampoo_root_job* jobs, int njobs, char* ws, const RootLayout& L,
+                                       int* total_up, int* total_full) {
+  std::vector<NewtonJob<T>> v(njobs);
+  int up = 0, full = 0;
+  for (int j = 0; j < njobs; ++j) {
+    const int n = jobs[j].n;
+    const size_t nn = align256((size_t)n * n * sizeof(T));
+    NewtonJob<T>& J = v[j];
+    J.A = jobs[j].A;
+    J.Xout = jobs[j].X;
+    J.part = reinterpret_cast<double*>(ws + L.part[j]);
+    J.vec = reinterpret_cast<double*>(ws + L.vec[j]);
+    char* base = ws + (sizeof(T) == 4 ? L.f32[j] : L.f64[j]);
+    if (sizeof(T) == 4) {
+      J.X[0] = reinterpret_cast<T*>(jobs[j].X);
+      J.X[1] = reinterpret_cast<T*>(base + 0 * nn);
+      J.M[0] = reinterpret_cast<T*>(base + 1 * nn);
+      J.M[1] = reinterpret_cast<T*>(base + 2 * nn);
+      J.S[0] = reinterpret_cast<T*>(base + 3 * nn);
+      J.S[1] = reinterpret_cast<T*>(base + 4 * nn);
+    } else {
+      J.X[0] = reinterpret_cast<T*>(base + 0 * nn);
+      J.X[1] = reinterpret_cast<T*>(base + 1 * nn);
+      J.M[0] = reinterpret_cast<T*>(base + 2 * nn);
+      J.M[1] = reinterpret_cast<T*>(base + 3 * nn);
+      J.S[0] = reinterpret_cast<T*>(base + 4 * nn);
+      J.S[1] = reinterpret_cast<T*>(base + 5 * nn);
+    }
+    J.n = n;
+    J.tiles_n = cdiv(n, kTile);
+    J.up_begin = up;
+    J.full_begin = full;
+    up += J.tiles_n * (J.tiles_n + 1) / 2;
+    full += J.tiles_n * J.tiles_n;
+  }
+  *total_up = up;
+  *total_full = full;
+  return v;
+}
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+extern "C" {
+
+const char* shampoo_version(void) { return "shampoo-mi355x 0.1 (gfx950)"; }
+
+void shampoo_root_params_default(shampoo_root_params* q) {
+  if (!q) return;
+  q->p = 4;
+  q->eps = 1e-6f;
+  q->eps_relative = 0;
+  q->tol = 1e-6f;
+  q->max_iters = 100;
+  q->precision = SHAMPOO_PRECISION_AUTO;
+  q->kappa32 = 1e4f;
+  q->maxsv_steps = 100;
+  q->maxsv_tol = 1e-6f;
+  q->poll = 1;
+}
+
+shampoo_status shampoo_create(void** handle, int device) {
+  if (!handle) return SHAMPOO_EINVAL;
+  *handle = nullptr;
+  int ndev = 0;
+  if (hipGetDeviceCount(&ndev) != hipSuccess || device < 0 || device >= ndev) return SHAMPOO_EINVAL;
+  Handle* h = new Handle();
+  h->device = device;
+  DeviceGuard g(device);
+  if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), (kCountRing + 2) * sizeof(int32_t),
+                    hipHostMallocDefault) != hipSuccess ||
+      hipEventCreateWithFlags(&h->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&h->poll_ev[1], hipEventDisableTiming) != hipSuccess) {
+    delete h;
+    return SHAMPOO_EHIP;
+  }
+  *handle = h;
+  return SHAMPOO_OK;
+}
+
+shampoo_status shampoo_destroy(void* handle) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  DeviceGuard g(h->device);
+  (void)hipDeviceSynchronize();
+  for (auto& e : h->cache) {
+    if (e.dev) (void)hipFree(e.dev);
+    if (e.host) (void)hipHostFree(e.host);
+    if (e.ev) (void)hipEventDestroy(e.ev);
+  }
+  for (auto& t : h->timed) {
+    (void)hipEventDestroy(t.a);
+    (void)hipEventDestroy(t.b);
+  }
+  for (auto e : h->spare_events) (void)hipEventDestroy(e);
+  if (h->scratch) (void)hipFree(h->scratch);
+  if (h->partial) (void)hipFree(h->partial);
+  if (h->pinned) (void)hipHostFree(h->pinned);
+  for (auto e : h->poll_ev)
+    if (e) (void)hipEventDestroy(e);
+  delete h;
+  return SHAMPOO_OK;
+}
+
+const char* shampoo_last_error(const void* handle) {
+  const Handle* h = static_cast<const Handle*>(handle);
+  return h ? h->err.c_str() : "invalid handle";
+}
+
+shampoo_status shampoo_update_stats(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                    float beta2, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
+  if (!(beta2 > 0.f && beta2 <= 1.f)) return fail(h, SHAMPOO_EINVAL, "beta2 %g outside (0, 1]", (double)beta2);
+  if (nblocks == 0) return SHAMPOO_OK;
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (g_dtype == SHAMPOO_F32) return stats_impl<float>(h, blocks, nblocks, beta2, s);
+  return stats_impl<uint16_t>(h, blocks, nblocks, beta2, s);
+}
+
+shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                    void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
+  for (int i = 0; i < nblocks; ++i)
+    if (!blocks[i].P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
+  if (nblocks == 0) return SHAMPOO_OK;
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (g_dtype == SHAMPOO_F32) return precond_impl<float>(h, blocks, nblocks, s);
+  return precond_impl<uint16_t>(h, blocks, nblocks, s);
+}
+
+shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
+                             float beta1, int use_shampoo, float* norms, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
+  if (!isfinite(eta0)) return fail(h, SHAMPOO_EINVAL, "eta0 is not finite");
+  if (!(beta1 >= 0.f && beta1 < 1.f)) return fail(h, SHAMPOO_EINVAL, "beta1 %g outside [0, 1)", (double)beta1);
+  for (int i = 0; i < nblocks; ++i) {
+    const shampoo_block& b = blocks[i];
+    if (!b.W || !b.D) return fail(h, SHAMPOO_EINVAL, "block %d: W or D is NULL", i);
+    if (use_shampoo && !b.P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
+    if (beta1 > 0.f && (!b.Mg || (use_shampoo && !b.Ps)))
+      return fail(h, SHAMPOO_EINVAL, "block %d: Mg/Ps needed when beta1 > 0", i);
+  }
+  if (nblocks == 0) return SHAMPOO_OK;
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (g_dtype == SHAMPOO_F32) return graft_impl<float>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+  return graft_impl<uint16_t>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+}
+
+size_t shampoo_inv_root_workspace_bytes(const shampoo_root_job* jobs, int njobs, int precision) {
+  if (njobs < 0 || (njobs > 0 && !jobs)) return 0;
+  if (precision < SHAMPOO_PRECISION_FP32 || precision > SHAMPOO_PRECISION_FP64) return 0;
+  for (int j = 0; j < njobs; ++j)
+    if (jobs[j].n < 1 || jobs[j].n > kMaxDim) return 0;
+  return root_layout(jobs, njobs, precision).total;
+}
+
+shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jobs, int njobs,
+                                        const shampoo_root_params* prm, void* workspace, size_t ws_bytes,
+                                        shampoo_root_info* info, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  if (!prm) return fail(h, SHAMPOO_EINVAL, "params is NULL");
+  if (njobs < 0) return fail(h, SHAMPOO_EINVAL, "njobs < 0");
+  if (njobs == 0) return SHAMPOO_OK;
+  if (!jobs || !info || !workspace) return fail(h, SHAMPOO_EINVAL, "jobs, info or workspace is NULL");
+  const int p = prm->p;
+  if (p != 1 && p != 2 && p != 4 && p != 8) return fail(h, SHAMPOO_EUNSUPPORTED, "p = %d not in {1, 2, 4, 8}", p);
+  if (!(prm->eps >= 0.f) || !isfinite(prm->eps)) return fail(h, SHAMPOO_EINVAL, "eps must be finite and >= 0");
+  if (!(prm->tol >= 0.f)) return fail(h, SHAMPOO_EINVAL, "tol must be >= 0");
+  if (prm->max_iters < 1) return fail(h, SHAMPOO_EINVAL, "max_iters must be >= 1");
+  if (prm->precision < 0 || prm->precision > 2) return fail(h, SHAMPOO_EINVAL, "bad precision %d", prm->precision);
+  if (prm->eps_relative && prm->maxsv_steps < 1) return fail(h, SHAMPOO_EINVAL, "maxsv_steps must be >= 1");
+  if (prm->precision == SHAMPOO_PRECISION_AUTO && !(prm->kappa32 >= 1.f))
+    return fail(h, SHAMPOO_EINVAL, "kappa32 must be >= 1");
+  for (int j = 0; j < njobs; ++j) {
+    if (jobs[j].n < 1 || jobs[j].n > kMaxDim)
+      return fail(h, SHAMPOO_EINVAL, "job %d: n = %d outside [1, %d]", j, jobs[j].n, kMaxDim);
+    if (!jobs[j].A || !jobs[j].X) return fail(h, SHAMPOO_EINVAL, "job %d: A or X is NULL", j);
+    if (jobs[j].A == jobs[j].X) return fail(h, SHAMPOO_EINVAL, "job %d: A and X alias", j);
+  }
+  const int prec = prm->precision;
+  const RootLayout L = root_layout(jobs, njobs, prec);
+  if (ws_bytes < L.total)
+    return fail(h, SHAMPOO_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  RootState* st = reinterpret_cast<RootState*>(ws + L.state);
+  int* dcount = reinterpret_cast<int*>(ws + L.counts);
+  int up = 0, full = 0;
+  const NewtonJob<float>* j32 = nullptr;
+  const NewtonJob<double>* j64 = nullptr;
+  if (prec != SHAMPOO_PRECISION_FP64) {
+    auto t = newton_table<float>(jobs, njobs, ws, L, &up, &full);
+    const void* d = nullptr;
+    STATUS_TRY(upload_table(h, t.data(), t.size() * sizeof(t[0]), s, &d));
+    j32 = static_cast<const NewtonJob<float>*>(d);
+  }
+  if (prec != SHAMPOO_PRECISION_FP32) {
+    auto t = newton_table<double>(jobs, njobs, ws, L, &up, &full);
+    const void* d = nullptr;
+    STATUS_TRY(upload_table(h, t.data(), t.size() * sizeof(t[0]), s, &d));
+    j64 = static_cast<const NewtonJob<double>*>(d);
+  }
+  const int nb1 = cdiv(njobs, 64);
+  const int tail_all = prec == SHAMPOO_PRECISION_FP64 ? 1 : 0;
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 0, tail_all ? 64 : 32);
+  }));
+  // Prologue, shared by both precisions: MaxSV, Frobenius partials, z.
+  const double eps = (double)prm->eps;
+  if (prm->eps_relative) {
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      if (j32)
+        hipLaunchKernelGGL(maxsv_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, st, prm->maxsv_steps,
+                           (double)prm->maxsv_tol, eps);
+      else
+        hipLaunchKernelGGL(maxsv_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, st, prm->maxsv_steps,
+                           (double)prm->maxsv_tol, eps);
+    }));
+  }
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    if (j32) {
+      hipLaunchKernelGGL(frob_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full);
+      hipLaunchKernelGGL(root_prep_kernel<float>, dim3(nb1), dim3(64), 0, s, j32, njobs, st, p, prm->eps_relative, eps);
+    } else {
+      hipLaunchKernelGGL(frob_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full);
+      hipLaunchKernelGGL(root_prep_kernel<double>, dim3(nb1), dim3(64), 0, s, j64, njobs, st, p, prm->eps_relative,
+                         eps);
+    }
+  }));
+  if (tail_all) {
+    // every matrix goes to the fp64 phase
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + kCountRing + 1);
+    }));
+  }
+  int run64 = tail_all;
+  if (j32) {
+    int cap = prm->max_iters;
+    if (prec == SHAMPOO_PRECISION_AUTO) {
+      const double m0 = std::min(1.0, (p + 1.0) / (2.0 * (double)prm->kappa32));
+      const int k32 = host_scalar_iters(m0, p, std::max((double)prm->tol, 1e-6), 1000) + 1;
+      cap = std::min(cap, std::max(k32, 1));
+    }
+    STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, p, prm->tol, cap, prm->poll,
+                                   SHAMPOO_KCLASS_NEWTON_F32, s));
+    if (prec == SHAMPOO_PRECISION_AUTO) {
+      STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+        hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + kCountRing + 1);
+      }));
+      if (prm->poll) {
+        HIP_TRY(h, hipMemcpyAsync(h->pinned + kCountRing + 1, dcount + kCountRing + 1, sizeof(int),
+                                  hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipStreamSynchronize(s));
+        run64 = h->pinned[kCountRing + 1] > 0;
+      } else {
+        run64 = 1;
+      }
+    }
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(root_output_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full, 0);
+    }));
+  }
+  if (run64) {
+    if (!tail_all) {
+      STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+        hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
+      }));
+    }
+    STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, p, prm->tol, prm->max_iters, prm->poll,
+                                    SHAMPOO_KCLASS_NEWTON_F64, s));
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1);
+    }));
+  }
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    if (j32)
+      hipLaunchKernelGGL(root_info_kernel<float>, dim3(nb1), dim3(64), 0, s, j32, njobs, st, p, prm->tol, (void*)info);
+    else
+      hipLaunchKernelGGL(root_info_kernel<double>, dim3(nb1), dim3(64), 0, s, j64, njobs, st, p, prm->tol, (void*)info);
+  }));
+  return tables_done(h, s);
+}
+
+shampoo_status shampoo_timing_enable(void* handle, int enable) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->timing = enable != 0;
+  return SHAMPOO_OK;
+}
+
+shampoo_status shampoo_timing_read(void* handle, int kclass, double* total_ms, int64_t* launches) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  if (kclass < 0 || kclass >= SHAMPOO_KCLASS_COUNT) return fail(h, SHAMPOO_EINVAL, "bad kernel class %d", kclass);
+  DeviceGuard g(h->device);
+  double ms = 0.0;
+  int64_t n = 0;
+  std::vector<TimedLaunch> keep;
+  for (auto& t : h->timed) {
+    if (t.cls != kclass) {
+      keep.push_back(t);
+      continue;
+    }
+    HIP_TRY(h, hipEventSynchronize(t.b));
+    float x = 0.f;
+    HIP_TRY(h, hipEventElapsedTime(&x, t.a, t.b));
+    ms += x;
+    ++n;
+    h->spare_events.push_back(t.a);
+    h->spare_events.push_back(t.b);
+  }
+  h->timed.swap(keep);
+  if (total_ms) *total_ms = ms;
+  if (launches) *launches = n;
+  return SHAMPOO_OK;
+}
+
+}  // extern "C"

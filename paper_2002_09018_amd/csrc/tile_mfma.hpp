@@ -1,0 +1,363 @@
+// MFMA tile machinery for gfx950 (CDNA4): one workgroup computes a 128 x 128
+// output tile C[m0:m0+128, n0:n0+128] = sum_k opA[m, k] * opB[k, n].
+//
+// Workgroup: 256 threads = 4 wave64s arranged 2 x 2, each owning a 64 x 64
+// sub-tile as a grid of MFMA blocks (fp32: 2 x 2 blocks of 32 x 32 with
+// v_mfma_f32_32x32x2_f32; fp64: 4 x 4 blocks of 16 x 16 with
+// v_mfma_f64_16x16x4_f64).  The k dimension is streamed through LDS in stages
+// of kBK (fp32: 32, fp64: 16), double-buffered: the global loads of stage s+1
+// are in flight in registers while the MFMAs of stage s run.
+//
+// LDS holds every operand stage k-major, lds[k][i] with i the output row (A)
+// or column (B) index, so the fragment read of a lane is a single
+// conflict-free 4/8-byte access.  Two global layouts feed it:
+//   kLayoutK   the stage is read from storage rows k0..k0+kBK, columns
+//              i0..i0+128 (the operand's contraction index is its storage row:
+//              B of C = A B, or A of C = A^T B, or any symmetric operand);
+//              16-byte vector loads and stores, no transpose.
+//   kLayoutRow the stage is read from storage rows i0..i0+128, columns
+//              k0..k0+kBK (contraction index contiguous: A of C = A B,
+//              B of C = A B^T); 16-byte loads, transposed scalar LDS stores
+//              with a one-element row pad so the stores do not conflict.
+// Source elements may be fp32, fp64 or bf16 (raw uint16 bits, up-cast
+// exactly); an optional affine map v -> mul * v + add * [row == col] is
+// applied while storing to LDS (used to form M1 = ((p+1) I - M) / p on the
+// fly).  Out-of-range elements are loaded as 0.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace shp {
+
+constexpr int kTile = 128;
+constexpr int kThreads = 256;
+constexpr int kWaveTile = 64;
+
+enum { kLayoutK = 0, kLayoutRow = 1 };
+
+template <typename T>
+struct Mfma;
+
+template <>
+struct Mfma<float> {
+  static constexpr int kBK = 32;  // k-depth of one LDS stage
+  static constexpr int kM = 32;   // MFMA block edge
+  static constexpr int kK = 2;    // k-depth of one MFMA
+  static constexpr int kAcc = 16; // accumulator elements per lane per block
+  typedef float acc_t __attribute__((ext_vector_type(16)));
+  static __device__ __forceinline__ acc_t mma(float a, float b, acc_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  // Position of accumulator element v of `lane` inside a 32 x 32 block.
+  static __device__ __forceinline__ int row(int lane, int v) {
+    return (v >> 2) * 8 + (lane >> 5) * 4 + (v & 3);
+  }
+  static __device__ __forceinline__ int col(int lane) { return lane & 31; }
+};
+
+template <>
+struct Mfma<double> {
+  static constexpr int kBK = 16;
+  static constexpr int kM = 16;
+  static constexpr int kK = 4;
+  static constexpr int kAcc = 4;
+  typedef double acc_t __attribute__((ext_vector_type(4)));
+  static __device__ __forceinline__ acc_t mma(double a, double b, acc_t c) {
+    return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
+  }
+  static __device__ __forceinline__ int row(int lane, int v) { return (lane >> 4) * 4 + v; }
+  static __device__ __forceinline__ int col(int lane) { return lane & 15; }
+};
+
+// Row pitch (elements) of one k-major LDS stage.  kLayoutK pads by 32 words so
+// the two half-waves of a fragment read (rows k and k+1) fall in different
+// bank halves; kLayoutRow pads by one element so transposed stores spread
+// over all banks.
+template <typename T, int LAYOUT>
+struct Pitch {
+  static constexpr int value =
+      LAYOUT == kLayoutK ? kTile + 128 / (int)sizeof(T) : kTile + 1;
+};
+
+template <typename T>
+struct StageBytes {
+  static constexpr int value = Mfma<T>::kBK * Pitch<T, kLayoutK>::value * (int)sizeof(T);
+};
+
+// Dynamic LDS of one GEMM workgroup: A and B, two stages each (sized for the
+// larger, k-layout pitch).
+template <typename T>
+constexpr int gemm_lds_bytes() { return 4 * StageBytes<T>::value; }
+
+template <typename S>
+struct SrcVec;
+template <>
+struct SrcVec<float> {
+  typedef float type __attribute__((ext_vector_type(4)));
+  static constexpr int n = 4;
+};
+template <>
+struct SrcVec<double> {
+  typedef double type __attribute__((ext_vector_type(2)));
+  static constexpr int n = 2;
+};
+template <>
+struct SrcVec<uint16_t> {
+  typedef uint16_t type __attribute__((ext_vector_type(8)));
+  static constexpr int n = 8;
+};
+
+template <typename T, typename S>
+__device__ __forceinline__ T cvt(S x) { return (T)x; }
+template <>
+__device__ __forceinline__ float cvt<float, uint16_t>(uint16_t x) {
+  return __uint_as_float(((uint32_t)x) << 16);
+}
+template <>
+__device__ __forceinline__ double cvt<double, uint16_t>(uint16_t x) {
+  return (double)__uint_as_float(((uint32_t)x) << 16);
+}
+
+// A matrix operand as stored: row-major, `rows` x `cols`, row stride `ld`.
+template <typename S>
+struct Operand {
+  const S* ptr;
+  int64_t ld;
+  int rows, cols;
+  bool aligned;  // ptr and ld allow 16-byte vector loads
+  // affine map applied on load (mul = 1, add = 0: none)
+  float mul, add;
+};
+
+// Per-thread staging registers for one operand stage.
+template <typename T, typename S, int LAYOUT>
+struct Loader {
+  typedef typename SrcVec<S>::type V;
+  static constexpr int VE = SrcVec<S>::n;
+  static constexpr int BK = Mfma<T>::kBK;
+  static constexpr int NVEC = BK * kTile / VE;
+  static constexpr int PER = NVEC / kThreads;
+  static constexpr int LDP = Pitch<T, LAYOUT>::value;
+  static_assert(NVEC % kThreads == 0, "stage must split evenly over the workgroup");
+  V buf[PER];
+
+  // Storage coordinates (relative to the stage origin) of vector slot i.
+  static __device__ __forceinline__ void slot(int tid, int i, int& sr, int& sc) {
+    const int v = tid + i * kThreads;
+    if (LAYOUT == kLayoutK) {
+      constexpr int VPR = kTile / VE;
+      sr = v / VPR;
+      sc = (v % VPR) * VE;
+    } else {
+      constexpr int VPR = BK / VE;
+      sr = v / VPR;
+      sc = (v % VPR) * VE;
+    }
+  }
+
+  // Global -> registers.  (r0, c0): storage origin of the stage.
+  __device__ __forceinline__ void load(const Operand<S>& op, int r0, int c0, int tid) {
+    constexpr int SR = LAYOUT == kLayoutK ? BK : kTile;
+    constexpr int SC = LAYOUT == kLayoutK ? kTile : BK;
+    const bool fast = op.aligned && (r0 + SR <= op.rows) && (c0 + SC <= op.cols);
+    if (fast) {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        int sr, sc;
+        slot(tid, i, sr, sc);
+        buf[i] = *reinterpret_cast<const V*>(op.ptr + (int64_t)(r0 + sr) * op.ld + (c0 + sc));
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) {
+        int sr, sc;
+        slot(tid, i, sr, sc);
+        const int gr = r0 + sr;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const int gc = c0 + sc + e;
+          buf[i][e] = (gr < op.rows && gc < op.cols) ? op.ptr[(int64_t)gr * op.ld + gc] : (S)0;
+        }
+      }
+    }
+  }
+
+  // Registers -> LDS stage (k-major), applying the affine map.
+  __device__ __forceinline__ void store(T* lds, const Operand<S>& op, int r0, int c0, int tid,
+                                        bool affine) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      int sr, sc;
+      slot(tid, i, sr, sc);
+      T v[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) v[e] = cvt<T, S>(buf[i][e]);
+      if (affine) {
+        const int gr = r0 + sr;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          const int gc = c0 + sc + e;
+          v[e] = (T)op.mul * v[e] + ((gr == gc && gr < op.rows) ? (T)op.add : (T)0);
+        }
+      }
+      if (LAYOUT == kLayoutK) {
+        T* dst = lds + sr * LDP + sc;
+        if (sizeof(T) == 4) {
+          typedef float f4 __attribute__((ext_vector_type(4)));
+#pragma unroll
+          for (int e = 0; e < VE; e += 4) {
+            f4 w = {(float)v[e], (float)v[e + 1], (float)v[e + 2], (float)v[e + 3]};
+            *reinterpret_cast<f4*>(reinterpret_cast<float*>(dst) + e) = w;
+          }
+        } else {
+          typedef double d2 __attribute__((ext_vector_type(2)));
+#pragma unroll
+          for (int e = 0; e < VE; e += 2) {
+            d2 w = {(double)v[e], (double)v[e + 1]};
+            *reinterpret_cast<d2*>(reinterpret_cast<double*>(dst) + e) = w;
+          }
+        }
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) lds[(sc + e) * LDP + sr] = v[e];
+      }
+    }
+  }
+};
+
+// Accumulators of one wave: an NB x NB grid of MFMA blocks covering 64 x 64.
+template <typename T>
+struct WaveAcc {
+  static constexpr int NB = kWaveTile / Mfma<T>::kM;
+  typename Mfma<T>::acc_t c[NB][NB];
+
+  __device__ __forceinline__ void zero() {
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int v = 0; v < Mfma<T>::kAcc; ++v) c[i][j][v] = (T)0;
+  }
+
+  // One LDS stage: kBK / kK MFMA k-steps over the wave's NB x NB blocks.
+  template <int LDPA, int LDPB>
+  __device__ __forceinline__ void stage(const T* __restrict__ a, const T* __restrict__ b, int wm0,
+                                        int wn0, int lane) {
+    constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;
+    const int kl = lane / Mfma<T>::kM;
+    const int ml = lane % Mfma<T>::kM;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+      T fa[NB], fb[NB];
+      const int k = s * Mfma<T>::kK + kl;
+#pragma unroll
+      for (int i = 0; i < NB; ++i) fa[i] = a[k * LDPA + wm0 + i * Mfma<T>::kM + ml];
+#pragma unroll
+      for (int j = 0; j < NB; ++j) fb[j] = b[k * LDPB + wn0 + j * Mfma<T>::kM + ml];
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) c[i][j] = Mfma<T>::mma(fa[i], fb[j], c[i][j]);
+    }
+  }
+};
+
+// Full k-loop of one 128 x 128 output tile.
+//   A: layout LA; kLayoutK reads storage rows k (cols m0..), kLayoutRow
+//      reads storage rows m0.. (cols k).
+//   B: layout LB; kLayoutK reads storage rows k (cols n0..), kLayoutRow
+//      reads storage rows n0.. (cols k).
+template <typename T, typename SA, int LA, typename SB, int LB>
+__device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, bool affA,
+                                         const Operand<SB>& B, bool affB, int m0, int n0, int K,
+                                         unsigned char* smem) {
+  typedef Loader<T, SA, LA> LdA;
+  typedef Loader<T, SB, LB> LdB;
+  constexpr int BK = Mfma<T>::kBK;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
+  const int wm0 = (wave >> 1) * kWaveTile;
+  const int wn0 = (wave & 1) * kWaveTile;
+
+  T* sA[2] = {reinterpret_cast<T*>(smem), reinterpret_cast<T*>(smem + StageBytes<T>::value)};
+  T* sB[2] = {reinterpret_cast<T*>(smem + 2 * StageBytes<T>::value),
+              reinterpret_cast<T*>(smem + 3 * StageBytes<T>::value)};
+
+  LdA la;
+  LdB lb;
+  const int nst = (K + BK - 1) / BK;
+  auto orgA = [&](int k0, int& r, int& c) {
+    if (LA == kLayoutK) { r = k0; c = m0; } else { r = m0; c = k0; }
+  };
+  auto orgB = [&](int k0, int& r, int& c) {
+    if (LB == kLayoutK) { r = k0; c = n0; } else { r = n0; c = k0; }
+  };
+  int ar, ac, br, bc;
+  orgA(0, ar, ac);
+  orgB(0, br, bc);
+  la.load(A, ar, ac, tid);
+  lb.load(B, br, bc, tid);
+  la.store(sA[0], A, ar, ac, tid, affA);
+  lb.store(sB[0], B, br, bc, tid, affB);
+  __syncthreads();
+  for (int st = 0; st < nst; ++st) {
+    const int cur = st & 1;
+    const bool more = st + 1 < nst;
+    if (more) {
+      orgA((st + 1) * BK, ar, ac);
+      orgB((st + 1) * BK, br, bc);
+      la.load(A, ar, ac, tid);
+      lb.load(B, br, bc, tid);
+    }
+    acc.template stage<LdA::LDP, LdB::LDP>(sA[cur], sB[cur], wm0, wn0, lane);
+    if (more) {
+      la.store(sA[cur ^ 1], A, ar, ac, tid, affA);
+      lb.store(sB[cur ^ 1], B, br, bc, tid, affB);
+    }
+    __syncthreads();
+  }
+}
+
+// Workgroup id -> logical tile index so that consecutive logical tiles land
+// on the same XCD (workgroups are dealt round-robin over the 8 XCDs, each
+// with its own L2): XCD x receives the contiguous logical range
+// [x*q + min(x, r), ...) where nwg = 8q + r.
+__device__ __forceinline__ int xcd_remap(int b, int nwg) {
+  const int q = nwg >> 3, r = nwg & 7;
+  const int x = b & 7, s = b >> 3;
+  return x * q + (x < r ? x : r) + s;
+}
+
+// Index t of the upper-triangular tile list of a T x T tile grid (row-major
+// over ti, tj >= ti) -> (ti, tj).
+__device__ __forceinline__ void unrank_upper(int t, int T, int& ti, int& tj) {
+  int i = 0;
+  while (t >= T - i) {
+    t -= T - i;
+    ++i;
+  }
+  ti = i;
+  tj = i + t;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_max(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    T w = __shfl_xor(v, o, 64);
+    v = v > w ? v : w;
+  }
+  return v;
+}
+
+template <typename T>
+__device__ __forceinline__ T wave_sum(T v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+}  // namespace shp

@@ -1,0 +1,200 @@
+"""GPU batched inverse p-th roots (shampoo_inv_root_batched) against the oracle.
+
+Bar (relative Frobenius error per matrix, against the eigendecomposition
+definition): <= 1e-3 when the damped condition number is <= 1e6, <= 5e-3 up
+to 1e8.  Iteration counts of fp32 runs are compared with the fp64
+transcript of Algorithm 1.  Status codes of degenerate inputs are checked,
+and neighbours of a failing matrix must be bit-identical to a clean run.
+"""
+import numpy as np
+import pytest
+
+import oracle.shampoo_oracle as O
+from synth import configs as cfg
+from tests.gpu_util import gpu_env, host, rel, say, spd, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def band(kappa):
+    return 1e-3 if kappa <= 1e6 else 5e-3
+
+
+@pytest.fixture(scope="module")
+def env():
+    torch, B, dev = gpu_env()
+    h = B.shampoo_create(0)
+    yield torch, B, dev, h
+    B.shampoo_destroy(h)
+
+
+def roots(env, As, **kw):
+    torch, B, dev, h = env
+    prm = B.shampoo_root_params_default(**kw)
+    dA = [to_dev(torch, a, dev) for a in As]
+    dX = [torch.full_like(a, float("nan")) for a in dA]
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([a.shape[0] for a in As], prm.precision),
+                     dtype=torch.uint8, device=dev)
+    info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_batched(h, dA, dX, prm, ws, info)
+    torch.cuda.synchronize()
+    return [host(x) for x in dX], B.decode_root_info(info)
+
+
+@pytest.mark.parametrize("p", [1, 2, 4, 8])
+def test_against_eigh_mixed_sizes(env, p):
+    say("roots mixed sizes p", p)
+    sizes = [1, 5, 127, 128, 129, 300, 513]
+    As = [spd(n, 100.0, 10 * n + p) for n in sizes]
+    Xs, info = roots(env, As, p=p, eps=1e-6)
+    for A, X, inf in zip(As, Xs, info):
+        Xo, st, _ = O.inv_root(A, p, 1e-6)
+        assert inf["status"] in (0, 1), inf
+        assert rel(X, Xo) <= 1e-3, (A.shape, inf, rel(X, Xo))
+        assert np.array_equal(X, X.T)
+
+
+def test_closed_forms(env):
+    say("roots closed forms")
+    d = np.array([0.5, 2.0, 7.0, 30.0, 1.0, 3.0], dtype=np.float32)
+    c = 3.7
+    As = [np.diag(d), (c * np.eye(40)).astype(np.float32)]
+    Xs, info = roots(env, As, p=4, eps=1e-4, precision=0)
+    Xd = Xs[0]
+    assert np.count_nonzero(Xd - np.diag(np.diag(Xd))) == 0  # off-diagonal zeros stay exact
+    assert rel(np.diag(Xd), (d.astype(np.float64) + 1e-4) ** -0.25) <= 1e-6
+    assert rel(Xs[1], (c + 1e-4) ** -0.25 * np.eye(40)) <= 1e-6
+    # p = 1 is the inverse
+    A = spd(64, 50.0, 3)
+    Xs, _ = roots(env, [A], p=1, eps=0.0)
+    assert rel(Xs[0], np.linalg.inv(A.astype(np.float64))) <= 1e-4
+
+
+def test_c2_full_size_grouped_sampled(env):
+    """C2: 96 Wishart statistics 1024 x 1024, p = 4, eps = 1e-6, one grouped
+    call; sampled matrices against eigh, iteration counts against the fp64
+    transcript."""
+    say("roots C2 96 x 1024^2")
+    As = [cfg.c2_stats(i) for i in range(96)]
+    Xs, info = roots(env, As, p=4, eps=1e-6)
+    assert all(i["status"] in (0, 1) and i["precision"] == 32 for i in info), info[:3]
+    for i in (0, 31, 64, 95):
+        Xo, _, _ = O.inv_root(As[i], 4, 1e-6)
+        assert rel(Xs[i], Xo) <= 1e-3, (i, rel(Xs[i], Xo))
+        tr = O.coupled_newton(As[i], 4, 1e-6, tol=1e-6)
+        assert abs(info[i]["iters"] - tr["iters"]) <= 1, (info[i], tr["iters"])
+    # the property X^4 A_d = I holds for every matrix (checked on the GPU result)
+    torch, B, dev, h = env
+    for i in range(0, 96, 12):
+        X = torch.tensor(Xs[i], device=dev, dtype=torch.float64)
+        Ad = torch.tensor(As[i], device=dev, dtype=torch.float64) + 1e-6 * torch.eye(1024, device=dev,
+                                                                                    dtype=torch.float64)
+        Rm = X @ X @ X @ X @ Ad - torch.eye(1024, device=dev, dtype=torch.float64)
+        assert float(torch.linalg.norm(Rm)) <= 4e-3
+
+
+@pytest.mark.parametrize("p", [2, 4])
+def test_c3_ill_conditioned_reduced(env, p):
+    """C3 recipe at n = 256 (spectrum log-uniform in [1e-6, 1e2], relative
+    damping 1e-6 and the 1e-8 variant); AUTO escalates to fp64."""
+    say("roots C3 n=256 p", p)
+    mats = [cfg.c3_matrix(i, n=256) for i in range(4)]
+    As = [m[0] for m in mats]
+    for eps in (1e-6, 1e-8):
+        Xs, info = roots(env, As, p=p, eps=eps, eps_relative=1)
+        for A, X, inf in zip(As, Xs, info):
+            lam = float(np.linalg.eigvalsh(0.5 * (A.astype(np.float64) + A.T)).max())
+            assert abs(inf["lambda_max"] - lam) <= 1e-4 * lam, (inf, lam)
+            Xo, st, e = O.inv_root(A, p, eps, eps_relative=True)
+            kappa = O.cond_damped(A, eps, True)
+            assert inf["status"] in (0, 1), inf
+            assert rel(X, Xo) <= band(kappa), (kappa, inf, rel(X, Xo))
+
+
+@pytest.mark.parametrize("p", [2, 4])
+def test_c3_full_size_two_matrices(env, p):
+    say("roots C3 n=2048 p", p)
+    mats = [cfg.c3_matrix(i, n=2048) for i in range(2)]
+    As = [m[0] for m in mats]
+    Xs, info = roots(env, As, p=p, eps=1e-6, eps_relative=1)
+    for A, X, inf in zip(As, Xs, info):
+        Xo, st, e = O.inv_root(A, p, 1e-6, eps_relative=True)
+        kappa = O.cond_damped(A, 1e-6, True)
+        assert inf["status"] in (0, 1) and inf["precision"] == 64, inf
+        assert rel(X, Xo) <= band(kappa), (kappa, inf, rel(X, Xo))
+
+
+def test_precision_policies_agree(env):
+    say("roots policies")
+    As = [spd(200, 1e3, 5), spd(256, 30.0, 6)]
+    X32, i32 = roots(env, As, p=4, eps=1e-6, precision=0)
+    X64, i64 = roots(env, As, p=4, eps=1e-6, precision=2)
+    for A, a, b, ia, ib in zip(As, X32, X64, i32, i64):
+        Xo, _, _ = O.inv_root(A, 4, 1e-6)
+        assert ia["precision"] == 32 and ib["precision"] == 64
+        assert rel(a, Xo) <= 1e-3 and rel(b, Xo) <= 1e-6
+
+
+def test_status_paths_and_isolation(env):
+    """MAXITER at a cap of 1, DIVERGED/NOT_PD on an indefinite matrix,
+    NOT_PD on a zero matrix without damping, DIVERGED on NaN; the healthy
+    neighbours are bit-identical to a clean grouped run."""
+    say("roots status paths")
+    good = [spd(96, 50.0, 11), spd(160, 10.0, 12)]
+    Xc, ic = roots(env, good, p=4, eps=1e-6, precision=0)
+    indef = np.diag(np.array([1.0, 2.0, -1.0, 3.0], dtype=np.float32))
+    nan = spd(64, 10.0, 13)
+    nan[3, 5] = nan[5, 3] = np.nan
+    zero = np.zeros((8, 8), np.float32)
+    Xs, info = roots(env, [good[0], indef, nan, zero, good[1]], p=4, eps=0.0, precision=0)
+    assert info[1]["status"] in (O.DIVERGED, O.NOT_PD)
+    assert info[2]["status"] in (O.DIVERGED, O.NOT_PD)
+    assert info[3]["status"] == O.NOT_PD
+    # eps = 0 vs 1e-6 changes the neighbours, so compare them to a clean
+    # eps = 0 run
+    Xc0, ic0 = roots(env, good, p=4, eps=0.0, precision=0)
+    assert np.array_equal(Xs[0], Xc0[0]) and np.array_equal(Xs[4], Xc0[1])
+    assert info[0]["iters"] == ic0[0]["iters"]
+    Xs, info = roots(env, [good[0]], p=4, eps=1e-6, precision=0, max_iters=1)
+    assert info[0]["status"] == O.MAXITER and info[0]["iters"] == 1
+    Xs, info = roots(env, [good[0]], p=4, eps=1e-6, precision=0, tol=0.0)
+    assert info[0]["status"] == O.STAGNATED
+    Xo, _, _ = O.inv_root(good[0], 4, 1e-6)
+    assert rel(Xs[0], Xo) <= 1e-3
+
+
+def test_grouped_equals_singleton_and_deterministic(env):
+    say("roots grouped == singleton")
+    As = [spd(n, 100.0, 20 + n) for n in (100, 256, 384)]
+    Xg, ig = roots(env, As, p=4, eps=1e-6)
+    Xg2, _ = roots(env, As, p=4, eps=1e-6)
+    for i, A in enumerate(As):
+        Xs, _ = roots(env, [A], p=4, eps=1e-6)
+        assert np.array_equal(Xs[0], Xg[i])
+        assert np.array_equal(Xg2[i], Xg[i])
+
+
+def test_async_mode_matches_polling(env):
+    say("roots poll=0")
+    As = [spd(192, 1e3, 31), cfg.c3_matrix(0, n=128)[0]]
+    Xa, ia = roots(env, As, p=4, eps=1e-6, eps_relative=1, poll=0, max_iters=60)
+    Xb, ib = roots(env, As, p=4, eps=1e-6, eps_relative=1, poll=1, max_iters=60)
+    for a, b, x, y in zip(Xa, Xb, ia, ib):
+        assert np.array_equal(a, b) and x == y
+
+
+def test_argument_errors(env):
+    torch, B, dev, h = env
+    say("roots errors")
+    A = torch.eye(4, device=dev)
+    X = torch.zeros(4, 4, device=dev)
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([4]), dtype=torch.uint8, device=dev)
+    info = torch.zeros(8, dtype=torch.int32, device=dev)
+    with pytest.raises(B.ShampooError) as e:
+        B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(p=3), ws, info)
+    assert e.value.code == B.SHAMPOO_EUNSUPPORTED
+    with pytest.raises(B.ShampooError) as e:
+        B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(), ws[:16], info)
+    assert e.value.code == B.SHAMPOO_ENOMEM
+    with pytest.raises(B.ShampooError):
+        B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(eps=-1.0), ws, info)
