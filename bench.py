@@ -1,0 +1,203 @@
+"""Throughput of the Shampoo hot path on one MI355X.
+
+Workload (C2): 96 blocks, each with statistics L (1024 x 1024) built from 19
+earlier gradients and a current gradient G (1024 x 4096) ~ N(0, 1/4096); a
+step is one pass of the whole hot path over the 96 blocks:
+    L += G G^T                       (grouped fp32-MFMA SYRK)
+    Lr = (L + 1e-6 I)^(-1/4)         (96 roots in one grouped coupled-Newton call)
+    P = Lr G                         (grouped fp32-MFMA GEMM; R side not tracked)
+    D += G o G, graft, W -= eta P    (two HBM passes)
+All inputs are resident in HBM before timing.  `value` is roots completed per
+second of whole-step time.  One JSON line is printed.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "1024² fp32 inverse-4th-roots/sec + stats+precondition step ms; fp32 MFMA util %"
+PEAK_F32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
+PEAK_F64_MFMA = 78.6
+PEAK_HBM = 8000.0       # GB/s
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def gen_block(i, n, k):
+    from synth import configs as cfg
+    L = cfg.wishart_bartlett(n, 19 * k, 1.0 / k, cfg.C2, i, 0).astype(np.float32)
+    G = cfg.c2_grad(i, n, k, 20)
+    D = cfg.c2_adagrad_state(i, n, k, 19)
+    W = cfg.c2_weight(i, n, k)
+    return L, G, D, W
+
+
+def cpu_baseline(sample, n, k, p, eps, eta0, budget_s=12.0):
+    """The oracle's step (fp64 stats, eigh root, precondition, graft) timed on
+    host cores over a bounded sample of the blocks."""
+    import oracle.shampoo_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([t.get("num_threads", 1) for t in threadpool_info()] + [1])
+    except Exception:
+        cores = os.cpu_count()
+    done, t0 = 0, time.perf_counter()
+    for (L, G, D, W) in sample:
+        Ln, _ = O.stats_update(L, None, G)
+        Lr, st, _ = O.inv_root(Ln, p, eps)
+        P = O.precondition(G, Lr, None)
+        O.graft_update(W, D, G, P, eta0)
+        done += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    dt = time.perf_counter() - t0
+    return dict(value=done / dt, unit="roots/s", cores=int(cores), kind="oracle",
+                sample=f"{done} of the 96 blocks, full fp64 step per block (stats L+GG^T, eigh root, "
+                       f"Lr G, graft), {dt:.1f} s")
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--blocks", type=int, default=96)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this implementation runs on one GPU; multi-GPU sharding of the blocks "
+                                   "is described in DESIGN.md and not built", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    from paper_2002_09018_amd import binding as B
+
+    dev = torch.device("cuda:0")
+    nb, n, k, p, eps, eta0 = args.blocks, 1024, 4096, 4, 1e-6, 1e-2
+    log(f"generating {nb} blocks")
+    t0 = time.time()
+    Ls, Gs, Ds, Ws = [], [], [], []
+    sample = []
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as ex:
+        for i, (L, G, D, W) in enumerate(ex.map(lambda i: gen_block(i, n, k), range(nb))):
+            Ls.append(torch.from_numpy(L).to(dev))
+            Gs.append(torch.from_numpy(G).to(dev))
+            Ds.append(torch.from_numpy(D).to(dev))
+            Ws.append(torch.from_numpy(W).to(dev))
+            if i < 24 and not args.no_cpu_baseline:
+                sample.append((L, G, D, W))
+            if (i + 1) % 24 == 0:
+                log(f"  {i + 1}/{nb} blocks resident ({time.time() - t0:.1f} s)")
+    Lrs = [torch.zeros(n, n, device=dev) for _ in range(nb)]
+    Ps = [torch.zeros(n, k, device=dev) for _ in range(nb)]
+    blocks = [B.Block(G=Gs[i], W=Ws[i], D=Ds[i], P=Ps[i], L=Ls[i], Lr=Lrs[i]) for i in range(nb)]
+    h = B.shampoo_create(0)
+    prm = B.shampoo_root_params_default(p=p, eps=eps)
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([n] * nb, prm.precision), dtype=torch.uint8, device=dev)
+    info = torch.zeros(8 * nb, dtype=torch.int32, device=dev)
+    infos = []
+
+    def step(record):
+        B.shampoo_update_stats(h, blocks)
+        B.shampoo_inv_root_batched(h, Ls, Lrs, prm, ws, info)
+        if record:
+            infos.append(info.clone())
+        B.shampoo_precondition(h, blocks)
+        B.shampoo_graft(h, blocks, eta0)
+
+    for w in range(args.warmup):
+        step(False)
+        torch.cuda.synchronize()
+        log(f"warmup step {w + 1}/{args.warmup} done")
+    B.shampoo_timing_enable(h, True)
+    for c in range(6):
+        B.shampoo_timing_read(h, c)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for s in range(args.steps):
+        step(True)
+        log(f"timed step {s + 1}/{args.steps} enqueued")
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    B.shampoo_timing_enable(h, False)
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
+
+    # algorithmic work
+    it32, it64, nf32, nf64 = 0, 0, 0, 0
+    prods = 4  # p = 4: X M1, M1 M1, (M1^2)^2, M1^4 M
+    for t in infos:
+        for inf in B.decode_root_info(t):
+            it32 += inf["iters_fp32"]
+            nf32 += inf["iters_fp32"]
+            if inf["precision"] == 64:
+                it64 += inf["iters"]
+    sym_prod = n * n * (n + 1)                     # symmetric product, upper-triangle counting
+    flops_newton32 = it32 * prods * sym_prod
+    flops_newton64 = it64 * prods * sym_prod
+    flops_stats = args.steps * nb * n * (n + 1) * k
+    flops_prec = args.steps * nb * 2 * n * n * k
+    graft_bytes = args.steps * nb * n * k * 28   # pass 1: G, D, D', P; pass 2: W, P, W'
+    ms_newton, launches_newton = times["newton_f32"]
+    achieved = flops_newton32 / (ms_newton * 1e-3) / 1e12 if ms_newton > 0 else 0.0
+    ms_step = elapsed * 1e3 / args.steps
+    stats_prec_ms = (times["stats"][0] + times["precond"][0]) / args.steps
+    out = {
+        "metric": METRIC,
+        "value": nb * args.steps / elapsed,
+        "unit": "roots/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "C2 step: 96 blocks, L 1024x1024 (Wishart, 19x4096 dof) + G 1024x4096 "
+                               "N(0,1/4096); stats + 96 inverse 4th roots (grouped coupled Newton, eps 1e-6, "
+                               "tol 1e-6, AUTO precision) + L^-1/4 G + AdaGrad graft",
+                   "blocks": nb, "n": n, "k": k, "p": p, "eps": eps},
+        "roofline": {
+            "kernel": "newton_stage_kernel<float> (grouped fp32-MFMA Newton products)",
+            "bound": "mfma", "achieved": achieved, "peak": PEAK_F32_MFMA, "unit": "TFLOP/s",
+            "frac": achieved / PEAK_F32_MFMA,
+            "flops_per_launch": flops_newton32 / max(launches_newton, 1),
+            "avg_launch_us": ms_newton * 1e3 / max(launches_newton, 1),
+            "traffic": None,
+        },
+        "stats_precondition_ms_per_step": stats_prec_ms,
+        "fp32_mfma_util": achieved / PEAK_F32_MFMA,
+        "phases_ms_per_step": {c: v[0] / args.steps for c, v in times.items()},
+        "launches_per_step": {c: v[1] / args.steps for c, v in times.items()},
+        "kernels": {
+            "stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12 if times["stats"][0] else None,
+            "precond_tflops": flops_prec / (times["precond"][0] * 1e-3) / 1e12 if times["precond"][0] else None,
+            "graft_gbs": graft_bytes / (times["graft"][0] * 1e-3) / 1e9 if times["graft"][0] else None,
+            "newton_f64_tflops": (flops_newton64 / (times["newton_f64"][0] * 1e-3) / 1e12
+                                  if times["newton_f64"][0] else None),
+        },
+        "newton_iters_mean": it32 / max(1, nb * args.steps),
+        "roots_per_s_root_phase": nb * args.steps / ((times["newton_f32"][0] + times["newton_f64"][0]
+                                                      + times["root_aux"][0]) * 1e-3),
+    }
+    if not args.no_cpu_baseline:
+        log("timing the oracle on a sample")
+        out["cpu_baseline"] = cpu_baseline(sample, n, k, p, eps, eta0)
+    B.shampoo_destroy(h)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

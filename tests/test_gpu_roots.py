@@ -103,8 +103,13 @@ def test_c3_ill_conditioned_reduced(env, p):
     for eps in (1e-6, 1e-8):
         Xs, info = roots(env, As, p=p, eps=eps, eps_relative=1)
         for A, X, inf in zip(As, Xs, info):
-            lam = float(np.linalg.eigvalsh(0.5 * (A.astype(np.float64) + A.T)).max())
-            assert abs(inf["lambda_max"] - lam) <= 1e-4 * lam, (inf, lam)
+            As64 = 0.5 * (A.astype(np.float64) + A.T)
+            lam = float(np.linalg.eigvalsh(As64).max())
+            lam_ps, _ = O.max_sv(As64)  # same power iteration and stop rule
+            # the GPU MaxSV follows the oracle's; both are Rayleigh quotients,
+            # so below the top eigenvalue and close to it
+            assert abs(inf["lambda_max"] - lam_ps) <= 1e-5 * lam_ps, (inf, lam_ps)
+            assert 0.95 * lam <= inf["lambda_max"] <= lam * (1 + 1e-6), (inf, lam)
             Xo, st, e = O.inv_root(A, p, eps, eps_relative=True)
             kappa = O.cond_damped(A, eps, True)
             assert inf["status"] in (0, 1), inf
