@@ -53,18 +53,17 @@ def cpu_baseline(sample, n, k, p, eps, eta0, budget_s=12.0):
     except Exception:
         cores = os.cpu_count()
     done, t0 = 0, time.perf_counter()
-    for (L, G, D, W) in sample:
+    while time.perf_counter() - t0 < budget_s:
+        L, G, D, W = sample[done % len(sample)]
         Ln, _ = O.stats_update(L, None, G)
         Lr, st, _ = O.inv_root(Ln, p, eps)
         P = O.precondition(G, Lr, None)
         O.graft_update(W, D, G, P, eta0)
         done += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
     dt = time.perf_counter() - t0
     return dict(value=done / dt, unit="roots/s", cores=int(cores), kind="oracle",
-                sample=f"{done} of the 96 blocks, full fp64 step per block (stats L+GG^T, eigh root, "
-                       f"Lr G, graft), {dt:.1f} s")
+                sample=f"{done} block-steps cycling over {len(sample)} of the 96 blocks, full fp64 step "
+                       f"per block (stats L+GG^T, eigh root, Lr G, graft), {dt:.1f} s")
 
 
 def main():
@@ -74,6 +73,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--blocks", type=int, default=96)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mb", type=int, default=0,
+                    help="before the steps, copy a buffer of this size once (a plain copy kernel of known "
+                         "traffic, to scale FETCH_SIZE/WRITE_SIZE counter readings)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(json.dumps({"error": "this implementation runs on one GPU; multi-GPU sharding of the blocks "
@@ -99,6 +101,14 @@ def main():
                 sample.append((L, G, D, W))
             if (i + 1) % 24 == 0:
                 log(f"  {i + 1}/{nb} blocks resident ({time.time() - t0:.1f} s)")
+    if args.calib_copy_mb:
+        src = torch.ones(args.calib_copy_mb * 2 ** 18, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"calibration copy of {args.calib_copy_mb} MiB done")
+        del src, dst
     Lrs = [torch.zeros(n, n, device=dev) for _ in range(nb)]
     Ps = [torch.zeros(n, k, device=dev) for _ in range(nb)]
     blocks = [B.Block(G=Gs[i], W=Ws[i], D=Ds[i], P=Ps[i], L=Ls[i], Lr=Lrs[i]) for i in range(nb)]

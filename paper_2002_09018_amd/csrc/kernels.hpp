@@ -74,9 +74,9 @@ __global__ __launch_bounds__(kThreads) void gemm_grouped_kernel(const GemmProble
         if (r >= P.M || c >= P.N) continue;
         if (diag && r > c) continue;
         float x = P.alpha * acc.c[i][j][v];
-        if (P.beta != 0.f) x += P.beta * P.C[(int64_t)r * P.ldc + c];
-        P.C[(int64_t)r * P.ldc + c] = x;
-        if (P.sym && r != c) P.C[(int64_t)c * P.ldc + r] = x;
+        if (P.beta != 0.f) x += P.beta * gload<float>(P.C + (int64_t)r * P.ldc + c);
+        gstore<float>(P.C + (int64_t)r * P.ldc + c, x);
+        if (P.sym && r != c) gstore<float>(P.C + (int64_t)c * P.ldc + r, x);
       }
 }
 
@@ -162,11 +162,13 @@ __global__ __launch_bounds__(kThreads) void newton_stage_kernel(const NewtonJob<
   const int t = l / two, prod = l % two;
   const int j = find_job_up(jobs, njobs, t);
   if (st[j].status != kActive) return;
-  const NewtonJob<T> J = jobs[j];
+  // Buffer pointers are read from the table with run-time indices (not from a
+  // local copy of the struct, which would be placed in scratch).
+  const NewtonJob<T>* J = jobs + j;
   const int par = st[j].parity;
   int ti, tj;
-  unrank_upper(t - J.up_begin, J.tiles_n, ti, tj);
-  const int n = J.n;
+  unrank_upper(t - J->up_begin, J->tiles_n, ti, tj);
+  const int n = J->n;
   const int m0 = ti * kTile, n0 = tj * kTile;
 
   const T* pa;
@@ -175,16 +177,16 @@ __global__ __launch_bounds__(kThreads) void newton_stage_kernel(const NewtonJob<
   bool affA = false, affB = false, resid = false;
   if (kind == kFirst || kind == kFirstP1) {
     if (prod == 0) {
-      pa = J.X[par]; pb = J.M[par]; pc = J.X[par ^ 1]; affB = true;
+      pa = J->X[par]; pb = J->M[par]; pc = J->X[par ^ 1]; affB = true;
     } else if (kind == kFirst) {
-      pa = J.M[par]; pb = J.M[par]; pc = J.S[dst]; affA = affB = true;
+      pa = J->M[par]; pb = J->M[par]; pc = J->S[dst]; affA = affB = true;
     } else {
-      pa = J.M[par]; pb = J.M[par]; pc = J.M[par ^ 1]; affA = true; resid = true;
+      pa = J->M[par]; pb = J->M[par]; pc = J->M[par ^ 1]; affA = true; resid = true;
     }
   } else if (kind == kSquare) {
-    pa = J.S[src]; pb = J.S[src]; pc = J.S[dst];
+    pa = J->S[src]; pb = J->S[src]; pc = J->S[dst];
   } else {
-    pa = J.S[src]; pb = J.M[par]; pc = J.M[par ^ 1]; resid = true;
+    pa = J->S[src]; pb = J->M[par]; pc = J->M[par ^ 1]; resid = true;
   }
   const bool al = (n % SrcVec<T>::n) == 0;
   Operand<T> A{pa, n, n, n, al, a, 0.f};
@@ -213,8 +215,8 @@ __global__ __launch_bounds__(kThreads) void newton_stage_kernel(const NewtonJob<
         if (r >= n || c >= n) continue;
         if (diag && r > c) continue;
         const T x = acc.c[i][jj][v];
-        pc[(int64_t)r * n + c] = x;
-        if (r != c) pc[(int64_t)c * n + r] = x;
+        gstore<T>(pc + (int64_t)r * n + c, x);
+        if (r != c) gstore<T>(pc + (int64_t)c * n + r, x);
         if (resid) {
           float d = (float)fabs((double)x - (r == c ? 1.0 : 0.0));
           if (!(d <= 3.0e38f)) d = INFINITY;  // NaN or overflow
@@ -523,15 +525,16 @@ __global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T
   if (phase_is_tail && !s.escalate) return;
   if (!phase_is_tail && s.escalate) return;
   if (s.status == kNotPD) return;
-  const NewtonJob<T> J = jobs[j];
-  const T* src = J.X[s.parity];
   if (sizeof(T) == 4 && s.parity == 0) return;  // already in place
-  const int lt = t - J.full_begin;
-  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
-  const int n = J.n;
+  const NewtonJob<T>* J = jobs + j;
+  const T* src = J->X[s.parity];
+  float* dst = J->Xout;
+  const int lt = t - J->full_begin;
+  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
+  const int n = J->n;
   for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
     const int r = ti * kTile + (e >> 7), c = tj * kTile + (e & 127);
-    if (r < n && c < n) J.Xout[(int64_t)r * n + c] = (float)src[(int64_t)r * n + c];
+    if (r < n && c < n) dst[(int64_t)r * n + c] = (float)src[(int64_t)r * n + c];
   }
 }
 

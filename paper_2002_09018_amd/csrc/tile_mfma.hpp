@@ -66,7 +66,7 @@ struct Mfma<double> {
   static __device__ __forceinline__ acc_t mma(double a, double b, acc_t c) {
     return __builtin_amdgcn_mfma_f64_16x16x4f64(a, b, c, 0, 0, 0);
   }
-  static __device__ __forceinline__ int row(int lane, int v) { return (lane >> 4) * 4 + v; }
+  static __device__ __forceinline__ int row(int lane, int v) { return v * 4 + (lane >> 4); }
   static __device__ __forceinline__ int col(int lane) { return lane & 15; }
 };
 
@@ -119,6 +119,18 @@ __device__ __forceinline__ double cvt<double, uint16_t>(uint16_t x) {
   return (double)__uint_as_float(((uint32_t)x) << 16);
 }
 
+// Global-memory (address space 1) access: keeps operand loads off the flat
+// path, whose completion counter is shared with LDS and would make every LDS
+// wait also wait for the prefetch of the next stage.
+template <typename V>
+__device__ __forceinline__ V gload(const void* p) {
+  return *(const __attribute__((address_space(1))) V*)(p);
+}
+template <typename V>
+__device__ __forceinline__ void gstore(void* p, V v) {
+  *(__attribute__((address_space(1))) V*)(p) = v;
+}
+
 // A matrix operand as stored: row-major, `rows` x `cols`, row stride `ld`.
 template <typename S>
 struct Operand {
@@ -166,7 +178,7 @@ struct Loader {
       for (int i = 0; i < PER; ++i) {
         int sr, sc;
         slot(tid, i, sr, sc);
-        buf[i] = *reinterpret_cast<const V*>(op.ptr + (int64_t)(r0 + sr) * op.ld + (c0 + sc));
+        buf[i] = gload<V>(op.ptr + (int64_t)(r0 + sr) * op.ld + (c0 + sc));
       }
     } else {
 #pragma unroll
@@ -177,7 +189,7 @@ struct Loader {
 #pragma unroll
         for (int e = 0; e < VE; ++e) {
           const int gc = c0 + sc + e;
-          buf[i][e] = (gr < op.rows && gc < op.cols) ? op.ptr[(int64_t)gr * op.ld + gc] : (S)0;
+          buf[i][e] = (gr < op.rows && gc < op.cols) ? gload<S>(op.ptr + (int64_t)gr * op.ld + gc) : (S)0;
         }
       }
     }
@@ -282,9 +294,10 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, 
   const int wm0 = (wave >> 1) * kWaveTile;
   const int wn0 = (wave & 1) * kWaveTile;
 
-  T* sA[2] = {reinterpret_cast<T*>(smem), reinterpret_cast<T*>(smem + StageBytes<T>::value)};
-  T* sB[2] = {reinterpret_cast<T*>(smem + 2 * StageBytes<T>::value),
-              reinterpret_cast<T*>(smem + 3 * StageBytes<T>::value)};
+  // LDS stages addressed arithmetically from the __shared__ base (a pointer
+  // array would lose the LDS address space and turn ds_reads into flat loads).
+  constexpr int SE = StageBytes<T>::value / (int)sizeof(T);  // elements per stage
+  T* const lds = reinterpret_cast<T*>(smem);
 
   LdA la;
   LdB lb;
@@ -300,8 +313,8 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, 
   orgB(0, br, bc);
   la.load(A, ar, ac, tid);
   lb.load(B, br, bc, tid);
-  la.store(sA[0], A, ar, ac, tid, affA);
-  lb.store(sB[0], B, br, bc, tid, affB);
+  la.store(lds, A, ar, ac, tid, affA);
+  lb.store(lds + 2 * SE, B, br, bc, tid, affB);
   __syncthreads();
   for (int st = 0; st < nst; ++st) {
     const int cur = st & 1;
@@ -312,10 +325,10 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, 
       la.load(A, ar, ac, tid);
       lb.load(B, br, bc, tid);
     }
-    acc.template stage<LdA::LDP, LdB::LDP>(sA[cur], sB[cur], wm0, wn0, lane);
+    acc.template stage<LdA::LDP, LdB::LDP>(lds + cur * SE, lds + (2 + cur) * SE, wm0, wn0, lane);
     if (more) {
-      la.store(sA[cur ^ 1], A, ar, ac, tid, affA);
-      lb.store(sB[cur ^ 1], B, br, bc, tid, affB);
+      la.store(lds + (cur ^ 1) * SE, A, ar, ac, tid, affA);
+      lb.store(lds + (2 + (cur ^ 1)) * SE, B, br, bc, tid, affB);
     }
     __syncthreads();
   }
