@@ -144,17 +144,20 @@ def main():
     times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
 
     # algorithmic work
-    it32, it64, nf32, nf64 = 0, 0, 0, 0
-    prods = 4  # p = 4: X M1, M1 M1, (M1^2)^2, M1^4 M
+    # Products per matrix: p = 4 takes X M1, M1 M1, (M1^2)^2 and M1^4 M per
+    # iteration, except the first, whose X product (with X0 a multiple of I)
+    # is not a GEMM.
+    it32, it64, prod32, prod64 = 0, 0, 0, 0
     for t in infos:
         for inf in B.decode_root_info(t):
             it32 += inf["iters_fp32"]
-            nf32 += inf["iters_fp32"]
+            prod32 += max(0, 4 * inf["iters_fp32"] - 1)
             if inf["precision"] == 64:
                 it64 += inf["iters"]
+                prod64 += max(0, 4 * inf["iters"] - 1)
     sym_prod = n * n * (n + 1)                     # symmetric product, upper-triangle counting
-    flops_newton32 = it32 * prods * sym_prod
-    flops_newton64 = it64 * prods * sym_prod
+    flops_newton32 = prod32 * sym_prod
+    flops_newton64 = prod64 * sym_prod
     flops_stats = args.steps * nb * n * (n + 1) * k
     flops_prec = args.steps * nb * 2 * n * n * k
     graft_bytes = args.steps * nb * n * k * 28   # pass 1: G, D, D', P; pass 2: W, P, W'

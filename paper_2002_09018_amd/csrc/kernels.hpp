@@ -7,6 +7,10 @@
 
 #include "tile_mfma.hpp"
 
+#ifndef SHP_EPI_VEC
+#define SHP_EPI_VEC 1
+#endif
+
 namespace shp {
 
 // ============================================================================
@@ -41,7 +45,7 @@ __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int n
 }
 
 template <typename SA, int LA, typename SB, int LB>
-__global__ __launch_bounds__(kThreads) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
+__global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
                                                                int nprob, int total_tiles) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   const int t = xcd_remap(blockIdx.x, gridDim.x);
@@ -57,12 +61,40 @@ __global__ __launch_bounds__(kThreads) void gemm_grouped_kernel(const GemmProble
   Operand<SB> B{reinterpret_cast<const SB*>(P.B), P.ldb, P.b_rows, P.b_cols, P.b_aligned != 0, 1.f, 0.f};
   WaveAcc<float> acc;
   acc.zero();
-  tile_mma<float, SA, LA, SB, LB>(acc, A, false, B, false, m0, n0, P.K, smem);
+  tile_mma<float, SA, LA, SB, LB>(acc, A, false, B, false, m0, n0, P.K, smem, P.sym && ti == tj);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
   const bool diag = P.sym && ti == tj;
   typedef Mfma<float> F;
+#if SHP_EPI_VEC
+  // Symmetric output, off-diagonal full tile: mirrored values go out as
+  // 16-byte stores (a lane's 4 consecutive rows are 4 consecutive columns of
+  // the transposed tile).
+  if (P.sym && !diag && m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
+      (reinterpret_cast<uintptr_t>(P.C) & 15) == 0) {
+#pragma unroll
+    for (int i = 0; i < WaveAcc<float>::NB; ++i)
+#pragma unroll
+      for (int j = 0; j < WaveAcc<float>::NB; ++j)
+#pragma unroll
+        for (int g = 0; g < F::kAcc / 4; ++g) {
+          const int r = wm0 + i * F::kM + F::row(lane, 4 * g);
+          const int c = wn0 + j * F::kM + F::col(lane);
+          typedef float f4 __attribute__((ext_vector_type(4)));
+          f4 w;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float x = P.alpha * acc.c[i][j][4 * g + q];
+            if (P.beta != 0.f) x += P.beta * gload<float>(P.C + (int64_t)(r + q) * P.ldc + c);
+            gstore<float>(P.C + (int64_t)(r + q) * P.ldc + c, x);
+            w[q] = x;
+          }
+          gstore<f4>(P.C + (int64_t)c * P.ldc + r, w);
+        }
+    return;
+  }
+#endif
 #pragma unroll
   for (int i = 0; i < WaveAcc<float>::NB; ++i)
 #pragma unroll
@@ -151,15 +183,18 @@ __device__ __forceinline__ int find_job_full(const NewtonJob<T>* jobs, int njobs
 enum : int { kFirst = 0, kFirstP1 = 1, kSquare = 2, kLast = 3 };
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
+__global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
                                                                int njobs, RootState* __restrict__ st,
                                                                int total_up, int kind, int src, int dst,
-                                                               float a, float b) {
+                                                               float a, float b, int skip_x) {
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int two = (kind == kFirst || kind == kFirstP1) ? 2 : 1;
+  // skip_x: first iteration, X' = X0 M1 = z^(1/p) M1 was written by the init
+  // kernel, so only the M-side product runs.
+  const bool first = kind == kFirst || kind == kFirstP1;
+  const int two = (first && !skip_x) ? 2 : 1;
   const int l = xcd_remap(blockIdx.x, gridDim.x);
   if (l >= two * total_up) return;
-  const int t = l / two, prod = l % two;
+  const int t = l / two, prod = (first && skip_x) ? 1 : l % two;
   const int j = find_job_up(jobs, njobs, t);
   if (st[j].status != kActive) return;
   // Buffer pointers are read from the table with run-time indices (not from a
@@ -197,32 +232,63 @@ __global__ __launch_bounds__(kThreads) void newton_stage_kernel(const NewtonJob<
   WaveAcc<T> acc;
   acc.zero();
   // All operands are symmetric, so both are read k-major (storage row = k).
-  tile_mma<T, T, kLayoutK, T, kLayoutK>(acc, A, affA, B, affB, m0, n0, n, smem);
+  tile_mma<T, T, kLayoutK, T, kLayoutK>(acc, A, affA, B, affB, m0, n0, n, smem, ti == tj);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
   const bool diag = ti == tj;
   typedef Mfma<T> F;
   float rmax = 0.f;
+  auto track = [&](T x, int r, int c) {
+    if (resid) {
+      float d = (float)fabs((double)x - (r == c ? 1.0 : 0.0));
+      if (!(d <= 3.0e38f)) d = INFINITY;  // NaN or overflow
+      rmax = rmax > d ? rmax : d;
+    }
+  };
+#if SHP_EPI_VEC
+  // Off-diagonal full tile of an fp32 product: the 4 consecutive rows a lane
+  // holds (v = 4g .. 4g+3) are 4 consecutive columns of the mirrored tile,
+  // written as one 16-byte store.
+  if (sizeof(T) == 4 && !diag && m0 + kTile <= n && n0 + kTile <= n && (n & 3) == 0) {
 #pragma unroll
-  for (int i = 0; i < WaveAcc<T>::NB; ++i)
+    for (int i = 0; i < WaveAcc<T>::NB; ++i)
 #pragma unroll
-    for (int jj = 0; jj < WaveAcc<T>::NB; ++jj)
+      for (int jj = 0; jj < WaveAcc<T>::NB; ++jj)
 #pragma unroll
-      for (int v = 0; v < F::kAcc; ++v) {
-        const int r = wm0 + i * F::kM + F::row(lane, v);
-        const int c = wn0 + jj * F::kM + F::col(lane);
-        if (r >= n || c >= n) continue;
-        if (diag && r > c) continue;
-        const T x = acc.c[i][jj][v];
-        gstore<T>(pc + (int64_t)r * n + c, x);
-        if (r != c) gstore<T>(pc + (int64_t)c * n + r, x);
-        if (resid) {
-          float d = (float)fabs((double)x - (r == c ? 1.0 : 0.0));
-          if (!(d <= 3.0e38f)) d = INFINITY;  // NaN or overflow
-          rmax = rmax > d ? rmax : d;
+        for (int g = 0; g < F::kAcc / 4; ++g) {
+          const int r = wm0 + i * F::kM + F::row(lane, 4 * g);
+          const int c = wn0 + jj * F::kM + F::col(lane);
+          typedef float f4 __attribute__((ext_vector_type(4)));
+          f4 w;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const T x = acc.c[i][jj][4 * g + q];
+            w[q] = (float)x;
+            gstore<T>(pc + (int64_t)(r + q) * n + c, x);
+            track(x, r + q, c);
+          }
+          gstore<f4>(reinterpret_cast<float*>(pc) + (int64_t)c * n + r, w);
         }
-      }
+  } else
+#endif
+  {
+#pragma unroll
+    for (int i = 0; i < WaveAcc<T>::NB; ++i)
+#pragma unroll
+      for (int jj = 0; jj < WaveAcc<T>::NB; ++jj)
+#pragma unroll
+        for (int v = 0; v < F::kAcc; ++v) {
+          const int r = wm0 + i * F::kM + F::row(lane, v);
+          const int c = wn0 + jj * F::kM + F::col(lane);
+          if (r >= n || c >= n) continue;
+          if (diag && r > c) continue;
+          const T x = acc.c[i][jj][v];
+          gstore<T>(pc + (int64_t)r * n + c, x);
+          if (r != c) gstore<T>(pc + (int64_t)c * n + r, x);
+          track(x, r, c);
+        }
+  }
   if (resid) {
     rmax = wave_max(rmax);
     if (lane == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
@@ -402,14 +468,19 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
   const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
   const double z = st[j].z, e = st[j].eps_eff;
   const T x0 = (T)pow(z, 1.0 / p);
+  const T a = (T)(p + 1) / (T)p, b = (T)-1 / (T)p;
   const int n = J.n;
   T* M = J.M[0];
   T* X = J.X[0];
+  T* X1 = J.X[1];
   float rmax = 0.f;
   sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
     const T m = (T)(z * (s + (r == c ? e : 0.0)));
     M[(int64_t)r * n + c] = m;
     X[(int64_t)r * n + c] = r == c ? x0 : (T)0;
+    // first iterate X1 = X0 M1 = z^(1/p) (a I + b M0), so the first
+    // iteration needs no X product
+    X1[(int64_t)r * n + c] = x0 * (b * m + (r == c ? a : (T)0));
     float d = (float)fabs((double)m - (r == c ? 1.0 : 0.0));
     if (!(d <= 3.0e38f)) d = INFINITY;
     rmax = rmax > d ? rmax : d;

@@ -438,27 +438,30 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
                        dcount + kCountRing);
   }));
   for (int it = 0; it < cap; ++it) {
+    // iteration 0: X1 = z^(1/p) M1 was written by the init kernel
+    const int skip_x = it == 0 ? 1 : 0;
+    const int first_grid = (skip_x ? 1 : 2) * total_up;
     if (p == 1) {
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(2 * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                           (int)kFirstP1, 0, 0, a, b);
+        hipLaunchKernelGGL(kstage, dim3(first_grid), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
+                           (int)kFirstP1, 0, 0, a, b, skip_x);
       }));
     } else {
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(2 * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                           (int)kFirst, 0, 0, a, b);
+        hipLaunchKernelGGL(kstage, dim3(first_grid), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
+                           (int)kFirst, 0, 0, a, b, skip_x);
       }));
       for (int q = 1; q < e; ++q) {
         const int src = (q - 1) & 1, dst = q & 1;
         STATUS_TRY(launch(h, cls, s, [&] {
           hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                             (int)kSquare, src, dst, a, b);
+                             (int)kSquare, src, dst, a, b, 0);
         }));
       }
       const int src = (e - 1) & 1;
       STATUS_TRY(launch(h, cls, s, [&] {
         hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                           (int)kLast, src, 0, a, b);
+                           (int)kLast, src, 0, a, b, 0);
       }));
     }
     int* slot = dcount + (it % kCountRing);

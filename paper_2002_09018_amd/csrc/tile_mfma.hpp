@@ -30,6 +30,13 @@
 
 namespace shp {
 
+#ifndef SHP_MIN_WAVES
+#define SHP_MIN_WAVES 2
+#endif
+// Minimum waves per SIMD requested from the register allocator for the MFMA
+// kernels (__launch_bounds__ second argument).
+constexpr int kMinWaves = SHP_MIN_WAVES;
+
 constexpr int kTile = 128;
 constexpr int kThreads = 256;
 constexpr int kWaveTile = 64;
@@ -39,9 +46,16 @@ enum { kLayoutK = 0, kLayoutRow = 1 };
 template <typename T>
 struct Mfma;
 
+#ifndef SHP_BK_F32
+#define SHP_BK_F32 16
+#endif
+#ifndef SHP_PADK_WORDS
+#define SHP_PADK_WORDS 0
+#endif
+
 template <>
 struct Mfma<float> {
-  static constexpr int kBK = 32;  // k-depth of one LDS stage
+  static constexpr int kBK = SHP_BK_F32;  // k-depth of one LDS stage
   static constexpr int kM = 32;   // MFMA block edge
   static constexpr int kK = 2;    // k-depth of one MFMA
   static constexpr int kAcc = 16; // accumulator elements per lane per block
@@ -70,20 +84,27 @@ struct Mfma<double> {
   static __device__ __forceinline__ int col(int lane) { return lane & 15; }
 };
 
-// Row pitch (elements) of one k-major LDS stage.  kLayoutK pads by 32 words so
-// the two half-waves of a fragment read (rows k and k+1) fall in different
-// bank halves; kLayoutRow pads by one element so transposed stores spread
-// over all banks.
+// Row pitch (elements) of one k-major LDS stage.  kLayoutK rows are written
+// and read as contiguous runs (no pad needed: measured conflict-free);
+// kLayoutRow pads by one element so its transposed scalar stores spread over
+// all banks.
 template <typename T, int LAYOUT>
 struct Pitch {
   static constexpr int value =
-      LAYOUT == kLayoutK ? kTile + 128 / (int)sizeof(T) : kTile + 1;
+      LAYOUT == kLayoutK ? kTile + SHP_PADK_WORDS * 4 / (int)sizeof(T) : kTile + 1;
 };
 
+// Bytes of one operand stage: sized for the larger of the two layouts' pitch
+// (the row layout pads one element per k-row, which exceeds an unpadded
+// k-layout stage).
 template <typename T>
 struct StageBytes {
-  static constexpr int value = Mfma<T>::kBK * Pitch<T, kLayoutK>::value * (int)sizeof(T);
+  static constexpr int pk = Pitch<T, kLayoutK>::value, pr = Pitch<T, kLayoutRow>::value;
+  static constexpr int value = Mfma<T>::kBK * (pk > pr ? pk : pr) * (int)sizeof(T);
 };
+static_assert(StageBytes<float>::value >= Mfma<float>::kBK * Pitch<float, kLayoutRow>::value * 4,
+              "row-layout stage must fit");
+static_assert(StageBytes<float>::value % 16 == 0, "stages must stay 16-byte aligned");
 
 // Dynamic LDS of one GEMM workgroup: A and B, two stages each (sized for the
 // larger, k-layout pitch).
@@ -260,31 +281,45 @@ struct WaveAcc {
     constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;
     const int kl = lane / Mfma<T>::kM;
     const int ml = lane % Mfma<T>::kM;
+    // Fragments are double-buffered in registers: the LDS reads of k-step
+    // s+1 are issued before the MFMAs of k-step s, so their latency overlaps
+    // the matrix-core work instead of stalling it.
+    T fa[2][NB], fb[2][NB];
+    const T* pa = a + kl * LDPA + wm0 + ml;
+    const T* pb = b + kl * LDPB + wn0 + ml;
+#pragma unroll
+    for (int i = 0; i < NB; ++i) fa[0][i] = pa[i * Mfma<T>::kM];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) fb[0][j] = pb[j * Mfma<T>::kM];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
-      T fa[NB], fb[NB];
-      const int k = s * Mfma<T>::kK + kl;
+      const int cur = s & 1;
+      if (s + 1 < KS) {
+        const int off = (s + 1) * Mfma<T>::kK;
 #pragma unroll
-      for (int i = 0; i < NB; ++i) fa[i] = a[k * LDPA + wm0 + i * Mfma<T>::kM + ml];
+        for (int i = 0; i < NB; ++i) fa[cur ^ 1][i] = pa[off * LDPA + i * Mfma<T>::kM];
 #pragma unroll
-      for (int j = 0; j < NB; ++j) fb[j] = b[k * LDPB + wn0 + j * Mfma<T>::kM + ml];
+        for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[off * LDPB + j * Mfma<T>::kM];
+      }
+      // Keep the reads of s+1 ahead of the MFMAs of s (the scheduler would
+      // otherwise sink them below to save registers).
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < NB; ++i)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) c[i][j] = Mfma<T>::mma(fa[i], fb[j], c[i][j]);
+        for (int j = 0; j < NB; ++j) c[i][j] = Mfma<T>::mma(fa[cur][i], fb[cur][j], c[i][j]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   }
 };
 
-// Full k-loop of one 128 x 128 output tile.
-//   A: layout LA; kLayoutK reads storage rows k (cols m0..), kLayoutRow
-//      reads storage rows m0.. (cols k).
-//   B: layout LB; kLayoutK reads storage rows k (cols n0..), kLayoutRow
-//      reads storage rows n0.. (cols k).
-template <typename T, typename SA, int LA, typename SB, int LB>
-__device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, bool affA,
-                                         const Operand<SB>& B, bool affB, int m0, int n0, int K,
-                                         unsigned char* smem) {
+// k-loop over LDS stages.  COMPUTE == false: the wave only helps to stage
+// operands (its MFMAs are skipped); the two variants are separate loops so the
+// wave-uniform choice costs no registers inside the loop.
+template <bool COMPUTE, typename T, typename SA, int LA, typename SB, int LB>
+__device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, bool affA,
+                                          const Operand<SB>& B, bool affB, int m0, int n0, int K,
+                                          unsigned char* smem) {
   typedef Loader<T, SA, LA> LdA;
   typedef Loader<T, SB, LB> LdB;
   constexpr int BK = Mfma<T>::kBK;
@@ -293,7 +328,6 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, 
   const int wave = tid >> 6;
   const int wm0 = (wave >> 1) * kWaveTile;
   const int wn0 = (wave & 1) * kWaveTile;
-
   // LDS stages addressed arithmetically from the __shared__ base (a pointer
   // array would lose the LDS address space and turn ds_reads into flat loads).
   constexpr int SE = StageBytes<T>::value / (int)sizeof(T);  // elements per stage
@@ -325,13 +359,36 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, 
       la.load(A, ar, ac, tid);
       lb.load(B, br, bc, tid);
     }
-    acc.template stage<LdA::LDP, LdB::LDP>(lds + cur * SE, lds + (2 + cur) * SE, wm0, wn0, lane);
+    if (COMPUTE)
+      acc.template stage<LdA::LDP, LdB::LDP>(lds + cur * SE, lds + (2 + cur) * SE, wm0, wn0, lane);
     if (more) {
       la.store(lds + (cur ^ 1) * SE, A, ar, ac, tid, affA);
       lb.store(lds + (2 + (cur ^ 1)) * SE, B, br, bc, tid, affB);
     }
     __syncthreads();
   }
+}
+
+// Full k-loop of one 128 x 128 output tile.
+//   A: layout LA; kLayoutK reads storage rows k (cols m0..), kLayoutRow
+//      reads storage rows m0.. (cols k).
+//   B: layout LB; kLayoutK reads storage rows k (cols n0..), kLayoutRow
+//      reads storage rows n0.. (cols k).
+// lower_idle: diagonal tile of a symmetric output, whose lower-left 64 x 64
+// quarter is never stored; that quarter's wave only stages operands.
+template <typename T, typename SA, int LA, typename SB, int LB>
+__device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, bool affA,
+                                         const Operand<SB>& B, bool affB, int m0, int n0, int K,
+                                         unsigned char* smem, bool lower_idle = false) {
+#ifndef SHP_IDLE_LOWER
+#define SHP_IDLE_LOWER 1
+#endif
+  const int wave = threadIdx.x >> 6;
+  const bool idle = SHP_IDLE_LOWER && lower_idle && (wave >> 1) > (wave & 1);
+  if (idle)
+    tile_loop<false, T, SA, LA, SB, LB>(acc, A, affA, B, affB, m0, n0, K, smem);
+  else
+    tile_loop<true, T, SA, LA, SB, LB>(acc, A, affA, B, affB, m0, n0, K, smem);
 }
 
 // Workgroup id -> logical tile index so that consecutive logical tiles land
