@@ -34,6 +34,24 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+def measured_traffic(name="newton_stage_kernel_c2_counters.txt"):
+    """HBM bytes per launch of the Newton kernel from the committed rocprofv3
+    counter summary, or None when the kernel sources changed since the
+    counters were taken (the summary records a hash of the sources)."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    kv = dict(line.strip().split("=", 1) for line in open(path) if "=" in line and not line.startswith("#"))
+    h = hashlib.sha256()
+    src = os.path.join(ROOT, "paper_2002_09018_amd", "csrc")
+    for f in sorted(os.listdir(src)):
+        h.update(open(os.path.join(src, f), "rb").read())
+    if kv.get("source_sha256") != h.hexdigest():
+        return None
+    return float(kv["bytes_per_launch"])
+
+
 def gen_block(i, n, k):
     from synth import configs as cfg
     L = cfg.wishart_bartlett(n, 19 * k, 1.0 / k, cfg.C2, i, 0).astype(np.float32)
@@ -66,12 +84,169 @@ def cpu_baseline(sample, n, k, p, eps, eta0, budget_s=12.0):
                        f"per block (stats L+GG^T, eigh root, Lr G, graft), {dt:.1f} s")
 
 
+def run_c4(args, torch, B):
+    """C4: 24 BERT-Large-shaped layers, 288 blocks of 1024 x 1024 (strided
+    views of the Q, K, V, O, FFN-in and FFN-out tensors); a step is the
+    two-sided statistics, preconditioning and graft over all blocks.  The
+    root refresh (every 100 steps in the workload) is timed separately."""
+    from synth import configs as cfg
+    dev = torch.device("cuda:0")
+    d, nl = 1024, cfg.C4_LAYERS
+    shapes = dict(cfg.c4_layer_tensors())
+    names = [nm for nm, _ in cfg.c4_layer_tensors()]
+    log("generating C4 tensors")
+    Wt, Dt, Pt, Gt = {}, {}, {}, {}
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as ex:
+        keys = [(l, t) for l in range(nl) for t in range(len(names))]
+        grads = list(ex.map(lambda lt: cfg.c4_grad(lt[0], lt[1], 1, shapes[names[lt[1]]]), keys))
+    for (l, t), g in zip(keys, grads):
+        sh = shapes[names[t]]
+        Gt[l, t] = torch.from_numpy(g).to(dev)
+        Wt[l, t] = (0.02 * torch.randn(sh, device=dev, generator=torch.Generator(device=dev).manual_seed(l * 8 + t)))
+        Dt[l, t] = torch.zeros(sh, device=dev)
+        Pt[l, t] = torch.zeros(sh, device=dev)
+    blocks, Ls, Rs, Lrs, Rrs = [], [], [], [], []
+    for l in range(nl):
+        for (t, r0, c0, rr, cc) in cfg.c4_blocks(d):
+            sl = (slice(r0, r0 + rr), slice(c0, c0 + cc))
+            L = torch.zeros(rr, rr, device=dev)
+            R = torch.zeros(cc, cc, device=dev)
+            Lr = torch.zeros(rr, rr, device=dev)
+            Rr = torch.zeros(cc, cc, device=dev)
+            Ls.append(L); Rs.append(R); Lrs.append(Lr); Rrs.append(Rr)
+            blocks.append(B.Block(G=Gt[l, t][sl], W=Wt[l, t][sl], D=Dt[l, t][sl], P=Pt[l, t][sl],
+                                  L=L, R=R, Lr=Lr, Rr=Rr))
+    nb = len(blocks)
+    h = B.shampoo_create(0)
+    # root refresh at step 100 of the workload: statistics of 100 gradients
+    # N(0, 1e-3) of a 1024 x 1024 block are Wishart(1024, 102400 dof)
+    for b in range(nb):
+        Ls[b].copy_(cfg.wishart_bartlett_device(d, 100 * d, 1e-3, torch, dev, cfg.C4, 7, b, 0))
+        Rs[b].copy_(cfg.wishart_bartlett_device(d, 100 * d, 1e-3, torch, dev, cfg.C4, 7, b, 1))
+    prm = B.shampoo_root_params_default(p=4, eps=1e-6)
+    As, Xs = Ls + Rs, Lrs + Rrs
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([d] * len(As), prm.precision), dtype=torch.uint8,
+                     device=dev)
+    info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info)
+    torch.cuda.synchronize()
+    root_ms = (time.perf_counter() - t0) * 1e3
+    iters = [i["iters"] for i in B.decode_root_info(info)]
+    log(f"root refresh: {len(As)} roots in {root_ms:.1f} ms")
+
+    def step():
+        B.shampoo_update_stats(h, blocks)
+        B.shampoo_precondition(h, blocks)
+        B.shampoo_graft(h, blocks, 6e-3)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    B.shampoo_timing_enable(h, True)
+    for c in range(6):
+        B.shampoo_timing_read(h, c)
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    B.shampoo_timing_enable(h, False)
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
+    B.shampoo_destroy(h)
+    K = args.steps
+    flops_stats = K * nb * 2 * d * d * (d + 1)
+    flops_prec = K * nb * 4 * d ** 3
+    bytes_graft = K * nb * d * d * 28
+    roof_ms = (flops_stats / PEAK_F32_MFMA + flops_prec / PEAK_F32_MFMA) / 1e9 / K + bytes_graft / PEAK_HBM / 1e6 / K
+    ms_step = elapsed * 1e3 / K
+    prods = sum(max(0, 4 * i - 1) for i in iters)
+    out = {
+        "metric": "C4 stats+precondition+graft step ms (288 blocks of 1024^2, two-sided)",
+        "value": ms_step, "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "C4: 24 layers x 12 blocks of 1024x1024 (BERT-Large shapes), G ~ N(0,1e-3) fp32, "
+                               "stats L,R + L^-1/4 G R^-1/4 + AdaGrad graft per step", "blocks": nb},
+        "phase_roofline_ms": roof_ms, "frac_of_phase_roofline": roof_ms / ms_step,
+        "phases_ms_per_step": {c: v[0] / K for c, v in times.items()},
+        "kernels": {"stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12,
+                    "precond_tflops": flops_prec / (times["precond"][0] * 1e-3) / 1e12,
+                    "graft_gbs": bytes_graft / (times["graft"][0] * 1e-3) / 1e9},
+        "root_refresh": {"roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
+                         "iters_mean": float(np.mean(iters)),
+                         "newton_tflops": prods * d * d * (d + 1) / (root_ms * 1e-3) / 1e12},
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_c3(args, torch, B):
+    """C3: 32 ill-conditioned 2048 x 2048 matrices (log-uniform spectrum in
+    [1e-6, 1e2]), scaled damping 1e-6 * lambda_max, one grouped call per p in
+    {2, 4}; AUTO precision (fp32 attempt, fp64 tail)."""
+    from synth import configs as cfg
+    dev = torch.device("cuda:0")
+    n, nm = 2048, 32
+    log("generating C3 matrices")
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as ex:
+        mats = list(ex.map(lambda i: cfg.c3_matrix(i, n)[0], range(nm)))
+    As = [torch.from_numpy(a).to(dev) for a in mats]
+    Xs = [torch.zeros_like(a) for a in As]
+    h = B.shampoo_create(0)
+    res = {}
+    for p in (2, 4):
+        prm = B.shampoo_root_params_default(p=p, eps=1e-6, eps_relative=1)
+        ws = torch.empty(B.shampoo_inv_root_workspace_bytes([n] * nm, prm.precision), dtype=torch.uint8,
+                         device=dev)
+        info = torch.zeros(8 * nm, dtype=torch.int32, device=dev)
+        B.shampoo_inv_root_batched(h, As[:2], Xs[:2], prm, ws, info)   # warm-up
+        torch.cuda.synchronize()
+        B.shampoo_timing_enable(h, True)
+        for c in range(6):
+            B.shampoo_timing_read(h, c)
+        t0 = time.perf_counter()
+        B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info)
+        torch.cuda.synchronize()
+        ms = (time.perf_counter() - t0) * 1e3
+        B.shampoo_timing_enable(h, False)
+        times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
+        inf = B.decode_root_info(info)
+        prods = 2 if p == 2 else 3
+        pr64 = sum(max(0, (prods + 1) * i["iters"] - 1) for i in inf if i["precision"] == 64)
+        pr32 = sum(max(0, (prods + 1) * i["iters_fp32"] - 1) for i in inf)
+        sym = n * n * (n + 1)
+        res[f"p{p}"] = {
+            "ms": ms, "roots_per_s": nm / ms * 1e3,
+            "iters_fp64": [i["iters"] for i in inf if i["precision"] == 64][:8],
+            "iters_fp32_attempt": inf[0]["iters_fp32"],
+            "n_fp64": sum(1 for i in inf if i["precision"] == 64),
+            "status": sorted(set(i["status"] for i in inf)),
+            "newton_f64_ms": times["newton_f64"][0], "newton_f32_ms": times["newton_f32"][0],
+            "root_aux_ms": times["root_aux"][0],
+            "newton_f64_tflops": pr64 * sym / (times["newton_f64"][0] * 1e-3) / 1e12 if times["newton_f64"][0] else None,
+            "newton_f64_frac": (pr64 * sym / (times["newton_f64"][0] * 1e-3) / 1e12 / PEAK_F64_MFMA
+                                if times["newton_f64"][0] else None),
+            "newton_f32_tflops": pr32 * sym / (times["newton_f32"][0] * 1e-3) / 1e12 if times["newton_f32"][0] else None,
+        }
+        log(f"p={p}: {ms:.1f} ms")
+    B.shampoo_destroy(h)
+    out = {"metric": "C3 ill-conditioned 2048^2 inverse roots (AUTO precision, fp64 tail)", "value": res["p4"]["ms"],
+           "unit": "ms per 32 roots (p=4)", "n_gpus": 1, "higher_is_better": False, "dtype": "f32/f64",
+           "data": "synthetic", "config": {"workload": "C3: 32 x 2048^2, lambda log-uniform [1e-6,1e2], "
+                                                       "eps 1e-6 * lambda_max, p in {2,4}"}, "results": res}
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--blocks", type=int, default=96)
+    ap.add_argument("--workload", choices=["c2", "c3", "c4"], default="c2",
+                    help="c2 (default): the metric's workload; c3: ill-conditioned roots; c4: the "
+                         "transformer-layer step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="before the steps, copy a buffer of this size once (a plain copy kernel of known "
@@ -85,6 +260,10 @@ def main():
     import torch
     from paper_2002_09018_amd import binding as B
 
+    if args.workload == "c4":
+        return run_c4(args, torch, B)
+    if args.workload == "c3":
+        return run_c3(args, torch, B)
     dev = torch.device("cuda:0")
     nb, n, k, p, eps, eta0 = args.blocks, 1024, 4096, 4, 1e-6, 1e-2
     log(f"generating {nb} blocks")
@@ -188,7 +367,8 @@ def main():
             "frac": achieved / PEAK_F32_MFMA,
             "flops_per_launch": flops_newton32 / max(launches_newton, 1),
             "avg_launch_us": ms_newton * 1e3 / max(launches_newton, 1),
-            "traffic": None,
+            "traffic": measured_traffic(),
+            "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
         },
         "stats_precondition_ms_per_step": stats_prec_ms,
         "fp32_mfma_util": achieved / PEAK_F32_MFMA,

@@ -13,6 +13,8 @@
 
 namespace shp {
 
+typedef float f4v __attribute__((ext_vector_type(4)));
+
 // ============================================================================
 // Grouped GEMM for statistics and preconditioning.
 // One "problem" per output matrix; workgroups enumerate the 128 x 128 output
@@ -47,7 +49,8 @@ __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int n
 template <typename SA, int LA, typename SB, int LB>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
                                                                int nprob, int total_tiles) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ __attribute__((aligned(16))) float sa0[TileSmem<float>::E], sa1[TileSmem<float>::E];
+  __shared__ __attribute__((aligned(16))) float sb0[TileSmem<float>::E], sb1[TileSmem<float>::E];
   const int t = xcd_remap(blockIdx.x, gridDim.x);
   if (t >= total_tiles) return;
   const GemmProblem P = probs[find_problem_gemm(probs, nprob, t)];
@@ -57,11 +60,11 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   else { ti = lt / P.tiles_n; tj = lt % P.tiles_n; }
   const int m0 = ti * kTile, n0 = tj * kTile;
 
-  Operand<SA> A{reinterpret_cast<const SA*>(P.A), P.lda, P.a_rows, P.a_cols, P.a_aligned != 0, 1.f, 0.f};
-  Operand<SB> B{reinterpret_cast<const SB*>(P.B), P.ldb, P.b_rows, P.b_cols, P.b_aligned != 0, 1.f, 0.f};
+  Operand<SA> A{reinterpret_cast<const SA*>(P.A), P.lda, P.a_rows, P.a_cols, P.a_aligned != 0};
+  Operand<SB> B{reinterpret_cast<const SB*>(P.B), P.ldb, P.b_rows, P.b_cols, P.b_aligned != 0};
   WaveAcc<float> acc;
   acc.zero();
-  tile_mma<float, SA, LA, SB, LB>(acc, A, false, B, false, m0, n0, P.K, smem, P.sym && ti == tj);
+  tile_mma<float, SA, LA, SB, LB>(acc, A, B, m0, n0, P.K, sa0, sa1, sb0, sb1, P.sym && ti == tj);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
@@ -131,6 +134,8 @@ struct RootState {
   float resid;       // residual after the last iteration
   int escalate;      // AUTO policy: redo in fp64
   int precision;     // 32 or 64: phase that produced the result
+  int sv_done;       // MaxSV stopped
+  int sv_steps;      // MaxSV power steps taken
   double z;          // Frobenius scaling (1 + p) / (2 ||A_d||_F)
   double eps_eff;    // damping added
   double lam_max;    // MaxSV estimate (relative damping)
@@ -146,7 +151,7 @@ struct NewtonJob {
   const float* A;   // input statistics (fp32, n x n)
   float* Xout;      // caller's output
   double* part;     // per-tile partial sums (tiles_n^2 x 2)
-  double* vec;      // MaxSV vectors (2 n)
+  double* vec;      // MaxSV vector and partials ((2 tiles_n + 1) n)
   int n;
   int tiles_n;      // ceil(n / 128)
   int up_begin;     // first logical upper-triangular tile
@@ -173,13 +178,15 @@ __device__ __forceinline__ int find_job_full(const NewtonJob<T>* jobs, int njobs
   return lo;
 }
 
-// Stage kinds of one Newton iteration (p = 2^e):
-//   kFirst  : X' = X M1  and  S[dst] = M1 M1         (two products per tile)
-//   kFirstP1: X' = X M1  and  M' = M1 M   (+residual) (p = 1)
+// Stage kinds of one Newton iteration (p = 2^e), with M1 = a I + b M
+// (a = (p+1)/p, b = -1/p) never stored: its products are expanded into a
+// plain product and an affine epilogue C = alpha acc + beta E + gamma I,
+//   kFirst  : X' = X M1 = b (X M) + a X           and
+//             S[dst] = M1 M1 = b^2 (M M) + 2ab M + a^2 I   (two products per tile)
+//   kFirstP1: X' = X M1  and  M' = M1 M = b (M M) + a M  (+residual) (p = 1)
 //   kSquare : S[dst] = S[src] S[src]
-//   kLast   : M' = S[src] M               (+residual)
-// with M1 = a I + b M formed while loading (a = (p+1)/p, b = -1/p), X, M the
-// buffers of the current parity and X', M' those of the other parity.
+//   kLast   : M' = S[src] M                        (+residual)
+// X, M are the buffers of the current parity and X', M' those of the other.
 enum : int { kFirst = 0, kFirstP1 = 1, kSquare = 2, kLast = 3 };
 
 template <typename T>
@@ -187,7 +194,8 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const
                                                                int njobs, RootState* __restrict__ st,
                                                                int total_up, int kind, int src, int dst,
                                                                float a, float b, int skip_x) {
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  __shared__ __attribute__((aligned(16))) T sa0[TileSmem<T>::E], sa1[TileSmem<T>::E];
+  __shared__ __attribute__((aligned(16))) T sb0[TileSmem<T>::E], sb1[TileSmem<T>::E];
   // skip_x: first iteration, X' = X0 M1 = z^(1/p) M1 was written by the init
   // kernel, so only the M-side product runs.
   const bool first = kind == kFirst || kind == kFirstP1;
@@ -209,30 +217,42 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const
   const T* pa;
   const T* pb;
   T* pc;
-  bool affA = false, affB = false, resid = false;
+  const T* pe = nullptr;  // E of the affine epilogue
+  T ca = (T)1, cb = (T)0, cg = (T)0;  // alpha, beta, gamma
+  bool resid = false;
+  const T ta = (T)a, tb = (T)b;
   if (kind == kFirst || kind == kFirstP1) {
     if (prod == 0) {
-      pa = J->X[par]; pb = J->M[par]; pc = J->X[par ^ 1]; affB = true;
+      pa = J->X[par]; pb = J->M[par]; pc = J->X[par ^ 1];
+      pe = J->X[par]; ca = tb; cb = ta;
     } else if (kind == kFirst) {
-      pa = J->M[par]; pb = J->M[par]; pc = J->S[dst]; affA = affB = true;
+      pa = J->M[par]; pb = J->M[par]; pc = J->S[dst];
+      pe = J->M[par]; ca = tb * tb; cb = (T)2 * ta * tb; cg = ta * ta;
     } else {
-      pa = J->M[par]; pb = J->M[par]; pc = J->M[par ^ 1]; affA = true; resid = true;
+      pa = J->M[par]; pb = J->M[par]; pc = J->M[par ^ 1]; resid = true;
+      pe = J->M[par]; ca = tb; cb = ta;
     }
   } else if (kind == kSquare) {
     pa = J->S[src]; pb = J->S[src]; pc = J->S[dst];
   } else {
     pa = J->S[src]; pb = J->M[par]; pc = J->M[par ^ 1]; resid = true;
   }
-  const bool al = (n % SrcVec<T>::n) == 0;
-  Operand<T> A{pa, n, n, n, al, a, 0.f};
-  Operand<T> B{pb, n, n, n, al, a, 0.f};
-  A.mul = affA ? b : 1.f; A.add = affA ? a : 0.f;
-  B.mul = affB ? b : 1.f; B.add = affB ? a : 0.f;
+  const bool al = (reinterpret_cast<uintptr_t>(pa) & 15) == 0 && (reinterpret_cast<uintptr_t>(pb) & 15) == 0 &&
+                  ((n * (int)sizeof(T)) & 15) == 0;
+  Operand<T> A{pa, n, n, n, al};
+  Operand<T> B{pb, n, n, n, al};
 
   WaveAcc<T> acc;
   acc.zero();
   // All operands are symmetric, so both are read k-major (storage row = k).
-  tile_mma<T, T, kLayoutK, T, kLayoutK>(acc, A, affA, B, affB, m0, n0, n, smem, ti == tj);
+  tile_mma<T, T, kLayoutK, T, kLayoutK>(acc, A, B, m0, n0, n, sa0, sa1, sb0, sb1, ti == tj);
+  // value of output element (r, c) from its accumulator
+  auto fin = [&](T v, int r, int c) -> T {
+    T x = ca * v;
+    if (pe) x += cb * gload<T>(pe + (int64_t)r * n + c);
+    if (r == c) x += cg;
+    return x;
+  };
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
@@ -263,7 +283,7 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const
           f4 w;
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const T x = acc.c[i][jj][4 * g + q];
+            const T x = fin(acc.c[i][jj][4 * g + q], r + q, c);
             w[q] = (float)x;
             gstore<T>(pc + (int64_t)(r + q) * n + c, x);
             track(x, r + q, c);
@@ -283,7 +303,7 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const
           const int c = wn0 + jj * F::kM + F::col(lane);
           if (r >= n || c >= n) continue;
           if (diag && r > c) continue;
-          const T x = acc.c[i][jj][v];
+          const T x = fin(acc.c[i][jj][v], r, c);
           gstore<T>(pc + (int64_t)r * n + c, x);
           if (r != c) gstore<T>(pc + (int64_t)c * n + r, x);
           track(x, r, c);
@@ -312,50 +332,97 @@ __device__ __forceinline__ double block_sum(double v, double* red) {
   return s;
 }
 
+// MaxSV, one power step over all matrices.  Workgroup (matrix, ti, tj)
+// stages tile A[ti, tj] in LDS and writes its row partials (A vh)_rows and
+// column partials (A^T vh)_cols; the last workgroup of a matrix (atomic
+// ticket, no waiting) reduces the partials in a fixed order to
+// v = A_s vh = (A vh + A^T vh) / 2, the Rayleigh quotient lambda = vh . v,
+// the stop test |lambda - lambda_old| <= tol lambda, and the next
+// vh = v / |v|.  Vector layout per matrix (doubles): [0, n) vh,
+// [n, n + T n) row partials by tile column, [n + T n, n + 2 T n) column
+// partials by tile row.
 template <typename T>
-__global__ __launch_bounds__(kThreads) void maxsv_kernel(const NewtonJob<T>* __restrict__ jobs,
-                                                        RootState* __restrict__ st, int n_step,
-                                                        double tol, double eps) {
+__global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                             RootState* __restrict__ st, int total_full,
+                                                             int* __restrict__ tickets, double tol, double eps,
+                                                             int last_step) {
+  __shared__ float tile[kTile * (kTile + 1)];
   __shared__ double red[kThreads / 64];
-  const NewtonJob<T> J = jobs[blockIdx.x];
-  const int n = J.n;
-  const float* A = J.A;
-  double* v = J.vec;       // current v
-  double* vh = J.vec + n;  // normalised v
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  for (int i = tid; i < n; i += kThreads) v[i] = 1.0;
-  __syncthreads();
-  double lam = 0.0;
-  for (int it = 0; it < n_step; ++it) {
-    double s = 0.0;
-    for (int i = tid; i < n; i += kThreads) s += v[i] * v[i];
-    const double nrm = sqrt(block_sum(s, red));
-    for (int i = tid; i < n; i += kThreads) vh[i] = nrm > 0.0 ? v[i] / nrm : 0.0;
-    __syncthreads();
-    // column form (A^T vh)_c, one thread per column, coalesced row reads
-    for (int c = tid; c < n; c += kThreads) {
-      double y = 0.0;
-      for (int r = 0; r < n; ++r) y += (double)A[(int64_t)r * n + c] * vh[r];
-      v[c] = 0.5 * y;
-    }
-    __syncthreads();
-    // row form (A vh)_r, one wave per row
-    for (int r = wave; r < n; r += kThreads / 64) {
-      double y = 0.0;
-      for (int c = lane; c < n; c += 64) y += (double)A[(int64_t)r * n + c] * vh[c];
-      y = wave_sum(y);
-      if (lane == 0) v[r] += 0.5 * y;
-    }
-    __syncthreads();
-    double q = 0.0;
-    for (int i = tid; i < n; i += kThreads) q += vh[i] * v[i];
-    const double lam_old = lam;
-    lam = block_sum(q, red);
-    if (fabs(lam - lam_old) <= tol * fabs(lam)) break;
+  __shared__ int is_last;
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive || st[j].sv_done) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int n = J->n, TN = J->tiles_n;
+  const int lt = t - J->full_begin;
+  const int ti = lt / TN, tj = lt % TN;
+  const int r0 = ti * kTile, c0 = tj * kTile;
+  double* vh = J->vec;
+  double* prow = J->vec + n;
+  double* pcol = J->vec + n + (int64_t)TN * n;
+  const float* A = J->A;
+  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+    const int r = e >> 7, c = e & 127;
+    tile[r * (kTile + 1) + c] = (r0 + r < n && c0 + c < n) ? A[(int64_t)(r0 + r) * n + c0 + c] : 0.f;
   }
-  if (tid == 0) {
-    st[blockIdx.x].lam_max = lam;
-    st[blockIdx.x].eps_eff = eps * lam;
+  __syncthreads();
+  {
+    const int q = threadIdx.x & 127;  // a row of the tile (first half) or a column (second half)
+    double acc = 0.0;
+    if (threadIdx.x < kTile) {
+      for (int c = 0; c < kTile && c0 + c < n; ++c) acc += (double)tile[q * (kTile + 1) + c] * vh[c0 + c];
+      if (r0 + q < n) prow[(int64_t)tj * n + r0 + q] = acc;
+    } else {
+      for (int r = 0; r < kTile && r0 + r < n; ++r) acc += (double)tile[r * (kTile + 1) + q] * vh[r0 + r];
+      if (c0 + q < n) pcol[(int64_t)ti * n + c0 + q] = acc;
+    }
+  }
+  __threadfence();  // release: this workgroup's partials before its ticket
+  __syncthreads();
+  if (threadIdx.x == 0) is_last = atomicAdd(&tickets[j], 1) == TN * TN - 1;
+  __syncthreads();
+  if (!is_last) return;
+  __threadfence();  // acquire: partials of the other workgroups (any XCD) are visible
+  // reduction by the last workgroup of this matrix
+  double q = 0.0, s2 = 0.0;
+  for (int i = threadIdx.x; i < n; i += kThreads) {
+    double a = 0.0, b = 0.0;
+    for (int k = 0; k < TN; ++k) {
+      a += prow[(int64_t)k * n + i];
+      b += pcol[(int64_t)k * n + i];
+    }
+    const double v = 0.5 * (a + b);
+    q += vh[i] * v;
+    s2 += v * v;
+    prow[i] = v;  // row partials of tile column 0 are consumed: reuse as v
+  }
+  const double lam = block_sum(q, red);
+  const double nrm = sqrt(block_sum(s2, red));
+  const double lam_old = st[j].lam_max;
+  for (int i = threadIdx.x; i < n; i += kThreads) vh[i] = nrm > 0.0 ? prow[i] / nrm : 0.0;
+  if (threadIdx.x == 0) {
+    st[j].lam_max = lam;
+    st[j].eps_eff = eps * lam;
+    st[j].sv_steps += 1;
+    if (fabs(lam - lam_old) <= tol * fabs(lam) || last_step) st[j].sv_done = 1;
+    tickets[j] = 0;
+  }
+}
+
+// Starting vector of MaxSV: vh = ones / sqrt(n).
+template <typename T>
+__global__ void maxsv_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, RootState* __restrict__ st,
+                                  int* __restrict__ tickets) {
+  const int j = blockIdx.x;
+  if (j >= njobs) return;
+  const int n = jobs[j].n;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) jobs[j].vec[i] = 1.0 / sqrt((double)n);
+  if (threadIdx.x == 0) {
+    st[j].lam_max = 0.0;
+    st[j].sv_done = 0;
+    st[j].sv_steps = 0;
+    tickets[j] = 0;
   }
 }
 
@@ -471,15 +538,15 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
   const T a = (T)(p + 1) / (T)p, b = (T)-1 / (T)p;
   const int n = J.n;
   T* M = J.M[0];
-  T* X = J.X[0];
   T* X1 = J.X[1];
   float rmax = 0.f;
+  // X0 = z^(1/p) I is not stored: the first iterate X1 = X0 M1 =
+  // z^(1/p) (a I + b M0) is written here, so the first iteration needs no X
+  // product; a matrix that stops before any iteration gets X0 from the
+  // output kernel.
   sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
     const T m = (T)(z * (s + (r == c ? e : 0.0)));
     M[(int64_t)r * n + c] = m;
-    X[(int64_t)r * n + c] = r == c ? x0 : (T)0;
-    // first iterate X1 = X0 M1 = z^(1/p) (a I + b M0), so the first
-    // iteration needs no X product
     X1[(int64_t)r * n + c] = x0 * (b * m + (r == c ? a : (T)0));
     float d = (float)fabs((double)m - (r == c ? 1.0 : 0.0));
     if (!(d <= 3.0e38f)) d = INFINITY;
@@ -581,14 +648,15 @@ __global__ __launch_bounds__(kThreads) void root_escalate_kernel(RootState* __re
   }
 }
 
-// Copies the final iterate into the caller's fp32 X: for the fp32 phase only
-// when it sits in the workspace buffer (parity 1; X[0] is the caller's X), for
-// the fp64 phase always (with rounding).  Only matrices whose result came
-// from this phase (`want_escalated` selects the fp64 tail of AUTO).
+// Writes the result into the caller's fp32 X: the final iterate when it sits
+// in a workspace buffer (fp32 parity 1, or any fp64 result, rounded), or
+// X0 = z^(1/p) I for a matrix that stopped before its first iteration.  Only
+// matrices whose result came from this phase are touched (`phase_is_tail`
+// selects the fp64 tail of AUTO).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
                                                               const RootState* __restrict__ st, int total_full,
-                                                              int phase_is_tail) {
+                                                              int phase_is_tail, int p) {
   const int t = blockIdx.x;
   if (t >= total_full) return;
   const int j = find_job_full(jobs, njobs, t);
@@ -596,16 +664,27 @@ __global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T
   if (phase_is_tail && !s.escalate) return;
   if (!phase_is_tail && s.escalate) return;
   if (s.status == kNotPD) return;
-  if (sizeof(T) == 4 && s.parity == 0) return;  // already in place
+  const bool ident = s.iters == 0;
+  if (!ident && sizeof(T) == 4 && s.parity == 0) return;  // already in place
   const NewtonJob<T>* J = jobs + j;
   const T* src = J->X[s.parity];
   float* dst = J->Xout;
+  const float x0 = (float)pow(s.z, 1.0 / p);
   const int lt = t - J->full_begin;
   const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
   const int n = J->n;
+  const int r0 = ti * kTile, c0 = tj * kTile;
+  if (!ident && sizeof(T) == 4 && (n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n) {
+    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
+      const int r = r0 + (e >> 5), c = c0 + 4 * (e & 31);
+      gstore<f4v>(dst + (int64_t)r * n + c, gload<f4v>(reinterpret_cast<const float*>(src) + (int64_t)r * n + c));
+    }
+    return;
+  }
   for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-    const int r = ti * kTile + (e >> 7), c = tj * kTile + (e & 127);
-    if (r < n && c < n) dst[(int64_t)r * n + c] = (float)src[(int64_t)r * n + c];
+    const int r = r0 + (e >> 7), c = c0 + (e & 127);
+    if (r < n && c < n)
+      dst[(int64_t)r * n + c] = ident ? (r == c ? x0 : 0.f) : (float)src[(int64_t)r * n + c];
   }
 }
 
@@ -694,6 +773,41 @@ __device__ __forceinline__ float load_g(const void* G, int64_t i) {
 // D^{-1/2} o G with 0 where D == 0.
 __device__ __forceinline__ float ada_dir(float g, float d) { return d > 0.f ? g / sqrtf(d) : 0.f; }
 
+// Element access of the graft passes: 4 consecutive elements of a row.
+template <typename SG>
+struct G4;
+template <>
+struct G4<float> {
+  static __device__ __forceinline__ void load(const void* G, int64_t i, float g[4]) {
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const f4 v = gload<f4>(reinterpret_cast<const float*>(G) + i);
+    g[0] = v[0]; g[1] = v[1]; g[2] = v[2]; g[3] = v[3];
+  }
+};
+template <>
+struct G4<uint16_t> {
+  static __device__ __forceinline__ void load(const void* G, int64_t i, float g[4]) {
+    typedef uint16_t u4 __attribute__((ext_vector_type(4)));
+    const u4 v = gload<u4>(reinterpret_cast<const uint16_t*>(G) + i);
+    g[0] = cvt<float, uint16_t>(v[0]); g[1] = cvt<float, uint16_t>(v[1]);
+    g[2] = cvt<float, uint16_t>(v[2]); g[3] = cvt<float, uint16_t>(v[3]);
+  }
+};
+// Calls f(i) for the element offsets of a chunk (rows r0..r1 of a block):
+// 4-wide (f(i, 4)) where the block allows vector access, else scalar
+// (f(i, 1)).  Whole rows per chunk keep index arithmetic free of divisions.
+template <typename F>
+__device__ __forceinline__ void for_chunk(const GraftBlock& B, int r0, int r1, F&& f) {
+  if (B.vec4) {
+    const int c4 = B.cols >> 2;
+    for (int r = r0; r < r1; ++r)
+      for (int c = threadIdx.x; c < c4; c += kThreads) f((int64_t)r * B.ld + 4 * c, 4);
+  } else {
+    for (int r = r0; r < r1; ++r)
+      for (int c = threadIdx.x; c < B.cols; c += kThreads) f((int64_t)r * B.ld + c, 1);
+  }
+}
+
 template <typename SG>
 __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock* __restrict__ blocks, int nb,
                                                               int total_chunks, float beta1, int use_shampoo,
@@ -707,23 +821,40 @@ __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock*
   const int r1 = min(B.rows, r0 + B.rows_per_chunk);
   const bool mom = beta1 > 0.f;
   float smg = 0.f, sps = 0.f;
-  const int64_t cnt = (int64_t)(r1 - r0) * B.cols;
-  for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
-    const int r = r0 + (int)(e / B.cols), c = (int)(e % B.cols);
-    const int64_t i = (int64_t)r * B.ld + c;
-    const float g = load_g<SG>(B.G, i);
-    const float d = B.D[i] + g * g;
-    B.D[i] = d;
-    const float u = ada_dir(g, d);
-    float mg = u;
-    if (mom) { mg = beta1 * B.Mg[i] + (1.f - beta1) * u; B.Mg[i] = mg; }
-    smg += mg * mg;
-    if (use_shampoo) {
-      float ps = B.P[i];
-      if (mom) { ps = beta1 * B.Ps[i] + (1.f - beta1) * ps; B.Ps[i] = ps; }
-      sps += ps * ps;
+  for_chunk(B, r0, r1, [&](int64_t i, int w) {
+    float g[4], d[4], pv[4];
+    if (w == 4) {
+      G4<SG>::load(B.G, i, g);
+      const f4v dv = gload<f4v>(B.D + i);
+      d[0] = dv[0]; d[1] = dv[1]; d[2] = dv[2]; d[3] = dv[3];
+      if (use_shampoo) {
+        const f4v p4 = gload<f4v>(B.P + i);
+        pv[0] = p4[0]; pv[1] = p4[1]; pv[2] = p4[2]; pv[3] = p4[3];
+      }
+    } else {
+      g[0] = load_g<SG>(B.G, i);
+      d[0] = gload<float>(B.D + i);
+      if (use_shampoo) pv[0] = gload<float>(B.P + i);
     }
-  }
+    f4v dn;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (e >= w) break;
+      const float de = d[e] + g[e] * g[e];
+      dn[e] = de;
+      const float u = ada_dir(g[e], de);
+      float mg = u;
+      if (mom) { mg = beta1 * B.Mg[i + e] + (1.f - beta1) * u; B.Mg[i + e] = mg; }
+      smg += mg * mg;
+      if (use_shampoo) {
+        float ps = pv[e];
+        if (mom) { ps = beta1 * B.Ps[i + e] + (1.f - beta1) * ps; B.Ps[i + e] = ps; }
+        sps += ps * ps;
+      }
+    }
+    if (w == 4) gstore<f4v>(B.D + i, dn);
+    else gstore<float>(B.D + i, dn[0]);
+  });
   const double a = block_sum((double)smg, red);
   const double b = block_sum((double)sps, red);
   if (threadIdx.x == 0) {
@@ -761,15 +892,37 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
   const int r0 = ch * B.rows_per_chunk;
   const int r1 = min(B.rows, r0 + B.rows_per_chunk);
   const bool mom = beta1 > 0.f;
-  const int64_t cnt = (int64_t)(r1 - r0) * B.cols;
-  for (int64_t e = threadIdx.x; e < cnt; e += kThreads) {
-    const int r = r0 + (int)(e / B.cols), c = (int)(e % B.cols);
-    const int64_t i = (int64_t)r * B.ld + c;
-    float step;
-    if (use_shampoo) step = mom ? B.Ps[i] : B.P[i];
-    else step = mom ? B.Mg[i] : ada_dir(load_g<SG>(B.G, i), B.D[i]);
-    B.W[i] -= etaf * step;
-  }
+  // direction: Ps (momentum) or P; before the roots Mg or D^{-1/2} o G
+  const float* dir = use_shampoo ? (mom ? B.Ps : B.P) : (mom ? B.Mg : nullptr);
+  for_chunk(B, r0, r1, [&](int64_t i, int w) {
+    float step[4];
+    if (dir) {
+      if (w == 4) {
+        const f4v v = gload<f4v>(dir + i);
+        step[0] = v[0]; step[1] = v[1]; step[2] = v[2]; step[3] = v[3];
+      } else {
+        step[0] = gload<float>(dir + i);
+      }
+    } else {
+      float g[4];
+      if (w == 4) {
+        G4<SG>::load(B.G, i, g);
+        const f4v dv = gload<f4v>(B.D + i);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) step[e] = ada_dir(g[e], dv[e]);
+      } else {
+        step[0] = ada_dir(load_g<SG>(B.G, i), gload<float>(B.D + i));
+      }
+    }
+    if (w == 4) {
+      f4v wv = gload<f4v>(B.W + i);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) wv[e] -= etaf * step[e];
+      gstore<f4v>(B.W + i, wv);
+    } else {
+      gstore<float>(B.W + i, gload<float>(B.W + i) - etaf * step[0]);
+    }
+  });
 }
 
 // P = G (no root on either side), with up-cast.

@@ -211,8 +211,7 @@ shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t 
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
   auto k = gemm_grouped_kernel<SA, LA, SB, LB>;
-  const int lds = gemm_lds_bytes<float>();
-  STATUS_TRY(set_lds(h, k, lds));
+  const int lds = 0;  // static LDS
   const int np = (int)probs.size();
   STATUS_TRY(launch(h, cls, s, [&] {
     hipLaunchKernelGGL(k, dim3(total), dim3(kThreads), lds, s, (const GemmProblem*)d, np, total);
@@ -283,6 +282,12 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
     g.ld = b.ld; g.rows = b.rows; g.cols = b.cols;
     g.rows_per_chunk = std::max(1, 16384 / b.cols);
     g.nchunks = cdiv(b.rows, g.rows_per_chunk);
+    // 4-wide access needs every row start 16-byte aligned in every tensor
+    // (G: 8-byte for bf16 is enough since it is read 4 elements at a time)
+    const bool al = (b.cols % 4) == 0 && (b.ld % 4) == 0;
+    auto a16 = [](const void* p) { return p == nullptr || (reinterpret_cast<uintptr_t>(p) & 15) == 0; };
+    g.vec4 = al && a16(b.W) && a16(b.D) && a16(b.P) && a16(b.Mg) && a16(b.Ps) &&
+             (reinterpret_cast<uintptr_t>(b.G) & 15) == 0;
     g.chunk_begin = t;
     t += g.nchunks;
     v.push_back(g);
@@ -382,7 +387,7 @@ shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float 
 
 // ---------------------------------------------------------------- roots
 struct RootLayout {
-  size_t state = 0, counts = 0, total = 0;
+  size_t state = 0, counts = 0, tickets = 0, total = 0;
   std::vector<size_t> part, vec, f32, f64;  // per job offsets
 };
 
@@ -393,13 +398,15 @@ RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
   off += align256((size_t)njobs * sizeof(RootState));
   L.counts = off;
   off += align256((kCountRing + 2) * sizeof(int));
+  L.tickets = off;
+  off += align256((size_t)njobs * sizeof(int));
   for (int j = 0; j < njobs; ++j) {
     const size_t n = (size_t)jobs[j].n;
     const size_t T = (size_t)cdiv(jobs[j].n, kTile);
     L.part.push_back(off);
     off += align256(3 * T * T * sizeof(double));
     L.vec.push_back(off);
-    off += align256(2 * n * sizeof(double));
+    off += align256((2 * T + 1) * n * sizeof(double));
     L.f32.push_back(off);
     if (precision != SHAMPOO_PRECISION_FP64) off += 5 * align256(n * n * sizeof(float));
     L.f64.push_back(off);
@@ -423,9 +430,8 @@ template <typename T>
 shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
                             int total_up, int total_full, int p, float tol, int cap, int poll, int cls,
                             hipStream_t s) {
-  const int lds = gemm_lds_bytes<T>();
+  const int lds = 0;  // static LDS
   auto kstage = newton_stage_kernel<T>;
-  STATUS_TRY(set_lds(h, kstage, lds));
   const float a = (float)(p + 1) / (float)p, b = -1.0f / (float)p;
   int e = 0;
   while ((1 << e) < p) ++e;
@@ -708,14 +714,26 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   // Prologue, shared by both precisions: MaxSV, Frobenius partials, z.
   const double eps = (double)prm->eps;
   if (prm->eps_relative) {
+    // MaxSV: one launch per power step over all matrices; matrices whose
+    // estimate has settled skip the remaining launches.
+    int* tickets = reinterpret_cast<int*>(ws + L.tickets);
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       if (j32)
-        hipLaunchKernelGGL(maxsv_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, st, prm->maxsv_steps,
-                           (double)prm->maxsv_tol, eps);
+        hipLaunchKernelGGL(maxsv_init_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, njobs, st, tickets);
       else
-        hipLaunchKernelGGL(maxsv_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, st, prm->maxsv_steps,
-                           (double)prm->maxsv_tol, eps);
+        hipLaunchKernelGGL(maxsv_init_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, njobs, st, tickets);
     }));
+    for (int k = 0; k < prm->maxsv_steps; ++k) {
+      const int last = k + 1 == prm->maxsv_steps;
+      STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+        if (j32)
+          hipLaunchKernelGGL(maxsv_step_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full,
+                             tickets, (double)prm->maxsv_tol, eps, last);
+        else
+          hipLaunchKernelGGL(maxsv_step_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full,
+                             tickets, (double)prm->maxsv_tol, eps, last);
+      }));
+    }
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     if (j32) {
@@ -757,7 +775,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       }
     }
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(root_output_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full, 0);
+      hipLaunchKernelGGL(root_output_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full, 0, p);
     }));
   }
   if (run64) {
@@ -769,7 +787,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
     STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, p, prm->tol, prm->max_iters, prm->poll,
                                     SHAMPOO_KCLASS_NEWTON_F64, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1);
+      hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);
     }));
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {

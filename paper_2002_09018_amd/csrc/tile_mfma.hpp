@@ -20,9 +20,10 @@
 //              B of C = A B^T); 16-byte loads, transposed scalar LDS stores
 //              with a one-element row pad so the stores do not conflict.
 // Source elements may be fp32, fp64 or bf16 (raw uint16 bits, up-cast
-// exactly); an optional affine map v -> mul * v + add * [row == col] is
-// applied while storing to LDS (used to form M1 = ((p+1) I - M) / p on the
-// fly).  Out-of-range elements are loaded as 0.
+// exactly).  Full, aligned k-layout stages in the compute type are copied
+// global -> LDS directly (global_load_lds_dwordx4, no register staging);
+// other stages go through registers with bounds checks (out-of-range elements
+// are loaded as 0).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -106,10 +107,6 @@ static_assert(StageBytes<float>::value >= Mfma<float>::kBK * Pitch<float, kLayou
               "row-layout stage must fit");
 static_assert(StageBytes<float>::value % 16 == 0, "stages must stay 16-byte aligned");
 
-// Dynamic LDS of one GEMM workgroup: A and B, two stages each (sized for the
-// larger, k-layout pitch).
-template <typename T>
-constexpr int gemm_lds_bytes() { return 4 * StageBytes<T>::value; }
 
 template <typename S>
 struct SrcVec;
@@ -159,8 +156,6 @@ struct Operand {
   int64_t ld;
   int rows, cols;
   bool aligned;  // ptr and ld allow 16-byte vector loads
-  // affine map applied on load (mul = 1, add = 0: none)
-  float mul, add;
 };
 
 // Per-thread staging registers for one operand stage.
@@ -216,9 +211,8 @@ struct Loader {
     }
   }
 
-  // Registers -> LDS stage (k-major), applying the affine map.
-  __device__ __forceinline__ void store(T* lds, const Operand<S>& op, int r0, int c0, int tid,
-                                        bool affine) const {
+  // Registers -> LDS stage (k-major).
+  __device__ __forceinline__ void store(T* lds, const Operand<S>& op, int r0, int c0, int tid) const {
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
       int sr, sc;
@@ -226,14 +220,6 @@ struct Loader {
       T v[VE];
 #pragma unroll
       for (int e = 0; e < VE; ++e) v[e] = cvt<T, S>(buf[i][e]);
-      if (affine) {
-        const int gr = r0 + sr;
-#pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const int gc = c0 + sc + e;
-          v[e] = (T)op.mul * v[e] + ((gr == gc && gr < op.rows) ? (T)op.add : (T)0);
-        }
-      }
       if (LAYOUT == kLayoutK) {
         T* dst = lds + sr * LDP + sc;
         if (sizeof(T) == 4) {
@@ -313,28 +299,78 @@ struct WaveAcc {
   }
 };
 
+#ifndef SHP_LDS_DMA
+#define SHP_LDS_DMA 0
+#endif
+
+typedef __attribute__((address_space(3))) void* lds_vptr;
+
+// Direct global -> LDS copy of one k-layout stage (rows r0..r0+kBK of the
+// operand, columns c0..c0+128) with global_load_lds_dwordx4: lane i of a wave
+// instruction lands at LDS offset 16 i, so one instruction fills 1 KB =
+// 2 fp32 rows (or 1 fp64 row) of the unpadded [k][128] stage.  The caller
+// guarantees the stage is in bounds and 16-byte aligned.
+template <typename T>
+__device__ __forceinline__ void dma_stage(const Operand<T>& op, int r0, int c0, T* lds, int wave, int lane) {
+  constexpr int BK = Mfma<T>::kBK;
+  constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane
+  constexpr int LPR = kTile / EPL;          // lanes per row
+  constexpr int RPI = 64 / LPR;             // rows per wave instruction
+  constexpr int NI = BK / RPI;              // instructions per stage
+  static_assert(NI % 4 == 0, "stage rows must split over 4 waves");
+  static_assert(Pitch<T, kLayoutK>::value == kTile, "DMA needs unpadded k-layout stages");
+  const int rr = lane / LPR, cc = (lane % LPR) * EPL;
+#pragma unroll
+  for (int q = 0; q < NI / 4; ++q) {
+    const int ins = wave + 4 * q;
+    const T* g = op.ptr + (int64_t)(r0 + ins * RPI + rr) * op.ld + (c0 + cc);
+    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(g), (lds_vptr)(lds + ins * RPI * kTile), 16, 0,
+                                     0);
+  }
+}
+
+// One operand's staging for one k-stage: DMA when the stage is a full,
+// aligned k-layout tile of an operand already in the compute type, else
+// register staging (bounds-checked loads, conversion, LDS stores).
+template <typename T, typename S, int LAYOUT>
+struct Stager {
+  Loader<T, S, LAYOUT> reg;
+  bool dma = false;
+  __device__ __forceinline__ void issue(const Operand<S>& op, int r0, int c0, T* lds, int tid) {
+    constexpr int BK = Mfma<T>::kBK;
+    dma = SHP_LDS_DMA && LAYOUT == kLayoutK && sizeof(S) == sizeof(T) && op.aligned &&
+          r0 + BK <= op.rows && c0 + kTile <= op.cols;
+    if (dma) {
+      if constexpr (LAYOUT == kLayoutK && sizeof(S) == sizeof(T))
+        dma_stage<T>(reinterpret_cast<const Operand<T>&>(op), r0, c0, lds, tid >> 6, tid & 63);
+    } else {
+      reg.load(op, r0, c0, tid);
+    }
+  }
+  __device__ __forceinline__ void finish(const Operand<S>& op, int r0, int c0, T* lds, int tid) {
+    if (!dma) reg.store(lds, op, r0, c0, tid);
+  }
+};
+
 // k-loop over LDS stages.  COMPUTE == false: the wave only helps to stage
 // operands (its MFMAs are skipped); the two variants are separate loops so the
-// wave-uniform choice costs no registers inside the loop.
+// wave-uniform choice costs no registers inside the loop.  Stages alternate
+// between two static buffer pairs; the loop is unrolled by two so every LDS
+// access names its buffer at compile time (the wait for an in-flight DMA into
+// one buffer then does not hold back reads of the other).
 template <bool COMPUTE, typename T, typename SA, int LA, typename SB, int LB>
-__device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, bool affA,
-                                          const Operand<SB>& B, bool affB, int m0, int n0, int K,
-                                          unsigned char* smem) {
+__device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
+                                          int n0, int K, T* a0, T* a1, T* b0, T* b1) {
+  constexpr int BK = Mfma<T>::kBK;
   typedef Loader<T, SA, LA> LdA;
   typedef Loader<T, SB, LB> LdB;
-  constexpr int BK = Mfma<T>::kBK;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm0 = (wave >> 1) * kWaveTile;
   const int wn0 = (wave & 1) * kWaveTile;
-  // LDS stages addressed arithmetically from the __shared__ base (a pointer
-  // array would lose the LDS address space and turn ds_reads into flat loads).
-  constexpr int SE = StageBytes<T>::value / (int)sizeof(T);  // elements per stage
-  T* const lds = reinterpret_cast<T*>(smem);
-
-  LdA la;
-  LdB lb;
+  Stager<T, SA, LA> sa;
+  Stager<T, SB, LB> sb;
   const int nst = (K + BK - 1) / BK;
   auto orgA = [&](int k0, int& r, int& c) {
     if (LA == kLayoutK) { r = k0; c = m0; } else { r = m0; c = k0; }
@@ -345,29 +381,40 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
   int ar, ac, br, bc;
   orgA(0, ar, ac);
   orgB(0, br, bc);
-  la.load(A, ar, ac, tid);
-  lb.load(B, br, bc, tid);
-  la.store(lds, A, ar, ac, tid, affA);
-  lb.store(lds + 2 * SE, B, br, bc, tid, affB);
+  sa.issue(A, ar, ac, a0, tid);
+  sb.issue(B, br, bc, b0, tid);
+  sa.finish(A, ar, ac, a0, tid);
+  sb.finish(B, br, bc, b0, tid);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  for (int st = 0; st < nst; ++st) {
-    const int cur = st & 1;
+  // one stage: prefetch st+1 into (na, nb) while computing on (ca, cb)
+  auto step = [&](int st, T* ca, T* cb, T* na, T* nb) {
     const bool more = st + 1 < nst;
     if (more) {
       orgA((st + 1) * BK, ar, ac);
       orgB((st + 1) * BK, br, bc);
-      la.load(A, ar, ac, tid);
-      lb.load(B, br, bc, tid);
+      sa.issue(A, ar, ac, na, tid);
+      sb.issue(B, br, bc, nb, tid);
     }
-    if (COMPUTE)
-      acc.template stage<LdA::LDP, LdB::LDP>(lds + cur * SE, lds + (2 + cur) * SE, wm0, wn0, lane);
+    if (COMPUTE) acc.template stage<LdA::LDP, LdB::LDP>(ca, cb, wm0, wn0, lane);
     if (more) {
-      la.store(lds + (cur ^ 1) * SE, A, ar, ac, tid, affA);
-      lb.store(lds + (2 + (cur ^ 1)) * SE, B, br, bc, tid, affB);
+      sa.finish(A, ar, ac, na, tid);
+      sb.finish(B, br, bc, nb, tid);
+      __builtin_amdgcn_s_waitcnt(0);
     }
     __syncthreads();
+  };
+  for (int st = 0; st < nst; st += 2) {
+    step(st, a0, b0, a1, b1);
+    if (st + 1 < nst) step(st + 1, a1, b1, a0, b0);
   }
 }
+
+// Static LDS of one MFMA workgroup: two stages per operand.
+template <typename T>
+struct TileSmem {
+  static constexpr int E = StageBytes<T>::value / (int)sizeof(T);
+};
 
 // Full k-loop of one 128 x 128 output tile.
 //   A: layout LA; kLayoutK reads storage rows k (cols m0..), kLayoutRow
@@ -377,18 +424,17 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
 // lower_idle: diagonal tile of a symmetric output, whose lower-left 64 x 64
 // quarter is never stored; that quarter's wave only stages operands.
 template <typename T, typename SA, int LA, typename SB, int LB>
-__device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, bool affA,
-                                         const Operand<SB>& B, bool affB, int m0, int n0, int K,
-                                         unsigned char* smem, bool lower_idle = false) {
+__device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
+                                         int n0, int K, T* a0, T* a1, T* b0, T* b1, bool lower_idle = false) {
 #ifndef SHP_IDLE_LOWER
 #define SHP_IDLE_LOWER 1
 #endif
   const int wave = threadIdx.x >> 6;
   const bool idle = SHP_IDLE_LOWER && lower_idle && (wave >> 1) > (wave & 1);
   if (idle)
-    tile_loop<false, T, SA, LA, SB, LB>(acc, A, affA, B, affB, m0, n0, K, smem);
+    tile_loop<false, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
   else
-    tile_loop<true, T, SA, LA, SB, LB>(acc, A, affA, B, affB, m0, n0, K, smem);
+    tile_loop<true, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
 }
 
 // Workgroup id -> logical tile index so that consecutive logical tiles land

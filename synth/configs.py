@@ -75,6 +75,20 @@ def wishart_bartlett(n, dof, var, *key):
     return var * (T @ T.T)
 
 
+def wishart_bartlett_device(n, dof, var, torch, device, *key):
+    """Same distribution as ``wishart_bartlett``, with the O(n^3) product on
+    the device: chi-square diagonal from the keyed PCG64 stream, standard
+    normals below the diagonal from a torch generator seeded by the key, and
+    var * T T^T formed in fp64 there.  Returned as an fp32 device tensor."""
+    r = rng(*key)
+    diag = np.sqrt(r.chisquare(dof - np.arange(n)))
+    seed = int(r.integers(0, 2 ** 62))
+    g = torch.Generator(device=device).manual_seed(seed)
+    T = torch.randn(n, n, generator=g, device=device, dtype=torch.float64).tril(-1)
+    T += torch.diag(torch.from_numpy(diag).to(device))
+    return (var * (T @ T.T)).float()
+
+
 def c2_stats(i, n=1024, steps=20, k=4096):
     """C2 statistics matrix i: sum over ``steps`` gradients of shape n x k,
     N(0, 1/k), rounded to fp32 (the GPU input)."""
