@@ -49,8 +49,8 @@ __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int n
 template <typename SA, int LA, typename SB, int LB>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
                                                                int nprob, int total_tiles) {
-  __shared__ __attribute__((aligned(16))) float sa0[TileSmem<float>::E], sa1[TileSmem<float>::E];
-  __shared__ __attribute__((aligned(16))) float sb0[TileSmem<float>::E], sb1[TileSmem<float>::E];
+  __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
+  __shared__ __attribute__((aligned(16))) float sb0[StageElems<float, LB>::value], sb1[StageElems<float, LB>::value];
   const int t = xcd_remap(blockIdx.x, gridDim.x);
   if (t >= total_tiles) return;
   const GemmProblem P = probs[find_problem_gemm(probs, nprob, t)];
@@ -190,12 +190,12 @@ __device__ __forceinline__ int find_job_full(const NewtonJob<T>* jobs, int njobs
 enum : int { kFirst = 0, kFirstP1 = 1, kSquare = 2, kLast = 3 };
 
 template <typename T>
-__global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
+__global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
                                                                int njobs, RootState* __restrict__ st,
                                                                int total_up, int kind, int src, int dst,
                                                                float a, float b, int skip_x) {
-  __shared__ __attribute__((aligned(16))) T sa0[TileSmem<T>::E], sa1[TileSmem<T>::E];
-  __shared__ __attribute__((aligned(16))) T sb0[TileSmem<T>::E], sb1[TileSmem<T>::E];
+  __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutK>::value], sa1[StageElems<T, kLayoutK>::value];
+  __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
   // skip_x: first iteration, X' = X0 M1 = z^(1/p) M1 was written by the init
   // kernel, so only the M-side product runs.
   const bool first = kind == kFirst || kind == kFirstP1;
@@ -281,9 +281,15 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void newton_stage_kernel(const
           const int c = wn0 + jj * F::kM + F::col(lane);
           typedef float f4 __attribute__((ext_vector_type(4)));
           f4 w;
+          // E is exactly symmetric (iterates are stored mirrored), so the
+          // four E values of rows r..r+3, column c are one 16-byte load of
+          // row c: E[c][r..r+3].
+          f4 e4 = {0.f, 0.f, 0.f, 0.f};
+          if (pe) e4 = gload<f4>(reinterpret_cast<const float*>(pe) + (int64_t)c * n + r);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            const T x = fin(acc.c[i][jj][4 * g + q], r + q, c);
+            T x = ca * acc.c[i][jj][4 * g + q] + cb * (T)e4[q];
+            if (r + q == c) x += cg;
             w[q] = (float)x;
             gstore<T>(pc + (int64_t)(r + q) * n + c, x);
             track(x, r + q, c);

@@ -8,17 +8,20 @@
 // of kBK (fp32: 32, fp64: 16), double-buffered: the global loads of stage s+1
 // are in flight in registers while the MFMAs of stage s run.
 //
-// LDS holds every operand stage k-major, lds[k][i] with i the output row (A)
-// or column (B) index, so the fragment read of a lane is a single
-// conflict-free 4/8-byte access.  Two global layouts feed it:
+// Each operand stage is copied into LDS in its global orientation, with
+// 16-byte loads and 16-byte LDS stores (no transpose):
 //   kLayoutK   the stage is read from storage rows k0..k0+kBK, columns
 //              i0..i0+128 (the operand's contraction index is its storage row:
 //              B of C = A B, or A of C = A^T B, or any symmetric operand);
-//              16-byte vector loads and stores, no transpose.
+//              LDS [k][i], unpadded.
 //   kLayoutRow the stage is read from storage rows i0..i0+128, columns
 //              k0..k0+kBK (contraction index contiguous: A of C = A B,
-//              B of C = A B^T); 16-byte loads, transposed scalar LDS stores
-//              with a one-element row pad so the stores do not conflict.
+//              B of C = A B^T); LDS [i][k] with a 16-byte row pad.
+// Within a stage, lane group g (lanes with the same lane / kM) takes the
+// contraction indices g*KS .. g*KS+KS-1 over the KS MFMA k-steps (a
+// permutation of k shared by both operands, so the sum is unchanged).  A
+// kLayoutRow fragment of a lane is then KS consecutive elements, read with
+// 16-byte LDS loads; a kLayoutK fragment is one element per k-step.
 // Source elements may be fp32, fp64 or bf16 (raw uint16 bits, up-cast
 // exactly).  Full, aligned k-layout stages in the compute type are copied
 // global -> LDS directly (global_load_lds_dwordx4, no register staging);
@@ -34,9 +37,22 @@ namespace shp {
 #ifndef SHP_MIN_WAVES
 #define SHP_MIN_WAVES 2
 #endif
-// Minimum waves per SIMD requested from the register allocator for the MFMA
-// kernels (__launch_bounds__ second argument).
+#ifndef SHP_MIN_WAVES_F64
+#define SHP_MIN_WAVES_F64 2
+#endif
+#ifndef SHP_MIN_WAVES_NEWTON_F32
+#define SHP_MIN_WAVES_NEWTON_F32 4
+#endif
+// Minimum waves per SIMD requested from the register allocator
+// (__launch_bounds__ second argument).  Measured per kernel: the grouped
+// GEMMs run best at 2 (the allocator then reaches 3-4 waves without
+// spilling), the fp32 Newton products at 4 (a few epilogue spills, +3%),
+// fp64 at 2.
 constexpr int kMinWaves = SHP_MIN_WAVES;
+template <typename T>
+struct MinWaves {
+  static constexpr int value = sizeof(T) == 8 ? SHP_MIN_WAVES_F64 : SHP_MIN_WAVES_NEWTON_F32;
+};
 
 constexpr int kTile = 128;
 constexpr int kThreads = 256;
@@ -85,27 +101,22 @@ struct Mfma<double> {
   static __device__ __forceinline__ int col(int lane) { return lane & 15; }
 };
 
-// Row pitch (elements) of one k-major LDS stage.  kLayoutK rows are written
-// and read as contiguous runs (no pad needed: measured conflict-free);
-// kLayoutRow pads by one element so its transposed scalar stores spread over
-// all banks.
+// Row pitch (elements) of one LDS stage.  kLayoutK: [k][128] rows read as
+// contiguous runs (no pad needed: measured conflict-free).  kLayoutRow:
+// [128][kBK] rows padded by 16 bytes, so the 16-byte fragment reads of 8
+// consecutive rows fall in distinct banks and every row stays 16-byte aligned.
 template <typename T, int LAYOUT>
 struct Pitch {
   static constexpr int value =
-      LAYOUT == kLayoutK ? kTile + SHP_PADK_WORDS * 4 / (int)sizeof(T) : kTile + 1;
+      LAYOUT == kLayoutK ? kTile + SHP_PADK_WORDS * 4 / (int)sizeof(T) : Mfma<T>::kBK + 16 / (int)sizeof(T);
 };
 
-// Bytes of one operand stage: sized for the larger of the two layouts' pitch
-// (the row layout pads one element per k-row, which exceeds an unpadded
-// k-layout stage).
-template <typename T>
-struct StageBytes {
-  static constexpr int pk = Pitch<T, kLayoutK>::value, pr = Pitch<T, kLayoutRow>::value;
-  static constexpr int value = Mfma<T>::kBK * (pk > pr ? pk : pr) * (int)sizeof(T);
+// Elements of one operand stage in LDS.
+template <typename T, int LAYOUT>
+struct StageElems {
+  static constexpr int value = (LAYOUT == kLayoutK ? Mfma<T>::kBK : kTile) * Pitch<T, LAYOUT>::value;
+  static_assert(value * (int)sizeof(T) % 16 == 0, "stages must stay 16-byte aligned");
 };
-static_assert(StageBytes<float>::value >= Mfma<float>::kBK * Pitch<float, kLayoutRow>::value * 4,
-              "row-layout stage must fit");
-static_assert(StageBytes<float>::value % 16 == 0, "stages must stay 16-byte aligned");
 
 
 template <typename S>
@@ -220,7 +231,7 @@ struct Loader {
       T v[VE];
 #pragma unroll
       for (int e = 0; e < VE; ++e) v[e] = cvt<T, S>(buf[i][e]);
-      if (LAYOUT == kLayoutK) {
+      {
         T* dst = lds + sr * LDP + sc;
         if (sizeof(T) == 4) {
           typedef float f4 __attribute__((ext_vector_type(4)));
@@ -237,9 +248,6 @@ struct Loader {
             *reinterpret_cast<d2*>(reinterpret_cast<double*>(dst) + e) = w;
           }
         }
-      } else {
-#pragma unroll
-        for (int e = 0; e < VE; ++e) lds[(sc + e) * LDP + sr] = v[e];
       }
     }
   }
@@ -261,31 +269,62 @@ struct WaveAcc {
   }
 
   // One LDS stage: kBK / kK MFMA k-steps over the wave's NB x NB blocks.
-  template <int LDPA, int LDPB>
+  template <int LA, int LB, int LDPA, int LDPB>
   __device__ __forceinline__ void stage(const T* __restrict__ a, const T* __restrict__ b, int wm0,
                                         int wn0, int lane) {
-    constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;
-    const int kl = lane / Mfma<T>::kM;
+    constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;  // k-steps per stage
+    constexpr int VP = 16 / (int)sizeof(T);         // elements per 16-byte LDS read
+    static_assert(KS % VP == 0, "row fragments are read 16 bytes at a time");
+    typedef T vec_t __attribute__((ext_vector_type(VP)));
+    const int g = lane / Mfma<T>::kM;  // this lane's k group: k = g * KS + s at k-step s
     const int ml = lane % Mfma<T>::kM;
-    // Fragments are double-buffered in registers: the LDS reads of k-step
-    // s+1 are issued before the MFMAs of k-step s, so their latency overlaps
-    // the matrix-core work instead of stalling it.
+    // kLayoutRow fragments: all KS values of the stage, 16 bytes at a time.
+    T ra[LA == kLayoutRow ? NB : 1][KS], rb[LB == kLayoutRow ? NB : 1][KS];
+    if (LA == kLayoutRow) {
+#pragma unroll
+      for (int i = 0; i < NB; ++i)
+#pragma unroll
+        for (int c = 0; c < KS / VP; ++c) {
+          const vec_t v = *reinterpret_cast<const vec_t*>(a + (wm0 + i * Mfma<T>::kM + ml) * LDPA + g * KS + c * VP);
+#pragma unroll
+          for (int e = 0; e < VP; ++e) ra[i][c * VP + e] = v[e];
+        }
+    }
+    if (LB == kLayoutRow) {
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int c = 0; c < KS / VP; ++c) {
+          const vec_t v = *reinterpret_cast<const vec_t*>(b + (wn0 + j * Mfma<T>::kM + ml) * LDPB + g * KS + c * VP);
+#pragma unroll
+          for (int e = 0; e < VP; ++e) rb[j][c * VP + e] = v[e];
+        }
+    }
+    // kLayoutK fragments: one element per k-step, double-buffered in
+    // registers so the reads of step s+1 are issued before the MFMAs of s.
     T fa[2][NB], fb[2][NB];
-    const T* pa = a + kl * LDPA + wm0 + ml;
-    const T* pb = b + kl * LDPB + wn0 + ml;
+    const T* pa = a + g * KS * LDPA + wm0 + ml;
+    const T* pb = b + g * KS * LDPB + wn0 + ml;
+    if (LA == kLayoutK) {
 #pragma unroll
-    for (int i = 0; i < NB; ++i) fa[0][i] = pa[i * Mfma<T>::kM];
+      for (int i = 0; i < NB; ++i) fa[0][i] = pa[i * Mfma<T>::kM];
+    }
+    if (LB == kLayoutK) {
 #pragma unroll
-    for (int j = 0; j < NB; ++j) fb[0][j] = pb[j * Mfma<T>::kM];
+      for (int j = 0; j < NB; ++j) fb[0][j] = pb[j * Mfma<T>::kM];
+    }
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
       const int cur = s & 1;
       if (s + 1 < KS) {
-        const int off = (s + 1) * Mfma<T>::kK;
+        if (LA == kLayoutK) {
 #pragma unroll
-        for (int i = 0; i < NB; ++i) fa[cur ^ 1][i] = pa[off * LDPA + i * Mfma<T>::kM];
+          for (int i = 0; i < NB; ++i) fa[cur ^ 1][i] = pa[(s + 1) * LDPA + i * Mfma<T>::kM];
+        }
+        if (LB == kLayoutK) {
 #pragma unroll
-        for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[off * LDPB + j * Mfma<T>::kM];
+          for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[(s + 1) * LDPB + j * Mfma<T>::kM];
+        }
       }
       // Keep the reads of s+1 ahead of the MFMAs of s (the scheduler would
       // otherwise sink them below to save registers).
@@ -293,7 +332,9 @@ struct WaveAcc {
 #pragma unroll
       for (int i = 0; i < NB; ++i)
 #pragma unroll
-        for (int j = 0; j < NB; ++j) c[i][j] = Mfma<T>::mma(fa[cur][i], fb[cur][j], c[i][j]);
+        for (int j = 0; j < NB; ++j)
+          c[i][j] = Mfma<T>::mma(LA == kLayoutRow ? ra[i][s] : fa[cur][i], LB == kLayoutRow ? rb[j][s] : fb[cur][j],
+                                 c[i][j]);
       __builtin_amdgcn_sched_barrier(0);
     }
   }
@@ -396,7 +437,7 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
       sa.issue(A, ar, ac, na, tid);
       sb.issue(B, br, bc, nb, tid);
     }
-    if (COMPUTE) acc.template stage<LdA::LDP, LdB::LDP>(ca, cb, wm0, wn0, lane);
+    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP>(ca, cb, wm0, wn0, lane);
     if (more) {
       sa.finish(A, ar, ac, na, tid);
       sb.finish(B, br, bc, nb, tid);
@@ -404,17 +445,21 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
     }
     __syncthreads();
   };
+#if SHP_LDS_DMA
   for (int st = 0; st < nst; st += 2) {
     step(st, a0, b0, a1, b1);
     if (st + 1 < nst) step(st + 1, a1, b1, a0, b0);
   }
+#else
+  // register staging only: a select between the two static buffers keeps the
+  // LDS address space and avoids the larger two-way unrolled body
+  for (int st = 0; st < nst; ++st) {
+    const bool odd = st & 1;
+    step(st, odd ? a1 : a0, odd ? b1 : b0, odd ? a0 : a1, odd ? b0 : b1);
+  }
+#endif
 }
 
-// Static LDS of one MFMA workgroup: two stages per operand.
-template <typename T>
-struct TileSmem {
-  static constexpr int E = StageBytes<T>::value / (int)sizeof(T);
-};
 
 // Full k-loop of one 128 x 128 output tile.
 //   A: layout LA; kLayoutK reads storage rows k (cols m0..), kLayoutRow
