@@ -39,7 +39,7 @@ extern "C" {
 typedef enum shampoo_status {
   SHAMPOO_OK = 0,
   SHAMPOO_EINVAL = -1,       /* bad argument: NULL where required, size out of range, ... */
-  SHAMPOO_EUNSUPPORTED = -2, /* valid but not implemented (e.g. p not in {1,2,4,8}) */
+  SHAMPOO_EUNSUPPORTED = -2, /* valid but not implemented (e.g. root order p outside [1, 16]) */
   SHAMPOO_EHIP = -3,         /* a HIP runtime call or kernel launch failed */
   SHAMPOO_ENOMEM = -4        /* workspace too small, or a library allocation failed */
 } shampoo_status;
@@ -108,7 +108,7 @@ typedef struct shampoo_root_job {
 /* Parameters of a root call (Algorithm 1).  shampoo_root_params_default()
  * fills the values used throughout the repository. */
 typedef struct shampoo_root_params {
-  int32_t p;            /* root order: X = A^(-1/p); one of 1, 2, 4, 8 */
+  int32_t p;            /* root order: X = A^(-1/p); 1 <= p <= 16 */
   float eps;            /* damping: eps_eff = eps, or eps * lambda_max when eps_relative */
   int32_t eps_relative; /* 1: scaled damping with lambda_max from MaxSV power iteration */
   float tol;            /* stop when max_ij |M - I|_ij <= tol */
@@ -175,13 +175,15 @@ size_t shampoo_inv_root_workspace_bytes(const shampoo_root_job* jobs, int njobs,
  *   X = z^(1/p) I;  M = z A_d;
  *   while max|M - I| > tol:  M1 = ((p + 1) I - M) / p;  X = X M1;  M = M1^p M.
  * Each matrix leaves the iteration on its own (CONVERGED, STAGNATED, MAXITER,
- * DIVERGED).  Products of the commuting symmetric iterates are computed on
- * their upper triangle and mirrored.  `workspace` is device memory of at least
+ * DIVERGED).  M1^p M is formed by binary powering over the bits of p
+ * (floor(log2 p) squarings plus popcount(p) products, launched in
+ * floor(log2 p) + 1 stages per iteration).  Products of the commuting
+ * symmetric iterates are computed on their upper triangle and mirrored.  `workspace` is device memory of at least
  * shampoo_inv_root_workspace_bytes(jobs, njobs, params->precision) bytes,
  * owned by the caller and used exclusively by this call until the stream
  * reaches its end.  `info` is a device array of njobs entries.
  * Errors: EINVAL (NULL pointers, n outside [1, 4096], eps < 0, tol < 0,
- * max_iters < 1), EUNSUPPORTED (p not in {1,2,4,8}), ENOMEM (ws_bytes too small).
+ * max_iters < 1), EUNSUPPORTED (p outside [1, 16]), ENOMEM (ws_bytes too small).
  */
 shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jobs, int njobs,
                                         const shampoo_root_params* params, void* workspace,

@@ -178,35 +178,56 @@ __device__ __forceinline__ int find_job_full(const NewtonJob<T>* jobs, int njobs
   return lo;
 }
 
-// Stage kinds of one Newton iteration (p = 2^e), with M1 = a I + b M
-// (a = (p+1)/p, b = -1/p) never stored: its products are expanded into a
-// plain product and an affine epilogue C = alpha acc + beta E + gamma I,
-//   kFirst  : X' = X M1 = b (X M) + a X           and
-//             S[dst] = M1 M1 = b^2 (M M) + 2ab M + a^2 I   (two products per tile)
-//   kFirstP1: X' = X M1  and  M' = M1 M = b (M M) + a M  (+residual) (p = 1)
-//   kSquare : S[dst] = S[src] S[src]
-//   kLast   : M' = S[src] M                        (+residual)
-// X, M are the buffers of the current parity and X', M' those of the other.
-enum : int { kFirst = 0, kFirstP1 = 1, kSquare = 2, kLast = 3 };
+// One launch of a Newton iteration runs up to three independent products
+// over all upper tiles of every active matrix.  Each product is
+//   C[dst] = ca (B[a] B[b]) + cb B[e] + cg I      (+ max|C - I| when resid)
+// over the six iterate buffers of a matrix, named by id:
+//   0 X (current), 1 X (next), 2 M (current), 3 M (next), 4 S0, 5 S1.
+// M1 = a I + b M (a = (p+1)/p, b = -1/p) is never stored: products with it
+// are expanded into a plain product of stored buffers and the affine terms
+// (X M1 = b X M + a X, M1 M = b M M + a M, M1 M1 = b^2 M M + 2ab M + a^2 I).
+// Every factor is a polynomial in the same symmetric A, so every product is
+// symmetric and only upper tiles are computed.
+enum : int { kBufXc = 0, kBufXn = 1, kBufMc = 2, kBufMn = 3, kBufS0 = 4, kBufS1 = 5, kBufNone = -1 };
+
+struct NewtonProd {
+  int a, b, e, dst;  // buffer ids (e = kBufNone: no affine E term)
+  int resid, pad;
+  double ca, cb, cg;
+};
+
+struct NewtonStage {
+  int nprod, pad;
+  NewtonProd q[3];
+};
+
+template <typename V>
+__device__ __forceinline__ V pick3(int i, V x0, V x1, V x2) {
+  return i == 0 ? x0 : (i == 1 ? x1 : x2);
+}
+
+template <typename T>
+__device__ __forceinline__ T* newton_buf(const NewtonJob<T>* J, int par, int id) {
+  // the table is read with run-time indices (a local copy of the struct would
+  // be placed in scratch)
+  if (id < 2) return J->X[(id & 1) ^ par];
+  if (id < 4) return J->M[(id & 1) ^ par];
+  return J->S[id & 1];
+}
 
 template <typename T>
 __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
                                                                int njobs, RootState* __restrict__ st,
-                                                               int total_up, int kind, int src, int dst,
-                                                               float a, float b, int skip_x) {
+                                                               int total_up, NewtonStage S) {
   __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutK>::value], sa1[StageElems<T, kLayoutK>::value];
   __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
-  // skip_x: first iteration, X' = X0 M1 = z^(1/p) M1 was written by the init
-  // kernel, so only the M-side product runs.
-  const bool first = kind == kFirst || kind == kFirstP1;
-  const int two = (first && !skip_x) ? 2 : 1;
+  const int np = S.nprod;
   const int l = xcd_remap(blockIdx.x, gridDim.x);
-  if (l >= two * total_up) return;
-  const int t = l / two, prod = (first && skip_x) ? 1 : l % two;
+  if (l >= np * total_up) return;
+  // the products of one tile run in neighbouring workgroups (shared operands)
+  const int t = l / np, prod = l - t * np;
   const int j = find_job_up(jobs, njobs, t);
   if (st[j].status != kActive) return;
-  // Buffer pointers are read from the table with run-time indices (not from a
-  // local copy of the struct, which would be placed in scratch).
   const NewtonJob<T>* J = jobs + j;
   const int par = st[j].parity;
   int ti, tj;
@@ -214,29 +235,18 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
   const int n = J->n;
   const int m0 = ti * kTile, n0 = tj * kTile;
 
-  const T* pa;
-  const T* pb;
-  T* pc;
-  const T* pe = nullptr;  // E of the affine epilogue
-  T ca = (T)1, cb = (T)0, cg = (T)0;  // alpha, beta, gamma
-  bool resid = false;
-  const T ta = (T)a, tb = (T)b;
-  if (kind == kFirst || kind == kFirstP1) {
-    if (prod == 0) {
-      pa = J->X[par]; pb = J->M[par]; pc = J->X[par ^ 1];
-      pe = J->X[par]; ca = tb; cb = ta;
-    } else if (kind == kFirst) {
-      pa = J->M[par]; pb = J->M[par]; pc = J->S[dst];
-      pe = J->M[par]; ca = tb * tb; cb = (T)2 * ta * tb; cg = ta * ta;
-    } else {
-      pa = J->M[par]; pb = J->M[par]; pc = J->M[par ^ 1]; resid = true;
-      pe = J->M[par]; ca = tb; cb = ta;
-    }
-  } else if (kind == kSquare) {
-    pa = J->S[src]; pb = J->S[src]; pc = J->S[dst];
-  } else {
-    pa = J->S[src]; pb = J->M[par]; pc = J->M[par ^ 1]; resid = true;
-  }
+  const int ia = pick3(prod, S.q[0].a, S.q[1].a, S.q[2].a);
+  const int ib = pick3(prod, S.q[0].b, S.q[1].b, S.q[2].b);
+  const int ie = pick3(prod, S.q[0].e, S.q[1].e, S.q[2].e);
+  const int id = pick3(prod, S.q[0].dst, S.q[1].dst, S.q[2].dst);
+  const bool resid = pick3(prod, S.q[0].resid, S.q[1].resid, S.q[2].resid) != 0;
+  const T ca = (T)pick3(prod, S.q[0].ca, S.q[1].ca, S.q[2].ca);  // alpha, beta, gamma
+  const T cb = (T)pick3(prod, S.q[0].cb, S.q[1].cb, S.q[2].cb);
+  const T cg = (T)pick3(prod, S.q[0].cg, S.q[1].cg, S.q[2].cg);
+  const T* pa = newton_buf(J, par, ia);
+  const T* pb = newton_buf(J, par, ib);
+  T* pc = newton_buf(J, par, id);
+  const T* pe = ie >= 0 ? newton_buf(J, par, ie) : nullptr;  // E of the affine epilogue
   const bool al = (reinterpret_cast<uintptr_t>(pa) & 15) == 0 && (reinterpret_cast<uintptr_t>(pb) & 15) == 0 &&
                   ((n * (int)sizeof(T)) & 15) == 0;
   Operand<T> A{pa, n, n, n, al};

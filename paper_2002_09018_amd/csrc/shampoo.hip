@@ -19,6 +19,7 @@ using namespace shp;
 namespace {
 
 constexpr int kMaxDim = 4096;
+constexpr int kMaxRootOrder = 16;  // largest p of X = A^(-1/p)
 constexpr int kCountRing = 64;  // device/pinned slots of per-iteration active counts
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -425,16 +426,124 @@ int host_scalar_iters(double m, int p, double tol, int cap) {
   return k;
 }
 
+// Product program of one coupled Newton iteration for a root order p
+// (Algorithm 1): X' = X M1 and M' = M1^p M.  M1^p M is formed right to left
+// over the bits of p, with P_s = M1^(2^s) and Y_s = M1^(p mod 2^s) M:
+//   stage s: Y <- P_s Y if bit s of p is set;  P_(s+1) = P_s P_s if s < top.
+// Both products of a stage read only P_s and Y, so they share one launch (the
+// X product joins stage 0).  The last Y product writes M' and carries the
+// residual.  Buffers for P and intermediate Y are chosen by a small search so
+// that no product writes a buffer that its own launch reads or that holds a
+// value still needed; X (current) is free from stage 1 on, since the state
+// machine always continues from the new iterate.
+struct NewtonProgram {
+  std::vector<NewtonStage> stages;  // stage 0 includes the X product (q[0])
+};
+
+namespace prog {
+struct Pick {
+  int y, p;
+};
+
+bool search(int p, int s, int top, int pbuf, int ybuf, int rem, std::vector<Pick>& out) {
+  if (s > top) return true;
+  const bool ybit = (p >> s) & 1;
+  std::vector<int> ycand, pcand;
+  if (ybit) {
+    if (rem == 1) ycand = {kBufMn};
+    else ycand = {kBufMn, kBufS1, kBufS0, kBufXc};
+  } else {
+    ycand = {kBufNone};
+  }
+  if (s < top) pcand = {kBufS0, kBufS1, kBufXc};
+  else pcand = {kBufNone};
+  const int pread = pbuf >= 0 ? pbuf : kBufMc;
+  for (int yd : ycand)
+    for (int pd : pcand) {
+      bool ok = true;
+      int written[2] = {kBufNone, kBufNone};
+      int k = 0;
+      for (int d : {yd, pd}) {
+        if (d == kBufNone) continue;
+        if (d == pread || d == ybuf) ok = false;                   // read in this launch / still live
+        if (s == 0 && (d == kBufXc || d == kBufMc || d == kBufXn)) ok = false;  // X product's operands
+        if (d == written[0]) ok = false;
+        written[k++] = d;
+      }
+      if (!ok) continue;
+      out.push_back({yd, pd});
+      if (search(p, s + 1, top, pd != kBufNone ? pd : pbuf, yd != kBufNone ? yd : ybuf, rem - (yd != kBufNone),
+                 out))
+        return true;
+      out.pop_back();
+    }
+  return false;
+}
+}  // namespace prog
+
+NewtonProd make_prod(int a, int b, int e, int dst, double ca, double cb, double cg, int resid) {
+  NewtonProd q{};
+  q.a = a;
+  q.b = b;
+  q.e = e;
+  q.dst = dst;
+  q.resid = resid;
+  q.ca = ca;
+  q.cb = cb;
+  q.cg = cg;
+  return q;
+}
+
+bool build_newton_program(int p, NewtonProgram* out) {
+  if (p < 1) return false;
+  int top = 0;
+  while ((p >> (top + 1)) != 0) ++top;
+  const int c = __builtin_popcount((unsigned)p);
+  std::vector<prog::Pick> picks;
+  if (!prog::search(p, 0, top, kBufNone, kBufMc, c, picks)) return false;
+  const double a = (p + 1.0) / p, b = -1.0 / p;
+  out->stages.clear();
+  int pbuf = kBufNone, ybuf = kBufMc;
+  for (int s = 0; s <= top; ++s) {
+    NewtonStage st{};
+    // X' = X M1 = b (X M) + a X
+    if (s == 0) st.q[st.nprod++] = make_prod(kBufXc, kBufMc, kBufXc, kBufXn, b, a, 0.0, 0);
+    const prog::Pick k = picks[s];
+    if (k.y != kBufNone) {
+      const int resid = k.y == kBufMn && s == top;
+      if (pbuf == kBufNone)  // M1 Y with Y = M: b (M M) + a M
+        st.q[st.nprod++] = make_prod(kBufMc, ybuf, kBufMc, k.y, b, a, 0.0, resid);
+      else
+        st.q[st.nprod++] = make_prod(pbuf, ybuf, kBufNone, k.y, 1.0, 0.0, 0.0, resid);
+    }
+    if (k.p != kBufNone) {
+      if (pbuf == kBufNone)  // M1 M1 = b^2 (M M) + 2ab M + a^2 I
+        st.q[st.nprod++] = make_prod(kBufMc, kBufMc, kBufMc, k.p, b * b, 2.0 * a * b, a * a, 0);
+      else
+        st.q[st.nprod++] = make_prod(pbuf, pbuf, kBufNone, k.p, 1.0, 0.0, 0.0, 0);
+    }
+    if (k.y != kBufNone) ybuf = k.y;
+    if (k.p != kBufNone) pbuf = k.p;
+    out->stages.push_back(st);
+  }
+  return ybuf == kBufMn;
+}
+
+// Stage 0 without its X product (first iteration: X1 is written by the init
+// kernel).
+NewtonStage drop_x(const NewtonStage& s0) {
+  NewtonStage r{};
+  for (int i = 1; i < s0.nprod; ++i) r.q[r.nprod++] = s0.q[i];
+  return r;
+}
+
 // One precision phase of the coupled Newton iteration.
 template <typename T>
 shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
-                            int total_up, int total_full, int p, float tol, int cap, int poll, int cls,
-                            hipStream_t s) {
+                            int total_up, int total_full, const NewtonProgram& prog, int p, float tol, int cap,
+                            int poll, int cls, hipStream_t s) {
   const int lds = 0;  // static LDS
   auto kstage = newton_stage_kernel<T>;
-  const float a = (float)(p + 1) / (float)p, b = -1.0f / (float)p;
-  int e = 0;
-  while ((1 << e) < p) ++e;
   // initial residual of M0
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p);
@@ -443,31 +552,13 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
     hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
                        dcount + kCountRing);
   }));
+  const NewtonStage first0 = drop_x(prog.stages[0]);
   for (int it = 0; it < cap; ++it) {
-    // iteration 0: X1 = z^(1/p) M1 was written by the init kernel
-    const int skip_x = it == 0 ? 1 : 0;
-    const int first_grid = (skip_x ? 1 : 2) * total_up;
-    if (p == 1) {
+    for (size_t q = 0; q < prog.stages.size(); ++q) {
+      // iteration 0: X1 = z^(1/p) M1 was written by the init kernel
+      const NewtonStage& S = (it == 0 && q == 0) ? first0 : prog.stages[q];
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(first_grid), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                           (int)kFirstP1, 0, 0, a, b, skip_x);
-      }));
-    } else {
-      STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(first_grid), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                           (int)kFirst, 0, 0, a, b, skip_x);
-      }));
-      for (int q = 1; q < e; ++q) {
-        const int src = (q - 1) & 1, dst = q & 1;
-        STATUS_TRY(launch(h, cls, s, [&] {
-          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                             (int)kSquare, src, dst, a, b, 0);
-        }));
-      }
-      const int src = (e - 1) & 1;
-      STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up,
-                           (int)kLast, src, 0, a, b, 0);
+        hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, S);
       }));
     }
     int* slot = dcount + (it % kCountRing);
@@ -668,7 +759,9 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   if (njobs == 0) return SHAMPOO_OK;
   if (!jobs || !info || !workspace) return fail(h, SHAMPOO_EINVAL, "jobs, info or workspace is NULL");
   const int p = prm->p;
-  if (p != 1 && p != 2 && p != 4 && p != 8) return fail(h, SHAMPOO_EUNSUPPORTED, "p = %d not in {1, 2, 4, 8}", p);
+  if (p < 1 || p > kMaxRootOrder) return fail(h, SHAMPOO_EUNSUPPORTED, "p = %d outside [1, %d]", p, kMaxRootOrder);
+  NewtonProgram prog;
+  if (!build_newton_program(p, &prog)) return fail(h, SHAMPOO_EUNSUPPORTED, "no product program for p = %d", p);
   if (!(prm->eps >= 0.f) || !isfinite(prm->eps)) return fail(h, SHAMPOO_EINVAL, "eps must be finite and >= 0");
   if (!(prm->tol >= 0.f)) return fail(h, SHAMPOO_EINVAL, "tol must be >= 0");
   if (prm->max_iters < 1) return fail(h, SHAMPOO_EINVAL, "max_iters must be >= 1");
@@ -759,7 +852,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       const int k32 = host_scalar_iters(m0, p, std::max((double)prm->tol, 1e-6), 1000) + 1;
       cap = std::min(cap, std::max(k32, 1));
     }
-    STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, p, prm->tol, cap, prm->poll,
+    STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, prog, p, prm->tol, cap, prm->poll,
                                    SHAMPOO_KCLASS_NEWTON_F32, s));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -784,7 +877,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
         hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
       }));
     }
-    STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, p, prm->tol, prm->max_iters, prm->poll,
+    STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, prog, p, prm->tol, prm->max_iters, prm->poll,
                                     SHAMPOO_KCLASS_NEWTON_F64, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);

@@ -148,7 +148,7 @@ def pin_lemma2(o):
 def pin_root_diagonal(o):
     """diag(d) + eps I -> diag((d + eps)^(-1/p))."""
     d = np.array([0.5, 2.0, 7.0, 1e-3, 30.0])
-    for p in (1, 2, 4, 8):
+    for p in (1, 2, 3, 4, 6, 8):
         X, st, _ = o.inv_root(np.diag(d), p, eps=1e-4)
         assert st == o.CONVERGED
         assert np.max(np.abs(X - np.diag((d + 1e-4) ** (-1.0 / p)))) < 1e-12 * np.max(X)
@@ -181,7 +181,7 @@ def pin_root_p2_square(o):
 
 def pin_root_invariant(o):
     """||X^p (A + eps I) - I||_F <= 1e-6 at condition numbers up to 1e6."""
-    for n, cond, p in ((64, 1e3, 4), (96, 1e6, 4), (80, 1e6, 2), (48, 1e5, 8)):
+    for n, cond, p in ((64, 1e3, 4), (96, 1e6, 4), (80, 1e6, 2), (48, 1e5, 8), (40, 1e4, 3), (36, 1e4, 6)):
         A = _spd(n, cond, 10 + n)
         X, _, _ = o.inv_root(A, p, eps=1e-6)
         res = np.linalg.matrix_power(X, p) @ (A + 1e-6 * np.eye(n)) - np.eye(n)
@@ -268,7 +268,8 @@ def pin_maxsv(o):
 # ------------------------------------------------------------------ coupled Newton (Algorithm 1)
 def pin_newton_vs_eigh(o):
     """The fp64 coupled iteration reaches the eigh-defined root to 1e-9."""
-    for n, cond, p in ((64, 1e2, 4), (64, 1e6, 4), (48, 1e6, 2), (32, 1e4, 8), (40, 1e3, 1)):
+    for n, cond, p in ((64, 1e2, 4), (64, 1e6, 4), (48, 1e6, 2), (32, 1e4, 8), (40, 1e3, 1), (40, 1e4, 3),
+                       (36, 1e3, 6), (30, 1e3, 7)):
         A = _spd(n, cond, 20 + n + p)
         res = o.coupled_newton(A, p, eps=1e-6, tol=1e-12)
         X, _, _ = o.inv_root(A, p, eps=1e-6)
@@ -281,7 +282,7 @@ def pin_newton_scalar_iters(o):
     m <- ((p+1-m)/p)^p m from m0 = z lambda_i, so the iteration count is
     the largest count over the diagonal, and the iterate stays diagonal."""
     d = np.array([1e-3, 0.1, 1.0, 3.0, 50.0])
-    for p in (2, 4):
+    for p in (2, 3, 4, 6):
         res = o.coupled_newton(np.diag(d), p, eps=0.0, tol=1e-12)
         z = (1.0 + p) / (2.0 * np.linalg.norm(d))
         want = max(o.scalar_newton_iters(z * x, p, 1e-12) for x in d)

@@ -41,8 +41,10 @@ def roots(env, As, **kw):
     return [host(x) for x in dX], B.decode_root_info(info)
 
 
-@pytest.mark.parametrize("p", [1, 2, 4, 8])
+@pytest.mark.parametrize("p", [1, 2, 3, 4, 5, 6, 7, 8, 12, 16])
 def test_against_eigh_mixed_sizes(env, p):
+    """Any root order 1 <= p <= 16 (powers of two and the product programs of
+    the others); iteration counts of one matrix against the fp64 transcript."""
     say("roots mixed sizes p", p)
     sizes = [1, 5, 127, 128, 129, 300, 513]
     As = [spd(n, 100.0, 10 * n + p) for n in sizes]
@@ -52,6 +54,8 @@ def test_against_eigh_mixed_sizes(env, p):
         assert inf["status"] in (0, 1), inf
         assert rel(X, Xo) <= 1e-3, (A.shape, inf, rel(X, Xo))
         assert np.array_equal(X, X.T)
+    tr = O.coupled_newton(As[5], p, 1e-6, tol=1e-6)
+    assert abs(info[5]["iters"] - tr["iters"]) <= 1, (info[5], tr["iters"])
 
 
 def test_closed_forms(env):
@@ -64,6 +68,11 @@ def test_closed_forms(env):
     assert np.count_nonzero(Xd - np.diag(np.diag(Xd))) == 0  # off-diagonal zeros stay exact
     assert rel(np.diag(Xd), (d.astype(np.float64) + 1e-4) ** -0.25) <= 1e-6
     assert rel(Xs[1], (c + 1e-4) ** -0.25 * np.eye(40)) <= 1e-6
+    # odd and composite orders on the diagonal matrix: X = (d + eps)^(-1/p)
+    for p in (3, 6, 7):
+        Xs, _ = roots(env, [np.diag(d)], p=p, eps=1e-4, precision=0)
+        assert np.count_nonzero(Xs[0] - np.diag(np.diag(Xs[0]))) == 0
+        assert rel(np.diag(Xs[0]), (d.astype(np.float64) + 1e-4) ** (-1.0 / p)) <= 1e-6, p
     # p = 1 is the inverse
     A = spd(64, 50.0, 3)
     Xs, _ = roots(env, [A], p=1, eps=0.0)
@@ -196,7 +205,10 @@ def test_argument_errors(env):
     ws = torch.empty(B.shampoo_inv_root_workspace_bytes([4]), dtype=torch.uint8, device=dev)
     info = torch.zeros(8, dtype=torch.int32, device=dev)
     with pytest.raises(B.ShampooError) as e:
-        B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(p=3), ws, info)
+        B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(p=17), ws, info)
+    assert e.value.code == B.SHAMPOO_EUNSUPPORTED
+    with pytest.raises(B.ShampooError) as e:
+        B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(p=0), ws, info)
     assert e.value.code == B.SHAMPOO_EUNSUPPORTED
     with pytest.raises(B.ShampooError) as e:
         B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(), ws[:16], info)
