@@ -34,6 +34,11 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
 * ``precondition``      -- Preliminaries (Shampoo update) and Lemma 1's
   one-sided forms.  Pinned by brute force with the Kronecker product of the
   full-matrix AdaGrad preconditioner on tiny shapes.
+* ``embedding_grad``, ``embedding_rows`` -- appendix "Shampoo for embedding
+  layers": the sparse gradient of a lookup and its active rows.  Pinned by
+  the dense lookup-matrix route G = S dy (S^T S = I for distinct one-hot
+  rows gives G^T G = dy^T dy), a hand-worked 5-row example with repeated
+  rows and weights, and the dropping of out-of-range entries.
 * ``graft_update``      -- Algorithm 2 (momentum on both directions) and the
   appendix "Further details on experiments", paragraph "Layer wise learning
   rates" (AdaGrad magnitude, Shampoo direction).  Pinned by the step-norm
@@ -59,6 +64,11 @@ R7  The ridge epsilon*I is added exactly once, at the root; statistics
 R8  D^{-1/2} o G is 0 where D is 0 (then G is 0 as well).
 R9  When ||P||_F = 0 the step size is 0.
 R10 The input to a root is symmetrised, A_s = (A + A^T)/2, before use.
+R11 Embedding statistics are those of the exact sparse gradient G of the
+    lookup: G^T G = dy^T (S^T S) dy with S the lookup matrix.  The appendix's
+    simplification S^T S = I (or diagonal for multi-hot) holds when the
+    features hit distinct rows; repeated rows are summed first.  Entries
+    with a row outside [0, vocab) or a feature outside [0, m) are dropped.
 """
 from __future__ import annotations
 
@@ -233,6 +243,38 @@ def scalar_newton_iters(m0, p, tol, max_iters=1000):
         m = ((p + 1.0 - m) / p) ** p * m
         k += 1
     return k
+
+
+# --------------------------------------------------------------------------
+# Embedding layers (appendix "Shampoo for embedding layers")
+# --------------------------------------------------------------------------
+def _valid_entries(idx, feat, weight, vocab, m):
+    idx = np.asarray(idx, dtype=np.int64)
+    nnz = idx.shape[0]
+    feat = np.arange(nnz, dtype=np.int64) if feat is None else np.asarray(feat, dtype=np.int64)
+    w = np.ones(nnz) if weight is None else _f64(weight)
+    ok = (idx >= 0) & (idx < vocab) & (feat >= 0) & (feat < m)
+    return idx[ok], feat[ok], w[ok]
+
+
+def embedding_grad(vocab, idx, feat, weight, dy):
+    """Gradient of the table (vocab x d, row-major) of a lookup whose entry e
+    reads row idx[e] into output row feat[e] with weight w[e]:
+    G = sum_e w[e] e_{idx[e]} dy[feat[e]]^T.  feat None: feat[e] = e (one
+    lookup per output row); weight None: w[e] = 1 (R11)."""
+    dy = _f64(dy)
+    i, f, w = _valid_entries(idx, feat, weight, vocab, dy.shape[0])
+    G = np.zeros((vocab, dy.shape[1]))
+    for e in range(i.shape[0]):
+        G[i[e]] += w[e] * dy[f[e]]
+    return G
+
+
+def embedding_rows(vocab, idx, feat, weight, dy):
+    """Active rows of the lookup (ascending) and the matching rows of G."""
+    i, _, _ = _valid_entries(idx, feat, weight, vocab, np.asarray(dy).shape[0])
+    rows = np.unique(i)
+    return rows, embedding_grad(vocab, idx, feat, weight, dy)[rows]
 
 
 # --------------------------------------------------------------------------

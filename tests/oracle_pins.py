@@ -89,6 +89,53 @@ def pin_stats_onehot_embedding(o):
     assert _relf(L, dy @ np.diag(counts) @ dy.T) < 1e-13
 
 
+def pin_embedding_lookup_matrix(o):
+    """Row-major table: G = S dy with S[idx_e, feat_e] += w_e the dense
+    lookup matrix (vocab x m); with distinct one-hot rows S^T S = I, so the
+    right statistic G^T G equals dy^T dy (appendix "Shampoo for embedding
+    layers"); with repeats it equals dy^T (S^T S) dy."""
+    r = rng(30)
+    V, d, m = 50, 4, 9
+    dy = r.standard_normal((m, d))
+    idx = r.choice(V, m, replace=False)
+    G = o.embedding_grad(V, idx, None, None, dy)
+    _, R = o.stats_update(None, np.zeros((d, d)), G)
+    assert _relf(R, dy.T @ dy) < 1e-13
+    # multi-hot with repeats and weights
+    nnz = 25
+    idx = r.integers(0, 12, nnz)
+    feat = r.integers(0, m, nnz)
+    w = r.standard_normal(nnz)
+    S = np.zeros((V, m))
+    for e in range(nnz):
+        S[idx[e], feat[e]] += w[e]
+    G = o.embedding_grad(V, idx, feat, w, dy)
+    assert _relf(G, S @ dy) < 1e-13
+    _, R = o.stats_update(None, np.zeros((d, d)), G)
+    assert _relf(R, dy.T @ (S.T @ S) @ dy) < 1e-12
+    rows, U = o.embedding_rows(V, idx, feat, w, dy)
+    assert list(rows) == sorted(set(int(i) for i in idx))
+    assert np.array_equal(U, G[rows])
+
+
+def pin_embedding_worked_example(o):
+    """5-row table, d = 2, dy rows (1,2), (3,4), (5,6); entries (row, feature,
+    weight): (3,0,1), (1,1,1), (3,2,1/2), (1,0,2), plus three invalid ones
+    (row 5, row -1, feature 3) that are dropped.  By hand: row 1 = dy1 +
+    2 dy0 = (5, 8), row 3 = dy0 + dy2/2 = (3.5, 5), all other rows 0."""
+    dy = np.array([[1.0, 2.0], [3.0, 4.0], [5.0, 6.0]])
+    idx = [3, 1, 3, 1, 5, -1, 0]
+    feat = [0, 1, 2, 0, 0, 1, 3]
+    w = [1.0, 1.0, 0.5, 2.0, 1.0, 1.0, 1.0]
+    G = o.embedding_grad(5, idx, feat, w, dy)
+    want = np.zeros((5, 2))
+    want[1] = [5.0, 8.0]
+    want[3] = [3.5, 5.0]
+    assert np.array_equal(G, want)
+    rows, U = o.embedding_rows(5, idx, feat, w, dy)
+    assert list(rows) == [1, 3] and np.array_equal(U, [[5.0, 8.0], [3.5, 5.0]])
+
+
 def pin_stats_ema(o):
     """beta2 < 1 with a constant gradient: L_t = (1 - beta2^t) G G^T
     (geometric series of Algorithm 2's EMA from L_0 = 0)."""

@@ -44,6 +44,14 @@ MUTATIONS = [
      [P.pin_graft_norm_identity, P.pin_graft_identity_roots]),
     ("graft_update", "beta1 * _f64(Ps) + (1.0 - beta1) * Pf", "beta1 * _f64(Ps) + Pf", [P.pin_graft_momentum_1x1]),
     ("graft_update", "W_new = W - eta * Mg_new", "W_new = W - eta * G", [P.pin_graft_adagrad_fallback]),
+    ("embedding_grad", "G[i[e]] += w[e] * dy[f[e]]", "G[i[e]] = w[e] * dy[f[e]]",
+     [P.pin_embedding_worked_example, P.pin_embedding_lookup_matrix]),
+    ("embedding_grad", "G[i[e]] += w[e] * dy[f[e]]", "G[i[e]] += dy[f[e]]", [P.pin_embedding_worked_example]),
+    ("embedding_grad", "G[i[e]] += w[e] * dy[f[e]]", "G[f[e]] += w[e] * dy[i[e] % dy.shape[0]]",
+     [P.pin_embedding_worked_example]),
+    ("_valid_entries", "(idx >= 0) & (idx < vocab)", "(idx >= -1) & (idx < vocab)",
+     [P.pin_embedding_worked_example]),
+    ("embedding_rows", "rows = np.unique(i)", "rows = i", [P.pin_embedding_lookup_matrix]),
 ]
 
 
