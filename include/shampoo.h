@@ -216,6 +216,85 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
                              float eta0, float beta1, int use_shampoo, float* norms, void* stream);
 
 /*
+ * Embedding layers (appendix "Shampoo for embedding layers", with the
+ * one-sided preconditioner of Lemma 1 for large layers).
+ *
+ * A table W (vocab x dim, row-major, row stride ldw) is read by nnz lookup
+ * entries: entry e reads row idx[e] into output row feat[e] of the layer
+ * output y (m x dim), with weight weight[e].  Its gradient
+ *   G = sum_e weight[e] e_{idx[e]} dy[feat[e], :]   (vocab x dim)
+ * is nonzero only on the active rows {idx[e]}, and the dim x dim statistic is
+ *   R = G^T G = dy^T (S^T S) dy,   S[idx[e], feat[e]] += weight[e],
+ * which is dy^T dy when every entry hits its own row (one-hot features on
+ * distinct rows), at O(nnz dim^2) cost instead of O(vocab dim^2).
+ * The step for the table is then
+ *   shampoo_embedding_rows -> shampoo_embedding_stats -> (roots: Rr = R^(-1/2),
+ *   shampoo_inv_root_batched with p = 2) -> shampoo_embedding_precondition
+ *   -> shampoo_embedding_graft,
+ * all on the compact rows.  Every count is read on the device: no call
+ * synchronizes the stream.
+ *
+ * Compact form (written by shampoo_embedding_rows, read by the others):
+ *   rows   int32[nnz]: the active rows in ascending order, then -1;
+ *   U      fp32 nnz x dim (row stride dim): U[i] = G[rows[i]] for i < u, the
+ *          sum taken over the entries of that row in entry order
+ *          (deterministic); zero rows for i >= u;
+ *   count  int32[2]: count[0] = u (active rows), count[1] = entries dropped
+ *          because idx is outside [0, vocab) or feat outside [0, m).
+ */
+
+/* Workspace (bytes) of shampoo_embedding_rows and shampoo_embedding_stats
+ * for nnz entries of width dim; 0 on invalid arguments (nnz outside
+ * [1, 2^26], dim outside [1, 4096]). */
+size_t shampoo_embedding_workspace_bytes(int nnz, int dim);
+
+/*
+ * Compacts the lookup gradient.  idx: nnz rows; feat: nnz output rows, or
+ * NULL for feat[e] = e (one entry per output row, m >= nnz); weight: nnz
+ * weights, or NULL for 1 (one-hot); dy: m x dim, row stride ld_dy.  All
+ * device pointers.  rows, U, count: outputs as above.  Sorting uses a stable
+ * device radix sort whose temporary storage the handle allocates and keeps.
+ * Errors: EINVAL (NULL pointers, nnz or dim out of range, vocab outside
+ * [1, 2^31 - 1), m < 1, ld_dy < dim), ENOMEM (workspace too small).
+ */
+shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const int32_t* feat, const float* weight,
+                                      int nnz, int64_t vocab, const float* dy, int m, int dim, int64_t ld_dy,
+                                      int32_t* rows, float* U, int32_t* count, void* workspace, size_t ws_bytes,
+                                      void* stream);
+
+/*
+ * R = beta2 R + c U^T U over the first count[0] rows of U (c = 1 if
+ * beta2 == 1 else 1 - beta2): the statistic of the table, dim x dim, kept
+ * exactly symmetric.  Split over the rows of U in fixed chunks whose partial
+ * products are added in chunk order (deterministic).
+ * Errors: EINVAL (NULL pointers, sizes, beta2 outside (0, 1]), ENOMEM.
+ */
+shampoo_status shampoo_embedding_stats(void* handle, const float* U, const int32_t* count, int nnz, int dim,
+                                       float* R, float beta2, void* workspace, size_t ws_bytes, void* stream);
+
+/*
+ * P = U Rr for the first count[0] rows (Rr symmetric, dim x dim): the
+ * preconditioned compact gradient G R^(-1/2) of Lemma 1's one-sided form.
+ * Rows of P at or past count[0] are not written.  Errors: EINVAL.
+ */
+shampoo_status shampoo_embedding_precondition(void* handle, const float* U, const int32_t* count, int nnz, int dim,
+                                              const float* Rr, float* P, void* stream);
+
+/*
+ * Grafted update of the active rows (beta1 = 0 form of shampoo_graft): for
+ * i < count[0] and r = rows[i],
+ *   D[r] += U[i] o U[i];  eta = eta0 ||D^(-1/2) o G||_F / ||P||_F  (norms over
+ *   the active rows, which are all of G's nonzeros);  W[r] -= eta P[i]
+ * (use_shampoo = 0: W[r] -= eta0 D[r]^(-1/2) o U[i]).  Rows of W and D that
+ * no entry touched are left exactly as they were.  norms (device, may be
+ * NULL): {||D^(-1/2) o G||_F, ||P||_F, eta}.
+ * Errors: EINVAL (NULL pointers, sizes, ldw < dim, non-finite eta0).
+ */
+shampoo_status shampoo_embedding_graft(void* handle, const int32_t* rows, const int32_t* count, int nnz, int dim,
+                                       const float* U, const float* P, float* W, float* D, int64_t vocab,
+                                       int64_t ldw, float eta0, int use_shampoo, float* norms, void* stream);
+
+/*
  * Measurement support.  While enabled, every launch of the timed kernel
  * classes below is bracketed by HIP events on its stream.
  * shampoo_timing_read synchronizes those events, returns the summed duration
@@ -228,7 +307,8 @@ enum {
   SHAMPOO_KCLASS_PRECOND = 3,    /* grouped preconditioning GEMMs */
   SHAMPOO_KCLASS_GRAFT = 4,      /* graft reduction and update passes */
   SHAMPOO_KCLASS_ROOT_AUX = 5,   /* root prologue/epilogue/state kernels */
-  SHAMPOO_KCLASS_COUNT = 6
+  SHAMPOO_KCLASS_EMB = 6,        /* embedding row compaction (sort, runs, segment sums) */
+  SHAMPOO_KCLASS_COUNT = 7
 };
 shampoo_status shampoo_timing_enable(void* handle, int enable);
 shampoo_status shampoo_timing_read(void* handle, int kclass, double* total_ms, int64_t* launches);

@@ -271,10 +271,19 @@ def embedding_grad(vocab, idx, feat, weight, dy):
 
 
 def embedding_rows(vocab, idx, feat, weight, dy):
-    """Active rows of the lookup (ascending) and the matching rows of G."""
-    i, _, _ = _valid_entries(idx, feat, weight, vocab, np.asarray(dy).shape[0])
-    rows = np.unique(i)
-    return rows, embedding_grad(vocab, idx, feat, weight, dy)[rows]
+    """Active rows of the lookup (ascending) and the matching rows of G,
+    accumulated per row in entry order without forming the vocab x d G."""
+    dy = _f64(dy)
+    i, f, w = _valid_entries(idx, feat, weight, vocab, dy.shape[0])
+    acc = {}
+    for e in range(i.shape[0]):
+        r = int(i[e])
+        if r not in acc:
+            acc[r] = np.zeros(dy.shape[1])
+        acc[r] += w[e] * dy[f[e]]
+    rows = np.array(sorted(acc), dtype=np.int64)
+    U = np.array([acc[r] for r in rows]).reshape(len(rows), dy.shape[1])
+    return rows, U
 
 
 # --------------------------------------------------------------------------

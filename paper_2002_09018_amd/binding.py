@@ -26,8 +26,8 @@ SHAMPOO_OK, SHAMPOO_EINVAL, SHAMPOO_EUNSUPPORTED, SHAMPOO_EHIP, SHAMPOO_ENOMEM =
 SHAMPOO_F32, SHAMPOO_BF16 = 0, 1
 ROOT_CONVERGED, ROOT_STAGNATED, ROOT_MAXITER, ROOT_DIVERGED, ROOT_NOT_PD = 0, 1, 2, 3, 4
 PRECISION_FP32, PRECISION_AUTO, PRECISION_FP64 = 0, 1, 2
-KCLASS_NEWTON_F32, KCLASS_NEWTON_F64, KCLASS_STATS, KCLASS_PRECOND, KCLASS_GRAFT, KCLASS_ROOT_AUX = range(6)
-KCLASS_NAMES = ["newton_f32", "newton_f64", "stats", "precond", "graft", "root_aux"]
+KCLASS_NEWTON_F32, KCLASS_NEWTON_F64, KCLASS_STATS, KCLASS_PRECOND, KCLASS_GRAFT, KCLASS_ROOT_AUX, KCLASS_EMB = range(7)
+KCLASS_NAMES = ["newton_f32", "newton_f64", "stats", "precond", "graft", "root_aux", "emb"]
 
 
 class shampoo_block(C.Structure):
@@ -55,7 +55,7 @@ class shampoo_root_info(C.Structure):
 
 ROOT_INFO_FIELDS = [f for f, _ in shampoo_root_info._fields_]
 
-_vp, _i, _f, _sz = C.c_void_p, C.c_int, C.c_float, C.c_size_t
+_vp, _i, _f, _sz, _i64 = C.c_void_p, C.c_int, C.c_float, C.c_size_t, C.c_int64
 _sig = {
     "shampoo_create": (_i, [C.POINTER(_vp), _i]),
     "shampoo_destroy": (_i, [_vp]),
@@ -68,6 +68,11 @@ _sig = {
                                       _vp, _sz, _vp, _vp]),
     "shampoo_precondition": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _vp]),
     "shampoo_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
+    "shampoo_embedding_workspace_bytes": (_sz, [_i, _i]),
+    "shampoo_embedding_rows": (_i, [_vp, _vp, _vp, _vp, _i, _i64, _vp, _i, _i, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
+    "shampoo_embedding_stats": (_i, [_vp, _vp, _vp, _i, _i, _vp, _f, _vp, _sz, _vp]),
+    "shampoo_embedding_precondition": (_i, [_vp, _vp, _vp, _i, _i, _vp, _vp, _vp]),
+    "shampoo_embedding_graft": (_i, [_vp, _vp, _vp, _i, _i, _vp, _vp, _vp, _vp, _i64, _i64, _f, _i, _vp, _vp]),
     "shampoo_timing_enable": (_i, [_vp, _i]),
     "shampoo_timing_read": (_i, [_vp, _i, C.POINTER(C.c_double), C.POINTER(C.c_int64)]),
 }
@@ -202,6 +207,45 @@ def shampoo_graft(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None,
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0), float(beta1),
                                       int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+
+
+def _nbytes(t):
+    return 0 if t is None else int(t.numel() * t.element_size())
+
+
+def shampoo_embedding_workspace_bytes(nnz, dim):
+    return int(_lib.shampoo_embedding_workspace_bytes(int(nnz), int(dim)))
+
+
+def shampoo_embedding_rows(handle, idx, feat, weight, vocab, dy, rows, U, count, workspace, stream=None):
+    """idx, feat (or None): int32 [nnz]; weight: fp32 [nnz] or None; dy: m x dim
+    fp32 (row-major view); rows int32 [nnz], U fp32 nnz x dim (contiguous),
+    count int32 [2]; workspace: uint8 device tensor."""
+    nnz = int(idx.numel())
+    m, dim = int(dy.shape[0]), int(dy.shape[1])
+    _check(handle, _lib.shampoo_embedding_rows(handle, _ptr(idx), _ptr(feat), _ptr(weight), nnz, int(vocab),
+                                               _ptr(dy), m, dim, int(dy.stride(0)), _ptr(rows), _ptr(U),
+                                               _ptr(count), _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def shampoo_embedding_stats(handle, U, count, R, beta2=1.0, workspace=None, stream=None):
+    nnz, dim = int(U.shape[0]), int(U.shape[1])
+    _check(handle, _lib.shampoo_embedding_stats(handle, _ptr(U), _ptr(count), nnz, dim, _ptr(R), float(beta2),
+                                                _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
+def shampoo_embedding_precondition(handle, U, count, Rr, P, stream=None):
+    nnz, dim = int(U.shape[0]), int(U.shape[1])
+    _check(handle, _lib.shampoo_embedding_precondition(handle, _ptr(U), _ptr(count), nnz, dim, _ptr(Rr), _ptr(P),
+                                                       _stream(stream)))
+
+
+def shampoo_embedding_graft(handle, rows, count, U, P, W, D, eta0, use_shampoo=True, norms=None, stream=None):
+    """W, D: vocab x dim fp32 tables (same row stride)."""
+    nnz, dim = int(U.shape[0]), int(U.shape[1])
+    _check(handle, _lib.shampoo_embedding_graft(handle, _ptr(rows), _ptr(count), nnz, dim, _ptr(U), _ptr(P),
+                                                _ptr(W), _ptr(D), int(W.shape[0]), int(W.stride(0)), float(eta0),
+                                                int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
 
 
 def shampoo_timing_enable(handle, enable=True):

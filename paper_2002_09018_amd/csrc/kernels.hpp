@@ -35,6 +35,12 @@ struct GemmProblem {
   int tiles_n;    // ceil(N / 128)
   int tile_begin; // first logical tile of this problem
   int a_aligned, b_aligned;
+  // Optional device-side limits (embedding rows, whose count is known only
+  // on the device): K is cut to *kcount - koff (>= 0) and the k-extent of
+  // the operands with it; tiles starting at or past row *mcount are skipped.
+  const int* kcount;
+  const int* mcount;
+  int koff, pad;
 };
 
 __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int nprob, int t) {
@@ -46,7 +52,9 @@ __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int n
   return lo;
 }
 
-template <typename SA, int LA, typename SB, int LB>
+// LIM: honour the device-side limits kcount / mcount (a separate
+// instantiation, so the plain kernels carry no extra registers).
+template <typename SA, int LA, typename SB, int LB, bool LIM = false>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
                                                                int nprob, int total_tiles) {
   __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
@@ -59,12 +67,20 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   if (P.sym) unrank_upper(lt, P.tiles_n, ti, tj);
   else { ti = lt / P.tiles_n; tj = lt % P.tiles_n; }
   const int m0 = ti * kTile, n0 = tj * kTile;
+  if (LIM && P.mcount && m0 >= *P.mcount) return;
 
   Operand<SA> A{reinterpret_cast<const SA*>(P.A), P.lda, P.a_rows, P.a_cols, P.a_aligned != 0};
   Operand<SB> B{reinterpret_cast<const SB*>(P.B), P.ldb, P.b_rows, P.b_cols, P.b_aligned != 0};
+  int K = P.K;
+  if (LIM && P.kcount) {
+    K = min(K, max(0, *P.kcount - P.koff));
+    // the k-extent is the stored rows of a k-major operand, else its columns
+    if (LA == kLayoutK) A.rows = min(A.rows, K); else A.cols = min(A.cols, K);
+    if (LB == kLayoutK) B.rows = min(B.rows, K); else B.cols = min(B.cols, K);
+  }
   WaveAcc<float> acc;
   acc.zero();
-  tile_mma<float, SA, LA, SB, LB>(acc, A, B, m0, n0, P.K, sa0, sa1, sb0, sb1, P.sym && ti == tj);
+  tile_mma<float, SA, LA, SB, LB>(acc, A, B, m0, n0, K, sa0, sa1, sb0, sb1, P.sym && ti == tj);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
@@ -769,7 +785,13 @@ struct GraftBlock {
   int chunk_begin;
   int nchunks;
   int rows_per_chunk;
-  int vec4;  // cols, ld and pointers allow 4-wide vector access
+  int vec4;  // cols, ld, ldw and pointers allow 4-wide vector access
+  // W, D, Mg, Ps rows: row r of the block is row wrows[r] (wrows NULL: r)
+  // with stride ldw; rows at or past *count are skipped (count NULL: none).
+  const int* wrows;
+  const int* count;
+  int64_t ldw;
+  int64_t wlimit;  // rows of the W/D tensor (a wrows entry outside is skipped)
 };
 
 __device__ __forceinline__ int find_block_graft(const GraftBlock* b, int nb, int t) {
@@ -809,18 +831,26 @@ struct G4<uint16_t> {
     g[2] = cvt<float, uint16_t>(v[2]); g[3] = cvt<float, uint16_t>(v[3]);
   }
 };
-// Calls f(i) for the element offsets of a chunk (rows r0..r1 of a block):
-// 4-wide (f(i, 4)) where the block allows vector access, else scalar
-// (f(i, 1)).  Whole rows per chunk keep index arithmetic free of divisions.
+// Calls f(ig, iw, w) for the elements of a chunk (rows r0..r1 of a block):
+// ig is the offset in G and P, iw the offset in W, D, Mg and Ps; 4-wide
+// (w = 4) where the block allows vector access, else scalar (w = 1).  Whole
+// rows per chunk keep index arithmetic free of divisions.
 template <typename F>
 __device__ __forceinline__ void for_chunk(const GraftBlock& B, int r0, int r1, F&& f) {
-  if (B.vec4) {
-    const int c4 = B.cols >> 2;
-    for (int r = r0; r < r1; ++r)
-      for (int c = threadIdx.x; c < c4; c += kThreads) f((int64_t)r * B.ld + 4 * c, 4);
-  } else {
-    for (int r = r0; r < r1; ++r)
-      for (int c = threadIdx.x; c < B.cols; c += kThreads) f((int64_t)r * B.ld + c, 1);
+  if (B.count) r1 = min(r1, *B.count);
+  for (int r = r0; r < r1; ++r) {
+    int64_t wr = r;
+    if (B.wrows) {
+      wr = B.wrows[r];
+      if (wr < 0 || wr >= B.wlimit) continue;
+    }
+    const int64_t g0 = (int64_t)r * B.ld, w0 = wr * B.ldw;
+    if (B.vec4) {
+      const int c4 = B.cols >> 2;
+      for (int c = threadIdx.x; c < c4; c += kThreads) f(g0 + 4 * c, w0 + 4 * c, 4);
+    } else {
+      for (int c = threadIdx.x; c < B.cols; c += kThreads) f(g0 + c, w0 + c, 1);
+    }
   }
 }
 
@@ -837,11 +867,11 @@ __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock*
   const int r1 = min(B.rows, r0 + B.rows_per_chunk);
   const bool mom = beta1 > 0.f;
   float smg = 0.f, sps = 0.f;
-  for_chunk(B, r0, r1, [&](int64_t i, int w) {
+  for_chunk(B, r0, r1, [&](int64_t i, int64_t iw, int w) {
     float g[4], d[4], pv[4];
     if (w == 4) {
       G4<SG>::load(B.G, i, g);
-      const f4v dv = gload<f4v>(B.D + i);
+      const f4v dv = gload<f4v>(B.D + iw);
       d[0] = dv[0]; d[1] = dv[1]; d[2] = dv[2]; d[3] = dv[3];
       if (use_shampoo) {
         const f4v p4 = gload<f4v>(B.P + i);
@@ -849,7 +879,7 @@ __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock*
       }
     } else {
       g[0] = load_g<SG>(B.G, i);
-      d[0] = gload<float>(B.D + i);
+      d[0] = gload<float>(B.D + iw);
       if (use_shampoo) pv[0] = gload<float>(B.P + i);
     }
     f4v dn;
@@ -860,16 +890,16 @@ __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock*
       dn[e] = de;
       const float u = ada_dir(g[e], de);
       float mg = u;
-      if (mom) { mg = beta1 * B.Mg[i + e] + (1.f - beta1) * u; B.Mg[i + e] = mg; }
+      if (mom) { mg = beta1 * B.Mg[iw + e] + (1.f - beta1) * u; B.Mg[iw + e] = mg; }
       smg += mg * mg;
       if (use_shampoo) {
         float ps = pv[e];
-        if (mom) { ps = beta1 * B.Ps[i + e] + (1.f - beta1) * ps; B.Ps[i + e] = ps; }
+        if (mom) { ps = beta1 * B.Ps[iw + e] + (1.f - beta1) * ps; B.Ps[iw + e] = ps; }
         sps += ps * ps;
       }
     }
-    if (w == 4) gstore<f4v>(B.D + i, dn);
-    else gstore<float>(B.D + i, dn[0]);
+    if (w == 4) gstore<f4v>(B.D + iw, dn);
+    else gstore<float>(B.D + iw, dn[0]);
   });
   const double a = block_sum((double)smg, red);
   const double b = block_sum((double)sps, red);
@@ -910,33 +940,36 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
   const bool mom = beta1 > 0.f;
   // direction: Ps (momentum) or P; before the roots Mg or D^{-1/2} o G
   const float* dir = use_shampoo ? (mom ? B.Ps : B.P) : (mom ? B.Mg : nullptr);
-  for_chunk(B, r0, r1, [&](int64_t i, int w) {
+  // P is laid out like G; momentum buffers like W
+  const int64_t dir_w = use_shampoo && !mom ? 0 : 1;
+  for_chunk(B, r0, r1, [&](int64_t i, int64_t iw, int w) {
     float step[4];
+    const int64_t id = dir_w ? iw : i;
     if (dir) {
       if (w == 4) {
-        const f4v v = gload<f4v>(dir + i);
+        const f4v v = gload<f4v>(dir + id);
         step[0] = v[0]; step[1] = v[1]; step[2] = v[2]; step[3] = v[3];
       } else {
-        step[0] = gload<float>(dir + i);
+        step[0] = gload<float>(dir + id);
       }
     } else {
       float g[4];
       if (w == 4) {
         G4<SG>::load(B.G, i, g);
-        const f4v dv = gload<f4v>(B.D + i);
+        const f4v dv = gload<f4v>(B.D + iw);
 #pragma unroll
         for (int e = 0; e < 4; ++e) step[e] = ada_dir(g[e], dv[e]);
       } else {
-        step[0] = ada_dir(load_g<SG>(B.G, i), gload<float>(B.D + i));
+        step[0] = ada_dir(load_g<SG>(B.G, i), gload<float>(B.D + iw));
       }
     }
     if (w == 4) {
-      f4v wv = gload<f4v>(B.W + i);
+      f4v wv = gload<f4v>(B.W + iw);
 #pragma unroll
       for (int e = 0; e < 4; ++e) wv[e] -= etaf * step[e];
-      gstore<f4v>(B.W + i, wv);
+      gstore<f4v>(B.W + iw, wv);
     } else {
-      gstore<float>(B.W + i, gload<float>(B.W + i) - etaf * step[0]);
+      gstore<float>(B.W + iw, gload<float>(B.W + iw) - etaf * step[0]);
     }
   });
 }

@@ -11,6 +11,11 @@
 #include <string>
 #include <vector>
 
+#include <rocprim/device/device_radix_sort.hpp>
+#include <rocprim/device/device_run_length_encode.hpp>
+#include <rocprim/device/device_scan.hpp>
+
+#include "embedding.hpp"
 #include "kernels.hpp"
 #include "shampoo.h"
 
@@ -20,6 +25,7 @@ namespace {
 
 constexpr int kMaxDim = 4096;
 constexpr int kMaxRootOrder = 16;  // largest p of X = A^(-1/p)
+constexpr int kMaxEmbEntries = 1 << 26;  // lookup entries of one embedding call
 constexpr int kCountRing = 64;  // device/pinned slots of per-iteration active counts
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
@@ -57,6 +63,8 @@ struct Handle {
   size_t scratch_cap = 0;
   void* partial = nullptr;
   size_t partial_cap = 0;
+  void* sort_tmp = nullptr;  // rocPRIM temporary storage of the embedding row compaction
+  size_t sort_tmp_cap = 0;
   int32_t* pinned = nullptr;  // kCountRing + 1 ints
   hipEvent_t poll_ev[2] = {nullptr, nullptr};
   bool timing = false;
@@ -200,7 +208,7 @@ shampoo_status set_lds(Handle* h, K kernel, int bytes) {
 }
 
 // ---------------------------------------------------------------- GEMM
-template <typename SA, int LA, typename SB, int LB>
+template <typename SA, int LA, typename SB, int LB, bool LIM = false>
 shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t s, int cls) {
   if (probs.empty()) return SHAMPOO_OK;
   int total = 0;
@@ -211,7 +219,7 @@ shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t 
   }
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
-  auto k = gemm_grouped_kernel<SA, LA, SB, LB>;
+  auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM>;
   const int lds = 0;  // static LDS
   const int np = (int)probs.size();
   STATUS_TRY(launch(h, cls, s, [&] {
@@ -281,6 +289,7 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
     GraftBlock g{};
     g.G = b.G; g.W = b.W; g.D = b.D; g.P = b.P; g.Mg = b.Mg; g.Ps = b.Ps;
     g.ld = b.ld; g.rows = b.rows; g.cols = b.cols;
+    g.ldw = b.ld; g.wrows = nullptr; g.count = nullptr; g.wlimit = b.rows;
     g.rows_per_chunk = std::max(1, 16384 / b.cols);
     g.nchunks = cdiv(b.rows, g.rows_per_chunk);
     // 4-wide access needs every row start 16-byte aligned in every tensor
@@ -618,6 +627,49 @@ std::vector<NewtonJob<T>> newton_table(const shampoo_root_job* jobs, int njobs, 
   return v;
 }
 
+// ---------------------------------------------------------------- embeddings
+// Workspace of the embedding calls: seven int32 arrays of nnz (sort keys and
+// values in and out, run keys, run lengths, run offsets), the run count, and
+// the split-K partial statistics (splits x dim^2 fp32).
+struct EmbLayout {
+  size_t keys = 0, vals = 0, keys_s = 0, vals_s = 0, uniq = 0, lens = 0, offs = 0, nruns = 0, part = 0;
+  size_t total = 0;
+  int splits = 1, chunk = 0;
+};
+
+EmbLayout emb_layout(int nnz, int dim) {
+  EmbLayout L;
+  const size_t a = align256((size_t)nnz * sizeof(int32_t));
+  size_t off = 0;
+  L.keys = off; off += a;
+  L.vals = off; off += a;
+  L.keys_s = off; off += a;
+  L.vals_s = off; off += a;
+  L.uniq = off; off += a;
+  L.lens = off; off += a;
+  L.offs = off; off += a;
+  L.nruns = off; off += 256;
+  // Split-K of R += U^T U: about 1024 workgroups over the upper tiles of R,
+  // each split at least 512 rows of U (a multiple of the 16-deep k stage).
+  const int t = cdiv(dim, kTile);
+  const int tiles = t * (t + 1) / 2;
+  int S = std::max(1, std::min(cdiv(1024, tiles), cdiv(nnz, 512)));
+  int chunk = cdiv(cdiv(nnz, S), 16) * 16;
+  S = cdiv(nnz, chunk);
+  L.splits = S;
+  L.chunk = chunk;
+  L.part = off;
+  if (S > 1) off += (size_t)S * align256((size_t)dim * dim * sizeof(float));
+  L.total = off;
+  return L;
+}
+
+shampoo_status emb_check(Handle* h, int nnz, int dim) {
+  if (nnz < 1 || nnz > kMaxEmbEntries) return fail(h, SHAMPOO_EINVAL, "nnz = %d outside [1, %d]", nnz, kMaxEmbEntries);
+  if (dim < 1 || dim > kMaxDim) return fail(h, SHAMPOO_EINVAL, "dim = %d outside [1, %d]", dim, kMaxDim);
+  return SHAMPOO_OK;
+}
+
 }  // namespace
 
 // ============================================================================
@@ -677,6 +729,7 @@ shampoo_status shampoo_destroy(void* handle) {
   for (auto e : h->spare_events) (void)hipEventDestroy(e);
   if (h->scratch) (void)hipFree(h->scratch);
   if (h->partial) (void)hipFree(h->partial);
+  if (h->sort_tmp) (void)hipFree(h->sort_tmp);
   if (h->pinned) (void)hipHostFree(h->pinned);
   for (auto e : h->poll_ev)
     if (e) (void)hipEventDestroy(e);
@@ -924,6 +977,186 @@ shampoo_status shampoo_timing_read(void* handle, int kclass, double* total_ms, i
   if (total_ms) *total_ms = ms;
   if (launches) *launches = n;
   return SHAMPOO_OK;
+}
+
+
+// ---------------------------------------------------------------- embeddings
+size_t shampoo_embedding_workspace_bytes(int nnz, int dim) {
+  if (nnz < 1 || nnz > kMaxEmbEntries || dim < 1 || dim > kMaxDim) return 0;
+  return emb_layout(nnz, dim).total;
+}
+
+shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const int32_t* feat, const float* weight,
+                                      int nnz, int64_t vocab, const float* dy, int m, int dim, int64_t ld_dy,
+                                      int32_t* rows, float* U, int32_t* count, void* workspace, size_t ws_bytes,
+                                      void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(emb_check(h, nnz, dim));
+  if (vocab < 1 || vocab >= INT32_MAX) return fail(h, SHAMPOO_EINVAL, "vocab = %lld outside [1, 2^31 - 1)", (long long)vocab);
+  if (m < 1) return fail(h, SHAMPOO_EINVAL, "m = %d < 1", m);
+  if (ld_dy < dim) return fail(h, SHAMPOO_EINVAL, "ld_dy %lld < dim %d", (long long)ld_dy, dim);
+  if (!idx || !dy || !rows || !U || !count || !workspace)
+    return fail(h, SHAMPOO_EINVAL, "idx, dy, rows, U, count or workspace is NULL");
+  const EmbLayout L = emb_layout(nnz, dim);
+  if (ws_bytes < L.total) return fail(h, SHAMPOO_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  int32_t* keys = reinterpret_cast<int32_t*>(ws + L.keys);
+  int32_t* vals = reinterpret_cast<int32_t*>(ws + L.vals);
+  int32_t* keys_s = reinterpret_cast<int32_t*>(ws + L.keys_s);
+  int32_t* vals_s = reinterpret_cast<int32_t*>(ws + L.vals_s);
+  int32_t* uniq = reinterpret_cast<int32_t*>(ws + L.uniq);
+  int32_t* lens = reinterpret_cast<int32_t*>(ws + L.lens);
+  int32_t* offs = reinterpret_cast<int32_t*>(ws + L.offs);
+  int32_t* nruns = reinterpret_cast<int32_t*>(ws + L.nruns);
+  const int32_t v32 = (int32_t)vocab;
+  int bits = 1;
+  while (bits < 31 && (int64_t(1) << bits) <= vocab) ++bits;  // keys lie in [0, vocab]
+  // rocPRIM temporary storage (sized by a query; grown on the handle)
+  size_t t_sort = 0, t_rle = 0, t_scan = 0;
+  HIP_TRY(h, rocprim::radix_sort_pairs(nullptr, t_sort, keys, keys_s, vals, vals_s, (unsigned)nnz, 0, bits, s));
+  HIP_TRY(h, rocprim::run_length_encode(nullptr, t_rle, keys_s, (unsigned)nnz, uniq, lens, nruns, s));
+  HIP_TRY(h, rocprim::exclusive_scan(nullptr, t_scan, lens, offs, 0, (unsigned)nnz, rocprim::plus<int32_t>(), s));
+  size_t tb = std::max(t_sort, std::max(t_rle, t_scan));
+  STATUS_TRY(grow(h, &h->sort_tmp, &h->sort_tmp_cap, std::max<size_t>(tb, 256)));
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
+    hipLaunchKernelGGL(emb_keys_kernel, dim3(cdiv(nnz, kThreads)), dim3(kThreads), 0, s, idx, feat, nnz, v32, m,
+                       keys, vals, lens);
+  }));
+  // stable sort by row (entries of a row keep their order), runs, run offsets
+  hipError_t re = hipSuccess;
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
+    size_t t = h->sort_tmp_cap;
+    re = rocprim::radix_sort_pairs(h->sort_tmp, t, keys, keys_s, vals, vals_s, (unsigned)nnz, 0, bits, s);
+  }));
+  HIP_TRY(h, re);
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
+    size_t t = h->sort_tmp_cap;
+    re = rocprim::run_length_encode(h->sort_tmp, t, keys_s, (unsigned)nnz, uniq, lens, nruns, s);
+  }));
+  HIP_TRY(h, re);
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
+    size_t t = h->sort_tmp_cap;
+    re = rocprim::exclusive_scan(h->sort_tmp, t, lens, offs, 0, (unsigned)nnz, rocprim::plus<int32_t>(), s);
+  }));
+  HIP_TRY(h, re);
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
+    hipLaunchKernelGGL(emb_segsum_kernel, dim3(nnz), dim3(kThreads), 0, s, uniq, lens, offs, nruns, vals_s, feat,
+                       weight, dy, ld_dy, dim, v32, nnz, rows, U, count);
+  }));
+  return SHAMPOO_OK;
+}
+
+shampoo_status shampoo_embedding_stats(void* handle, const float* U, const int32_t* count, int nnz, int dim,
+                                       float* R, float beta2, void* workspace, size_t ws_bytes, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(emb_check(h, nnz, dim));
+  if (!U || !count || !R) return fail(h, SHAMPOO_EINVAL, "U, count or R is NULL");
+  if (!(beta2 > 0.f && beta2 <= 1.f)) return fail(h, SHAMPOO_EINVAL, "beta2 %g outside (0, 1]", (double)beta2);
+  const EmbLayout L = emb_layout(nnz, dim);
+  if (L.splits > 1 && (!workspace || ws_bytes < L.total))
+    return fail(h, SHAMPOO_ENOMEM, "workspace %zu bytes < %zu needed", ws_bytes, L.total);
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const float c = beta2 == 1.0f ? 1.0f : 1.0f - beta2;
+  const bool al = aligned16(U) && (dim % 4) == 0;
+  const size_t pstride = align256((size_t)dim * dim * sizeof(float)) / sizeof(float);
+  float* part = L.splits > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + L.part) : nullptr;
+  std::vector<GemmProblem> probs;
+  for (int q = 0; q < L.splits; ++q) {
+    const int r0 = q * L.chunk;
+    const int kr = std::min(L.chunk, nnz - r0);
+    GemmProblem p{};
+    p.A = U + (int64_t)r0 * dim; p.B = p.A;
+    p.lda = p.ldb = dim;
+    p.a_rows = p.b_rows = kr; p.a_cols = p.b_cols = dim;
+    p.M = p.N = dim; p.K = kr;
+    p.sym = 1;
+    p.a_aligned = p.b_aligned = al;
+    p.kcount = count; p.koff = r0;
+    if (part) {
+      p.C = part + (size_t)q * pstride; p.ldc = dim; p.alpha = 1.f; p.beta = 0.f;
+    } else {
+      p.C = R; p.ldc = dim; p.alpha = c; p.beta = beta2;
+    }
+    probs.push_back(p);
+  }
+  // R = U^T U: both operands read row by row of U (k = row of U).
+  STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK, true>(h, probs, s, SHAMPOO_KCLASS_STATS)));
+  if (part) {
+    const int64_t n = (int64_t)dim * dim;
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_STATS, s, [&] {
+      hipLaunchKernelGGL(emb_reduce_kernel, dim3((unsigned)cdiv((int)cdiv(n, 4), kThreads)), dim3(kThreads), 0, s,
+                         (const float*)part, L.splits, (int64_t)pstride, n, c, beta2, R);
+    }));
+  }
+  return tables_done(h, s);
+}
+
+shampoo_status shampoo_embedding_precondition(void* handle, const float* U, const int32_t* count, int nnz, int dim,
+                                              const float* Rr, float* P, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(emb_check(h, nnz, dim));
+  if (!U || !count || !Rr || !P) return fail(h, SHAMPOO_EINVAL, "U, count, Rr or P is NULL");
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  std::vector<GemmProblem> probs(1);
+  GemmProblem& p = probs[0];
+  p = GemmProblem{};
+  p.A = U; p.lda = dim; p.a_rows = nnz; p.a_cols = dim; p.a_aligned = aligned16(U) && (dim % 4) == 0;
+  p.B = Rr; p.ldb = dim; p.b_rows = dim; p.b_cols = dim; p.b_aligned = aligned16(Rr) && (dim % 4) == 0;
+  p.C = P; p.ldc = dim; p.M = nnz; p.N = dim; p.K = dim;
+  p.alpha = 1.f; p.beta = 0.f;
+  p.mcount = count;
+  STATUS_TRY((run_gemm<float, kLayoutRow, float, kLayoutK, true>(h, probs, s, SHAMPOO_KCLASS_PRECOND)));
+  return tables_done(h, s);
+}
+
+shampoo_status shampoo_embedding_graft(void* handle, const int32_t* rows, const int32_t* count, int nnz, int dim,
+                                       const float* U, const float* P, float* W, float* D, int64_t vocab,
+                                       int64_t ldw, float eta0, int use_shampoo, float* norms, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(emb_check(h, nnz, dim));
+  if (vocab < 1 || vocab >= INT32_MAX) return fail(h, SHAMPOO_EINVAL, "vocab = %lld outside [1, 2^31 - 1)", (long long)vocab);
+  if (ldw < dim) return fail(h, SHAMPOO_EINVAL, "ldw %lld < dim %d", (long long)ldw, dim);
+  if (!rows || !count || !U || !W || !D || (use_shampoo && !P))
+    return fail(h, SHAMPOO_EINVAL, "rows, count, U, W, D or P is NULL");
+  if (!isfinite(eta0)) return fail(h, SHAMPOO_EINVAL, "eta0 is not finite");
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  GraftBlock b{};
+  b.G = U; b.P = use_shampoo ? P : nullptr; b.W = W; b.D = D; b.Mg = nullptr; b.Ps = nullptr;
+  b.ld = dim; b.rows = nnz; b.cols = dim;
+  b.wrows = rows; b.count = count; b.ldw = ldw; b.wlimit = vocab;
+  b.rows_per_chunk = std::max(1, 16384 / dim);
+  b.nchunks = cdiv(nnz, b.rows_per_chunk);
+  b.chunk_begin = 0;
+  b.vec4 = (dim % 4) == 0 && (ldw % 4) == 0 && aligned16(U) && aligned16(W) && aligned16(D) &&
+           (!b.P || aligned16(b.P));
+  const int total = b.nchunks;
+  const void* d = nullptr;
+  STATUS_TRY(upload_table(h, &b, sizeof(b), s, &d));
+  STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)total * 2 * sizeof(double)));
+  double* part = static_cast<double*>(h->partial);
+  const GraftBlock* db = static_cast<const GraftBlock*>(d);
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
+    hipLaunchKernelGGL(graft_pass1_kernel<float>, dim3(total), dim3(kThreads), 0, s, db, 1, total, 0.f, use_shampoo,
+                       part);
+  }));
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
+    hipLaunchKernelGGL(graft_pass2_kernel<float>, dim3(total), dim3(kThreads), 0, s, db, 1, total, eta0, 0.f,
+                       use_shampoo, (const double*)part, norms);
+  }));
+  return tables_done(h, s);
 }
 
 }  // extern "C"

@@ -20,6 +20,11 @@ Workloads (shapes follow the paper's experiments; no dataset is used):
 * C5  a 32768 x 1024 embedding (32 row blocks of 1024 x 1024) plus 200
       square blocks, side drawn uniformly from {128, 256, 512, 1024, 2048};
       gradients N(0, 1e-3) stored as bfloat16.
+* C6  embedding lookups: a vocab x dim table read by token lookups whose
+      rows follow a Zipf law (P(rank k) ~ (k + 1)^-s, s = 1.07, ranks mapped
+      to rows by a keyed permutation); one-hot (one row per output row) or
+      multi-hot bags of 1..8 rows averaged (weights 1/bag size); output
+      gradients dy ~ N(0, 1e-3).
 """
 from __future__ import annotations
 
@@ -172,3 +177,45 @@ def c5_grad_bf16(block, step, shape):
 
 def c5_weight(block, shape):
     return gaussian(shape, 0.02 ** 2, C5, 2, block)
+
+
+# ---------------------------------------------------------------- C6
+C6 = 6
+C6_S = 1.07
+
+
+def zipf_rows(n, vocab, s, *key):
+    """n int32 row ids in [0, vocab), P(rank k) proportional to (k+1)^-s, rank
+    k stored at row perm[k] of a keyed permutation."""
+    r = rng(*key)
+    w = 1.0 / np.arange(1, vocab + 1, dtype=np.float64) ** s
+    ranks = r.choice(vocab, size=n, p=w / w.sum())
+    perm = r.permutation(vocab)
+    return perm[ranks].astype(np.int32)
+
+
+def c6_lookup(step, nnz, vocab, multi=False, seed=0):
+    """(idx, feat, weight, m) of one step's lookups.  One-hot: m = nnz,
+    feat = weight = None.  Multi-hot: bags of 1..8 entries, each bag one
+    output row, weights 1 / bag size; nnz entries in total."""
+    idx = zipf_rows(nnz, vocab, C6_S, C6, seed, 0, step)
+    if not multi:
+        return idx, None, None, nnz
+    r = rng(C6, seed, 1, step)
+    sizes = []
+    left = nnz
+    while left > 0:
+        b = int(min(left, r.integers(1, 9)))
+        sizes.append(b)
+        left -= b
+    feat = np.repeat(np.arange(len(sizes), dtype=np.int32), sizes)
+    weight = np.repeat(1.0 / np.array(sizes, dtype=np.float32), sizes).astype(np.float32)
+    return idx, feat, weight, len(sizes)
+
+
+def c6_dy(step, m, dim, seed=0):
+    return gaussian((m, dim), 1e-3, C6, seed, 2, step)
+
+
+def c6_table(vocab, dim, seed=0):
+    return gaussian((vocab, dim), 0.02 ** 2, C6, seed, 3)

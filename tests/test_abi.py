@@ -28,7 +28,9 @@ def lib():
 def test_header_declares_the_boundary():
     names = declared()
     for n in ("shampoo_update_stats", "shampoo_inv_root_batched", "shampoo_precondition", "shampoo_graft",
-              "shampoo_create", "shampoo_destroy", "shampoo_last_error", "shampoo_inv_root_workspace_bytes"):
+              "shampoo_create", "shampoo_destroy", "shampoo_last_error", "shampoo_inv_root_workspace_bytes",
+              "shampoo_embedding_rows", "shampoo_embedding_stats", "shampoo_embedding_precondition",
+              "shampoo_embedding_graft", "shampoo_embedding_workspace_bytes"):
         assert n in names
 
 
@@ -56,6 +58,15 @@ def test_host_only_entry_points(lib):
     assert 5 * 4 * 1024 ** 2 <= w32 < 5 * 4 * 1024 ** 2 + 10 ** 6
     assert 6 * 8 * 1024 ** 2 <= w64 < 6 * 8 * 1024 ** 2 + 10 ** 6
     assert wa >= w32 + w64 - 10 ** 6
+    # embedding workspace: 7 int32 arrays of nnz plus split-K partials of dim^2
+    assert lib.shampoo_embedding_workspace_bytes(0, 64) == 0
+    assert lib.shampoo_embedding_workspace_bytes(10, 0) == 0
+    assert lib.shampoo_embedding_workspace_bytes(10, 4097) == 0
+    assert lib.shampoo_embedding_workspace_bytes((1 << 26) + 1, 64) == 0
+    small = lib.shampoo_embedding_workspace_bytes(100, 64)      # one split: no partials
+    assert 7 * 4 * 100 <= small < 7 * 4 * 100 + 4096
+    big = lib.shampoo_embedding_workspace_bytes(65536, 1024)    # split-K over 36 upper tiles
+    assert big >= 7 * 4 * 65536 + 2 * 4 * 1024 ** 2
 
 
 def test_struct_layouts_match_header(lib):

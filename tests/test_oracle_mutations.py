@@ -51,7 +51,10 @@ MUTATIONS = [
      [P.pin_embedding_worked_example]),
     ("_valid_entries", "(idx >= 0) & (idx < vocab)", "(idx >= -1) & (idx < vocab)",
      [P.pin_embedding_worked_example]),
-    ("embedding_rows", "rows = np.unique(i)", "rows = i", [P.pin_embedding_lookup_matrix]),
+    ("embedding_rows", "acc[r] += w[e] * dy[f[e]]", "acc[r] = w[e] * dy[f[e]]",
+     [P.pin_embedding_lookup_matrix, P.pin_embedding_worked_example]),
+    ("embedding_rows", "rows = np.array(sorted(acc), dtype=np.int64)", "rows = np.array(list(acc), dtype=np.int64)",
+     [P.pin_embedding_lookup_matrix, P.pin_embedding_worked_example]),
 ]
 
 
