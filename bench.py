@@ -145,7 +145,7 @@ def run_c4(args, torch, B):
         step()
     torch.cuda.synchronize()
     B.shampoo_timing_enable(h, True)
-    for c in range(6):
+    for c in range(len(B.KCLASS_NAMES)):
         B.shampoo_timing_read(h, c)
     t0 = time.perf_counter()
     for s_ in range(args.steps):
@@ -153,7 +153,7 @@ def run_c4(args, torch, B):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     B.shampoo_timing_enable(h, False)
-    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
     B.shampoo_destroy(h)
     K = args.steps
     flops_stats = K * nb * 2 * d * d * (d + 1)
@@ -181,6 +181,90 @@ def run_c4(args, torch, B):
     print(json.dumps(out), flush=True)
 
 
+def run_c6(args, torch, B):
+    """C6: an embedding table (vocab x 1024, default 32768 rows: the C5
+    embedding) read by 65536 one-hot Zipf lookups per step.  A step is the
+    compaction of the lookup gradient, the 1024 x 1024 statistic U^T U over
+    the active rows, the one-sided preconditioned rows U R^(-1/2) and the
+    grafted update of the active rows.  The root refresh (p = 2) is timed
+    separately.  Each step has its own lookups; all are resident in HBM."""
+    from synth import configs as cfg
+    dev = torch.device("cuda:0")
+    vocab, nnz, dim, eta0 = args.vocab, args.lookups, 1024, 1e-2
+    nsteps = args.warmup + args.steps
+    log(f"generating C6 lookups: {nsteps} steps of {nnz} over {vocab} rows")
+    idx_d, dy_d = [], []
+    for t in range(nsteps):
+        idx, _, _, m = cfg.c6_lookup(t + 1, nnz, vocab)
+        idx_d.append(torch.from_numpy(idx).to(dev))
+        dy_d.append(torch.from_numpy(cfg.c6_dy(t + 1, m, dim)).to(dev))
+    W = 0.02 * torch.randn(vocab, dim, device=dev, generator=torch.Generator(device=dev).manual_seed(6))
+    D = torch.zeros(vocab, dim, device=dev)
+    R = cfg.wishart_bartlett_device(dim, 100 * nnz, 1e-3, torch, dev, cfg.C6, 8, 0)
+    Rr = torch.zeros(dim, dim, device=dev)
+    rows = torch.zeros(nnz, dtype=torch.int32, device=dev)
+    U = torch.zeros(nnz, dim, device=dev)
+    P = torch.zeros(nnz, dim, device=dev)
+    counts = torch.zeros(nsteps, 2, dtype=torch.int32, device=dev)
+    ws = torch.empty(B.shampoo_embedding_workspace_bytes(nnz, dim), dtype=torch.uint8, device=dev)
+    h = B.shampoo_create(0)
+    prm = B.shampoo_root_params_default(p=2, eps=1e-6)
+    rws = torch.empty(B.shampoo_inv_root_workspace_bytes([dim], prm.precision), dtype=torch.uint8, device=dev)
+    info = torch.zeros(8, dtype=torch.int32, device=dev)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    B.shampoo_inv_root_batched(h, [R], [Rr], prm, rws, info)
+    torch.cuda.synchronize()
+    root_ms = (time.perf_counter() - t0) * 1e3
+
+    def step(t):
+        c = counts[t]
+        B.shampoo_embedding_rows(h, idx_d[t], None, None, vocab, dy_d[t], rows, U, c, ws)
+        B.shampoo_embedding_stats(h, U, c, R, 1.0, ws)
+        B.shampoo_embedding_precondition(h, U, c, Rr, P)
+        B.shampoo_embedding_graft(h, rows, c, U, P, W, D, eta0)
+
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+    B.shampoo_timing_enable(h, True)
+    for c in range(len(B.KCLASS_NAMES)):
+        B.shampoo_timing_read(h, c)
+    t0 = time.perf_counter()
+    for t in range(args.warmup, nsteps):
+        step(t)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    B.shampoo_timing_enable(h, False)
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
+    B.shampoo_destroy(h)
+    K = args.steps
+    u = counts[args.warmup:, 0].cpu().numpy().astype(np.float64)
+    flops_stats = float(np.sum(u)) * dim * (dim + 1)          # upper triangle of U^T U
+    flops_prec = float(np.sum(u)) * 2 * dim * dim
+    bytes_graft = float(np.sum(u)) * dim * 28
+    bytes_emb = K * nnz * dim * 8.0                          # dy read + U written
+    ms_step = elapsed * 1e3 / K
+    st_ms, pr_ms = times["stats"][0], times["precond"][0]
+    out = {
+        "metric": f"C6 embedding step: lookups/s ({vocab} x {dim} table, {nnz} one-hot Zipf lookups per step)",
+        "value": K * nnz / elapsed, "unit": "lookups/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": f"C6: embedding {vocab}x{dim}, {nnz} Zipf(1.07) one-hot lookups/step; compact "
+                               "rows + R += U^T U + U R^-1/2 + row-indexed AdaGrad graft",
+                   "vocab": vocab, "dim": dim, "lookups": nnz},
+        "active_rows_mean": float(np.mean(u)),
+        "phases_ms_per_step": {c: v[0] / K for c, v in times.items()},
+        "kernels": {"stats_tflops": flops_stats / (st_ms * 1e-3) / 1e12,
+                    "precond_tflops": flops_prec / (pr_ms * 1e-3) / 1e12,
+                    "graft_gbs": bytes_graft / (times["graft"][0] * 1e-3) / 1e9,
+                    "emb_compaction_gbs": bytes_emb / (times["emb"][0] * 1e-3) / 1e9},
+        "root_refresh": {"roots": 1, "p": 2, "ms": root_ms, "iters": B.decode_root_info(info)[0]["iters"]},
+    }
+    print(json.dumps(out), flush=True)
+
+
 def run_c3(args, torch, B):
     """C3: 32 ill-conditioned 2048 x 2048 matrices (log-uniform spectrum in
     [1e-6, 1e2]), scaled damping 1e-6 * lambda_max, one grouped call per p in
@@ -203,14 +287,14 @@ def run_c3(args, torch, B):
         B.shampoo_inv_root_batched(h, As[:2], Xs[:2], prm, ws, info)   # warm-up
         torch.cuda.synchronize()
         B.shampoo_timing_enable(h, True)
-        for c in range(6):
+        for c in range(len(B.KCLASS_NAMES)):
             B.shampoo_timing_read(h, c)
         t0 = time.perf_counter()
         B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info)
         torch.cuda.synchronize()
         ms = (time.perf_counter() - t0) * 1e3
         B.shampoo_timing_enable(h, False)
-        times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
+        times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
         inf = B.decode_root_info(info)
         prods = 2 if p == 2 else 3
         pr64 = sum(max(0, (prods + 1) * i["iters"] - 1) for i in inf if i["precision"] == 64)
@@ -244,17 +328,20 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--blocks", type=int, default=96)
-    ap.add_argument("--workload", choices=["c2", "c3", "c4"], default="c2",
+    ap.add_argument("--workload", choices=["c2", "c3", "c4", "c6"], default="c2",
                     help="c2 (default): the metric's workload; c3: ill-conditioned roots; c4: the "
-                         "transformer-layer step")
+                         "transformer-layer step; c6: the embedding-table step")
+    ap.add_argument("--vocab", type=int, default=32768, help="c6: table rows")
+    ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="before the steps, copy a buffer of this size once (a plain copy kernel of known "
                          "traffic, to scale FETCH_SIZE/WRITE_SIZE counter readings)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(json.dumps({"error": "this implementation runs on one GPU; multi-GPU sharding of the blocks "
-                                   "is described in DESIGN.md and not built", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "this implementation runs on one GPU only (blocks would shard across GPUs "
+                                   "with no communication inside the optimizer; that path is not built)",
+                          "n_gpus": args.gpus}))
         sys.exit(2)
 
     import torch
@@ -264,6 +351,8 @@ def main():
         return run_c4(args, torch, B)
     if args.workload == "c3":
         return run_c3(args, torch, B)
+    if args.workload == "c6":
+        return run_c6(args, torch, B)
     dev = torch.device("cuda:0")
     nb, n, k, p, eps, eta0 = args.blocks, 1024, 4096, 4, 1e-6, 1e-2
     log(f"generating {nb} blocks")
@@ -310,7 +399,7 @@ def main():
         torch.cuda.synchronize()
         log(f"warmup step {w + 1}/{args.warmup} done")
     B.shampoo_timing_enable(h, True)
-    for c in range(6):
+    for c in range(len(B.KCLASS_NAMES)):
         B.shampoo_timing_read(h, c)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
@@ -320,7 +409,7 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     B.shampoo_timing_enable(h, False)
-    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(6)}
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
 
     # algorithmic work
     # Products per matrix: p = 4 takes X M1, M1 M1, (M1^2)^2 and M1^4 M per

@@ -236,9 +236,10 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
  *
  * Compact form (written by shampoo_embedding_rows, read by the others):
  *   rows   int32[nnz]: the active rows in ascending order, then -1;
- *   U      fp32 nnz x dim (row stride dim): U[i] = G[rows[i]] for i < u, the
- *          sum taken over the entries of that row in entry order
- *          (deterministic); zero rows for i >= u;
+ *   U      fp32 nnz x dim (row stride dim): U[i] = G[rows[i]] for i < u,
+ *          summed over the entries of that row in entry order within fixed
+ *          chunks of 64 sorted entries, the chunk sums then added in order
+ *          (deterministic); rows i >= u are not written;
  *   count  int32[2]: count[0] = u (active rows), count[1] = entries dropped
  *          because idx is outside [0, vocab) or feat outside [0, m).
  */
@@ -265,8 +266,9 @@ shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const in
 /*
  * R = beta2 R + c U^T U over the first count[0] rows of U (c = 1 if
  * beta2 == 1 else 1 - beta2): the statistic of the table, dim x dim, kept
- * exactly symmetric.  Split over the rows of U in fixed chunks whose partial
- * products are added in chunk order (deterministic).
+ * exactly symmetric.  The active rows are split into a fixed number of
+ * equal parts (set from nnz and dim); their partial products are added in
+ * part order (deterministic).
  * Errors: EINVAL (NULL pointers, sizes, beta2 outside (0, 1]), ENOMEM.
  */
 shampoo_status shampoo_embedding_stats(void* handle, const float* U, const int32_t* count, int nnz, int dim,

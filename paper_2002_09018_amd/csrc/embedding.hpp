@@ -26,15 +26,89 @@ __global__ __launch_bounds__(kThreads) void emb_keys_kernel(const int32_t* __res
   lens[e] = 0;  // run lengths past the last run stay 0 for the offset scan
 }
 
-// One workgroup per potential run i of the sorted keys: row i of U is the
-// weighted sum, in entry order, of the dy rows of the entries of run i;
-// rows past the active ones (and the dropped-entry run) are zero, their row
-// id -1.  count[0] = active rows, count[1] = dropped entries.
-__global__ __launch_bounds__(kThreads) void emb_segsum_kernel(
+// Segment sums of the sorted entries in fixed chunks of kEmbChunk entries,
+// one workgroup per chunk.  A run (the entries of one table row) that lies
+// inside the chunk is summed into its row of U directly; the run holding
+// the chunk's first entry, if it reaches outside the chunk, goes to partial
+// slot 0 of the chunk, and the chunk's last run, if different and reaching
+// past the end, to slot 1.  Entries are added in sorted (= entry) order.
+constexpr int kEmbChunk = 64;
+
+template <bool VEC>
+__device__ __forceinline__ void emb_chunk_cols(int c, const int32_t* __restrict__ uniq, const int32_t* __restrict__ lens,
+                                               const int32_t* __restrict__ offs, int R, const int32_t* __restrict__ vals,
+                                               const int32_t* __restrict__ feat, const float* __restrict__ weight,
+                                               const float* __restrict__ dy, int64_t ld_dy, int dim, int32_t vocab,
+                                               int nnz, float* __restrict__ U, float* __restrict__ part) {
+  const int t0 = c * kEmbChunk, t1 = min(t0 + kEmbChunk, nnz);
+  // run holding t0: the last run starting at or before t0
+  int lo = 0, hi = R - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (offs[mid] <= t0) lo = mid; else hi = mid - 1;
+  }
+  constexpr int W = VEC ? 4 : 1;
+  for (int col = W * threadIdx.x; col < dim; col += W * kThreads) {
+    int i = lo;
+    int rs = offs[i], re = rs + lens[i];
+    bool skip = uniq[i] == vocab;
+    f4v acc = {0.f, 0.f, 0.f, 0.f};
+    auto flush = [&]() {
+      if (skip) return;
+      float* dst;
+      if (rs >= t0 && re <= t1) dst = U + (int64_t)i * dim;              // whole run in this chunk
+      else if (i == lo) dst = part + ((int64_t)c * 2 + 0) * dim;         // run of the first entry
+      else dst = part + ((int64_t)c * 2 + 1) * dim;                      // last run, continues
+      if (VEC) gstore<f4v>(dst + col, acc);
+      else gstore<float>(dst + col, acc[0]);
+    };
+    for (int t = t0; t < t1; ++t) {
+      if (t >= re) {
+        flush();
+        ++i;
+        rs = offs[i];
+        re = rs + lens[i];
+        skip = uniq[i] == vocab;
+        acc = f4v{0.f, 0.f, 0.f, 0.f};
+      }
+      if (skip) continue;
+      const int e = vals[t];
+      const int f = feat ? feat[e] : e;
+      const float w = weight ? weight[e] : 1.f;
+      const float* src = dy + (int64_t)f * ld_dy + col;
+      if (VEC) acc += w * gload<f4v>(src);
+      else acc[0] += w * gload<float>(src);
+    }
+    flush();
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void emb_chunk_kernel(
     const int32_t* __restrict__ uniq, const int32_t* __restrict__ lens, const int32_t* __restrict__ offs,
     const int32_t* __restrict__ nruns, const int32_t* __restrict__ vals, const int32_t* __restrict__ feat,
     const float* __restrict__ weight, const float* __restrict__ dy, int64_t ld_dy, int dim, int32_t vocab, int nnz,
-    int32_t* __restrict__ rows, float* __restrict__ U, int32_t* __restrict__ count) {
+    float* __restrict__ U, float* __restrict__ part) {
+  const int c = blockIdx.x;
+  if (c * kEmbChunk >= nnz) return;
+  const int R = *nruns;
+  if (R < 1) return;
+  const bool vec = (dim & 3) == 0 && (ld_dy & 3) == 0 && (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(U) & 15) == 0;
+  if (vec) emb_chunk_cols<true>(c, uniq, lens, offs, R, vals, feat, weight, dy, ld_dy, dim, vocab, nnz, U, part);
+  else emb_chunk_cols<false>(c, uniq, lens, offs, R, vals, feat, weight, dy, ld_dy, dim, vocab, nnz, U, part);
+}
+
+// One workgroup per potential run i: the row id (-1 past the active rows),
+// the counts (count[0] = active rows, count[1] = dropped entries), and for a
+// run that spans several chunks the sum of its chunk partials in chunk
+// order.  Rows of U at or past the active count are not written.
+__global__ __launch_bounds__(kThreads) void emb_fix_kernel(const int32_t* __restrict__ uniq,
+                                                          const int32_t* __restrict__ lens,
+                                                          const int32_t* __restrict__ offs,
+                                                          const int32_t* __restrict__ nruns, int dim, int32_t vocab,
+                                                          int nnz, const float* __restrict__ part,
+                                                          int32_t* __restrict__ rows, float* __restrict__ U,
+                                                          int32_t* __restrict__ count) {
   const int i = blockIdx.x;
   if (i >= nnz) return;
   const int R = *nruns;
@@ -45,38 +119,17 @@ __global__ __launch_bounds__(kThreads) void emb_segsum_kernel(
   }
   const bool active = i < R && uniq[i] != vocab;
   if (threadIdx.x == 0) rows[i] = active ? uniq[i] : -1;
-  float* u = U + (int64_t)i * dim;
-  const bool vec = (dim & 3) == 0 && (ld_dy & 3) == 0 && (reinterpret_cast<uintptr_t>(dy) & 15) == 0 &&
-                   (reinterpret_cast<uintptr_t>(U) & 15) == 0;
-  if (vec) {
-    for (int c = 4 * threadIdx.x; c < dim; c += 4 * kThreads) {
-      f4v acc = {0.f, 0.f, 0.f, 0.f};
-      if (active) {
-        const int t0 = offs[i], t1 = t0 + lens[i];
-        for (int t = t0; t < t1; ++t) {
-          const int e = vals[t];
-          const int f = feat ? feat[e] : e;
-          const float w = weight ? weight[e] : 1.f;
-          const f4v v = gload<f4v>(dy + (int64_t)f * ld_dy + c);
-          acc += w * v;
-        }
-      }
-      gstore<f4v>(u + c, acc);
+  if (!active) return;
+  const int rs = offs[i], re = rs + lens[i];
+  const int c0 = rs / kEmbChunk, c1 = (re - 1) / kEmbChunk;
+  if (c0 == c1) return;  // summed in place by its chunk
+  for (int col = threadIdx.x; col < dim; col += kThreads) {
+    float acc = 0.f;
+    for (int c = c0; c <= c1; ++c) {
+      const int slot = (c == c0 && rs != c0 * kEmbChunk) ? 1 : 0;
+      acc += gload<float>(part + ((int64_t)c * 2 + slot) * dim + col);
     }
-  } else {
-    for (int c = threadIdx.x; c < dim; c += kThreads) {
-      float acc = 0.f;
-      if (active) {
-        const int t0 = offs[i], t1 = t0 + lens[i];
-        for (int t = t0; t < t1; ++t) {
-          const int e = vals[t];
-          const int f = feat ? feat[e] : e;
-          const float w = weight ? weight[e] : 1.f;
-          acc += w * gload<float>(dy + (int64_t)f * ld_dy + c);
-        }
-      }
-      gstore<float>(u + c, acc);
-    }
+    gstore<float>(U + (int64_t)i * dim + col, acc);
   }
 }
 

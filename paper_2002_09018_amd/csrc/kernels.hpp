@@ -36,11 +36,15 @@ struct GemmProblem {
   int tile_begin; // first logical tile of this problem
   int a_aligned, b_aligned;
   // Optional device-side limits (embedding rows, whose count is known only
-  // on the device): K is cut to *kcount - koff (>= 0) and the k-extent of
-  // the operands with it; tiles starting at or past row *mcount are skipped.
+  // on the device), honoured by the LIM instantiation:
+  //   ksplit == 0: K is cut to *kcount - koff (>= 0);
+  //   ksplit  > 0: split koff of ksplit equal parts of the first *kcount
+  //                k-indices (parts rounded up to the 16-deep k stage);
+  // the k-extent of the operands is cut with K; tiles starting at or past
+  // row *mcount are skipped.
   const int* kcount;
   const int* mcount;
-  int koff, pad;
+  int koff, ksplit;
 };
 
 __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int nprob, int t) {
@@ -59,7 +63,9 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
                                                                int nprob, int total_tiles) {
   __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
   __shared__ __attribute__((aligned(16))) float sb0[StageElems<float, LB>::value], sb1[StageElems<float, LB>::value];
-  const int t = xcd_remap(blockIdx.x, gridDim.x);
+  // LIM: work depends on device-side counts and sits in the first logical
+  // tiles; dispatch order (round robin over the XCDs) spreads it evenly.
+  const int t = LIM ? (int)blockIdx.x : xcd_remap(blockIdx.x, gridDim.x);
   if (t >= total_tiles) return;
   const GemmProblem P = probs[find_problem_gemm(probs, nprob, t)];
   int ti, tj;
@@ -73,7 +79,20 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   Operand<SB> B{reinterpret_cast<const SB*>(P.B), P.ldb, P.b_rows, P.b_cols, P.b_aligned != 0};
   int K = P.K;
   if (LIM && P.kcount) {
-    K = min(K, max(0, *P.kcount - P.koff));
+    const int cnt = *P.kcount;
+    if (P.ksplit > 0) {
+      const int kc = ((cnt + P.ksplit - 1) / P.ksplit + 15) & ~15;
+      const int k0 = P.koff * kc;
+      K = max(0, min(kc, cnt - k0));
+      if (K > 0) {
+        if (LA == kLayoutK) A.ptr += (int64_t)k0 * A.ld; else A.ptr += k0;
+        if (LB == kLayoutK) B.ptr += (int64_t)k0 * B.ld; else B.ptr += k0;
+        if (LA == kLayoutK) A.rows -= k0; else A.cols -= k0;
+        if (LB == kLayoutK) B.rows -= k0; else B.cols -= k0;
+      }
+    } else {
+      K = min(K, max(0, cnt - P.koff));
+    }
     // the k-extent is the stored rows of a k-major operand, else its columns
     if (LA == kLayoutK) A.rows = min(A.rows, K); else A.cols = min(A.cols, K);
     if (LB == kLayoutK) B.rows = min(B.rows, K); else B.cols = min(B.cols, K);
@@ -914,15 +933,20 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
                                                               int total_chunks, float eta0, float beta1,
                                                               int use_shampoo, const double* __restrict__ partial,
                                                               float* __restrict__ norms) {
+  __shared__ double red[kThreads / 64];
   const int t = blockIdx.x;
   if (t >= total_chunks) return;
   const int bi = find_block_graft(blocks, nb, t);
   const GraftBlock B = blocks[bi];
+  // the block's norms from its chunk partials, reduced cooperatively in a
+  // fixed order (every workgroup of the block gets the same bits)
   double smg = 0.0, sps = 0.0;
-  for (int q = 0; q < B.nchunks; ++q) {
+  for (int q = threadIdx.x; q < B.nchunks; q += kThreads) {
     smg += partial[2 * (B.chunk_begin + q) + 0];
     sps += partial[2 * (B.chunk_begin + q) + 1];
   }
+  smg = block_sum(smg, red);
+  sps = block_sum(sps, red);
   const double nm = sqrt(smg), nps = sqrt(sps);
   double eta;
   if (use_shampoo) eta = nps > 0.0 ? (double)eta0 * nm / nps : 0.0;

@@ -629,12 +629,13 @@ std::vector<NewtonJob<T>> newton_table(const shampoo_root_job* jobs, int njobs, 
 
 // ---------------------------------------------------------------- embeddings
 // Workspace of the embedding calls: seven int32 arrays of nnz (sort keys and
-// values in and out, run keys, run lengths, run offsets), the run count, and
-// the split-K partial statistics (splits x dim^2 fp32).
+// values in and out, run keys, run lengths, run offsets), the run count, the
+// chunk partial sums of the compaction (2 rows of dim per chunk of entries),
+// and the split-K partial statistics (splits x dim^2 fp32).
 struct EmbLayout {
-  size_t keys = 0, vals = 0, keys_s = 0, vals_s = 0, uniq = 0, lens = 0, offs = 0, nruns = 0, part = 0;
+  size_t keys = 0, vals = 0, keys_s = 0, vals_s = 0, uniq = 0, lens = 0, offs = 0, nruns = 0, cpart = 0, part = 0;
   size_t total = 0;
-  int splits = 1, chunk = 0;
+  int splits = 1;
 };
 
 EmbLayout emb_layout(int nnz, int dim) {
@@ -649,15 +650,14 @@ EmbLayout emb_layout(int nnz, int dim) {
   L.lens = off; off += a;
   L.offs = off; off += a;
   L.nruns = off; off += 256;
-  // Split-K of R += U^T U: about 1024 workgroups over the upper tiles of R,
-  // each split at least 512 rows of U (a multiple of the 16-deep k stage).
+  L.cpart = off; off += align256((size_t)cdiv(nnz, kEmbChunk) * 2 * dim * sizeof(float));
+  // Split-K of R += U^T U: about 1024 workgroups over the upper tiles of R.
+  // The rows of a split are set on the device from the active-row count u
+  // (ceil(u / splits) rounded up to the 16-deep k stage).
   const int t = cdiv(dim, kTile);
   const int tiles = t * (t + 1) / 2;
-  int S = std::max(1, std::min(cdiv(1024, tiles), cdiv(nnz, 512)));
-  int chunk = cdiv(cdiv(nnz, S), 16) * 16;
-  S = cdiv(nnz, chunk);
+  const int S = std::max(1, std::min(cdiv(1024, tiles), cdiv(nnz, 256)));
   L.splits = S;
-  L.chunk = chunk;
   L.part = off;
   if (S > 1) off += (size_t)S * align256((size_t)dim * dim * sizeof(float));
   L.total = off;
@@ -1012,6 +1012,7 @@ shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const in
   int32_t* lens = reinterpret_cast<int32_t*>(ws + L.lens);
   int32_t* offs = reinterpret_cast<int32_t*>(ws + L.offs);
   int32_t* nruns = reinterpret_cast<int32_t*>(ws + L.nruns);
+  float* cpart = reinterpret_cast<float*>(ws + L.cpart);
   const int32_t v32 = (int32_t)vocab;
   int bits = 1;
   while (bits < 31 && (int64_t(1) << bits) <= vocab) ++bits;  // keys lie in [0, vocab]
@@ -1044,8 +1045,12 @@ shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const in
   }));
   HIP_TRY(h, re);
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
-    hipLaunchKernelGGL(emb_segsum_kernel, dim3(nnz), dim3(kThreads), 0, s, uniq, lens, offs, nruns, vals_s, feat,
-                       weight, dy, ld_dy, dim, v32, nnz, rows, U, count);
+    hipLaunchKernelGGL(emb_chunk_kernel, dim3(cdiv(nnz, kEmbChunk)), dim3(kThreads), 0, s, uniq, lens, offs, nruns,
+                       vals_s, feat, weight, dy, ld_dy, dim, v32, nnz, U, cpart);
+  }));
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
+    hipLaunchKernelGGL(emb_fix_kernel, dim3(nnz), dim3(kThreads), 0, s, uniq, lens, offs, nruns, dim, v32, nnz,
+                       (const float*)cpart, rows, U, count);
   }));
   return SHAMPOO_OK;
 }
@@ -1069,16 +1074,14 @@ shampoo_status shampoo_embedding_stats(void* handle, const float* U, const int32
   float* part = L.splits > 1 ? reinterpret_cast<float*>(static_cast<char*>(workspace) + L.part) : nullptr;
   std::vector<GemmProblem> probs;
   for (int q = 0; q < L.splits; ++q) {
-    const int r0 = q * L.chunk;
-    const int kr = std::min(L.chunk, nnz - r0);
     GemmProblem p{};
-    p.A = U + (int64_t)r0 * dim; p.B = p.A;
+    p.A = U; p.B = U;
     p.lda = p.ldb = dim;
-    p.a_rows = p.b_rows = kr; p.a_cols = p.b_cols = dim;
-    p.M = p.N = dim; p.K = kr;
+    p.a_rows = p.b_rows = nnz; p.a_cols = p.b_cols = dim;
+    p.M = p.N = dim; p.K = nnz;
     p.sym = 1;
     p.a_aligned = p.b_aligned = al;
-    p.kcount = count; p.koff = r0;
+    p.kcount = count; p.koff = q; p.ksplit = L.splits;  // split q of the active rows
     if (part) {
       p.C = part + (size_t)q * pstride; p.ldc = dim; p.alpha = 1.f; p.beta = 0.f;
     } else {
