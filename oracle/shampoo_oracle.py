@@ -39,6 +39,10 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
   the dense lookup-matrix route G = S dy (S^T S = I for distinct one-hot
   rows gives G^T G = dy^T dy), a hand-worked 5-row example with repeated
   rows and weights, and the dropping of out-of-range entries.
+* ``lamb_graft_update`` -- the LARS/LAMB layer-wise magnitude of the same
+  appendix paragraph (R12).  Pinned by the step-norm identity
+  ||dW||_F = eta0 ||W||_F, invariance under scaling G and P, and hand-worked
+  1 x 2 and 1 x 1 momentum examples.
 * ``graft_update``      -- Algorithm 2 (momentum on both directions) and the
   appendix "Further details on experiments", paragraph "Layer wise learning
   rates" (AdaGrad magnitude, Shampoo direction).  Pinned by the step-norm
@@ -64,6 +68,10 @@ R7  The ridge epsilon*I is added exactly once, at the root; statistics
 R8  D^{-1/2} o G is 0 where D is 0 (then G is 0 as well).
 R9  When ||P||_F = 0 the step size is 0.
 R10 The input to a root is symmetrised, A_s = (A + A^T)/2, before use.
+R12 The LARS/LAMB layer-wise learning rate ||W||_F / ||G||_F of the appendix,
+    grafted like the AdaGrad magnitude, makes the step eta0 ||W||_F long
+    along the unit Shampoo direction (along G / ||G||_F before the roots);
+    ||W||_F is that of the block before the step.
 R11 Embedding statistics are those of the exact sparse gradient G of the
     lookup: G^T G = dy^T (S^T S) dy with S the lookup matrix.  The appendix's
     simplification S^T S = I (or diagonal for multi-hot) holds when the
@@ -349,6 +357,43 @@ def graft_update(W, D, G, P=None, eta0=1.0, beta1=0.0, Mg=None, Ps=None,
         W_new = W - eta * Mg_new
     return dict(W=W_new, D=D, Mg=Mg_new, Ps=Ps_new, eta=eta, norm_mg=nm,
                 norm_ps=nps)
+
+
+def lamb_graft_update(W, G, P=None, eta0=1.0, beta1=0.0, Mg=None, Ps=None,
+                      use_shampoo=True):
+    """Layer-wise (LARS/LAMB) graft, the alternative magnitude of the
+    appendix "Further details on experiments", paragraph "Layer wise learning
+    rates" (R12): the layer learning rate eta0 ||W||_F / ||G||_F applied to
+    the first-order step G gives a step of norm eta0 ||W||_F, kept along the
+    unit Shampoo direction.
+
+        Mg <- beta1 Mg + (1 - beta1) G
+        if use_shampoo:
+            Ps  <- beta1 Ps + (1 - beta1) P
+            eta <- eta0 ||W||_F / ||Ps||_F      (0 when ||Ps||_F = 0, R9)
+            W   <- W - eta Ps
+        else:
+            eta <- eta0 ||W||_F / ||Mg||_F      (LARS step before the roots)
+            W   <- W - eta Mg
+
+    ||W||_F is taken before the step.  Returns W, Mg, Ps, eta, norm_w and
+    norm_dir.
+    """
+    W = _f64(W)
+    Gf = _f64(G)
+    Mg_new = Gf if beta1 == 0.0 or Mg is None else beta1 * _f64(Mg) + (1.0 - beta1) * Gf
+    Ps_new = None if Ps is None else _f64(Ps)
+    nw = float(np.linalg.norm(W))
+    if use_shampoo:
+        Pf = _f64(P)
+        Ps_new = Pf if beta1 == 0.0 or Ps is None else beta1 * _f64(Ps) + (1.0 - beta1) * Pf
+        direction = Ps_new
+    else:
+        direction = Mg_new
+    nd = float(np.linalg.norm(direction))
+    eta = 0.0 if nd == 0.0 else eta0 * nw / nd
+    return dict(W=W - eta * direction, Mg=Mg_new, Ps=Ps_new, eta=eta, norm_w=nw,
+                norm_dir=nd)
 
 
 # --------------------------------------------------------------------------

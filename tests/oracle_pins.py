@@ -453,4 +453,42 @@ def pin_graft_momentum_1x1(o):
     assert o3['eta'] == 0.0 and o3['W'][0, 0] == o2['W'][0, 0]
 
 
+def pin_lamb_step_norm(o):
+    """LARS/LAMB magnitude: ||dW||_F = eta0 ||W||_F along -P/||P||_F (and
+    along -G/||G||_F before the roots), unchanged when G or P is scaled."""
+    r = rng(54)
+    W, G, P = r.standard_normal((6, 4)), r.standard_normal((6, 4)), r.standard_normal((6, 4))
+    nw = np.linalg.norm(W)
+    out = o.lamb_graft_update(W, G, P, eta0=0.2)
+    dW = out['W'] - W
+    assert abs(np.linalg.norm(dW) - 0.2 * nw) < 1e-13 * nw
+    assert _relf(dW, -0.2 * nw * P / np.linalg.norm(P)) < 1e-13
+    out2 = o.lamb_graft_update(W, 7.0 * G, 3.0 * P, eta0=0.2)
+    assert _relf(out2['W'], out['W']) < 1e-14
+    out3 = o.lamb_graft_update(W, G, None, eta0=0.2, use_shampoo=False)
+    assert _relf(out3['W'] - W, -0.2 * nw * G / np.linalg.norm(G)) < 1e-13
+
+
+def pin_lamb_worked(o):
+    """By hand: W = (3, 4), ||W|| = 5, G = (1, 0), P = (0, 2), eta0 = 0.1:
+    Shampoo direction: eta = 0.1 * 5 / 2 = 0.25, W -> (3, 3.5);
+    before the roots: eta = 0.5, W -> (2.5, 4); P = 0 gives no step.
+    Momentum on a 1 x 1 block, beta1 = 1/2, eta0 = 1/2, W = 4:
+      t=1: G = 4, P = 2:  Mg = 2,   Ps = 1,    eta = 2,   W = 2
+      t=2: G = 1, P = -6: Mg = 1.5, Ps = -2.5, eta = 0.4, W = 3."""
+    W, G, P = np.array([[3.0, 4.0]]), np.array([[1.0, 0.0]]), np.array([[0.0, 2.0]])
+    a = o.lamb_graft_update(W, G, P, eta0=0.1)
+    assert abs(a['eta'] - 0.25) < 1e-15 and np.allclose(a['W'], [[3.0, 3.5]], rtol=0, atol=1e-15)
+    b = o.lamb_graft_update(W, G, None, eta0=0.1, use_shampoo=False)
+    assert abs(b['eta'] - 0.5) < 1e-15 and np.allclose(b['W'], [[2.5, 4.0]], rtol=0, atol=1e-15)
+    c = o.lamb_graft_update(W, G, np.zeros((1, 2)), eta0=0.1)
+    assert c['eta'] == 0.0 and np.array_equal(c['W'], W)
+    z = np.zeros((1, 1))
+    s1 = o.lamb_graft_update(np.array([[4.0]]), np.array([[4.0]]), np.array([[2.0]]), 0.5, 0.5, z, z)
+    assert abs(s1['eta'] - 2.0) < 1e-15 and abs(s1['W'][0, 0] - 2.0) < 1e-15 and s1['Mg'][0, 0] == 2.0
+    s2 = o.lamb_graft_update(s1['W'], np.array([[1.0]]), np.array([[-6.0]]), 0.5, 0.5, s1['Mg'], s1['Ps'])
+    assert abs(s2['Mg'][0, 0] - 1.5) < 1e-15 and abs(s2['Ps'][0, 0] + 2.5) < 1e-15
+    assert abs(s2['eta'] - 0.4) < 1e-15 and abs(s2['W'][0, 0] - 3.0) < 1e-14
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith('pin_')]

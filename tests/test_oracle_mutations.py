@@ -44,6 +44,14 @@ MUTATIONS = [
      [P.pin_graft_norm_identity, P.pin_graft_identity_roots]),
     ("graft_update", "beta1 * _f64(Ps) + (1.0 - beta1) * Pf", "beta1 * _f64(Ps) + Pf", [P.pin_graft_momentum_1x1]),
     ("graft_update", "W_new = W - eta * Mg_new", "W_new = W - eta * G", [P.pin_graft_adagrad_fallback]),
+    ("lamb_graft_update", "nw = float(np.linalg.norm(W))", "nw = float(np.linalg.norm(Gf))",
+     [P.pin_lamb_step_norm]),
+    ("lamb_graft_update", "eta = 0.0 if nd == 0.0 else eta0 * nw / nd", "eta = 0.0 if nd == 0.0 else eta0 * nw",
+     [P.pin_lamb_step_norm, P.pin_lamb_worked]),
+    ("lamb_graft_update", "beta1 * _f64(Ps) + (1.0 - beta1) * Pf", "beta1 * _f64(Ps) + Pf", [P.pin_lamb_worked]),
+    ("lamb_graft_update", "beta1 * _f64(Mg) + (1.0 - beta1) * Gf", "(1.0 - beta1) * Gf", [P.pin_lamb_worked]),
+    ("lamb_graft_update", "        direction = Mg_new", "        direction = Gf * 0 + np.sign(Gf)",
+     [P.pin_lamb_step_norm]),
     ("embedding_grad", "G[i[e]] += w[e] * dy[f[e]]", "G[i[e]] = w[e] * dy[f[e]]",
      [P.pin_embedding_worked_example, P.pin_embedding_lookup_matrix]),
     ("embedding_grad", "G[i[e]] += w[e] * dy[f[e]]", "G[i[e]] += dy[f[e]]", [P.pin_embedding_worked_example]),
