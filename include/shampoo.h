@@ -216,6 +216,24 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
                              float eta0, float beta1, int use_shampoo, float* norms, void* stream);
 
 /*
+ * Grafted update with the LARS/LAMB layer-wise magnitude of the same appendix
+ * paragraph ("Layer wise learning rates": learning rate ||W||_F / ||G||_F per
+ * layer, applied per block here): the step is eta0 ||W||_F long, W taken
+ * before the step,
+ *   Mg = beta1 Mg + (1 - beta1) G
+ *   use_shampoo:  Ps  = beta1 Ps + (1 - beta1) P
+ *                 eta = eta0 ||W||_F / ||Ps||_F     (0 when ||Ps||_F == 0)
+ *                 W   = W - eta Ps
+ *   otherwise:    eta = eta0 ||W||_F / ||Mg||_F     (LARS step, before the roots)
+ *                 W   = W - eta Mg
+ * D is not used (may be NULL).  With beta1 == 0, Mg and Ps are not stored.
+ * norms (device, may be NULL): per block {||W||_F, ||direction||_F, eta}.
+ * Errors: as shampoo_graft (D may be NULL).
+ */
+shampoo_status shampoo_graft_lamb(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                  float eta0, float beta1, int use_shampoo, float* norms, void* stream);
+
+/*
  * Embedding layers (appendix "Shampoo for embedding layers", with the
  * one-sided preconditioner of Lemma 1 for large layers).
  *

@@ -873,7 +873,13 @@ __device__ __forceinline__ void for_chunk(const GraftBlock& B, int r0, int r1, F
   }
 }
 
-template <typename SG>
+// Graft pass 1: per chunk, the squared norms of the magnitude and direction
+// terms (partial[2t], partial[2t+1]) and the state updates.
+//   AdaGrad (LAMB = false): D += G o G; magnitude Mg = momentum of
+//     D^{-1/2} o G; direction Ps = momentum of P.
+//   LARS/LAMB (LAMB = true): magnitude ||W||_F (W before the step);
+//     direction Ps = momentum of P, or before the roots Mg = momentum of G.
+template <typename SG, bool LAMB = false>
 __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock* __restrict__ blocks, int nb,
                                                               int total_chunks, float beta1, int use_shampoo,
                                                               double* __restrict__ partial) {
@@ -886,6 +892,38 @@ __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock*
   const int r1 = min(B.rows, r0 + B.rows_per_chunk);
   const bool mom = beta1 > 0.f;
   float smg = 0.f, sps = 0.f;
+  if constexpr (LAMB) {
+    for_chunk(B, r0, r1, [&](int64_t i, int64_t iw, int w) {
+      float g[4], wv[4], pv[4];
+      if (w == 4) {
+        G4<SG>::load(B.G, i, g);
+        const f4v w4 = gload<f4v>(B.W + iw);
+        wv[0] = w4[0]; wv[1] = w4[1]; wv[2] = w4[2]; wv[3] = w4[3];
+        if (use_shampoo) {
+          const f4v p4 = gload<f4v>(B.P + i);
+          pv[0] = p4[0]; pv[1] = p4[1]; pv[2] = p4[2]; pv[3] = p4[3];
+        }
+      } else {
+        g[0] = load_g<SG>(B.G, i);
+        wv[0] = gload<float>(B.W + iw);
+        if (use_shampoo) pv[0] = gload<float>(B.P + i);
+      }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        if (e >= w) break;
+        smg += wv[e] * wv[e];
+        float mg = g[e];
+        if (mom) { mg = beta1 * B.Mg[iw + e] + (1.f - beta1) * g[e]; B.Mg[iw + e] = mg; }
+        if (use_shampoo) {
+          float ps = pv[e];
+          if (mom) { ps = beta1 * B.Ps[iw + e] + (1.f - beta1) * ps; B.Ps[iw + e] = ps; }
+          sps += ps * ps;
+        } else {
+          sps += mg * mg;
+        }
+      }
+    });
+  } else
   for_chunk(B, r0, r1, [&](int64_t i, int64_t iw, int w) {
     float g[4], d[4], pv[4];
     if (w == 4) {
@@ -928,7 +966,8 @@ __global__ __launch_bounds__(kThreads) void graft_pass1_kernel(const GraftBlock*
   }
 }
 
-template <typename SG>
+// Graft pass 2: eta from the block's norms, then W -= eta * direction.
+template <typename SG, bool LAMB = false>
 __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock* __restrict__ blocks, int nb,
                                                               int total_chunks, float eta0, float beta1,
                                                               int use_shampoo, const double* __restrict__ partial,
@@ -949,7 +988,7 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
   sps = block_sum(sps, red);
   const double nm = sqrt(smg), nps = sqrt(sps);
   double eta;
-  if (use_shampoo) eta = nps > 0.0 ? (double)eta0 * nm / nps : 0.0;
+  if (use_shampoo || LAMB) eta = nps > 0.0 ? (double)eta0 * nm / nps : 0.0;
   else eta = eta0;
   const float etaf = (float)eta;
   const int ch = t - B.chunk_begin;
@@ -962,7 +1001,8 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
   const int r0 = ch * B.rows_per_chunk;
   const int r1 = min(B.rows, r0 + B.rows_per_chunk);
   const bool mom = beta1 > 0.f;
-  // direction: Ps (momentum) or P; before the roots Mg or D^{-1/2} o G
+  // direction: Ps (momentum) or P; before the roots Mg or (at beta1 = 0)
+  // D^{-1/2} o G, or G itself for LAMB
   const float* dir = use_shampoo ? (mom ? B.Ps : B.P) : (mom ? B.Mg : nullptr);
   // P is laid out like G; momentum buffers like W
   const int64_t dir_w = use_shampoo && !mom ? 0 : 1;
@@ -976,6 +1016,9 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
       } else {
         step[0] = gload<float>(dir + id);
       }
+    } else if (LAMB) {
+      if (w == 4) G4<SG>::load(B.G, i, step);
+      else step[0] = load_g<SG>(B.G, i);
     } else {
       float g[4];
       if (w == 4) {

@@ -374,7 +374,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
   return tables_done(h, s);
 }
 
-template <typename SG>
+template <typename SG, bool LAMB>
 shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float eta0, float beta1, int use_shampoo,
                           float* norms, hipStream_t s) {
   int total = 0;
@@ -385,11 +385,11 @@ shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float 
   double* part = static_cast<double*>(h->partial);
   const GraftBlock* db = static_cast<const GraftBlock*>(d);
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
-    hipLaunchKernelGGL(graft_pass1_kernel<SG>, dim3(total), dim3(kThreads), 0, s, db, nb, total, beta1,
+    hipLaunchKernelGGL((graft_pass1_kernel<SG, LAMB>), dim3(total), dim3(kThreads), 0, s, db, nb, total, beta1,
                        use_shampoo, part);
   }));
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
-    hipLaunchKernelGGL(graft_pass2_kernel<SG>, dim3(total), dim3(kThreads), 0, s, db, nb, total, eta0, beta1,
+    hipLaunchKernelGGL((graft_pass2_kernel<SG, LAMB>), dim3(total), dim3(kThreads), 0, s, db, nb, total, eta0, beta1,
                        use_shampoo, (const double*)part, norms);
   }));
   return tables_done(h, s);
@@ -670,6 +670,32 @@ shampoo_status emb_check(Handle* h, int nnz, int dim) {
   return SHAMPOO_OK;
 }
 
+shampoo_status graft_entry(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
+                           float beta1, int use_shampoo, float* norms, void* stream, bool lamb) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
+  if (!isfinite(eta0)) return fail(h, SHAMPOO_EINVAL, "eta0 is not finite");
+  if (!(beta1 >= 0.f && beta1 < 1.f)) return fail(h, SHAMPOO_EINVAL, "beta1 %g outside [0, 1)", (double)beta1);
+  for (int i = 0; i < nblocks; ++i) {
+    const shampoo_block& b = blocks[i];
+    if (!b.W || (!lamb && !b.D)) return fail(h, SHAMPOO_EINVAL, "block %d: W or D is NULL", i);
+    if (use_shampoo && !b.P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
+    if (beta1 > 0.f && (!b.Mg || (use_shampoo && !b.Ps)))
+      return fail(h, SHAMPOO_EINVAL, "block %d: Mg/Ps needed when beta1 > 0", i);
+  }
+  if (nblocks == 0) return SHAMPOO_OK;
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (lamb) {
+    if (g_dtype == SHAMPOO_F32) return graft_impl<float, true>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+    return graft_impl<uint16_t, true>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+  }
+  if (g_dtype == SHAMPOO_F32) return graft_impl<float, false>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+  return graft_impl<uint16_t, false>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+}
+
 }  // namespace
 
 // ============================================================================
@@ -773,24 +799,12 @@ shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, i
 
 shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
                              float beta1, int use_shampoo, float* norms, void* stream) {
-  Handle* h = static_cast<Handle*>(handle);
-  if (!h) return SHAMPOO_EINVAL;
-  h->err.clear();
-  STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
-  if (!isfinite(eta0)) return fail(h, SHAMPOO_EINVAL, "eta0 is not finite");
-  if (!(beta1 >= 0.f && beta1 < 1.f)) return fail(h, SHAMPOO_EINVAL, "beta1 %g outside [0, 1)", (double)beta1);
-  for (int i = 0; i < nblocks; ++i) {
-    const shampoo_block& b = blocks[i];
-    if (!b.W || !b.D) return fail(h, SHAMPOO_EINVAL, "block %d: W or D is NULL", i);
-    if (use_shampoo && !b.P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
-    if (beta1 > 0.f && (!b.Mg || (use_shampoo && !b.Ps)))
-      return fail(h, SHAMPOO_EINVAL, "block %d: Mg/Ps needed when beta1 > 0", i);
-  }
-  if (nblocks == 0) return SHAMPOO_OK;
-  DeviceGuard g(h->device);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (g_dtype == SHAMPOO_F32) return graft_impl<float>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
-  return graft_impl<uint16_t>(h, blocks, nblocks, eta0, beta1, use_shampoo, norms, s);
+  return graft_entry(handle, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, norms, stream, false);
+}
+
+shampoo_status shampoo_graft_lamb(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
+                                  float beta1, int use_shampoo, float* norms, void* stream) {
+  return graft_entry(handle, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, norms, stream, true);
 }
 
 size_t shampoo_inv_root_workspace_bytes(const shampoo_root_job* jobs, int njobs, int precision) {
@@ -1152,11 +1166,11 @@ shampoo_status shampoo_embedding_graft(void* handle, const int32_t* rows, const 
   double* part = static_cast<double*>(h->partial);
   const GraftBlock* db = static_cast<const GraftBlock*>(d);
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
-    hipLaunchKernelGGL(graft_pass1_kernel<float>, dim3(total), dim3(kThreads), 0, s, db, 1, total, 0.f, use_shampoo,
+    hipLaunchKernelGGL((graft_pass1_kernel<float, false>), dim3(total), dim3(kThreads), 0, s, db, 1, total, 0.f, use_shampoo,
                        part);
   }));
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
-    hipLaunchKernelGGL(graft_pass2_kernel<float>, dim3(total), dim3(kThreads), 0, s, db, 1, total, eta0, 0.f,
+    hipLaunchKernelGGL((graft_pass2_kernel<float, false>), dim3(total), dim3(kThreads), 0, s, db, 1, total, eta0, 0.f,
                        use_shampoo, (const double*)part, norms);
   }));
   return tables_done(h, s);

@@ -150,3 +150,75 @@ def test_c1_end_to_end(env):
         assert rel(host(L), st["L"]) <= 1e-4
     print("C1 per-step update errors", ["%.1e" % e for e in errs])
     assert max(errs) <= TOL, errs
+
+
+@pytest.mark.parametrize("beta1,use_shampoo", [(0.0, True), (0.0, False), (0.9, True), (0.9, False)])
+def test_graft_lamb(env, beta1, use_shampoo):
+    """LARS/LAMB magnitude eta0 ||W||_F along the unit direction."""
+    torch, B, dev, h = env
+    say("graft lamb", beta1, use_shampoo)
+    shapes = [(128, 128), (300, 70), (1, 5), (1024, 1024)]
+    r = np.random.default_rng(15)
+    blocks, refs, outs = [], [], []
+    for (m, n) in shapes:
+        W = r.standard_normal((m, n)).astype(np.float32)
+        G = r.standard_normal((m, n)).astype(np.float32)
+        P = r.standard_normal((m, n)).astype(np.float32)
+        Mg = r.standard_normal((m, n)).astype(np.float32)
+        Ps = r.standard_normal((m, n)).astype(np.float32)
+        dW, dG, dP = (to_dev(torch, x, dev) for x in (W, G, P))
+        dMg, dPs = to_dev(torch, Mg, dev), to_dev(torch, Ps, dev)
+        blocks.append(B.Block(G=dG, W=dW, P=dP, Mg=dMg if beta1 else None, Ps=dPs if beta1 else None))
+        refs.append((W, O.lamb_graft_update(W, G, P, 0.05, beta1, Mg if beta1 else None, Ps if beta1 else None,
+                                            use_shampoo)))
+        outs.append((dW, dMg, dPs))
+    norms = torch.zeros(3 * len(shapes), device=dev)
+    B.shampoo_graft_lamb(h, blocks, 0.05, beta1=beta1, use_shampoo=use_shampoo, norms=norms)
+    torch.cuda.synchronize()
+    nh = host(norms).reshape(-1, 3)
+    for k, ((W0, ref), (dW, dMg, dPs)) in enumerate(zip(refs, outs)):
+        assert rel(host(dW) - W0, ref["W"] - W0) <= TOL
+        assert abs(nh[k, 0] - ref["norm_w"]) <= 1e-5 * ref["norm_w"]
+        assert abs(nh[k, 1] - ref["norm_dir"]) <= 1e-5 * ref["norm_dir"]
+        assert abs(nh[k, 2] - ref["eta"]) <= 1e-5 * ref["eta"]
+        if beta1:
+            assert rel(host(dMg), ref["Mg"]) <= 1e-6
+            if use_shampoo:
+                assert rel(host(dPs), ref["Ps"]) <= 1e-6
+
+
+def test_graft_lamb_bf16_and_c1_steps(env):
+    """bf16 gradients, then six C1 steps with roots every step under the
+    LAMB graft against the oracle's own trajectory (per-step dW)."""
+    torch, B, dev, h = env
+    say("graft lamb bf16 + C1 steps")
+    bits = cfg.c5_grad_bf16(3, 1, (256, 128))
+    g = to_dev(torch, bits.view(np.int16), dev).view(torch.bfloat16)
+    W0 = np.random.default_rng(2).standard_normal((256, 128)).astype(np.float32)
+    W = to_dev(torch, W0, dev)
+    B.shampoo_graft_lamb(h, [B.Block(G=g, W=W)], 0.1, use_shampoo=False)
+    torch.cuda.synchronize()
+    ref = O.lamb_graft_update(W0, cfg.bf16_bits_to_f32(bits), None, 0.1, use_shampoo=False)
+    assert rel(host(W) - W0, ref["W"] - W0) <= TOL
+    n, p, eps, eta0 = 128, 4, 1e-6, 1e-2
+    W0 = cfg.c1_weight()
+    W = to_dev(torch, W0, dev)
+    P, L, R, Lr, Rr = (torch.zeros(n, n, device=dev) for _ in range(5))
+    prm = B.shampoo_root_params_default(p=p, eps=eps)
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([n, n]), dtype=torch.uint8, device=dev)
+    info = torch.zeros(16, dtype=torch.int32, device=dev)
+    Lo, Ro, Wo = np.zeros((n, n)), np.zeros((n, n)), W0.astype(np.float64)
+    for t in range(1, 7):
+        G = cfg.c1_grad(t)
+        Wprev = host(W).astype(np.float64)
+        blk = B.Block(G=to_dev(torch, G, dev), W=W, P=P, L=L, R=R, Lr=Lr, Rr=Rr)
+        B.shampoo_update_stats(h, [blk])
+        B.shampoo_inv_root_batched(h, [L, R], [Lr, Rr], prm, ws, info)
+        B.shampoo_precondition(h, [blk])
+        B.shampoo_graft_lamb(h, [blk], eta0)
+        torch.cuda.synchronize()
+        Lo, Ro = O.stats_update(Lo, Ro, G)
+        Po = O.precondition(G, O.inv_root(Lo, p, eps)[0], O.inv_root(Ro, p, eps)[0])
+        out = O.lamb_graft_update(Wo, G, Po, eta0)
+        assert rel(host(W) - Wprev, out["W"] - Wo) <= TOL, t
+        Wo = out["W"]
