@@ -40,7 +40,7 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
   rows gives G^T G = dy^T dy), a hand-worked 5-row example with repeated
   rows and weights, and the dropping of out-of-range entries.
 * ``lamb_graft_update`` -- the LARS/LAMB layer-wise magnitude of the same
-  appendix paragraph (R12).  Pinned by the step-norm identity
+  appendix paragraph (R17).  Pinned by the step-norm identity
   ||dW||_F = eta0 ||W||_F, invariance under scaling G and P, and hand-worked
   1 x 2 and 1 x 1 momentum examples.
 * ``graft_update``      -- Algorithm 2 (momentum on both directions) and the
@@ -68,15 +68,15 @@ R7  The ridge epsilon*I is added exactly once, at the root; statistics
 R8  D^{-1/2} o G is 0 where D is 0 (then G is 0 as well).
 R9  When ||P||_F = 0 the step size is 0.
 R10 The input to a root is symmetrised, A_s = (A + A^T)/2, before use.
-R12 The LARS/LAMB layer-wise learning rate ||W||_F / ||G||_F of the appendix,
-    grafted like the AdaGrad magnitude, makes the step eta0 ||W||_F long
-    along the unit Shampoo direction (along G / ||G||_F before the roots);
-    ||W||_F is that of the block before the step.
-R11 Embedding statistics are those of the exact sparse gradient G of the
+R16 Embedding statistics are those of the exact sparse gradient G of the
     lookup: G^T G = dy^T (S^T S) dy with S the lookup matrix.  The appendix's
     simplification S^T S = I (or diagonal for multi-hot) holds when the
     features hit distinct rows; repeated rows are summed first.  Entries
     with a row outside [0, vocab) or a feature outside [0, m) are dropped.
+R17 The LARS/LAMB layer-wise learning rate ||W||_F / ||G||_F of the appendix,
+    grafted like the AdaGrad magnitude, makes the step eta0 ||W||_F long
+    along the unit Shampoo direction (along G / ||G||_F before the roots);
+    ||W||_F is that of the block before the step.
 """
 from __future__ import annotations
 
@@ -269,7 +269,7 @@ def embedding_grad(vocab, idx, feat, weight, dy):
     """Gradient of the table (vocab x d, row-major) of a lookup whose entry e
     reads row idx[e] into output row feat[e] with weight w[e]:
     G = sum_e w[e] e_{idx[e]} dy[feat[e]]^T.  feat None: feat[e] = e (one
-    lookup per output row); weight None: w[e] = 1 (R11)."""
+    lookup per output row); weight None: w[e] = 1 (R16)."""
     dy = _f64(dy)
     i, f, w = _valid_entries(idx, feat, weight, vocab, dy.shape[0])
     G = np.zeros((vocab, dy.shape[1]))
@@ -363,7 +363,7 @@ def lamb_graft_update(W, G, P=None, eta0=1.0, beta1=0.0, Mg=None, Ps=None,
                       use_shampoo=True):
     """Layer-wise (LARS/LAMB) graft, the alternative magnitude of the
     appendix "Further details on experiments", paragraph "Layer wise learning
-    rates" (R12): the layer learning rate eta0 ||W||_F / ||G||_F applied to
+    rates" (R17): the layer learning rate eta0 ||W||_F / ||G||_F applied to
     the first-order step G gives a step of norm eta0 ||W||_F, kept along the
     unit Shampoo direction.
 
