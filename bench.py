@@ -52,6 +52,21 @@ def measured_traffic(name="newton_stage_kernel_c2_counters.txt"):
     return float(kv["bytes_per_launch"])
 
 
+def newton_products(iters, p, power):
+    """Symmetric products one matrix takes in a precision phase of `iters`
+    iterations: 1 + floor(log2 p) + popcount(p) per iteration, less the
+    first X product (X0 is a multiple of I).  The power-bound start adds M0^2
+    and M0^4 and turns the first iteration's M-only products of its first
+    stage (M1 M1, and M1 M for odd p) into an elementwise pass."""
+    per = 1 + (p.bit_length() - 1) + bin(p).count("1")
+    stage0 = 2 if (p & 1 and p > 1) else 1
+    if iters <= 0:
+        return 2 if power else 0
+    if power:
+        return 2 + (per - 1 - stage0) + per * (iters - 1)
+    return per * iters - 1
+
+
 def gen_block(i, n, k):
     from synth import configs as cfg
     L = cfg.wishart_bartlett(n, 19 * k, 1.0 / k, cfg.C2, i, 0).astype(np.float32)
@@ -161,7 +176,7 @@ def run_c4(args, torch, B):
     bytes_graft = K * nb * d * d * 28
     roof_ms = (flops_stats / PEAK_F32_MFMA + flops_prec / PEAK_F32_MFMA) / 1e9 / K + bytes_graft / PEAK_HBM / 1e6 / K
     ms_step = elapsed * 1e3 / K
-    prods = sum(max(0, 4 * i - 1) for i in iters)
+    prods = sum(newton_products(i, 4, True) for i in iters)
     out = {
         "metric": "C4 stats+precondition+graft step ms (288 blocks of 1024^2, two-sided)",
         "value": ms_step, "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": args.warmup,
@@ -296,9 +311,8 @@ def run_c3(args, torch, B):
         B.shampoo_timing_enable(h, False)
         times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
         inf = B.decode_root_info(info)
-        prods = 2 if p == 2 else 3
-        pr64 = sum(max(0, (prods + 1) * i["iters"] - 1) for i in inf if i["precision"] == 64)
-        pr32 = sum(max(0, (prods + 1) * i["iters_fp32"] - 1) for i in inf)
+        pr64 = sum(newton_products(i["iters"], p, True) for i in inf if i["precision"] == 64)
+        pr32 = sum(newton_products(i["iters_fp32"], p, True) for i in inf)
         sym = n * n * (n + 1)
         res[f"p{p}"] = {
             "ms": ms, "roots_per_s": nm / ms * 1e3,
@@ -331,6 +345,9 @@ def main():
     ap.add_argument("--workload", choices=["c2", "c3", "c4", "c6"], default="c2",
                     help="c2 (default): the metric's workload; c3: ill-conditioned roots; c4: the "
                          "transformer-layer step; c6: the embedding-table step")
+    ap.add_argument("--scaling", choices=["power4", "frobenius"], default="power4",
+                    help="cold-start scaling of the roots: power4 (library default, bound ||A^4||_F^(1/4)) or "
+                         "frobenius (Algorithm 1 as printed)")
     ap.add_argument("--vocab", type=int, default=32768, help="c6: table rows")
     ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -381,7 +398,8 @@ def main():
     Ps = [torch.zeros(n, k, device=dev) for _ in range(nb)]
     blocks = [B.Block(G=Gs[i], W=Ws[i], D=Ds[i], P=Ps[i], L=Ls[i], Lr=Lrs[i]) for i in range(nb)]
     h = B.shampoo_create(0)
-    prm = B.shampoo_root_params_default(p=p, eps=eps)
+    scaling = B.SCALING_POWER4 if args.scaling == "power4" else B.SCALING_FROBENIUS
+    prm = B.shampoo_root_params_default(p=p, eps=eps, scaling=scaling)
     ws = torch.empty(B.shampoo_inv_root_workspace_bytes([n] * nb, prm.precision), dtype=torch.uint8, device=dev)
     info = torch.zeros(8 * nb, dtype=torch.int32, device=dev)
     infos = []
@@ -411,18 +429,35 @@ def main():
     B.shampoo_timing_enable(h, False)
     times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
 
+    # The same roots under the other scaling, for comparison (roots call only).
+    other = B.SCALING_FROBENIUS if scaling == B.SCALING_POWER4 else B.SCALING_POWER4
+    prm_o = B.shampoo_root_params_default(p=p, eps=eps, scaling=other)
+    Xo = [torch.zeros(n, n, device=dev) for _ in range(nb)]
+    B.shampoo_inv_root_batched(h, Ls, Xo, prm_o, ws, info)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    for _ in range(3):
+        B.shampoo_inv_root_batched(h, Ls, Xo, prm_o, ws, info)
+    torch.cuda.synchronize()
+    other_ms = (time.perf_counter() - t1) * 1e3 / 3
+    other_iters = float(np.mean([i["iters"] for i in B.decode_root_info(info)]))
+    del Xo
+
     # algorithmic work
-    # Products per matrix: p = 4 takes X M1, M1 M1, (M1^2)^2 and M1^4 M per
-    # iteration, except the first, whose X product (with X0 a multiple of I)
-    # is not a GEMM.
+    # Products per matrix at p = 4: X M1, M1 M1, (M1^2)^2 and M1^4 M per
+    # iteration, except the first, whose X product (X0 a multiple of I) is
+    # not a GEMM: 4 iters - 1.  The power-bound scaling adds M0^2 and M0^4
+    # and makes the first iteration's M1 M1 elementwise: 4 iters.
+    def products(iters):
+        return newton_products(iters, p, scaling == B.SCALING_POWER4)
     it32, it64, prod32, prod64 = 0, 0, 0, 0
     for t in infos:
         for inf in B.decode_root_info(t):
             it32 += inf["iters_fp32"]
-            prod32 += max(0, 4 * inf["iters_fp32"] - 1)
+            prod32 += products(inf["iters_fp32"])
             if inf["precision"] == 64:
                 it64 += inf["iters"]
-                prod64 += max(0, 4 * inf["iters"] - 1)
+                prod64 += products(inf["iters"])
     sym_prod = n * n * (n + 1)                     # symmetric product, upper-triangle counting
     flops_newton32 = prod32 * sym_prod
     flops_newton64 = prod64 * sym_prod
@@ -449,7 +484,7 @@ def main():
         "config": {"workload": "C2 step: 96 blocks, L 1024x1024 (Wishart, 19x4096 dof) + G 1024x4096 "
                                "N(0,1/4096); stats + 96 inverse 4th roots (grouped coupled Newton, eps 1e-6, "
                                "tol 1e-6, AUTO precision) + L^-1/4 G + AdaGrad graft",
-                   "blocks": nb, "n": n, "k": k, "p": p, "eps": eps},
+                   "blocks": nb, "n": n, "k": k, "p": p, "eps": eps, "root_scaling": args.scaling},
         "roofline": {
             "kernel": "newton_stage_kernel<float> (grouped fp32-MFMA Newton products)",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_F32_MFMA, "unit": "TFLOP/s",
@@ -473,6 +508,10 @@ def main():
         "newton_iters_mean": it32 / max(1, nb * args.steps),
         "roots_per_s_root_phase": nb * args.steps / ((times["newton_f32"][0] + times["newton_f64"][0]
                                                       + times["root_aux"][0]) * 1e-3),
+        "newton_products_per_root": prod32 / max(1, nb * args.steps),
+        "other_scaling": {"scaling": "frobenius" if scaling == B.SCALING_POWER4 else "power4",
+                          "roots_call_ms": other_ms, "roots_per_s_roots_call": nb / (other_ms * 1e-3),
+                          "iters_mean": other_iters},
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")

@@ -73,6 +73,9 @@ R16 Embedding statistics are those of the exact sparse gradient G of the
     simplification S^T S = I (or diagonal for multi-hot) holds when the
     features hit distinct rows; repeated rows are summed first.  Entries
     with a row outside [0, vocab) or a feature outside [0, m) are dropped.
+R20 The appendix leaves the start constant free (X0 = I / c); Algorithm 1
+    takes z = (1+p) / (2 ||A_d||_F).  The 'power4' option takes the tighter
+    upper bound ||A_d^4||_F^(1/4) = (sum lambda^8)^(1/8) >= lambda_max.
 R17 The LARS/LAMB layer-wise learning rate ||W||_F / ||G||_F of the appendix,
     grafted like the AdaGrad magnitude, makes the step eta0 ||W||_F long
     along the unit Shampoo direction (along G / ||G||_F before the roots);
@@ -187,7 +190,7 @@ def cond_damped(A, eps=0.0, eps_relative=False, lam_max=None):
 
 
 def coupled_newton(A, p, eps=0.0, tol=1e-10, max_iters=100,
-                   eps_relative=False, lam_max=None, X0=None):
+                   eps_relative=False, lam_max=None, X0=None, scaling='frobenius'):
     """Algorithm 1, CoupledIteration, in float64.
 
     Steps in the paper's order: optional MaxSV and scaled damping; cold start
@@ -212,6 +215,11 @@ def coupled_newton(A, p, eps=0.0, tol=1e-10, max_iters=100,
         z = None
     else:
         z = (1.0 + p) / (2.0 * np.linalg.norm(Ad, 'fro'))
+        if scaling == 'power4':
+            # R20: the tighter bound ||A_d^4||_F^(1/4) >= lambda_max in place
+            # of ||A_d||_F, computed on z A_d (eigenvalues <= (p+1)/2)
+            rho = np.linalg.norm(np.linalg.matrix_power(z * Ad, 4), 'fro') ** 0.25
+            z *= max(1.0, (1.0 + p) / (2.0 * rho))
         X = z ** (1.0 / p) * I
         M = z * Ad
     r = float(np.max(np.abs(M - I)))

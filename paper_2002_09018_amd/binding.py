@@ -26,6 +26,7 @@ SHAMPOO_OK, SHAMPOO_EINVAL, SHAMPOO_EUNSUPPORTED, SHAMPOO_EHIP, SHAMPOO_ENOMEM =
 SHAMPOO_F32, SHAMPOO_BF16 = 0, 1
 ROOT_CONVERGED, ROOT_STAGNATED, ROOT_MAXITER, ROOT_DIVERGED, ROOT_NOT_PD = 0, 1, 2, 3, 4
 PRECISION_FP32, PRECISION_AUTO, PRECISION_FP64 = 0, 1, 2
+SCALING_FROBENIUS, SCALING_POWER4 = 0, 1
 KCLASS_NEWTON_F32, KCLASS_NEWTON_F64, KCLASS_STATS, KCLASS_PRECOND, KCLASS_GRAFT, KCLASS_ROOT_AUX, KCLASS_EMB = range(7)
 KCLASS_NAMES = ["newton_f32", "newton_f64", "stats", "precond", "graft", "root_aux", "emb"]
 
@@ -44,7 +45,8 @@ class shampoo_root_job(C.Structure):
 class shampoo_root_params(C.Structure):
     _fields_ = [("p", C.c_int32), ("eps", C.c_float), ("eps_relative", C.c_int32), ("tol", C.c_float),
                 ("max_iters", C.c_int32), ("precision", C.c_int32), ("kappa32", C.c_float),
-                ("maxsv_steps", C.c_int32), ("maxsv_tol", C.c_float), ("poll", C.c_int32)]
+                ("maxsv_steps", C.c_int32), ("maxsv_tol", C.c_float), ("poll", C.c_int32),
+                ("scaling", C.c_int32)]
 
 
 class shampoo_root_info(C.Structure):

@@ -171,7 +171,8 @@ struct RootState {
   int precision;     // 32 or 64: phase that produced the result
   int sv_done;       // MaxSV stopped
   int sv_steps;      // MaxSV power steps taken
-  double z;          // Frobenius scaling (1 + p) / (2 ||A_d||_F)
+  double z;          // scaling of M0 = z A_d: (1 + p) / (2 ||A_d||_F), times zc
+  double zc;         // tightening factor of the power-bound scaling (1: Frobenius)
   double eps_eff;    // damping added
   double lam_max;    // MaxSV estimate (relative damping)
   double diag_min;   // smallest diagonal entry of A_d
@@ -569,13 +570,15 @@ __global__ void root_prep_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
     return;
   }
   st[j].z = (1.0 + p) / (2.0 * sqrt(fro2));
+  st[j].zc = 1.0;
 }
 
 // M0 = z (A_s + eps I), X0 = z^(1/p) I (Algorithm 1 cold start); residual of
 // M0 accumulated into resid_bits.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                            RootState* __restrict__ st, int total_full, int p) {
+                                                            RootState* __restrict__ st, int total_full, int p,
+                                                            int write_x) {
   __shared__ float lds[kTile * 33];
   const int t = blockIdx.x;
   if (t >= total_full) return;
@@ -595,16 +598,156 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
   // z^(1/p) (a I + b M0) is written here, so the first iteration needs no X
   // product; a matrix that stops before any iteration gets X0 from the
   // output kernel.
+  // write_x == 0: only M0 (the power-bound scaling rescales it later)
   sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
     const T m = (T)(z * (s + (r == c ? e : 0.0)));
     M[(int64_t)r * n + c] = m;
-    X1[(int64_t)r * n + c] = x0 * (b * m + (r == c ? a : (T)0));
-    float d = (float)fabs((double)m - (r == c ? 1.0 : 0.0));
-    if (!(d <= 3.0e38f)) d = INFINITY;
-    rmax = rmax > d ? rmax : d;
+    if (write_x) {
+      X1[(int64_t)r * n + c] = x0 * (b * m + (r == c ? a : (T)0));
+      float d = (float)fabs((double)m - (r == c ? 1.0 : 0.0));
+      if (!(d <= 3.0e38f)) d = INFINITY;
+      rmax = rmax > d ? rmax : d;
+    }
   });
   rmax = wave_max(rmax);
   if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+}
+
+// Power-bound scaling.  ||M0^4||_F^(1/4) = (sum_i mu_i^8)^(1/8) bounds the
+// largest eigenvalue mu_max of M0 = z A_d from above, much more tightly than
+// ||M0||_F.  With S1 = M0^4 formed by two products, rho = ||S1||_F^(1/4) and
+// c = (p + 1) / (2 rho) >= 1, the start M0 <- c M0 keeps the largest
+// eigenvalue at or below (p + 1) / 2 (the margin Algorithm 1 keeps with the
+// Frobenius bound) while lifting the whole spectrum towards 1.
+//
+// Per full tile: sum of squares of S1 (buffer S[1]) into part[3 t].
+template <typename T>
+__global__ __launch_bounds__(kThreads) void frob_s1_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                          const RootState* __restrict__ st, int total_full) {
+  __shared__ double red[kThreads / 64];
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int lt = t - J->full_begin;
+  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
+  const int n = J->n;
+  const T* S = J->S[1];
+  double ss = 0.0;
+  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+    const int r = ti * kTile + (e >> 7), c = tj * kTile + (e & 127);
+    if (r < n && c < n) {
+      const double x = (double)S[(int64_t)r * n + c];
+      ss += x * x;
+    }
+  }
+  ss = block_sum(ss, red);
+  if (threadIdx.x == 0) J->part[3 * lt + 0] = ss;
+}
+
+// One thread per matrix: rho from the tile partials (fixed order), c, z *= c.
+template <typename T>
+__global__ void root_rescale_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, RootState* __restrict__ st,
+                                    int p) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= njobs || st[j].status != kActive) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int nt = J->tiles_n * J->tiles_n;
+  double ss = 0.0;
+  for (int q = 0; q < nt; ++q) ss += J->part[3 * q + 0];
+  const double rho = pow(ss, 0.125);  // ||S1||_F^(1/4)
+  double c = (rho > 0.0 && isfinite(rho)) ? (1.0 + p) / (2.0 * rho) : 1.0;
+  c = c > 1.0 ? c : 1.0;  // never looser than the Frobenius bound
+  st[j].zc = c;
+  st[j].z *= c;
+}
+
+// M0 <- c M0 in place, X1 = z^(1/p) (a I + b M0), residual of M0.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void root_scale_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                             RootState* __restrict__ st, int total_full, int p) {
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int lt = t - J->full_begin;
+  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
+  const int n = J->n;
+  const T c = (T)st[j].zc;
+  const T x0 = (T)pow(st[j].z, 1.0 / p);
+  const T a = (T)(p + 1) / (T)p, b = (T)-1 / (T)p;
+  T* M = J->M[0];
+  T* X1 = J->X[1];
+  float rmax = 0.f;
+  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+    const int r = ti * kTile + (e >> 7), col = tj * kTile + (e & 127);
+    if (r < n && col < n) {
+      const int64_t i = (int64_t)r * n + col;
+      const T m = c * M[i];
+      M[i] = m;
+      X1[i] = x0 * (b * m + (r == col ? a : (T)0));
+      float d = (float)fabs((double)m - (r == col ? 1.0 : 0.0));
+      if (!(d <= 3.0e38f)) d = INFINITY;
+      rmax = rmax > d ? rmax : d;
+    }
+  }
+  rmax = wave_max(rmax);
+  if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+}
+
+// First stage of iteration 0 under the power-bound scaling.  Its products
+// (other than X M1, whose result the init kernel wrote) are all M M with an
+// affine epilogue, and M0^2 = c^2 S0 is known from the bound (S0 held the
+// square of the unscaled M0), so the stage is elementwise:
+//   C_q = ca_q c^2 S0 + cb_q M + cg_q I.
+// Each element is read once and every output written after both are formed
+// (a product may write S0 itself).
+template <typename T>
+__global__ __launch_bounds__(kThreads) void newton_poly0_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                               RootState* __restrict__ st, int total_full,
+                                                               NewtonStage S) {
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int par = st[j].parity;
+  const int lt = t - J->full_begin;
+  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
+  const int n = J->n;
+  const T c2 = (T)(st[j].zc * st[j].zc);
+  const T* S0 = J->S[0];
+  const T* M = newton_buf(J, par, kBufMc);
+  const int np = S.nprod;
+  T* d0 = newton_buf(J, par, S.q[0].dst);
+  T* d1 = np > 1 ? newton_buf(J, par, S.q[1].dst) : nullptr;
+  const T a0 = (T)S.q[0].ca, b0 = (T)S.q[0].cb, g0 = (T)S.q[0].cg;
+  const T a1 = (T)S.q[1].ca, b1 = (T)S.q[1].cb, g1 = (T)S.q[1].cg;
+  const bool r0 = S.q[0].resid != 0, r1 = np > 1 && S.q[1].resid != 0;
+  float rmax = 0.f;
+  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+    const int r = ti * kTile + (e >> 7), col = tj * kTile + (e & 127);
+    if (r < n && col < n) {
+      const int64_t i = (int64_t)r * n + col;
+      const T m2 = c2 * S0[i], m = M[i];
+      const bool dg = r == col;
+      const T x0 = a0 * m2 + b0 * m + (dg ? g0 : (T)0);
+      const T x1 = a1 * m2 + b1 * m + (dg ? g1 : (T)0);
+      d0[i] = x0;
+      if (d1) d1[i] = x1;
+      float d = 0.f;
+      if (r0) d = (float)fabs((double)x0 - (dg ? 1.0 : 0.0));
+      if (r1) d = (float)fabs((double)x1 - (dg ? 1.0 : 0.0));
+      if (!(d <= 3.0e38f)) d = INFINITY;
+      rmax = rmax > d ? rmax : d;
+    }
+  }
+  if (r0 || r1) {
+    rmax = wave_max(rmax);
+    if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+  }
 }
 
 // Resets the state of the matrices that take part in a phase.
@@ -623,6 +766,7 @@ __global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int pha
     s.eps_eff = 0.0;
     s.diag_min = 0.0;
     s.z = 0.0;
+    s.zc = 1.0;
   } else if (!s.escalate) {
     return;
   } else {

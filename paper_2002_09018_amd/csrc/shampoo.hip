@@ -549,14 +549,35 @@ NewtonStage drop_x(const NewtonStage& s0) {
 // One precision phase of the coupled Newton iteration.
 template <typename T>
 shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
-                            int total_up, int total_full, const NewtonProgram& prog, int p, float tol, int cap,
-                            int poll, int cls, hipStream_t s) {
+                            int total_up, int total_full, const NewtonProgram& prog, int p, int scaling, float tol,
+                            int cap, int poll, int cls, hipStream_t s) {
   const int lds = 0;  // static LDS
   auto kstage = newton_stage_kernel<T>;
-  // initial residual of M0
+  const bool power = scaling == SHAMPOO_SCALING_POWER4;
+  const int nb1 = cdiv(njobs, 64);
+  // M0 (and, with the Frobenius scaling, X1 and the residual of M0)
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p);
+    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p,
+                       power ? 0 : 1);
   }));
+  if (power) {
+    // S0 = M0^2, S1 = S0^2, rho = ||S1||_F^(1/4), M0 <- c M0 with c = (p+1)/(2 rho)
+    NewtonStage sq0{}, sq1{};
+    sq0.nprod = sq1.nprod = 1;
+    sq0.q[0] = make_prod(kBufMc, kBufMc, kBufNone, kBufS0, 1.0, 0.0, 0.0, 0);
+    sq1.q[0] = make_prod(kBufS0, kBufS0, kBufNone, kBufS1, 1.0, 0.0, 0.0, 0);
+    for (const NewtonStage* S : {&sq0, &sq1}) {
+      STATUS_TRY(launch(h, cls, s, [&] {
+        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, *S);
+      }));
+    }
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(frob_s1_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full);
+      hipLaunchKernelGGL(root_rescale_kernel<T>, dim3(nb1), dim3(64), 0, s, djobs, njobs, st, p);
+      hipLaunchKernelGGL(root_scale_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full,
+                         p);
+    }));
+  }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
                        dcount + kCountRing);
@@ -566,6 +587,14 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
     for (size_t q = 0; q < prog.stages.size(); ++q) {
       // iteration 0: X1 = z^(1/p) M1 was written by the init kernel
       const NewtonStage& S = (it == 0 && q == 0) ? first0 : prog.stages[q];
+      if (power && it == 0 && q == 0) {
+        // M0^2 = c^2 S0 is known: the stage is elementwise
+        STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+          hipLaunchKernelGGL(newton_poly0_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st,
+                             total_full, S);
+        }));
+        continue;
+      }
       STATUS_TRY(launch(h, cls, s, [&] {
         hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, S);
       }));
@@ -717,6 +746,7 @@ void shampoo_root_params_default(shampoo_root_params* q) {
   q->maxsv_steps = 100;
   q->maxsv_tol = 1e-6f;
   q->poll = 1;
+  q->scaling = SHAMPOO_SCALING_POWER4;
 }
 
 shampoo_status shampoo_create(void** handle, int device) {
@@ -834,6 +864,8 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   if (prm->max_iters < 1) return fail(h, SHAMPOO_EINVAL, "max_iters must be >= 1");
   if (prm->precision < 0 || prm->precision > 2) return fail(h, SHAMPOO_EINVAL, "bad precision %d", prm->precision);
   if (prm->eps_relative && prm->maxsv_steps < 1) return fail(h, SHAMPOO_EINVAL, "maxsv_steps must be >= 1");
+  if (prm->scaling != SHAMPOO_SCALING_FROBENIUS && prm->scaling != SHAMPOO_SCALING_POWER4)
+    return fail(h, SHAMPOO_EINVAL, "bad scaling %d", prm->scaling);
   if (prm->precision == SHAMPOO_PRECISION_AUTO && !(prm->kappa32 >= 1.f))
     return fail(h, SHAMPOO_EINVAL, "kappa32 must be >= 1");
   for (int j = 0; j < njobs; ++j) {
@@ -919,7 +951,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       const int k32 = host_scalar_iters(m0, p, std::max((double)prm->tol, 1e-6), 1000) + 1;
       cap = std::min(cap, std::max(k32, 1));
     }
-    STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, prog, p, prm->tol, cap, prm->poll,
+    STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap, prm->poll,
                                    SHAMPOO_KCLASS_NEWTON_F32, s));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -944,7 +976,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
         hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
       }));
     }
-    STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, prog, p, prm->tol, prm->max_iters, prm->poll,
+    STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
                                     SHAMPOO_KCLASS_NEWTON_F64, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);

@@ -347,6 +347,26 @@ def pin_newton_scalar_iters(o):
         assert _relf(np.diag(res['X']), (d2 + eps) ** (-1.0 / p)) < 1e-12
 
 
+def pin_newton_power4_scaling(o):
+    """Power-bound start: z = (p+1) / (2 (sum_i lambda_i^8)^(1/8)) on a
+    diagonal input (the bound from its eigenvalues directly), so the count is
+    the scalar recurrence's from z lambda_i; the result is the eigh root, and
+    a flat spectrum needs far fewer iterations than the Frobenius start."""
+    d = np.array([0.7, 1.0, 1.3, 1.1, 0.9, 1.2] * 40)
+    for p in (2, 4):
+        res = o.coupled_newton(np.diag(d), p, eps=0.0, tol=1e-12, scaling='power4')
+        z = (1.0 + p) / (2.0 * np.sum(d ** 8) ** 0.125)
+        want = max(o.scalar_newton_iters(z * x, p, 1e-12) for x in d)
+        assert abs(res['iters'] - want) <= 1
+        assert _relf(np.diag(res['X']), d ** (-1.0 / p)) < 1e-10
+        fro = o.coupled_newton(np.diag(d), p, eps=0.0, tol=1e-12)
+        assert res['iters'] + 2 <= fro['iters']
+    A = _spd(48, 1e4, 77)
+    res = o.coupled_newton(A, 4, eps=1e-6, tol=1e-12, scaling='power4')
+    X, _, _ = o.inv_root(A, 4, eps=1e-6)
+    assert _relf(res['X'], X) < 1e-9
+
+
 def pin_newton_status_rules(o):
     """MAXITER at a tiny cap, DIVERGED on an indefinite matrix, STAGNATED
     when the tolerance is below what fp64 can reach, MaxSV damping used."""

@@ -47,6 +47,7 @@ def test_host_only_entry_points(lib):
     assert "gfx950" in lib.shampoo_version()
     p = lib.shampoo_root_params_default()
     assert (p.p, p.max_iters, p.precision, p.poll) == (4, 100, lib.PRECISION_AUTO, 1)
+    assert p.scaling == lib.SCALING_POWER4
     assert abs(p.eps - 1e-6) < 1e-12 and abs(p.kappa32 - 1e4) < 1e-3
     assert lib.shampoo_inv_root_workspace_bytes([0]) == 0
     assert lib.shampoo_inv_root_workspace_bytes([4097]) == 0
@@ -73,5 +74,5 @@ def test_struct_layouts_match_header(lib):
     import ctypes as C
     assert C.sizeof(lib.shampoo_block) == 96
     assert C.sizeof(lib.shampoo_root_job) == 24
-    assert C.sizeof(lib.shampoo_root_params) == 40
+    assert C.sizeof(lib.shampoo_root_params) == 44
     assert C.sizeof(lib.shampoo_root_info) == 32

@@ -54,8 +54,28 @@ def test_against_eigh_mixed_sizes(env, p):
         assert inf["status"] in (0, 1), inf
         assert rel(X, Xo) <= 1e-3, (A.shape, inf, rel(X, Xo))
         assert np.array_equal(X, X.T)
-    tr = O.coupled_newton(As[5], p, 1e-6, tol=1e-6)
+    tr = O.coupled_newton(As[5], p, 1e-6, tol=1e-6, scaling="power4")  # the library default
     assert abs(info[5]["iters"] - tr["iters"]) <= 1, (info[5], tr["iters"])
+
+
+@pytest.mark.parametrize("scaling", ["frobenius", "power4"])
+@pytest.mark.parametrize("p", [3, 4])
+def test_scalings_against_transcript(env, scaling, p):
+    """Both cold-start scalings: results against eigh, iteration counts
+    against the fp64 transcript with the same scaling (C2-like flat spectrum
+    and a cond-1e3 spread), in fp32 and fp64."""
+    say("roots scaling", scaling, p)
+    torch, B, dev, h = env
+    code = B.SCALING_POWER4 if scaling == "power4" else B.SCALING_FROBENIUS
+    As = [cfg.wishart_bartlett(384, 40 * 384, 1.0 / 384, 99, p).astype(np.float32), spd(257, 1e3, 3 + p)]
+    for prec in (0, 2):
+        Xs, info = roots(env, As, p=p, eps=1e-6, scaling=code, precision=prec)
+        for A, X, inf in zip(As, Xs, info):
+            Xo, _, _ = O.inv_root(A, p, 1e-6)
+            assert inf["status"] in (0, 1), inf
+            assert rel(X, Xo) <= (1e-3 if prec == 0 else 1e-6), (inf, rel(X, Xo))
+            tr = O.coupled_newton(A, p, 1e-6, tol=1e-6, scaling=scaling)
+            assert abs(inf["iters"] - tr["iters"]) <= 1, (inf, tr["iters"])
 
 
 def test_closed_forms(env):
@@ -90,7 +110,7 @@ def test_c2_full_size_grouped_sampled(env):
     for i in (0, 31, 64, 95):
         Xo, _, _ = O.inv_root(As[i], 4, 1e-6)
         assert rel(Xs[i], Xo) <= 1e-3, (i, rel(Xs[i], Xo))
-        tr = O.coupled_newton(As[i], 4, 1e-6, tol=1e-6)
+        tr = O.coupled_newton(As[i], 4, 1e-6, tol=1e-6, scaling="power4")
         assert abs(info[i]["iters"] - tr["iters"]) <= 1, (info[i], tr["iters"])
     # the property X^4 A_d = I holds for every matrix (checked on the GPU result)
     torch, B, dev, h = env

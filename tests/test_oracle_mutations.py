@@ -35,6 +35,10 @@ MUTATIONS = [
      [P.pin_newton_vs_eigh]),
     ("coupled_newton", "z = (1.0 + p) / (2.0 * np.linalg.norm(Ad, 'fro'))",
      "z = (1.0 + p) / (2.0 * np.linalg.norm(As, 'fro'))", [P.pin_newton_scalar_iters]),
+    ("coupled_newton", "np.linalg.matrix_power(z * Ad, 4), 'fro') ** 0.25", "np.linalg.matrix_power(z * Ad, 2), 'fro') ** 0.5",
+     [P.pin_newton_power4_scaling]),
+    ("coupled_newton", "z *= max(1.0, (1.0 + p) / (2.0 * rho))", "z *= max(1.0, (1.0 + p) / rho)",
+     [P.pin_newton_power4_scaling]),
     ("precondition", "P = _f64(Lr) @ P", "P = _f64(Lr).T @ P", [P.pin_precondition_kronecker]),
     ("precondition", "P = P @ _f64(Rr)", "P = P @ _f64(Rr).T",
      [P.pin_precondition_kronecker]),
