@@ -348,6 +348,8 @@ def main():
     ap.add_argument("--scaling", choices=["power4", "frobenius"], default="power4",
                     help="cold-start scaling of the roots: power4 (library default, bound ||A^4||_F^(1/4)) or "
                          "frobenius (Algorithm 1 as printed)")
+    ap.add_argument("--no-compare-scaling", action="store_true",
+                    help="skip the comparison roots call under the other scaling (for profiling runs)")
     ap.add_argument("--vocab", type=int, default=32768, help="c6: table rows")
     ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -431,17 +433,19 @@ def main():
 
     # The same roots under the other scaling, for comparison (roots call only).
     other = B.SCALING_FROBENIUS if scaling == B.SCALING_POWER4 else B.SCALING_POWER4
-    prm_o = B.shampoo_root_params_default(p=p, eps=eps, scaling=other)
-    Xo = [torch.zeros(n, n, device=dev) for _ in range(nb)]
-    B.shampoo_inv_root_batched(h, Ls, Xo, prm_o, ws, info)
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    for _ in range(3):
+    other_ms, other_iters = None, None
+    if not args.no_compare_scaling:
+        prm_o = B.shampoo_root_params_default(p=p, eps=eps, scaling=other)
+        Xo = [torch.zeros(n, n, device=dev) for _ in range(nb)]
         B.shampoo_inv_root_batched(h, Ls, Xo, prm_o, ws, info)
-    torch.cuda.synchronize()
-    other_ms = (time.perf_counter() - t1) * 1e3 / 3
-    other_iters = float(np.mean([i["iters"] for i in B.decode_root_info(info)]))
-    del Xo
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(3):
+            B.shampoo_inv_root_batched(h, Ls, Xo, prm_o, ws, info)
+        torch.cuda.synchronize()
+        other_ms = (time.perf_counter() - t1) * 1e3 / 3
+        other_iters = float(np.mean([i["iters"] for i in B.decode_root_info(info)]))
+        del Xo
 
     # algorithmic work
     # Products per matrix at p = 4: X M1, M1 M1, (M1^2)^2 and M1^4 M per
@@ -509,9 +513,9 @@ def main():
         "roots_per_s_root_phase": nb * args.steps / ((times["newton_f32"][0] + times["newton_f64"][0]
                                                       + times["root_aux"][0]) * 1e-3),
         "newton_products_per_root": prod32 / max(1, nb * args.steps),
-        "other_scaling": {"scaling": "frobenius" if scaling == B.SCALING_POWER4 else "power4",
-                          "roots_call_ms": other_ms, "roots_per_s_roots_call": nb / (other_ms * 1e-3),
-                          "iters_mean": other_iters},
+        "other_scaling": None if other_ms is None else {
+            "scaling": "frobenius" if scaling == B.SCALING_POWER4 else "power4",
+            "roots_call_ms": other_ms, "roots_per_s_roots_call": nb / (other_ms * 1e-3), "iters_mean": other_iters},
     }
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")

@@ -384,23 +384,22 @@ __device__ __forceinline__ double block_sum(double v, double* red) {
   return s;
 }
 
-// MaxSV, one power step over all matrices.  Workgroup (matrix, ti, tj)
-// stages tile A[ti, tj] in LDS and writes its row partials (A vh)_rows and
-// column partials (A^T vh)_cols; the last workgroup of a matrix (atomic
-// ticket, no waiting) reduces the partials in a fixed order to
+// MaxSV, one power step over all matrices, in two launches.  Tile pass:
+// workgroup (matrix, ti, tj) stages tile A[ti, tj] in LDS and writes its
+// row partials (A vh)_rows and column partials (A^T vh)_cols.  Reduce pass
+// (maxsv_reduce_kernel): the partials in a fixed order give
 // v = A_s vh = (A vh + A^T vh) / 2, the Rayleigh quotient lambda = vh . v,
 // the stop test |lambda - lambda_old| <= tol lambda, and the next
-// vh = v / |v|.  Vector layout per matrix (doubles): [0, n) vh,
-// [n, n + T n) row partials by tile column, [n + T n, n + 2 T n) column
-// partials by tile row.
+// vh = v / |v|.  No workgroup waits on or signals another (a device-scope
+// fence per workgroup would write back and invalidate the XCD L2s).
+// Vector layout per matrix (doubles): [0, n) vh, [n, n + T n) row partials
+// by tile column, [n + T n, n + 2 T n) column partials by tile row.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                             RootState* __restrict__ st, int total_full,
-                                                             int* __restrict__ tickets, double tol, double eps,
-                                                             int last_step) {
+                                                             const RootState* __restrict__ st, int total_full) {
   __shared__ float tile[kTile * (kTile + 1)];
-  __shared__ double red[kThreads / 64];
-  __shared__ int is_last;
+  __shared__ double vr[kTile], vc[kTile];       // v on the tile's rows and columns
+  __shared__ double half_sum[2][kTile];
   const int t = blockIdx.x;
   if (t >= total_full) return;
   const int j = find_job_full(jobs, njobs, t);
@@ -414,29 +413,60 @@ __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>
   double* prow = J->vec + n;
   double* pcol = J->vec + n + (int64_t)TN * n;
   const float* A = J->A;
-  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-    const int r = e >> 7, c = e & 127;
-    tile[r * (kTile + 1) + c] = (r0 + r < n && c0 + c < n) ? A[(int64_t)(r0 + r) * n + c0 + c] : 0.f;
+  if (threadIdx.x < kTile) {
+    const int i = threadIdx.x;
+    vc[i] = c0 + i < n ? vh[c0 + i] : 0.0;
+    vr[i] = r0 + i < n ? vh[r0 + i] : 0.0;
   }
-  __syncthreads();
-  {
-    const int q = threadIdx.x & 127;  // a row of the tile (first half) or a column (second half)
-    double acc = 0.0;
-    if (threadIdx.x < kTile) {
-      for (int c = 0; c < kTile && c0 + c < n; ++c) acc += (double)tile[q * (kTile + 1) + c] * vh[c0 + c];
-      if (r0 + q < n) prow[(int64_t)tj * n + r0 + q] = acc;
-    } else {
-      for (int r = 0; r < kTile && r0 + r < n; ++r) acc += (double)tile[r * (kTile + 1) + q] * vh[r0 + r];
-      if (c0 + q < n) pcol[(int64_t)ti * n + c0 + q] = acc;
+  if ((n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n && (reinterpret_cast<uintptr_t>(A) & 15) == 0) {
+    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
+      const int r = e >> 5, c = (e & 31) * 4;
+      const f4v v = gload<f4v>(A + (int64_t)(r0 + r) * n + c0 + c);
+      float* d = tile + r * (kTile + 1) + c;
+      d[0] = v[0]; d[1] = v[1]; d[2] = v[2]; d[3] = v[3];
+    }
+  } else {
+    for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+      const int r = e >> 7, c = e & 127;
+      tile[r * (kTile + 1) + c] = (r0 + r < n && c0 + c < n) ? A[(int64_t)(r0 + r) * n + c0 + c] : 0.f;
     }
   }
-  __threadfence();  // release: this workgroup's partials before its ticket
   __syncthreads();
-  if (threadIdx.x == 0) is_last = atomicAdd(&tickets[j], 1) == TN * TN - 1;
+  // (A v) on the tile's rows and (A^T v) on its columns, each dot product
+  // split over the two halves of the workgroup
+  const int qi = threadIdx.x & 127, hf = threadIdx.x >> 7;
+  {
+    double acc = 0.0;
+    for (int c = hf * 64; c < hf * 64 + 64; ++c) acc += (double)tile[qi * (kTile + 1) + c] * vc[c];
+    half_sum[hf][qi] = acc;
+  }
   __syncthreads();
-  if (!is_last) return;
-  __threadfence();  // acquire: partials of the other workgroups (any XCD) are visible
-  // reduction by the last workgroup of this matrix
+  if (hf == 0 && r0 + qi < n) prow[(int64_t)tj * n + r0 + qi] = half_sum[0][qi] + half_sum[1][qi];
+  __syncthreads();
+  {
+    double acc = 0.0;
+    for (int r = hf * 64; r < hf * 64 + 64; ++r) acc += (double)tile[r * (kTile + 1) + qi] * vr[r];
+    half_sum[hf][qi] = acc;
+  }
+  __syncthreads();
+  if (hf == 0 && c0 + qi < n) pcol[(int64_t)ti * n + c0 + qi] = half_sum[0][qi] + half_sum[1][qi];
+}
+
+// MaxSV reduction, one workgroup per matrix: v = (A v + A^T v) / 2 from the
+// tile partials (fixed order), lambda = vh . v, vh = v / ||v||.  The kernel
+// boundary after the tile pass makes every partial visible.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void maxsv_reduce_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                               RootState* __restrict__ st, double tol, double eps,
+                                                               int last_step) {
+  __shared__ double red[kThreads / 64];
+  const int j = blockIdx.x;
+  if (j >= njobs || st[j].status != kActive || st[j].sv_done) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int n = J->n, TN = J->tiles_n;
+  double* vh = J->vec;
+  double* prow = J->vec + n;
+  double* pcol = J->vec + n + (int64_t)TN * n;
   double q = 0.0, s2 = 0.0;
   for (int i = threadIdx.x; i < n; i += kThreads) {
     double a = 0.0, b = 0.0;
@@ -458,14 +488,12 @@ __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>
     st[j].eps_eff = eps * lam;
     st[j].sv_steps += 1;
     if (fabs(lam - lam_old) <= tol * fabs(lam) || last_step) st[j].sv_done = 1;
-    tickets[j] = 0;
   }
 }
 
 // Starting vector of MaxSV: vh = ones / sqrt(n).
 template <typename T>
-__global__ void maxsv_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, RootState* __restrict__ st,
-                                  int* __restrict__ tickets) {
+__global__ void maxsv_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, RootState* __restrict__ st) {
   const int j = blockIdx.x;
   if (j >= njobs) return;
   const int n = jobs[j].n;
@@ -474,7 +502,6 @@ __global__ void maxsv_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njo
     st[j].lam_max = 0.0;
     st[j].sv_done = 0;
     st[j].sv_steps = 0;
-    tickets[j] = 0;
   }
 }
 
@@ -781,8 +808,12 @@ __global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int pha
 
 // Per-iteration state machine, one workgroup; also counts active matrices.
 //   init != 0: evaluates the residual of M0 only.
+// esc_thr (AUTO fp32 phase, else NULL): esc_thr[k-1] is the largest residual
+// after k iterations of a matrix that can still converge within the phase's
+// cap; a matrix above it leaves the phase at once (MAXITER, escalated).
 __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __restrict__ st, int njobs, int init,
-                                                              float tol, int max_iters, int* __restrict__ count) {
+                                                              float tol, int max_iters, int* __restrict__ count,
+                                                              const float* __restrict__ esc_thr, int esc_n) {
   __shared__ int red[kThreads / 64];
   int active = 0;
   for (int j = threadIdx.x; j < njobs; j += kThreads) {
@@ -803,6 +834,7 @@ __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __rest
       else if (r <= tol) s.status = kConverged;
       else if (prev < kStagGate && r >= prev) s.status = kStagnated;
       else if (s.iters >= max_iters) s.status = kMaxIter;
+      else if (esc_thr && s.iters <= esc_n && r > esc_thr[s.iters - 1]) s.status = kMaxIter;
     }
     if (s.status == kActive) ++active;
   }

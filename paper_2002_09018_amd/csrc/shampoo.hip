@@ -397,7 +397,7 @@ shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float 
 
 // ---------------------------------------------------------------- roots
 struct RootLayout {
-  size_t state = 0, counts = 0, tickets = 0, total = 0;
+  size_t state = 0, counts = 0, total = 0;
   std::vector<size_t> part, vec, f32, f64;  // per job offsets
 };
 
@@ -408,8 +408,6 @@ RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
   off += align256((size_t)njobs * sizeof(RootState));
   L.counts = off;
   off += align256((kCountRing + 2) * sizeof(int));
-  L.tickets = off;
-  off += align256((size_t)njobs * sizeof(int));
   for (int j = 0; j < njobs; ++j) {
     const size_t n = (size_t)jobs[j].n;
     const size_t T = (size_t)cdiv(jobs[j].n, kTile);
@@ -550,7 +548,7 @@ NewtonStage drop_x(const NewtonStage& s0) {
 template <typename T>
 shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
                             int total_up, int total_full, const NewtonProgram& prog, int p, int scaling, float tol,
-                            int cap, int poll, int cls, hipStream_t s) {
+                            int cap, int poll, int cls, const float* esc_thr, int esc_n, hipStream_t s) {
   const int lds = 0;  // static LDS
   auto kstage = newton_stage_kernel<T>;
   const bool power = scaling == SHAMPOO_SCALING_POWER4;
@@ -580,7 +578,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
-                       dcount + kCountRing);
+                       dcount + kCountRing, (const float*)nullptr, 0);
   }));
   const NewtonStage first0 = drop_x(prog.stages[0]);
   for (int it = 0; it < cap; ++it) {
@@ -601,7 +599,8 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
     }
     int* slot = dcount + (it % kCountRing);
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, cap, slot);
+      hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, cap, slot, esc_thr,
+                         esc_n);
     }));
     if (poll) {
       HIP_TRY(h, hipMemcpyAsync(h->pinned + (it % kCountRing), slot, sizeof(int), hipMemcpyDeviceToHost, s));
@@ -906,24 +905,29 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   // Prologue, shared by both precisions: MaxSV, Frobenius partials, z.
   const double eps = (double)prm->eps;
   if (prm->eps_relative) {
-    // MaxSV: one launch per power step over all matrices; matrices whose
-    // estimate has settled skip the remaining launches.
-    int* tickets = reinterpret_cast<int*>(ws + L.tickets);
+    // MaxSV: a tile pass and a reduce pass per power step over all
+    // matrices; matrices whose estimate has settled skip the rest.
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       if (j32)
-        hipLaunchKernelGGL(maxsv_init_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, njobs, st, tickets);
+        hipLaunchKernelGGL(maxsv_init_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, njobs, st);
       else
-        hipLaunchKernelGGL(maxsv_init_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, njobs, st, tickets);
+        hipLaunchKernelGGL(maxsv_init_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, njobs, st);
     }));
+    const double mtol = (double)prm->maxsv_tol;
     for (int k = 0; k < prm->maxsv_steps; ++k) {
       const int last = k + 1 == prm->maxsv_steps;
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-        if (j32)
-          hipLaunchKernelGGL(maxsv_step_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full,
-                             tickets, (double)prm->maxsv_tol, eps, last);
-        else
-          hipLaunchKernelGGL(maxsv_step_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full,
-                             tickets, (double)prm->maxsv_tol, eps, last);
+        if (j32) {
+          hipLaunchKernelGGL(maxsv_step_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs,
+                             (const RootState*)st, full);
+          hipLaunchKernelGGL(maxsv_reduce_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, njobs, st, mtol,
+                             eps, last);
+        } else {
+          hipLaunchKernelGGL(maxsv_step_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs,
+                             (const RootState*)st, full);
+          hipLaunchKernelGGL(maxsv_reduce_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, njobs, st, mtol,
+                             eps, last);
+        }
       }));
     }
   }
@@ -946,13 +950,35 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   int run64 = tail_all;
   if (j32) {
     int cap = prm->max_iters;
+    const float* esc = nullptr;
+    int esc_n = 0;
     if (prec == SHAMPOO_PRECISION_AUTO) {
+      const double tl = std::max((double)prm->tol, 1e-6);
       const double m0 = std::min(1.0, (p + 1.0) / (2.0 * (double)prm->kappa32));
-      const int k32 = host_scalar_iters(m0, p, std::max((double)prm->tol, 1e-6), 1000) + 1;
+      const int k32 = host_scalar_iters(m0, p, tl, 1000) + 1;
       cap = std::min(cap, std::max(k32, 1));
+      // Early escalation: m1 is the smallest scaled eigenvalue that still
+      // converges within the cap; after k iterations it has reached f^k(m1)
+      // (f(m) = ((p+1-m)/p)^p m), so a residual above 1 - f^k(m1) means the
+      // matrix would reach the cap unconverged.
+      double lo = 1e-300, hi = 1.0;
+      for (int b = 0; b < 200; ++b) {
+        const double mid = sqrt(lo * hi);
+        if (host_scalar_iters(mid, p, tl, cap + 1) <= cap) hi = mid; else lo = mid;
+      }
+      std::vector<float> thr(cap);
+      double m = hi;
+      for (int k = 0; k < cap; ++k) {
+        m = pow((p + 1.0 - m) / p, p) * m;
+        thr[k] = (float)(1.0 - m);  // escalating a borderline matrix early is harmless
+      }
+      const void* d = nullptr;
+      STATUS_TRY(upload_table(h, thr.data(), thr.size() * sizeof(float), s, &d));
+      esc = static_cast<const float*>(d);
+      esc_n = cap;
     }
     STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap, prm->poll,
-                                   SHAMPOO_KCLASS_NEWTON_F32, s));
+                                   SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
         hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + kCountRing + 1);
@@ -977,7 +1003,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       }));
     }
     STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
-                                    SHAMPOO_KCLASS_NEWTON_F64, s));
+                                    SHAMPOO_KCLASS_NEWTON_F64, nullptr, 0, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);
     }));

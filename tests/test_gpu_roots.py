@@ -169,6 +169,23 @@ def test_precision_policies_agree(env):
         assert rel(a, Xo) <= 1e-3 and rel(b, Xo) <= 1e-6
 
 
+def test_auto_escalates_early(env):
+    """AUTO: a matrix whose condition number is far above kappa32 leaves the
+    fp32 phase before the cap (its residual max|M - I| is above what the
+    slowest matrix that still converges within the cap can have); one below
+    kappa32 stays in fp32.  Both agree with eigh.  The cap is the scalar
+    recurrence's count from (p+1) / (2 kappa32), plus one."""
+    say("roots AUTO early escalation")
+    A_ok, A_bad = spd(200, 1e3, 21), spd(200, 1e7, 22)
+    Xs, info = roots(env, [A_ok, A_bad], p=4, eps=0.0)
+    cap = O.scalar_newton_iters(5.0 / (2.0 * 1e4), 4, 1e-6) + 1
+    assert info[0]["precision"] == 32, info[0]
+    assert info[1]["precision"] == 64 and 1 <= info[1]["iters_fp32"] < cap, (info[1], cap)
+    for A, X, inf in zip((A_ok, A_bad), Xs, info):
+        Xo, _, _ = O.inv_root(A, 4, 0.0)
+        assert rel(X, Xo) <= band(O.cond_damped(A, 0.0)), (inf, rel(X, Xo))
+
+
 def test_status_paths_and_isolation(env):
     """MAXITER at a cap of 1, DIVERGED/NOT_PD on an indefinite matrix,
     NOT_PD on a zero matrix without damping, DIVERGED on NaN; the healthy
