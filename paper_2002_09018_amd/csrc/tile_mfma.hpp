@@ -66,6 +66,9 @@ struct Mfma;
 #ifndef SHP_BK_F32
 #define SHP_BK_F32 16
 #endif
+#ifndef SHP_SPLIT_STAGE
+#define SHP_SPLIT_STAGE 0
+#endif
 #ifndef SHP_PADK_WORDS
 #define SHP_PADK_WORDS 0
 #endif
@@ -268,23 +271,25 @@ struct WaveAcc {
         for (int v = 0; v < Mfma<T>::kAcc; ++v) c[i][j][v] = (T)0;
   }
 
-  // One LDS stage: kBK / kK MFMA k-steps over the wave's NB x NB blocks.
-  template <int LA, int LB, int LDPA, int LDPB>
+  // MFMA k-steps [S0, S1) of one LDS stage (kBK / kK steps in all) over the
+  // wave's NB x NB blocks.
+  template <int LA, int LB, int LDPA, int LDPB, int S0 = 0, int S1 = Mfma<T>::kBK / Mfma<T>::kK>
   __device__ __forceinline__ void stage(const T* __restrict__ a, const T* __restrict__ b, int wm0,
                                         int wn0, int lane) {
     constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;  // k-steps per stage
     constexpr int VP = 16 / (int)sizeof(T);         // elements per 16-byte LDS read
     static_assert(KS % VP == 0, "row fragments are read 16 bytes at a time");
+    static_assert(S0 % VP == 0 && S1 % VP == 0 && S0 < S1 && S1 <= KS, "k-step range of whole 16-byte reads");
     typedef T vec_t __attribute__((ext_vector_type(VP)));
     const int g = lane / Mfma<T>::kM;  // this lane's k group: k = g * KS + s at k-step s
     const int ml = lane % Mfma<T>::kM;
-    // kLayoutRow fragments: all KS values of the stage, 16 bytes at a time.
+    // kLayoutRow fragments: the range's values, 16 bytes at a time.
     T ra[LA == kLayoutRow ? NB : 1][KS], rb[LB == kLayoutRow ? NB : 1][KS];
     if (LA == kLayoutRow) {
 #pragma unroll
       for (int i = 0; i < NB; ++i)
 #pragma unroll
-        for (int c = 0; c < KS / VP; ++c) {
+        for (int c = S0 / VP; c < S1 / VP; ++c) {
           const vec_t v = *reinterpret_cast<const vec_t*>(a + (wm0 + i * Mfma<T>::kM + ml) * LDPA + g * KS + c * VP);
 #pragma unroll
           for (int e = 0; e < VP; ++e) ra[i][c * VP + e] = v[e];
@@ -294,7 +299,7 @@ struct WaveAcc {
 #pragma unroll
       for (int j = 0; j < NB; ++j)
 #pragma unroll
-        for (int c = 0; c < KS / VP; ++c) {
+        for (int c = S0 / VP; c < S1 / VP; ++c) {
           const vec_t v = *reinterpret_cast<const vec_t*>(b + (wn0 + j * Mfma<T>::kM + ml) * LDPB + g * KS + c * VP);
 #pragma unroll
           for (int e = 0; e < VP; ++e) rb[j][c * VP + e] = v[e];
@@ -307,16 +312,16 @@ struct WaveAcc {
     const T* pb = b + g * KS * LDPB + wn0 + ml;
     if (LA == kLayoutK) {
 #pragma unroll
-      for (int i = 0; i < NB; ++i) fa[0][i] = pa[i * Mfma<T>::kM];
+      for (int i = 0; i < NB; ++i) fa[S0 & 1][i] = pa[S0 * LDPA + i * Mfma<T>::kM];
     }
     if (LB == kLayoutK) {
 #pragma unroll
-      for (int j = 0; j < NB; ++j) fb[0][j] = pb[j * Mfma<T>::kM];
+      for (int j = 0; j < NB; ++j) fb[S0 & 1][j] = pb[S0 * LDPB + j * Mfma<T>::kM];
     }
 #pragma unroll
-    for (int s = 0; s < KS; ++s) {
+    for (int s = S0; s < S1; ++s) {
       const int cur = s & 1;
-      if (s + 1 < KS) {
+      if (s + 1 < S1) {
         if (LA == kLayoutK) {
 #pragma unroll
           for (int i = 0; i < NB; ++i) fa[cur ^ 1][i] = pa[(s + 1) * LDPA + i * Mfma<T>::kM];
@@ -428,7 +433,13 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
   sb.finish(B, br, bc, b0, tid);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
-  // one stage: prefetch st+1 into (na, nb) while computing on (ca, cb)
+  // one stage: prefetch st+1 into (na, nb) while computing on (ca, cb).
+  // SHP_SPLIT_STAGE: the LDS writes of st+1 go between the two halves of
+  // the stage's MFMAs (the buffer they fill was released by the previous
+  // barrier), so their latency hides under the second half instead of
+  // stalling every wave at the stage end.
+  constexpr int KSTEPS = Mfma<T>::kBK / Mfma<T>::kK;
+  constexpr int KH = SHP_SPLIT_STAGE ? KSTEPS / 2 : KSTEPS;
   auto step = [&](int st, T* ca, T* cb, T* na, T* nb) {
     const bool more = st + 1 < nst;
     if (more) {
@@ -437,11 +448,14 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
       sa.issue(A, ar, ac, na, tid);
       sb.issue(B, br, bc, nb, tid);
     }
-    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP>(ca, cb, wm0, wn0, lane);
+    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, 0, KH>(ca, cb, wm0, wn0, lane);
     if (more) {
       sa.finish(A, ar, ac, na, tid);
       sb.finish(B, br, bc, nb, tid);
-      __builtin_amdgcn_s_waitcnt(0);
+      if (!SHP_SPLIT_STAGE) __builtin_amdgcn_s_waitcnt(0);
+    }
+    if constexpr (KH < KSTEPS) {
+      if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, KH, KSTEPS>(ca, cb, wm0, wn0, lane);
     }
     __syncthreads();
   };
