@@ -336,15 +336,207 @@ def run_c3(args, torch, B):
     print(json.dumps(out), flush=True)
 
 
+def run_c5(args, torch, B):
+    """C5: a 32768 x 1024 embedding (32 row blocks of 1024 x 1024) and 200
+    square blocks with sides drawn from {128, ..., 2048}, bf16-stored
+    gradients N(0, 1e-3) and fp32 statistics L and R for every block.  Ten
+    statistics steps build the factors; one grouped call then roots all 464
+    factors (p = 4, per-matrix early exit); the call is timed, and each size
+    class is also rooted alone.  A step is the statistics, the two-sided
+    preconditioning and the graft over the 232 blocks."""
+    from synth import configs as cfg
+    dev = torch.device("cuda:0")
+    nemb = cfg.C5_EMB_ROWS // cfg.C5_D
+    shp = [(cfg.C5_D, cfg.C5_D)] * nemb + [(k, k) for k in cfg.c5_mixed_sizes()]
+    nb = len(shp)
+    gen = torch.Generator(device=dev).manual_seed(5)
+    emb = torch.empty(cfg.C5_EMB_ROWS, cfg.C5_D, dtype=torch.bfloat16, device=dev)
+    mixed = [torch.empty(s, dtype=torch.bfloat16, device=dev) for s in shp[nemb:]]
+    tensors = [emb] + mixed
+    Gv = [emb[i * cfg.C5_D:(i + 1) * cfg.C5_D] for i in range(nemb)] + mixed
+    Wt = [0.02 * torch.randn(t.shape, device=dev, generator=gen) for t in tensors]
+    Dt = [torch.zeros(t.shape, device=dev) for t in tensors]
+    Pt = [torch.zeros(t.shape, device=dev) for t in tensors]
+
+    def view(ts, b):
+        return ts[0][b * cfg.C5_D:(b + 1) * cfg.C5_D] if b < nemb else ts[1 + b - nemb]
+
+    Ls = [torch.zeros(m, m, device=dev) for m, _ in shp]
+    Rs = [torch.zeros(n, n, device=dev) for _, n in shp]
+    Lrs = [torch.zeros_like(a) for a in Ls]
+    Rrs = [torch.zeros_like(a) for a in Rs]
+    blocks = [B.Block(G=Gv[b], W=view(Wt, b), D=view(Dt, b), P=view(Pt, b), L=Ls[b], R=Rs[b], Lr=Lrs[b],
+                      Rr=Rrs[b]) for b in range(nb)]
+    h = B.shampoo_create(0)
+
+    def fill_grads():
+        for t in tensors:
+            t.copy_((torch.randn(t.shape, device=dev, generator=gen) * 1e-3 ** 0.5).to(torch.bfloat16))
+
+    log(f"C5: {nb} blocks, 10 statistics steps")
+    for t in range(10):
+        fill_grads()
+        B.shampoo_update_stats(h, blocks)
+    torch.cuda.synchronize()
+    As, Xs = Ls + Rs, Lrs + Rrs
+    ns = [a.shape[0] for a in As]
+    prm = B.shampoo_root_params_default(p=4, eps=1e-6)
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes(ns, prm.precision), dtype=torch.uint8, device=dev)
+    info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_batched(h, As[:2], Xs[:2], prm, ws, info)     # warm-up
+    torch.cuda.synchronize()
+    B.shampoo_timing_enable(h, True)
+    for c in range(len(B.KCLASS_NAMES)):
+        B.shampoo_timing_read(h, c)
+    t0 = time.perf_counter()
+    B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info)
+    torch.cuda.synchronize()
+    root_ms = (time.perf_counter() - t0) * 1e3
+    B.shampoo_timing_enable(h, False)
+    rt = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
+    inf = B.decode_root_info(info)
+    log(f"grouped roots: {len(As)} in {root_ms:.1f} ms")
+    sym = [n * n * (n + 1) for n in ns]
+    prods = [newton_products(i["iters"], 4, True) for i in inf]
+    executed = sum(pq * s for pq, s in zip(prods, sym))
+    kmax = max(i["iters"] for i in inf)
+    no_exit = newton_products(kmax, 4, True) * sum(sym)
+    classes = {}
+    for k in sorted(set(ns)):
+        sel = [j for j, n in enumerate(ns) if n == k]
+        a_k, x_k = [As[j] for j in sel], [Xs[j] for j in sel]
+        info_k = torch.zeros(8 * len(sel), dtype=torch.int32, device=dev)
+        B.shampoo_inv_root_batched(h, a_k, x_k, prm, ws, info_k)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        B.shampoo_inv_root_batched(h, a_k, x_k, prm, ws, info_k)
+        torch.cuda.synchronize()
+        ms_k = (time.perf_counter() - t1) * 1e3
+        it_k = [inf[j]["iters"] for j in sel]
+        classes[str(k)] = {"roots": len(sel), "iters_min": min(it_k), "iters_max": max(it_k),
+                           "iters_mean": float(np.mean(it_k)), "alone_ms": ms_k,
+                           "alone_roots_per_s": len(sel) / ms_k * 1e3,
+                           "alone_newton_tflops": sum(prods[j] * sym[j] for j in sel) / (ms_k * 1e-3) / 1e12}
+        log(f"  class {k}: {len(sel)} roots alone in {ms_k:.2f} ms")
+
+    def step():
+        B.shampoo_update_stats(h, blocks)
+        B.shampoo_precondition(h, blocks)
+        B.shampoo_graft(h, blocks, 1e-2)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    B.shampoo_timing_enable(h, True)
+    for c in range(len(B.KCLASS_NAMES)):
+        B.shampoo_timing_read(h, c)
+    t0 = time.perf_counter()
+    for s_ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    B.shampoo_timing_enable(h, False)
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
+    B.shampoo_destroy(h)
+    K = args.steps
+    flops_stats = K * sum(m * (m + 1) * n + n * (n + 1) * m for m, n in shp)
+    flops_prec = K * sum(2 * m * m * n + 2 * m * n * n for m, n in shp)
+    bytes_graft = K * sum(m * n for m, n in shp) * 26     # bf16 G: 2 + 3 * 4 B pass 1, 3 * 4 B pass 2
+    roof_ms = ((flops_stats + flops_prec) / PEAK_F32_MFMA / 1e9 + bytes_graft / PEAK_HBM / 1e6) / K
+    ms_step = elapsed * 1e3 / K
+    ms_newton = rt["newton_f32"][0] + rt["newton_f64"][0]
+    out = {
+        "metric": "C5 grouped inverse roots (464 factors, sizes 128..2048) + bf16 stats+precondition+graft step",
+        "value": ms_step, "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+        "ms_per_step": ms_step, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32 (bf16-stored G)", "data": "synthetic",
+        "config": {"workload": "C5: embedding 32768x1024 as 32 row blocks + 200 square blocks k in "
+                               "{128,256,512,1024,2048}; G ~ N(0,1e-3) stored bf16; 10 stats steps; p=4, "
+                               "eps 1e-6", "blocks": nb, "factors": len(As)},
+        "phase_roofline_ms": roof_ms, "frac_of_phase_roofline": roof_ms / ms_step,
+        "phases_ms_per_step": {c: v[0] / K for c, v in times.items()},
+        "kernels": {"stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12,
+                    "precond_tflops": flops_prec / (times["precond"][0] * 1e-3) / 1e12,
+                    "graft_gbs": bytes_graft / (times["graft"][0] * 1e-3) / 1e9},
+        "grouped_roots": {
+            "roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
+            "newton_ms": ms_newton, "root_aux_ms": rt["root_aux"][0],
+            "newton_tflops": executed / (ms_newton * 1e-3) / 1e12 if ms_newton else None,
+            "statuses": sorted(set(i["status"] for i in inf)),
+            "n_fp64": sum(1 for i in inf if i["precision"] == 64),
+            "executed_gflop": executed / 1e9, "no_early_exit_gflop": no_exit / 1e9,
+            "early_exit_saving": 1.0 - executed / no_exit,
+            "by_size": classes,
+        },
+    }
+    print(json.dumps(out), flush=True)
+
+
+def run_c1(args, torch, B):
+    """C1: one 128 x 128 block, ten steps of gradients N(0, 1/128); each step
+    is the two-sided statistics, both inverse 4th roots (one grouped call),
+    the preconditioning and the graft.  Latency-bound: the ten steps are run
+    `--steps` times from the same initial state and timed per step."""
+    from synth import configs as cfg
+    dev = torch.device("cuda:0")
+    n, nsteps = 128, 10
+    Gs = [torch.from_numpy(cfg.c1_grad(t)).to(dev) for t in range(1, nsteps + 1)]
+    W0 = torch.from_numpy(cfg.c1_weight()).to(dev)
+    G = torch.zeros(n, n, device=dev)
+    W, D, P = W0.clone(), torch.zeros(n, n, device=dev), torch.zeros(n, n, device=dev)
+    L, R = torch.zeros(n, n, device=dev), torch.zeros(n, n, device=dev)
+    Lr, Rr = torch.zeros(n, n, device=dev), torch.zeros(n, n, device=dev)
+    blk = [B.Block(G=G, W=W, D=D, P=P, L=L, R=R, Lr=Lr, Rr=Rr)]
+    h = B.shampoo_create(0)
+    prm = B.shampoo_root_params_default(p=4, eps=1e-6)
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([n, n], prm.precision), dtype=torch.uint8, device=dev)
+    info = torch.zeros(16, dtype=torch.int32, device=dev)
+    iters = []
+
+    def run10(record):
+        W.copy_(W0); D.zero_(); L.zero_(); R.zero_()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for t in range(nsteps):
+            G.copy_(Gs[t])
+            B.shampoo_update_stats(h, blk)
+            B.shampoo_inv_root_batched(h, [L, R], [Lr, Rr], prm, ws, info)
+            B.shampoo_precondition(h, blk)
+            B.shampoo_graft(h, blk, 1e-2)
+            if record:
+                iters.append([i["iters"] for i in B.decode_root_info(info)])
+        torch.cuda.synchronize()
+        return time.perf_counter() - t0
+
+    for _ in range(args.warmup):
+        run10(False)
+    ts = [run10(False) for _ in range(args.steps)]
+    run10(True)
+    B.shampoo_destroy(h)
+    us = float(np.median(ts)) / nsteps * 1e6
+    out = {
+        "metric": "C1 single 128x128 block: us per step (stats L,R + 2 inverse 4th roots + precondition + graft)",
+        "value": us, "unit": "us/step", "n_gpus": 1, "steps": args.steps * nsteps, "warmup": args.warmup,
+        "ms_per_step": us / 1e3, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "f32", "data": "synthetic",
+        "config": {"workload": "C1: one 128x128 block, 10 steps of G ~ N(0,1/128), roots every step, p=4, "
+                               "eps 1e-6, eta0 1e-2"},
+        "us_per_step_min": min(ts) / nsteps * 1e6, "us_per_step_max": max(ts) / nsteps * 1e6,
+        "root_iters_per_step": iters,
+    }
+    print(json.dumps(out), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--blocks", type=int, default=96)
-    ap.add_argument("--workload", choices=["c2", "c3", "c4", "c6"], default="c2",
-                    help="c2 (default): the metric's workload; c3: ill-conditioned roots; c4: the "
-                         "transformer-layer step; c6: the embedding-table step")
+    ap.add_argument("--workload", choices=["c1", "c2", "c3", "c4", "c5", "c6"], default="c2",
+                    help="c2 (default): the metric's workload; c1: single-block latency; c3: ill-conditioned "
+                         "roots; c4: the transformer-layer step; c5: mixed-size grouped roots and bf16 step; "
+                         "c6: the embedding-table step")
     ap.add_argument("--scaling", choices=["power4", "frobenius"], default="power4",
                     help="cold-start scaling of the roots: power4 (library default, bound ||A^4||_F^(1/4)) or "
                          "frobenius (Algorithm 1 as printed)")
@@ -372,6 +564,10 @@ def main():
         return run_c3(args, torch, B)
     if args.workload == "c6":
         return run_c6(args, torch, B)
+    if args.workload == "c5":
+        return run_c5(args, torch, B)
+    if args.workload == "c1":
+        return run_c1(args, torch, B)
     dev = torch.device("cuda:0")
     nb, n, k, p, eps, eta0 = args.blocks, 1024, 4096, 4, 1e-6, 1e-2
     log(f"generating {nb} blocks")
