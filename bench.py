@@ -57,13 +57,15 @@ def newton_products(iters, p, power):
     iterations: 1 + floor(log2 p) + popcount(p) per iteration, less the
     first X product (X0 is a multiple of I).  The power-bound start adds M0^2
     and M0^4 and turns the first iteration's M-only products of its first
-    stage (M1 M1, and M1 M for odd p) into an elementwise pass."""
+    stage (M1 M1, and M1 M for odd p) into an elementwise pass; at p = 4 the
+    whole first M update is one product (M0^2 and M0^4 are known)."""
     per = 1 + (p.bit_length() - 1) + bin(p).count("1")
     stage0 = 2 if (p & 1 and p > 1) else 1
     if iters <= 0:
         return 2 if power else 0
     if power:
-        return 2 + (per - 1 - stage0) + per * (iters - 1)
+        first = 1 if p == 4 else per - 1 - stage0
+        return 2 + first + per * (iters - 1)
     return per * iters - 1
 
 

@@ -535,24 +535,28 @@ __device__ __forceinline__ void sym_tile_pass(const float* __restrict__ A, int n
   }
 }
 
-// Per full tile: sum of s^2 over the tile, trace and minimum of its diagonal.
+// Per upper tile (ti <= tj): sum of s^2 over the tile, doubled off the
+// diagonal (the lower mirror has the same values), trace and minimum of the
+// diagonal.  Every element of A is read once from memory.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void frob_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                       const RootState* __restrict__ st, int total_full) {
+                                                       const RootState* __restrict__ st, int total_up) {
   __shared__ float lds[kTile * 33];
   __shared__ double red[kThreads / 64];
   const int t = blockIdx.x;
-  if (t >= total_full) return;
-  const int j = find_job_full(jobs, njobs, t);
+  if (t >= total_up) return;
+  const int j = find_job_up(jobs, njobs, t);
   if (st[j].status != kActive) return;
   const NewtonJob<T> J = jobs[j];
-  const int lt = t - J.full_begin;
-  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
+  const int lt = t - J.up_begin;
+  int ti, tj;
+  unrank_upper(lt, J.tiles_n, ti, tj);
   double ss = 0.0, tr = 0.0, dmin = INFINITY;
   sym_tile_pass(J.A, J.n, ti, tj, lds, [&](int r, int c, double s) {
     ss += s * s;
     if (r == c) { tr += s; dmin = dmin < s ? dmin : s; }
   });
+  if (ti != tj) ss *= 2.0;
   ss = block_sum(ss, red);
   tr = block_sum(tr, red);
   // min over the block
@@ -579,7 +583,7 @@ __global__ void root_prep_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= njobs || st[j].status != kActive) return;
   const NewtonJob<T> J = jobs[j];
-  const int nt = J.tiles_n * J.tiles_n;
+  const int nt = J.tiles_n * (J.tiles_n + 1) / 2;  // upper-tile partials
   double ss = 0.0, tr = 0.0, dmin = INFINITY;
   for (int q = 0; q < nt; ++q) {
     ss += J.part[3 * q + 0];
@@ -601,19 +605,21 @@ __global__ void root_prep_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
 }
 
 // M0 = z (A_s + eps I), X0 = z^(1/p) I (Algorithm 1 cold start); residual of
-// M0 accumulated into resid_bits.
+// M0 accumulated into resid_bits.  One workgroup per upper tile writes the
+// tile and its mirror (two symmetrised passes; the second one re-reads from
+// L2 what the first fetched).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                            RootState* __restrict__ st, int total_full, int p,
+                                                            RootState* __restrict__ st, int total_up, int p,
                                                             int write_x) {
   __shared__ float lds[kTile * 33];
   const int t = blockIdx.x;
-  if (t >= total_full) return;
-  const int j = find_job_full(jobs, njobs, t);
+  if (t >= total_up) return;
+  const int j = find_job_up(jobs, njobs, t);
   if (st[j].status != kActive) return;
   const NewtonJob<T> J = jobs[j];
-  const int lt = t - J.full_begin;
-  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
+  int ti, tj;
+  unrank_upper(t - J.up_begin, J.tiles_n, ti, tj);
   const double z = st[j].z, e = st[j].eps_eff;
   const T x0 = (T)pow(z, 1.0 / p);
   const T a = (T)(p + 1) / (T)p, b = (T)-1 / (T)p;
@@ -626,7 +632,7 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
   // product; a matrix that stops before any iteration gets X0 from the
   // output kernel.
   // write_x == 0: only M0 (the power-bound scaling rescales it later)
-  sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
+  auto f = [&](int r, int c, double s) {
     const T m = (T)(z * (s + (r == c ? e : 0.0)));
     M[(int64_t)r * n + c] = m;
     if (write_x) {
@@ -635,7 +641,9 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
       if (!(d <= 3.0e38f)) d = INFINITY;
       rmax = rmax > d ? rmax : d;
     }
-  });
+  };
+  sym_tile_pass(J.A, n, ti, tj, lds, f);
+  if (ti != tj) sym_tile_pass(J.A, n, tj, ti, lds, f);
   rmax = wave_max(rmax);
   if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
 }
@@ -647,28 +655,40 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
 // eigenvalue at or below (p + 1) / 2 (the margin Algorithm 1 keeps with the
 // Frobenius bound) while lifting the whole spectrum towards 1.
 //
-// Per full tile: sum of squares of S1 (buffer S[1]) into part[3 t].
+// Per upper tile: sum of squares of S1 (buffer S[1], exactly symmetric),
+// doubled off the diagonal, into part[3 t].
 template <typename T>
 __global__ __launch_bounds__(kThreads) void frob_s1_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                          const RootState* __restrict__ st, int total_full) {
+                                                          const RootState* __restrict__ st, int total_up) {
   __shared__ double red[kThreads / 64];
   const int t = blockIdx.x;
-  if (t >= total_full) return;
-  const int j = find_job_full(jobs, njobs, t);
+  if (t >= total_up) return;
+  const int j = find_job_up(jobs, njobs, t);
   if (st[j].status != kActive) return;
   const NewtonJob<T>* J = jobs + j;
-  const int lt = t - J->full_begin;
-  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
+  const int lt = t - J->up_begin;
+  int ti, tj;
+  unrank_upper(lt, J->tiles_n, ti, tj);
   const int n = J->n;
   const T* S = J->S[1];
+  const int r0 = ti * kTile, c0 = tj * kTile;
   double ss = 0.0;
-  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-    const int r = ti * kTile + (e >> 7), c = tj * kTile + (e & 127);
-    if (r < n && c < n) {
-      const double x = (double)S[(int64_t)r * n + c];
-      ss += x * x;
+  if (sizeof(T) == 4 && (n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n) {
+    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
+      const f4v x = gload<f4v>(reinterpret_cast<const float*>(S) + (int64_t)(r0 + (e >> 5)) * n + c0 + 4 * (e & 31));
+#pragma unroll
+      for (int q = 0; q < 4; ++q) ss += (double)x[q] * (double)x[q];
+    }
+  } else {
+    for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+      const int r = r0 + (e >> 7), c = c0 + (e & 127);
+      if (r < n && c < n) {
+        const double x = (double)S[(int64_t)r * n + c];
+        ss += x * x;
+      }
     }
   }
+  if (ti != tj) ss *= 2.0;
   ss = block_sum(ss, red);
   if (threadIdx.x == 0) J->part[3 * lt + 0] = ss;
 }
@@ -680,7 +700,7 @@ __global__ void root_rescale_kernel(const NewtonJob<T>* __restrict__ jobs, int n
   const int j = blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= njobs || st[j].status != kActive) return;
   const NewtonJob<T>* J = jobs + j;
-  const int nt = J->tiles_n * J->tiles_n;
+  const int nt = J->tiles_n * (J->tiles_n + 1) / 2;  // upper-tile partials
   double ss = 0.0;
   for (int q = 0; q < nt; ++q) ss += J->part[3 * q + 0];
   const double rho = pow(ss, 0.125);  // ||S1||_F^(1/4)
@@ -775,6 +795,87 @@ __global__ __launch_bounds__(kThreads) void newton_poly0_kernel(const NewtonJob<
     rmax = wave_max(rmax);
     if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
   }
+}
+
+// Start and first iteration at p = 4 under the power-bound scaling, in one
+// elementwise pass over the unscaled M0' (as the init kernel wrote it), with
+// M0 = c M0'.  M' = M1^4 M0 is a degree-5 polynomial of M0,
+// f(M) = sum_i C(4,i) a^(4-i) b^i M^(i+1), and the even powers
+// M0^2 = c^2 S0 and M0^4 = c^4 S1 are known from the bound, so
+//   M' = M0' (c (k3 M0^2 + k5 M0^4)) + (k1 M0 + k2 M0^2 + k4 M0^4)
+// takes one symmetric product.  This pass writes the right operand
+// c (k3 M0^2 + k5 M0^4) into S1, the affine term into S0 (in place: every
+// element is read, then written, by one thread), the first iterate
+// X1 = z^(1/p) (a I + b M0) and the residual max|M0 - I|.  M0 itself is never
+// stored.  All outputs stay exactly symmetric.
+template <typename T>
+__global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                                RootState* __restrict__ st, int total_full,
+                                                                double k1, double k2, double k3, double k4,
+                                                                double k5) {
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int lt = t - J->full_begin;
+  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
+  const int n = J->n;
+  const double cd = st[j].zc;
+  const T c = (T)cd, c2 = (T)(cd * cd), c4 = (T)(cd * cd * cd * cd);
+  const T K1 = (T)k1, K2 = (T)k2, K3c = (T)(k3 * cd), K4 = (T)k4, K5c = (T)(k5 * cd);
+  const T x0 = (T)pow(st[j].z, 0.25);
+  const T a = (T)1.25, b = (T)-0.25;
+  T* S0 = J->S[0];
+  T* S1 = J->S[1];
+  T* X1 = J->X[1];
+  const T* M = J->M[0];
+  const int r0 = ti * kTile, col0 = tj * kTile;
+  float rmax = 0.f;
+  auto one = [&](T mu, T s0, T s1, bool dg, T& e, T& r, T& x) {
+    const T m = c * mu, m2 = c2 * s0, m4 = c4 * s1;
+    r = K3c * m2 + K5c * m4;
+    e = K1 * m + K2 * m2 + K4 * m4;
+    x = x0 * (b * m + (dg ? a : (T)0));
+    float d = (float)fabs((double)m - (dg ? 1.0 : 0.0));
+    if (!(d <= 3.0e38f)) d = INFINITY;
+    rmax = rmax > d ? rmax : d;
+  };
+  if (sizeof(T) == 4 && (n & 3) == 0 && r0 + kTile <= n && col0 + kTile <= n) {
+    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
+      const int r = r0 + (e >> 5), cc = col0 + 4 * (e & 31);
+      const int64_t i = (int64_t)r * n + cc;
+      const f4v m = gload<f4v>(reinterpret_cast<const float*>(M) + i);
+      const f4v s0 = gload<f4v>(reinterpret_cast<const float*>(S0) + i);
+      const f4v s1 = gload<f4v>(reinterpret_cast<const float*>(S1) + i);
+      f4v eo, ro, xo;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        T ee, rr, xx;
+        one((T)m[q], (T)s0[q], (T)s1[q], r == cc + q, ee, rr, xx);
+        eo[q] = (float)ee;
+        ro[q] = (float)rr;
+        xo[q] = (float)xx;
+      }
+      gstore<f4v>(reinterpret_cast<float*>(S0) + i, eo);
+      gstore<f4v>(reinterpret_cast<float*>(S1) + i, ro);
+      gstore<f4v>(reinterpret_cast<float*>(X1) + i, xo);
+    }
+  } else {
+    for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
+      const int r = r0 + (e >> 7), col = col0 + (e & 127);
+      if (r < n && col < n) {
+        const int64_t i = (int64_t)r * n + col;
+        T ee, rr, xx;
+        one(M[i], S0[i], S1[i], r == col, ee, rr, xx);
+        S0[i] = ee;
+        S1[i] = rr;
+        X1[i] = xx;
+      }
+    }
+  }
+  rmax = wave_max(rmax);
+  if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
 }
 
 // Resets the state of the matrices that take part in a phase.
@@ -944,7 +1045,7 @@ __global__ void root_info_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
     if (scalar_iters(lo, p, tl, 400) <= s.iters) {
       kappa = 1.0;
     } else {
-      for (int b = 0; b < 100; ++b) {
+      for (int b = 0; b < 40; ++b) {  // hi / lo = 1e30^(2^-40) < 1 + 1e-10
         const double mid = sqrt(lo * hi);
         if (scalar_iters(mid, p, tl, 400) <= s.iters) hi = mid; else lo = mid;
       }

@@ -555,9 +555,13 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
   const int nb1 = cdiv(njobs, 64);
   // M0 (and, with the Frobenius scaling, X1 and the residual of M0)
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p,
+    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_up), dim3(kThreads), 0, s, djobs, njobs, st, total_up, p,
                        power ? 0 : 1);
   }));
+  // p = 4 under the power-bound scaling: the whole first M update is one
+  // product M' = M0' (c (k3 M0^2 + k5 M0^4)) + (k1 M0 + k2 M0^2 + k4 M0^4)
+  // with the coefficients of (a + b m)^4 m, a = 5/4, b = -1/4
+  const bool first4 = power && p == 4;
   if (power) {
     // S0 = M0^2, S1 = S0^2, rho = ||S1||_F^(1/4), M0 <- c M0 with c = (p+1)/(2 rho)
     NewtonStage sq0{}, sq1{};
@@ -569,11 +573,17 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
         hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, *S);
       }));
     }
+    const double a = 1.25, b = -0.25;
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(frob_s1_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full);
+      hipLaunchKernelGGL(frob_s1_kernel<T>, dim3(total_up), dim3(kThreads), 0, s, djobs, njobs, st, total_up);
       hipLaunchKernelGGL(root_rescale_kernel<T>, dim3(nb1), dim3(64), 0, s, djobs, njobs, st, p);
-      hipLaunchKernelGGL(root_scale_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full,
-                         p);
+      if (first4)
+        hipLaunchKernelGGL(newton_first4_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st,
+                           total_full, a * a * a * a, 4.0 * a * a * a * b, 6.0 * a * a * b * b, 4.0 * a * b * b * b,
+                           b * b * b * b);
+      else
+        hipLaunchKernelGGL(root_scale_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st,
+                           total_full, p);
     }));
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -585,6 +595,16 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
     for (size_t q = 0; q < prog.stages.size(); ++q) {
       // iteration 0: X1 = z^(1/p) M1 was written by the init kernel
       const NewtonStage& S = (it == 0 && q == 0) ? first0 : prog.stages[q];
+      if (first4 && it == 0) {
+        // A = the unscaled M0' (Mc), B = S1, E = S0 as the first4 pass left them
+        NewtonStage f{};
+        f.nprod = 1;
+        f.q[0] = make_prod(kBufMc, kBufS1, kBufS0, kBufMn, 1.0, 1.0, 0.0, 1);
+        STATUS_TRY(launch(h, cls, s, [&] {
+          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, f);
+        }));
+        break;  // the iteration's remaining stages are folded into this product
+      }
       if (power && it == 0 && q == 0) {
         // M0^2 = c^2 S0 is known: the stage is elementwise
         STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -933,10 +953,10 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     if (j32) {
-      hipLaunchKernelGGL(frob_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full);
+      hipLaunchKernelGGL(frob_kernel<float>, dim3(up), dim3(kThreads), 0, s, j32, njobs, st, up);
       hipLaunchKernelGGL(root_prep_kernel<float>, dim3(nb1), dim3(64), 0, s, j32, njobs, st, p, prm->eps_relative, eps);
     } else {
-      hipLaunchKernelGGL(frob_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full);
+      hipLaunchKernelGGL(frob_kernel<double>, dim3(up), dim3(kThreads), 0, s, j64, njobs, st, up);
       hipLaunchKernelGGL(root_prep_kernel<double>, dim3(nb1), dim3(64), 0, s, j64, njobs, st, p, prm->eps_relative,
                          eps);
     }
