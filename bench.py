@@ -96,9 +96,29 @@ def cpu_baseline(sample, n, k, p, eps, eta0, budget_s=12.0):
         O.graft_update(W, D, G, P, eta0)
         done += 1
     dt = time.perf_counter() - t0
-    return dict(value=done / dt, unit="roots/s", cores=int(cores), kind="oracle",
-                sample=f"{done} block-steps cycling over {len(sample)} of the 96 blocks, full fp64 step "
-                       f"per block (stats L+GG^T, eigh root, Lr G, graft), {dt:.1f} s")
+    out = dict(value=done / dt, unit="roots/s", cores=int(cores), kind="oracle",
+               sample=f"{done} block-steps cycling over {len(sample)} of the 96 blocks, full fp64 step "
+                      f"per block (stats L+GG^T, eigh root, Lr G, graft), {dt:.1f} s")
+    # The paper's CPU root service: Algorithm 1 transcribed in fp64 (two
+    # roots), and the eigh root on one thread (per-root latency).
+    t1 = time.perf_counter()
+    its = []
+    for L, G, D, W in sample[:2]:
+        Ln, _ = O.stats_update(L, None, G)
+        its.append(O.coupled_newton(Ln, p, eps=eps, tol=1e-6)["iters"])
+    out["newton_transcript_s_per_root"] = (time.perf_counter() - t1) / 2
+    out["newton_transcript_iters"] = its
+    try:
+        from threadpoolctl import threadpool_limits
+        L, G, D, W = sample[0]
+        Ln, _ = O.stats_update(L, None, G)
+        with threadpool_limits(limits=1):
+            t1 = time.perf_counter()
+            O.inv_root(Ln, p, eps)
+            out["eigh_root_s_1thread"] = time.perf_counter() - t1
+    except Exception as e:  # threadpoolctl missing: no 1-thread figure
+        log(f"no 1-thread figure: {e}")
+    return out
 
 
 def run_c4(args, torch, B):
@@ -715,6 +735,19 @@ def main():
             "scaling": "frobenius" if scaling == B.SCALING_POWER4 else "power4",
             "roots_call_ms": other_ms, "roots_per_s_roots_call": nb / (other_ms * 1e-3), "iters_mean": other_iters},
     }
+    # device copy bandwidth (a plain 1 GiB copy), the practical ceiling of
+    # the HBM-bound graft passes
+    src = torch.empty(2 ** 28, device=dev)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(5):
+        dst.copy_(src)
+    e1.record()
+    torch.cuda.synchronize()
+    out["hbm_copy_gbs"] = 5 * 2 * src.numel() * 4 / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del src, dst
     if not args.no_cpu_baseline:
         log("timing the oracle on a sample")
         out["cpu_baseline"] = cpu_baseline(sample, n, k, p, eps, eta0)
