@@ -31,6 +31,12 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
 * ``coupled_newton``    -- Algorithm 1, procedure CoupledIteration, fp64.
   Pinned against ``inv_root`` (<= 1e-9) and against the scalar recurrence
   for iteration counts on diagonal inputs.
+* ``coupled_newton_warm`` -- the warm start of the coupled-Newton appendix
+  with its commutator monitor (R21).  Pinned by the exact previous root
+  (zero iterations), commuting diagonal starts (scalar recurrence, exact
+  root), the non-commuting limit X0 (X0^p A)^{-1/p} from scipy's Schur-Pade
+  fractional power, and the abort with cold fallback on an ill-conditioned
+  drift.  Not built on the GPU (measured: see the design notes).
 * ``precondition``      -- Preliminaries (Shampoo update) and Lemma 1's
   one-sided forms.  Pinned by brute force with the Kronecker product of the
   full-matrix AdaGrad preconditioner on tiny shapes.
@@ -76,6 +82,10 @@ R16 Embedding statistics are those of the exact sparse gradient G of the
 R20 The appendix leaves the start constant free (X0 = I / c); Algorithm 1
     takes z = (1+p) / (2 ||A_d||_F).  The 'power4' option takes the tighter
     upper bound ||A_d^4||_F^(1/4) = (sum lambda^8)^(1/8) >= lambda_max.
+R21 The warm start's commutator monitor has no threshold in the paper:
+    abort when max|XM - MX| > comm_tol * max|X| * max|M| (1e-3) after an
+    iteration, when the residual grew twice in a row, or when the warm
+    iteration stops unconverged; the root then comes from the cold start.
 R17 The LARS/LAMB layer-wise learning rate ||W||_F / ||G||_F of the appendix,
     grafted like the AdaGrad magnitude, makes the step eta0 ||W||_F long
     along the unit Shampoo direction (along G / ||G||_F before the roots);
@@ -248,6 +258,65 @@ def coupled_newton(A, p, eps=0.0, tol=1e-10, max_iters=100,
         r = r_new
     return dict(X=X, iters=k, resid=r, status=status, eps_eff=eps_eff, z=z,
                 lam_max=lam)
+
+
+def coupled_newton_warm(A, p, X0, eps=0.0, tol=1e-10, max_iters=100,
+                        eps_relative=False, lam_max=None, comm_tol=1e-3,
+                        scaling='frobenius'):
+    """Warm start of the coupled-Newton appendix, in float64.
+
+    X = X0 (the previous root), M = X0^p A_d, then the iteration of
+    ``coupled_newton``.  The commutator [X, M] = XM - MX is monitored after
+    every iteration (R21): the warm start is aborted, and the root computed
+    from the cold start instead, when max|XM - MX| exceeds
+    comm_tol * max|X| * max|M|, when the residual grew in two consecutive
+    iterations, or when the warm iteration stops unconverged.  When X0
+    commutes with A_d the limit is A_d^{-1/p}; otherwise it is
+    X0 (X0^p A_d)^{-1/p}, which differs from the root by an amount that
+    grows with the commutator.
+
+    Returns the dict of ``coupled_newton`` plus ``warm_aborted``,
+    ``warm_iters`` (iterations spent before an abort, or all of them) and
+    ``comm`` (the relative commutator after each warm iteration).
+    """
+    A = _f64(A)
+    n = A.shape[0]
+    As = 0.5 * (A + A.T)
+    eps_eff, lam = damping(As, eps, eps_relative, lam_max)
+    Ad = As + eps_eff * np.eye(n)
+    I = np.eye(n)
+    alpha = -1.0 / p
+    X = _f64(X0)
+    M = np.linalg.matrix_power(X, p) @ Ad
+    r = float(np.max(np.abs(M - I)))
+    k, grew, comm = 0, 0, []
+    aborted = False
+    status = CONVERGED
+    while not (r <= tol):
+        if not np.isfinite(r) or r > DIVERGE_AT or k >= max_iters:
+            aborted = True
+            break
+        M1 = (1.0 - alpha) * I + alpha * M
+        X = X @ M1
+        M = np.linalg.matrix_power(M1, p) @ M
+        k += 1
+        r_new = float(np.max(np.abs(M - I)))
+        c = float(np.max(np.abs(X @ M - M @ X)))
+        scale = float(np.max(np.abs(X))) * float(np.max(np.abs(M)))
+        comm.append(c / scale if scale > 0 else np.inf)
+        grew = grew + 1 if r_new > r else 0
+        r = r_new
+        if not (c <= comm_tol * scale) or grew >= 2:
+            aborted = True
+            break
+    if aborted:
+        res = coupled_newton(A, p, eps=eps, tol=tol, max_iters=max_iters,
+                             eps_relative=eps_relative, lam_max=lam,
+                             scaling=scaling)
+        res.update(warm_aborted=True, warm_iters=k, comm=comm)
+        return res
+    return dict(X=X, iters=k, resid=r, status=status, eps_eff=eps_eff, z=None,
+                lam_max=lam, warm_aborted=False, warm_iters=k, comm=comm)
 
 
 def scalar_newton_iters(m0, p, tol, max_iters=1000):

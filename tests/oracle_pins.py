@@ -380,6 +380,47 @@ def pin_newton_status_rules(o):
     assert abs(res['eps_eff'] - 1e-3 * lmax) < 1e-6 * lmax
 
 
+def pin_newton_warm(o):
+    """Warm start (coupled-Newton appendix): the exact previous root needs
+    no iteration; a commuting diagonal start follows the scalar recurrence
+    from m0 = x0^p d to the exact root; a non-commuting start converges to
+    X0 (X0^p A)^{-1/p} (scipy's Schur-Pade power of a non-symmetric matrix);
+    an ill-conditioned drift trips the commutator monitor and falls back to
+    the cold root."""
+    from scipy.linalg import fractional_matrix_power
+    A = _spd(24, 1e2, 90)
+    X, _, _ = o.inv_root(A, 4, eps=1e-6)
+    res = o.coupled_newton_warm(A, 4, X, eps=1e-6, tol=1e-9)
+    assert res['iters'] == 0 and not res['warm_aborted'] and np.array_equal(res['X'], X)
+    d = np.array([0.5, 1.0, 2.0, 4.0])
+    for p in (2, 4):
+        x0 = d ** (-1.0 / p) * np.array([1.1, 0.9, 1.05, 0.8])
+        res = o.coupled_newton_warm(np.diag(d), p, np.diag(x0), tol=1e-12)
+        want = max(o.scalar_newton_iters(x ** p * y, p, 1e-12) for x, y in zip(x0, d))
+        assert not res['warm_aborted'] and abs(res['iters'] - want) <= 1
+        assert _relf(np.diag(res['X']), d ** (-1.0 / p)) < 1e-12
+    B = A + 1e-3 * _spd(24, 10.0, 91)
+    res = o.coupled_newton_warm(B, 4, X, eps=1e-6, tol=1e-12)
+    Bd = B + 1e-6 * np.eye(24)
+    lim = X @ np.real(fractional_matrix_power(np.linalg.matrix_power(X, 4) @ Bd, -0.25))
+    assert not res['warm_aborted'] and _relf(res['X'], lim) < 1e-8
+    C = _spd(48, 1e6, 92)
+    Xc, _, _ = o.inv_root(C, 4, eps=1e-6, eps_relative=True)
+    C2 = C + 1e-3 * C.max() * _spd(48, 1e1, 93) / 48
+    res = o.coupled_newton_warm(C2, 4, Xc, eps=1e-6, eps_relative=True, tol=1e-12)
+    Xt, _, _ = o.inv_root(C2, 4, eps=1e-6, eps_relative=True, lam_max=res['lam_max'])
+    assert res['warm_aborted'] and _relf(res['X'], Xt) < 1e-9
+    # a drift whose warm iteration converges smoothly (no residual growth)
+    # to a matrix 4% away: only the commutator (2.7e-2 after one iteration)
+    # stops it
+    C = _spd(48, 1e3, 92)
+    Xc, _, _ = o.inv_root(C, 4, eps=1e-6)
+    C2 = C + 1e-2 * 1e3 * _spd(48, 1e1, 93) / 48
+    Xt, _, _ = o.inv_root(C2, 4, eps=1e-6)
+    res = o.coupled_newton_warm(C2, 4, Xc, eps=1e-6, tol=1e-12)
+    assert res['warm_aborted'] and res['warm_iters'] == 1 and _relf(res['X'], Xt) < 1e-9
+
+
 # ------------------------------------------------------------------ precondition
 def pin_precondition_kronecker(o):
     """vec(Lr G Rr) = (Lr (x) Rr^T) vec(G) with row-stacking vec, on

@@ -39,6 +39,13 @@ MUTATIONS = [
      [P.pin_newton_power4_scaling]),
     ("coupled_newton", "z *= max(1.0, (1.0 + p) / (2.0 * rho))", "z *= max(1.0, (1.0 + p) / rho)",
      [P.pin_newton_power4_scaling]),
+    ("coupled_newton_warm", "M = np.linalg.matrix_power(X, p) @ Ad", "M = np.linalg.matrix_power(X, p - 1) @ Ad",
+     [P.pin_newton_warm]),
+    ("coupled_newton_warm", "X = X @ M1", "X = M1 @ X", [P.pin_newton_warm]),
+    ("coupled_newton_warm", "if not (c <= comm_tol * scale) or grew >= 2:",
+     "if not (c <= 1e6 * comm_tol * scale) or grew >= 2:", [P.pin_newton_warm]),
+    ("coupled_newton_warm", "    if aborted:\n        res = coupled_newton(", "    if False:\n        res = coupled_newton(",
+     [P.pin_newton_warm]),
     ("precondition", "P = _f64(Lr) @ P", "P = _f64(Lr).T @ P", [P.pin_precondition_kronecker]),
     ("precondition", "P = P @ _f64(Rr)", "P = P @ _f64(Rr).T",
      [P.pin_precondition_kronecker]),
