@@ -567,6 +567,8 @@ def main():
     ap.add_argument("--vocab", type=int, default=32768, help="c6: table rows")
     ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-kernel-timing", action="store_true",
+                    help="c2: no per-launch HIP events in the timed steps (whole-step time only)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
                     help="before the steps, copy a buffer of this size once (a plain copy kernel of known "
                          "traffic, to scale FETCH_SIZE/WRITE_SIZE counter readings)")
@@ -636,7 +638,7 @@ def main():
         step(False)
         torch.cuda.synchronize()
         log(f"warmup step {w + 1}/{args.warmup} done")
-    B.shampoo_timing_enable(h, True)
+    B.shampoo_timing_enable(h, not args.no_kernel_timing)
     for c in range(len(B.KCLASS_NAMES)):
         B.shampoo_timing_read(h, c)
     torch.cuda.synchronize()
@@ -728,8 +730,9 @@ def main():
                                   if times["newton_f64"][0] else None),
         },
         "newton_iters_mean": it32 / max(1, nb * args.steps),
-        "roots_per_s_root_phase": nb * args.steps / ((times["newton_f32"][0] + times["newton_f64"][0]
-                                                      + times["root_aux"][0]) * 1e-3),
+        "roots_per_s_root_phase": (nb * args.steps / ((times["newton_f32"][0] + times["newton_f64"][0]
+                                                       + times["root_aux"][0]) * 1e-3)
+                                   if times["newton_f32"][0] else None),
         "newton_products_per_root": prod32 / max(1, nb * args.steps),
         "other_scaling": None if other_ms is None else {
             "scaling": "frobenius" if scaling == B.SCALING_POWER4 else "power4",

@@ -907,7 +907,10 @@ __global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int pha
   s.precision = precision;
 }
 
-// Per-iteration state machine, one workgroup; also counts active matrices.
+// Per-iteration state machine, one workgroup.  count[0]: matrices still
+// active; count[1]: matrices stopped with a result that is not accepted
+// (MAXITER or DIVERGED), which the host reads with count[0] to decide on the
+// fp64 tail without another synchronisation.
 //   init != 0: evaluates the residual of M0 only.
 // esc_thr (AUTO fp32 phase, else NULL): esc_thr[k-1] is the largest residual
 // after k iterations of a matrix that can still converge within the phase's
@@ -915,11 +918,14 @@ __global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int pha
 __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __restrict__ st, int njobs, int init,
                                                               float tol, int max_iters, int* __restrict__ count,
                                                               const float* __restrict__ esc_thr, int esc_n) {
-  __shared__ int red[kThreads / 64];
-  int active = 0;
+  __shared__ int red[2 * (kThreads / 64)];
+  int active = 0, fails = 0;
   for (int j = threadIdx.x; j < njobs; j += kThreads) {
     RootState& s = st[j];
-    if (s.status != kActive) continue;
+    if (s.status != kActive) {
+      fails += s.status == kMaxIter || s.status == kDiverged;
+      continue;
+    }
     const float r = __uint_as_float(s.resid_bits);
     s.resid_bits = 0u;
     if (init) {
@@ -938,17 +944,28 @@ __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __rest
       else if (esc_thr && s.iters <= esc_n && r > esc_thr[s.iters - 1]) s.status = kMaxIter;
     }
     if (s.status == kActive) ++active;
+    else fails += s.status == kMaxIter || s.status == kDiverged;
   }
   // block reduce
-  int a = active;
+  int a = active, f = fails;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) a += __shfl_xor(a, o, 64);
-  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = a;
+  for (int o = 32; o > 0; o >>= 1) {
+    a += __shfl_xor(a, o, 64);
+    f += __shfl_xor(f, o, 64);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6] = a;
+    red[kThreads / 64 + (threadIdx.x >> 6)] = f;
+  }
   __syncthreads();
   if (threadIdx.x == 0) {
-    int s = 0;
-    for (int w = 0; w < kThreads / 64; ++w) s += red[w];
-    *count = s;
+    int sa = 0, sf = 0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+      sa += red[w];
+      sf += red[kThreads / 64 + w];
+    }
+    count[0] = sa;
+    count[1] = sf;
   }
 }
 

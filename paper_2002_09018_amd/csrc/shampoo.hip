@@ -26,7 +26,10 @@ namespace {
 constexpr int kMaxDim = 4096;
 constexpr int kMaxRootOrder = 16;  // largest p of X = A^(-1/p)
 constexpr int kMaxEmbEntries = 1 << 26;  // lookup entries of one embedding call
-constexpr int kCountRing = 64;  // device/pinned slots of per-iteration active counts
+constexpr int kCountRing = 64;  // device/pinned slots (pairs) of per-iteration counts
+// count pairs: kCountRing per-iteration slots, the initial residual check, the
+// AUTO escalation count
+constexpr int kCountInts = 2 * (kCountRing + 2);
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -65,7 +68,7 @@ struct Handle {
   size_t partial_cap = 0;
   void* sort_tmp = nullptr;  // rocPRIM temporary storage of the embedding row compaction
   size_t sort_tmp_cap = 0;
-  int32_t* pinned = nullptr;  // kCountRing + 1 ints
+  int32_t* pinned = nullptr;  // kCountInts ints
   hipEvent_t poll_ev[2] = {nullptr, nullptr};
   bool timing = false;
   std::vector<TimedLaunch> timed;
@@ -407,7 +410,7 @@ RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
   L.state = off;
   off += align256((size_t)njobs * sizeof(RootState));
   L.counts = off;
-  off += align256((kCountRing + 2) * sizeof(int));
+  off += align256(kCountInts * sizeof(int));
   for (int j = 0; j < njobs; ++j) {
     const size_t n = (size_t)jobs[j].n;
     const size_t T = (size_t)cdiv(jobs[j].n, kTile);
@@ -548,7 +551,11 @@ NewtonStage drop_x(const NewtonStage& s0) {
 template <typename T>
 shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
                             int total_up, int total_full, const NewtonProgram& prog, int p, int scaling, float tol,
-                            int cap, int poll, int cls, const float* esc_thr, int esc_n, hipStream_t s) {
+                            int cap, int poll, int cls, const float* esc_thr, int esc_n, hipStream_t s,
+                            int* fails_out = nullptr) {
+  // fails_out: set to the number of matrices stopped unaccepted (MAXITER,
+  // DIVERGED) when the polled counts showed that every matrix stopped; left
+  // untouched otherwise.
   const int lds = 0;  // static LDS
   auto kstage = newton_stage_kernel<T>;
   const bool power = scaling == SHAMPOO_SCALING_POWER4;
@@ -588,7 +595,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
-                       dcount + kCountRing, (const float*)nullptr, 0);
+                       dcount + 2 * kCountRing, (const float*)nullptr, 0);
   }));
   const NewtonStage first0 = drop_x(prog.stages[0]);
   for (int it = 0; it < cap; ++it) {
@@ -617,17 +624,23 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
         hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, S);
       }));
     }
-    int* slot = dcount + (it % kCountRing);
+    const int ring = 2 * (it % kCountRing);
+    int* slot = dcount + ring;
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, cap, slot, esc_thr,
                          esc_n);
     }));
     if (poll) {
-      HIP_TRY(h, hipMemcpyAsync(h->pinned + (it % kCountRing), slot, sizeof(int), hipMemcpyDeviceToHost, s));
+      HIP_TRY(h, hipMemcpyAsync(h->pinned + ring, slot, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
       HIP_TRY(h, hipEventRecord(h->poll_ev[it & 1], s));
       if (it >= 1) {
         HIP_TRY(h, hipEventSynchronize(h->poll_ev[(it - 1) & 1]));
-        if (h->pinned[(it - 1) % kCountRing] == 0) break;
+        const int32_t* c = h->pinned + 2 * ((it - 1) % kCountRing);
+        if (c[0] == 0) {
+          // every matrix has stopped: the unaccepted ones are final too
+          if (fails_out) *fails_out = c[1];
+          break;
+        }
       }
     }
   }
@@ -776,7 +789,7 @@ shampoo_status shampoo_create(void** handle, int device) {
   Handle* h = new Handle();
   h->device = device;
   DeviceGuard g(device);
-  if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), (kCountRing + 2) * sizeof(int32_t),
+  if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), kCountInts * sizeof(int32_t),
                     hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&h->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&h->poll_ev[1], hipEventDisableTiming) != hipSuccess) {
@@ -964,7 +977,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   if (tail_all) {
     // every matrix goes to the fp64 phase
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + kCountRing + 1);
+      hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + 2 * kCountRing + 2);
     }));
   }
   int run64 = tail_all;
@@ -997,19 +1010,23 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       esc = static_cast<const float*>(d);
       esc_n = cap;
     }
+    int fails = -1;
     STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap, prm->poll,
-                                   SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s));
+                                   SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
     if (prec == SHAMPOO_PRECISION_AUTO) {
+      int* esc_count = dcount + 2 * kCountRing + 2;
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-        hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + kCountRing + 1);
+        hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, esc_count);
       }));
-      if (prm->poll) {
-        HIP_TRY(h, hipMemcpyAsync(h->pinned + kCountRing + 1, dcount + kCountRing + 1, sizeof(int),
-                                  hipMemcpyDeviceToHost, s));
-        HIP_TRY(h, hipStreamSynchronize(s));
-        run64 = h->pinned[kCountRing + 1] > 0;
-      } else {
+      if (!prm->poll) {
         run64 = 1;
+      } else if (fails >= 0) {
+        run64 = fails > 0;  // known from the last poll: no synchronisation
+      } else {
+        // the phase ended at its cap with matrices still running
+        HIP_TRY(h, hipMemcpyAsync(h->pinned + 2 * kCountRing + 2, esc_count, sizeof(int), hipMemcpyDeviceToHost, s));
+        HIP_TRY(h, hipStreamSynchronize(s));
+        run64 = h->pinned[2 * kCountRing + 2] > 0;
       }
     }
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
