@@ -309,10 +309,8 @@ def run_c3(args, torch, B):
     from synth import configs as cfg
     dev = torch.device("cuda:0")
     n, nm = 2048, 32
-    log("generating C3 matrices")
-    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as ex:
-        mats = list(ex.map(lambda i: cfg.c3_matrix(i, n)[0], range(nm)))
-    As = [torch.from_numpy(a).to(dev) for a in mats]
+    log("generating C3 matrices on the device")
+    As = [cfg.c3_matrix_device(i, torch, dev, n)[0] for i in range(nm)]
     Xs = [torch.zeros_like(a) for a in As]
     h = B.shampoo_create(0)
     res = {}

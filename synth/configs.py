@@ -130,6 +130,23 @@ def c3_matrix(i, n=2048, lo=-6.0, hi=2.0):
     return A.astype(np.float32), lam, Q
 
 
+def c3_matrix_device(i, torch, device, n=2048, lo=-6.0, hi=2.0):
+    """C3 matrix i with the same recipe as ``c3_matrix``, the O(n^3) work on
+    the device: Gaussian Z from a torch generator seeded by the key, Q from
+    its QR (signs fixed by diag R), lambda = 10^U(lo, hi) from the keyed PCG64
+    stream, Q diag(lambda) Q^T in fp64, symmetrised and rounded to fp32.
+    Returns (A_fp32 device tensor, lambda sorted ascending as numpy)."""
+    r = rng(C3, i, n, 1)
+    seed = int(r.integers(0, 2 ** 62))
+    lam = np.sort(10.0 ** r.uniform(lo, hi, size=n))
+    g = torch.Generator(device=device).manual_seed(seed)
+    Z = torch.randn(n, n, generator=g, device=device, dtype=torch.float64)
+    Q, Rm = torch.linalg.qr(Z)
+    Q = Q * torch.sign(torch.diagonal(Rm))
+    A = (Q * torch.from_numpy(lam).to(device)) @ Q.T
+    return (0.5 * (A + A.T)).float(), lam
+
+
 # ---------------------------------------------------------------- C4
 C4_LAYERS, C4_BLOCKS, C4_D, C4_FF = 24, 12, 1024, 4096
 

@@ -145,17 +145,33 @@ def test_c3_ill_conditioned_reduced(env, p):
             assert rel(X, Xo) <= band(kappa), (kappa, inf, rel(X, Xo))
 
 
+@pytest.fixture(scope="module")
+def c3_full(env):
+    torch, B, dev, h = env
+    say("roots C3: generating 32 x 2048^2 on the device")
+    return [cfg.c3_matrix_device(i, torch, dev)[0] for i in range(32)]
+
+
 @pytest.mark.parametrize("p", [2, 4])
-def test_c3_full_size_two_matrices(env, p):
-    say("roots C3 n=2048 p", p)
-    mats = [cfg.c3_matrix(i, n=2048) for i in range(2)]
-    As = [m[0] for m in mats]
-    Xs, info = roots(env, As, p=p, eps=1e-6, eps_relative=1)
-    for A, X, inf in zip(As, Xs, info):
+def test_c3_full_size_grouped_sampled(env, c3_full, p):
+    """C3 as benchmarked: all 32 matrices of 2048 x 2048 in one grouped call
+    (AUTO: fp32 attempt, fp64 tail); sampled matrices against eigh."""
+    torch, B, dev, h = env
+    say("roots C3 32 x 2048^2 p", p)
+    prm = B.shampoo_root_params_default(p=p, eps=1e-6, eps_relative=1)
+    dX = [torch.full_like(a, float("nan")) for a in c3_full]
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([2048] * 32, prm.precision), dtype=torch.uint8,
+                     device=dev)
+    info_t = torch.zeros(8 * 32, dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_batched(h, c3_full, dX, prm, ws, info_t)
+    torch.cuda.synchronize()
+    info = B.decode_root_info(info_t)
+    assert all(i["status"] in (0, 1) and i["precision"] == 64 for i in info), info[:3]
+    for i in (0, 31):
+        A = host(c3_full[i])
         Xo, st, e = O.inv_root(A, p, 1e-6, eps_relative=True)
         kappa = O.cond_damped(A, 1e-6, True)
-        assert inf["status"] in (0, 1) and inf["precision"] == 64, inf
-        assert rel(X, Xo) <= band(kappa), (kappa, inf, rel(X, Xo))
+        assert rel(host(dX[i]), Xo) <= band(kappa), (i, kappa, info[i], rel(host(dX[i]), Xo))
 
 
 def test_precision_policies_agree(env):
