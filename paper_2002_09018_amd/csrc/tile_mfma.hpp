@@ -21,7 +21,9 @@
 // contraction indices g*KS .. g*KS+KS-1 over the KS MFMA k-steps (a
 // permutation of k shared by both operands, so the sum is unchanged).  A
 // kLayoutRow fragment of a lane is then KS consecutive elements, read with
-// 16-byte LDS loads; a kLayoutK fragment is one element per k-step.
+// 16-byte LDS loads one chunk of 4 k-steps at a time (holding a whole
+// stage's row fragments cost the statistics GEMM an occupancy step); a
+// kLayoutK fragment is one element per k-step.
 // Source elements may be fp32, fp64 or bf16 (raw uint16 bits, up-cast
 // exactly).  Full, aligned k-layout stages in the compute type are copied
 // global -> LDS directly (global_load_lds_dwordx4, no register staging);
@@ -283,28 +285,6 @@ struct WaveAcc {
     typedef T vec_t __attribute__((ext_vector_type(VP)));
     const int g = lane / Mfma<T>::kM;  // this lane's k group: k = g * KS + s at k-step s
     const int ml = lane % Mfma<T>::kM;
-    // kLayoutRow fragments: the range's values, 16 bytes at a time.
-    T ra[LA == kLayoutRow ? NB : 1][KS], rb[LB == kLayoutRow ? NB : 1][KS];
-    if (LA == kLayoutRow) {
-#pragma unroll
-      for (int i = 0; i < NB; ++i)
-#pragma unroll
-        for (int c = S0 / VP; c < S1 / VP; ++c) {
-          const vec_t v = *reinterpret_cast<const vec_t*>(a + (wm0 + i * Mfma<T>::kM + ml) * LDPA + g * KS + c * VP);
-#pragma unroll
-          for (int e = 0; e < VP; ++e) ra[i][c * VP + e] = v[e];
-        }
-    }
-    if (LB == kLayoutRow) {
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-#pragma unroll
-        for (int c = S0 / VP; c < S1 / VP; ++c) {
-          const vec_t v = *reinterpret_cast<const vec_t*>(b + (wn0 + j * Mfma<T>::kM + ml) * LDPB + g * KS + c * VP);
-#pragma unroll
-          for (int e = 0; e < VP; ++e) rb[j][c * VP + e] = v[e];
-        }
-    }
     // kLayoutK fragments: one element per k-step, double-buffered in
     // registers so the reads of step s+1 are issued before the MFMAs of s.
     T fa[2][NB], fb[2][NB];
@@ -318,29 +298,44 @@ struct WaveAcc {
 #pragma unroll
       for (int j = 0; j < NB; ++j) fb[S0 & 1][j] = pb[S0 * LDPB + j * Mfma<T>::kM];
     }
+    // kLayoutRow fragments: VP k-steps per 16-byte read, read per chunk of
+    // VP steps (the registers of one chunk only)
 #pragma unroll
-    for (int s = S0; s < S1; ++s) {
-      const int cur = s & 1;
-      if (s + 1 < S1) {
-        if (LA == kLayoutK) {
+    for (int cch = S0 / VP; cch < S1 / VP; ++cch) {
+      vec_t ra[LA == kLayoutRow ? NB : 1], rb[LB == kLayoutRow ? NB : 1];
+      if (LA == kLayoutRow) {
 #pragma unroll
-          for (int i = 0; i < NB; ++i) fa[cur ^ 1][i] = pa[(s + 1) * LDPA + i * Mfma<T>::kM];
-        }
-        if (LB == kLayoutK) {
-#pragma unroll
-          for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[(s + 1) * LDPB + j * Mfma<T>::kM];
-        }
+        for (int i = 0; i < NB; ++i)
+          ra[i] = *reinterpret_cast<const vec_t*>(a + (wm0 + i * Mfma<T>::kM + ml) * LDPA + g * KS + cch * VP);
       }
-      // Keep the reads of s+1 ahead of the MFMAs of s (the scheduler would
-      // otherwise sink them below to save registers).
-      __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-      for (int i = 0; i < NB; ++i)
+      if (LB == kLayoutRow) {
 #pragma unroll
         for (int j = 0; j < NB; ++j)
-          c[i][j] = Mfma<T>::mma(LA == kLayoutRow ? ra[i][s] : fa[cur][i], LB == kLayoutRow ? rb[j][s] : fb[cur][j],
-                                 c[i][j]);
-      __builtin_amdgcn_sched_barrier(0);
+          rb[j] = *reinterpret_cast<const vec_t*>(b + (wn0 + j * Mfma<T>::kM + ml) * LDPB + g * KS + cch * VP);
+      }
+#pragma unroll
+      for (int e = 0; e < VP; ++e) {
+        const int s = cch * VP + e;
+        const int cur = s & 1;
+        if (s + 1 < S1) {
+          if (LA == kLayoutK) {
+#pragma unroll
+            for (int i = 0; i < NB; ++i) fa[cur ^ 1][i] = pa[(s + 1) * LDPA + i * Mfma<T>::kM];
+          }
+          if (LB == kLayoutK) {
+#pragma unroll
+            for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[(s + 1) * LDPB + j * Mfma<T>::kM];
+          }
+        }
+        if (LA == kLayoutK || LB == kLayoutK) __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            c[i][j] = Mfma<T>::mma(LA == kLayoutRow ? ra[i][e] : fa[cur][i], LB == kLayoutRow ? rb[j][e] : fb[cur][j],
+                                   c[i][j]);
+        if (LA == kLayoutK || LB == kLayoutK) __builtin_amdgcn_sched_barrier(0);
+      }
     }
   }
 };
