@@ -717,6 +717,10 @@ def main():
             "traffic_unit": "bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
         },
         "stats_precondition_ms_per_step": stats_prec_ms,
+        # both passes are fp32-MFMA bound: roofline time of their algorithmic
+        # flops (symmetric counting for the statistics) over the measured time
+        "stats_precondition_roofline_frac": ((flops_stats + flops_prec) / args.steps / (PEAK_F32_MFMA * 1e12)
+                                             / (stats_prec_ms * 1e-3) if stats_prec_ms else None),
         "fp32_mfma_util": achieved / PEAK_F32_MFMA,
         "phases_ms_per_step": {c: v[0] / args.steps for c, v in times.items()},
         "launches_per_step": {c: v[1] / args.steps for c, v in times.items()},
