@@ -102,12 +102,16 @@ def cpu_baseline(sample, n, k, p, eps, eta0, budget_s=12.0):
     # The paper's CPU root service: Algorithm 1 transcribed in fp64 (two
     # roots), and the eigh root on one thread (per-root latency).
     t1 = time.perf_counter()
-    its = []
+    its, its4 = [], []
     for L, G, D, W in sample[:2]:
         Ln, _ = O.stats_update(L, None, G)
         its.append(O.coupled_newton(Ln, p, eps=eps, tol=1e-6)["iters"])
     out["newton_transcript_s_per_root"] = (time.perf_counter() - t1) / 2
-    out["newton_transcript_iters"] = its
+    out["newton_transcript_iters"] = its          # Algorithm 1 as printed (Frobenius start)
+    for L, G, D, W in sample[:2]:
+        Ln, _ = O.stats_update(L, None, G)
+        its4.append(O.coupled_newton(Ln, p, eps=eps, tol=1e-6, scaling="power4")["iters"])
+    out["newton_transcript_iters_power4"] = its4  # the start the GPU uses
     try:
         from threadpoolctl import threadpool_limits
         L, G, D, W = sample[0]
@@ -310,7 +314,9 @@ def run_c3(args, torch, B):
     dev = torch.device("cuda:0")
     n, nm = 2048, 32
     log("generating C3 matrices on the device")
-    As = [cfg.c3_matrix_device(i, torch, dev, n)[0] for i in range(nm)]
+    gen = [cfg.c3_matrix_device(i, torch, dev, n) for i in range(nm)]
+    As = [a for a, _ in gen]
+    lams = [lam for _, lam in gen]
     Xs = [torch.zeros_like(a) for a in As]
     h = B.shampoo_create(0)
     res = {}
@@ -331,6 +337,25 @@ def run_c3(args, torch, B):
         B.shampoo_timing_enable(h, False)
         times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
         inf = B.decode_root_info(info)
+        # accuracy on two sampled matrices: relative error against the
+        # oracle (eigh), the true residual ||X^p A_d - I||_F in fp64 and the
+        # damped condition number from the constructed spectrum
+        acc = []
+        if not args.no_cpu_baseline:
+            import oracle.shampoo_oracle as O
+            for q in (0, nm - 1):
+                A64 = As[q].double()
+                Ad = A64 + inf[q]["eps_eff"] * torch.eye(n, device=dev, dtype=torch.float64)
+                Xq = Xs[q].double()
+                Rm = torch.linalg.matrix_power(Xq, p) @ Ad - torch.eye(n, device=dev, dtype=torch.float64)
+                Xo, _, _ = O.inv_root(As[q].cpu().numpy(), p, 1e-6, eps_relative=True,
+                                      lam_max=inf[q]["lambda_max"])
+                Xh = Xs[q].cpu().numpy().astype(np.float64)
+                acc.append({"matrix": q, "status": inf[q]["status"], "final_resid": inf[q]["resid"],
+                            "true_resid_fro": float(torch.linalg.norm(Rm)),
+                            "rel_err_vs_eigh": float(np.linalg.norm(Xh - Xo) / np.linalg.norm(Xo)),
+                            "kappa_damped": float((lams[q].max() + inf[q]["eps_eff"]) /
+                                                  (lams[q].min() + inf[q]["eps_eff"]))})
         pr64 = sum(newton_products(i["iters"], p, True) for i in inf if i["precision"] == 64)
         pr32 = sum(newton_products(i["iters_fp32"], p, True) for i in inf)
         sym = n * n * (n + 1)
@@ -346,6 +371,7 @@ def run_c3(args, torch, B):
             "newton_f64_frac": (pr64 * sym / (times["newton_f64"][0] * 1e-3) / 1e12 / PEAK_F64_MFMA
                                 if times["newton_f64"][0] else None),
             "newton_f32_tflops": pr32 * sym / (times["newton_f32"][0] * 1e-3) / 1e12 if times["newton_f32"][0] else None,
+            "accuracy": acc,
         }
         log(f"p={p}: {ms:.1f} ms")
     B.shampoo_destroy(h)
