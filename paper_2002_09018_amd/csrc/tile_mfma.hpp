@@ -275,7 +275,10 @@ struct WaveAcc {
 
   // MFMA k-steps [S0, S1) of one LDS stage (kBK / kK steps in all) over the
   // wave's NB x NB blocks.
-  template <int LA, int LB, int LDPA, int LDPB, int S0 = 0, int S1 = Mfma<T>::kBK / Mfma<T>::kK>
+  // SKIP: the wave's square sits on the diagonal of a symmetric output; its
+  // MFMA blocks wholly below the diagonal (i > j) are never stored and are
+  // skipped.
+  template <int LA, int LB, int LDPA, int LDPB, int S0 = 0, int S1 = Mfma<T>::kBK / Mfma<T>::kK, bool SKIP = false>
   __device__ __forceinline__ void stage(const T* __restrict__ a, const T* __restrict__ b, int wm0,
                                         int wn0, int lane) {
     constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;  // k-steps per stage
@@ -331,9 +334,11 @@ struct WaveAcc {
 #pragma unroll
         for (int i = 0; i < NB; ++i)
 #pragma unroll
-          for (int j = 0; j < NB; ++j)
+          for (int j = 0; j < NB; ++j) {
+            if (SKIP && i > j) continue;
             c[i][j] = Mfma<T>::mma(LA == kLayoutRow ? ra[i][e] : fa[cur][i], LB == kLayoutRow ? rb[j][e] : fb[cur][j],
                                    c[i][j]);
+          }
         if (LA == kLayoutK || LB == kLayoutK) __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -399,7 +404,7 @@ struct Stager {
 // between two static buffer pairs; the loop is unrolled by two so every LDS
 // access names its buffer at compile time (the wait for an in-flight DMA into
 // one buffer then does not hold back reads of the other).
-template <bool COMPUTE, typename T, typename SA, int LA, typename SB, int LB>
+template <bool COMPUTE, typename T, typename SA, int LA, typename SB, int LB, bool SKIP = false>
 __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
                                           int n0, int K, T* a0, T* a1, T* b0, T* b1) {
   constexpr int BK = Mfma<T>::kBK;
@@ -443,14 +448,14 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
       sa.issue(A, ar, ac, na, tid);
       sb.issue(B, br, bc, nb, tid);
     }
-    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, 0, KH>(ca, cb, wm0, wn0, lane);
+    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, 0, KH, SKIP>(ca, cb, wm0, wn0, lane);
     if (more) {
       sa.finish(A, ar, ac, na, tid);
       sb.finish(B, br, bc, nb, tid);
       if (!SHP_SPLIT_STAGE) __builtin_amdgcn_s_waitcnt(0);
     }
     if constexpr (KH < KSTEPS) {
-      if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, KH, KSTEPS>(ca, cb, wm0, wn0, lane);
+      if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, KH, KSTEPS, SKIP>(ca, cb, wm0, wn0, lane);
     }
     __syncthreads();
   };
@@ -476,7 +481,8 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
 //   B: layout LB; kLayoutK reads storage rows k (cols n0..), kLayoutRow
 //      reads storage rows n0.. (cols k).
 // lower_idle: diagonal tile of a symmetric output, whose lower-left 64 x 64
-// quarter is never stored; that quarter's wave only stages operands.
+// quarter is never stored; that quarter's wave only stages operands, and the
+// two waves on the diagonal skip their MFMA blocks below it.
 template <typename T, typename SA, int LA, typename SB, int LB>
 __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
                                          int n0, int K, T* a0, T* a1, T* b0, T* b1, bool lower_idle = false) {
@@ -485,8 +491,11 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, 
 #endif
   const int wave = threadIdx.x >> 6;
   const bool idle = SHP_IDLE_LOWER && lower_idle && (wave >> 1) > (wave & 1);
+  const bool ondiag = lower_idle && (wave >> 1) == (wave & 1);
   if (idle)
     tile_loop<false, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
+  else if (ondiag)
+    tile_loop<true, T, SA, LA, SB, LB, true>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
   else
     tile_loop<true, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
 }
