@@ -505,31 +505,51 @@ __global__ void maxsv_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njo
   }
 }
 
-// Symmetrised tile pass over the full tile grid: thread sees
-// s = (A[r][c] + A[c][r]) / 2 for its elements of tile (ti, tj); the
-// transposed block is staged through LDS so both reads are coalesced.
-// Computing every tile (not only the upper ones) keeps the result exactly
+// Symmetrised tile pass: thread sees s = (A[r][c] + A[c][r]) / 2 for its
+// elements of tile (ti, tj); the transposed block is staged through LDS so
+// both reads are coalesced (16-byte loads when the tile is full and aligned).
+// Computing a tile and its mirror separately keeps the result exactly
 // symmetric because fl(x + y) = fl(y + x).
 template <typename F>
 __device__ __forceinline__ void sym_tile_pass(const float* __restrict__ A, int n, int ti, int tj,
                                               float* lds /* 128 x 33 */, F&& f) {
   const int r0 = ti * kTile, c0 = tj * kTile;
   const int tid = threadIdx.x;
+  const bool vec = (n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n && (reinterpret_cast<uintptr_t>(A) & 15) == 0;
   for (int q = 0; q < kTile; q += 32) {  // 32-row slab of the tile
     __syncthreads();
     // lds[c][rr] = A[c0 + c][r0 + q + rr]
-    for (int e = tid; e < kTile * 32; e += kThreads) {
-      const int c = e >> 5, rr = e & 31;
-      const int gr = c0 + c, gc = r0 + q + rr;
-      lds[c * 33 + rr] = (gr < n && gc < n) ? A[(int64_t)gr * n + gc] : 0.f;
+    if (vec) {
+      for (int e = tid; e < kTile * 8; e += kThreads) {
+        const int c = e >> 3, rr = (e & 7) * 4;
+        const f4v v = gload<f4v>(A + (int64_t)(c0 + c) * n + r0 + q + rr);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) lds[c * 33 + rr + k] = v[k];
+      }
+    } else {
+      for (int e = tid; e < kTile * 32; e += kThreads) {
+        const int c = e >> 5, rr = e & 31;
+        const int gr = c0 + c, gc = r0 + q + rr;
+        lds[c * 33 + rr] = (gr < n && gc < n) ? A[(int64_t)gr * n + gc] : 0.f;
+      }
     }
     __syncthreads();
-    for (int e = tid; e < 32 * kTile; e += kThreads) {
-      const int rr = e >> 7, c = e & 127;
-      const int r = r0 + q + rr, cc = c0 + c;
-      if (r < n && cc < n) {
-        const double s = 0.5 * ((double)A[(int64_t)r * n + cc] + (double)lds[c * 33 + rr]);
-        f(r, cc, s);
+    if (vec) {
+      for (int e = tid; e < 32 * 32; e += kThreads) {
+        const int rr = e >> 5, c = (e & 31) * 4;
+        const int r = r0 + q + rr;
+        const f4v v = gload<f4v>(A + (int64_t)r * n + c0 + c);
+#pragma unroll
+        for (int k = 0; k < 4; ++k) f(r, c0 + c + k, 0.5 * ((double)v[k] + (double)lds[(c + k) * 33 + rr]));
+      }
+    } else {
+      for (int e = tid; e < 32 * kTile; e += kThreads) {
+        const int rr = e >> 7, c = e & 127;
+        const int r = r0 + q + rr, cc = c0 + c;
+        if (r < n && cc < n) {
+          const double s = 0.5 * ((double)A[(int64_t)r * n + cc] + (double)lds[c * 33 + rr]);
+          f(r, cc, s);
+        }
       }
     }
   }
@@ -605,21 +625,21 @@ __global__ void root_prep_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
 }
 
 // M0 = z (A_s + eps I), X0 = z^(1/p) I (Algorithm 1 cold start); residual of
-// M0 accumulated into resid_bits.  One workgroup per upper tile writes the
-// tile and its mirror (two symmetrised passes; the second one re-reads from
-// L2 what the first fetched).
+// M0 accumulated into resid_bits.  One workgroup per tile of the full grid
+// (a version over upper tiles that wrote each tile and its mirror was
+// measured slower).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                            RootState* __restrict__ st, int total_up, int p,
+                                                            RootState* __restrict__ st, int total_full, int p,
                                                             int write_x) {
   __shared__ float lds[kTile * 33];
   const int t = blockIdx.x;
-  if (t >= total_up) return;
-  const int j = find_job_up(jobs, njobs, t);
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
   if (st[j].status != kActive) return;
   const NewtonJob<T> J = jobs[j];
-  int ti, tj;
-  unrank_upper(t - J.up_begin, J.tiles_n, ti, tj);
+  const int lt = t - J.full_begin;
+  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
   const double z = st[j].z, e = st[j].eps_eff;
   const T x0 = (T)pow(z, 1.0 / p);
   const T a = (T)(p + 1) / (T)p, b = (T)-1 / (T)p;
@@ -632,7 +652,7 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
   // product; a matrix that stops before any iteration gets X0 from the
   // output kernel.
   // write_x == 0: only M0 (the power-bound scaling rescales it later)
-  auto f = [&](int r, int c, double s) {
+  sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
     const T m = (T)(z * (s + (r == c ? e : 0.0)));
     M[(int64_t)r * n + c] = m;
     if (write_x) {
@@ -641,9 +661,7 @@ __global__ __launch_bounds__(kThreads) void root_init_kernel(const NewtonJob<T>*
       if (!(d <= 3.0e38f)) d = INFINITY;
       rmax = rmax > d ? rmax : d;
     }
-  };
-  sym_tile_pass(J.A, n, ti, tj, lds, f);
-  if (ti != tj) sym_tile_pass(J.A, n, tj, ti, lds, f);
+  });
   rmax = wave_max(rmax);
   if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
 }

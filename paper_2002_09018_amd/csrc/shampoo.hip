@@ -562,7 +562,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
   const int nb1 = cdiv(njobs, 64);
   // M0 (and, with the Frobenius scaling, X1 and the residual of M0)
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_up), dim3(kThreads), 0, s, djobs, njobs, st, total_up, p,
+    hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p,
                        power ? 0 : 1);
   }));
   // p = 4 under the power-bound scaling: the whole first M update is one
