@@ -56,6 +56,21 @@ __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int n
   return lo;
 }
 
+// Epilogue row stores: a wave's MFMA block row (kM rows x 64 columns, laid
+// out row-major in `epi` by the caller) goes out as 16-byte row segments
+// instead of the accumulators' column-wise 4-byte stores.  `epi` is the
+// wave's own slice of the (then unused) stage buffers, so only the wave's
+// own LDS ordering is involved.
+__device__ __forceinline__ void epi_rows(const float* epi, float* dst, int64_t ld, int lane) {
+  constexpr int kM = Mfma<float>::kM;
+  constexpr int kSeg = kWaveTile / 4;  // 16-byte segments per row
+#pragma unroll
+  for (int k = 0; k < kM * kSeg / 64; ++k) {
+    const int idx = lane + 64 * k, rr = idx / kSeg, c4 = (idx % kSeg) * 4;
+    gstore<f4v>(dst + (int64_t)rr * ld + c4, *reinterpret_cast<const f4v*>(epi + rr * kWaveTile + c4));
+  }
+}
+
 // LIM: honour the device-side limits kcount / mcount (a separate
 // instantiation, so the plain kernels carry no extra registers).
 template <typename SA, int LA, typename SB, int LB, bool LIM = false>
@@ -130,6 +145,29 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
           }
           gstore<f4>(P.C + (int64_t)c * P.ldc + r, w);
         }
+    return;
+  }
+  // Full tile of a plain output: rows through LDS, 16-byte row segments
+  // (not compiled into the row x row instantiation, which only forms
+  // symmetric statistics and would lose an occupancy step to it).
+  if constexpr (!(LA == kLayoutRow && LB == kLayoutRow))
+  if (!P.sym && m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
+      (reinterpret_cast<uintptr_t>(P.C) & 15) == 0) {
+    float* epi = reinterpret_cast<float*>(wave == 0 ? sa0 : (wave == 1 ? sa1 : (wave == 2 ? sb0 : sb1)));
+#pragma unroll
+    for (int i = 0; i < WaveAcc<float>::NB; ++i) {
+#pragma unroll
+      for (int j = 0; j < WaveAcc<float>::NB; ++j)
+#pragma unroll
+        for (int v = 0; v < F::kAcc; ++v) {
+          const int r = wm0 + i * F::kM + F::row(lane, v);
+          const int c = wn0 + j * F::kM + F::col(lane);
+          float x = P.alpha * acc.c[i][j][v];
+          if (P.beta != 0.f) x += P.beta * gload<float>(P.C + (int64_t)r * P.ldc + c);
+          epi[F::row(lane, v) * kWaveTile + j * F::kM + F::col(lane)] = x;
+        }
+      epi_rows(epi, P.C + (int64_t)(wm0 + i * F::kM) * P.ldc + wn0, P.ldc, lane);
+    }
     return;
   }
 #endif
