@@ -37,19 +37,30 @@ def log(*a):
 def measured_traffic(name="newton_stage_kernel_c2_counters.txt"):
     """HBM bytes per launch of the Newton kernel from the committed rocprofv3
     counter summary, or None when the kernel sources changed since the
-    counters were taken (the summary records a hash of the sources)."""
-    import hashlib
+    counters were taken (the summary records a digest of the sources)."""
     path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     kv = dict(line.strip().split("=", 1) for line in open(path) if "=" in line and not line.startswith("#"))
-    h = hashlib.sha256()
-    src = os.path.join(ROOT, "paper_2002_09018_amd", "csrc")
-    for f in sorted(os.listdir(src)):
-        h.update(open(os.path.join(src, f), "rb").read())
-    if kv.get("source_sha256") != h.hexdigest():
+    if kv.get("source_code_sha256") != source_code_digest():
         return None
     return float(kv["bytes_per_launch"])
+
+
+def source_code_digest(src=None):
+    """SHA-256 over the kernel sources with comments and white space removed,
+    so that an edit of comments alone keeps the counter summary valid while
+    any change of the code voids it."""
+    import hashlib
+    import re
+    src = src or os.path.join(ROOT, "paper_2002_09018_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(src)):
+        text = open(os.path.join(src, f), encoding="utf-8").read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(f.encode() + b"\0" + " ".join(text.split()).encode())
+    return h.hexdigest()
 
 
 def newton_products(iters, p, power):

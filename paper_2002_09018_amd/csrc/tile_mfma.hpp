@@ -5,8 +5,8 @@
 // sub-tile as a grid of MFMA blocks (fp32: 2 x 2 blocks of 32 x 32 with
 // v_mfma_f32_32x32x2_f32; fp64: 4 x 4 blocks of 16 x 16 with
 // v_mfma_f64_16x16x4_f64).  The k dimension is streamed through LDS in stages
-// of kBK (fp32: 32, fp64: 16), double-buffered: the global loads of stage s+1
-// are in flight in registers while the MFMAs of stage s run.
+// of kBK = 16, double-buffered: the global loads of stage s+1 are in flight in
+// registers while the MFMAs of stage s run.
 //
 // Each operand stage is copied into LDS in its global orientation, with
 // 16-byte loads and 16-byte LDS stores (no transpose):
@@ -25,10 +25,11 @@
 // stage's row fragments cost the statistics GEMM an occupancy step); a
 // kLayoutK fragment is one element per k-step.
 // Source elements may be fp32, fp64 or bf16 (raw uint16 bits, up-cast
-// exactly).  Full, aligned k-layout stages in the compute type are copied
-// global -> LDS directly (global_load_lds_dwordx4, no register staging);
-// other stages go through registers with bounds checks (out-of-range elements
-// are loaded as 0).
+// exactly).  Stages go through registers: full, aligned stages with 16-byte
+// loads, others with bounds checks (out-of-range elements are loaded as 0).
+// A direct global -> LDS copy (global_load_lds_dwordx4) of full, aligned
+// k-layout stages is available under SHP_LDS_DMA; it measured slower than
+// register staging in this loop and is off by default.
 #pragma once
 
 #include <hip/hip_runtime.h>
