@@ -6,7 +6,8 @@
 // v_mfma_f32_32x32x2_f32; fp64: 4 x 4 blocks of 16 x 16 with
 // v_mfma_f64_16x16x4_f64).  The k dimension is streamed through LDS in stages
 // of kBK = 16, double-buffered: the global loads of stage s+1 are in flight in
-// registers while the MFMAs of stage s run.
+// registers while the MFMAs of stage s run (on interior tiles spread over the
+// stage's k-steps, see tile_loop).
 //
 // Each operand stage is copied into LDS in its global orientation, with
 // 16-byte loads and 16-byte LDS stores (no transpose):
@@ -27,9 +28,6 @@
 // Source elements may be fp32, fp64 or bf16 (raw uint16 bits, up-cast
 // exactly).  Stages go through registers: full, aligned stages with 16-byte
 // loads, others with bounds checks (out-of-range elements are loaded as 0).
-// A direct global -> LDS copy (global_load_lds_dwordx4) of full, aligned
-// k-layout stages is available under SHP_LDS_DMA; it measured slower than
-// register staging in this loop and is off by default.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -68,12 +66,6 @@ struct Mfma;
 
 #ifndef SHP_BK_F32
 #define SHP_BK_F32 16
-#endif
-#ifndef SHP_SPLIT_STAGE
-#define SHP_SPLIT_STAGE 0
-#endif
-#ifndef SHP_PADK_WORDS
-#define SHP_PADK_WORDS 0
 #endif
 
 template <>
@@ -114,7 +106,7 @@ struct Mfma<double> {
 template <typename T, int LAYOUT>
 struct Pitch {
   static constexpr int value =
-      LAYOUT == kLayoutK ? kTile + SHP_PADK_WORDS * 4 / (int)sizeof(T) : Mfma<T>::kBK + 16 / (int)sizeof(T);
+      LAYOUT == kLayoutK ? kTile : Mfma<T>::kBK + 16 / (int)sizeof(T);
 };
 
 // Elements of one operand stage in LDS.
@@ -201,61 +193,65 @@ struct Loader {
     }
   }
 
-  // Global -> registers.  (r0, c0): storage origin of the stage.
-  __device__ __forceinline__ void load(const Operand<S>& op, int r0, int c0, int tid) {
+  // Whether the stage with storage origin (r0, c0) lies inside the operand
+  // and is 16-byte aligned (plain 16-byte loads, no bounds checks).
+  static __device__ __forceinline__ bool full(const Operand<S>& op, int r0, int c0) {
     constexpr int SR = LAYOUT == kLayoutK ? BK : kTile;
     constexpr int SC = LAYOUT == kLayoutK ? kTile : BK;
-    const bool fast = op.aligned && (r0 + SR <= op.rows) && (c0 + SC <= op.cols);
+    return op.aligned && (r0 + SR <= op.rows) && (c0 + SC <= op.cols);
+  }
+
+  // Global -> registers, vector slot i of the stage at (r0, c0): a 16-byte
+  // load when `fast`, else element loads with bounds checks.
+  __device__ __forceinline__ void load_slot(const Operand<S>& op, int r0, int c0, int tid, int i, bool fast) {
+    int sr, sc;
+    slot(tid, i, sr, sc);
     if (fast) {
-#pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        int sr, sc;
-        slot(tid, i, sr, sc);
-        buf[i] = gload<V>(op.ptr + (int64_t)(r0 + sr) * op.ld + (c0 + sc));
-      }
+      buf[i] = gload<V>(op.ptr + (int64_t)(r0 + sr) * op.ld + (c0 + sc));
     } else {
+      const int gr = r0 + sr;
 #pragma unroll
-      for (int i = 0; i < PER; ++i) {
-        int sr, sc;
-        slot(tid, i, sr, sc);
-        const int gr = r0 + sr;
-#pragma unroll
-        for (int e = 0; e < VE; ++e) {
-          const int gc = c0 + sc + e;
-          buf[i][e] = (gr < op.rows && gc < op.cols) ? gload<S>(op.ptr + (int64_t)gr * op.ld + gc) : (S)0;
-        }
+      for (int e = 0; e < VE; ++e) {
+        const int gc = c0 + sc + e;
+        buf[i][e] = (gr < op.rows && gc < op.cols) ? gload<S>(op.ptr + (int64_t)gr * op.ld + gc) : (S)0;
       }
     }
   }
 
-  // Registers -> LDS stage (k-major).
-  __device__ __forceinline__ void store(T* lds, const Operand<S>& op, int r0, int c0, int tid) const {
+  __device__ __forceinline__ void load(const Operand<S>& op, int r0, int c0, int tid) {
+    const bool fast = full(op, r0, c0);
 #pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      int sr, sc;
-      slot(tid, i, sr, sc);
-      T v[VE];
+    for (int i = 0; i < PER; ++i) load_slot(op, r0, c0, tid, i, fast);
+  }
+
+  // Registers -> LDS stage, vector slot i (converted to the compute type).
+  __device__ __forceinline__ void store_slot(T* lds, int tid, int i) const {
+    int sr, sc;
+    slot(tid, i, sr, sc);
+    T v[VE];
 #pragma unroll
-      for (int e = 0; e < VE; ++e) v[e] = cvt<T, S>(buf[i][e]);
-      {
-        T* dst = lds + sr * LDP + sc;
-        if (sizeof(T) == 4) {
-          typedef float f4 __attribute__((ext_vector_type(4)));
+    for (int e = 0; e < VE; ++e) v[e] = cvt<T, S>(buf[i][e]);
+    T* dst = lds + sr * LDP + sc;
+    if (sizeof(T) == 4) {
+      typedef float f4 __attribute__((ext_vector_type(4)));
 #pragma unroll
-          for (int e = 0; e < VE; e += 4) {
-            f4 w = {(float)v[e], (float)v[e + 1], (float)v[e + 2], (float)v[e + 3]};
-            *reinterpret_cast<f4*>(reinterpret_cast<float*>(dst) + e) = w;
-          }
-        } else {
-          typedef double d2 __attribute__((ext_vector_type(2)));
+      for (int e = 0; e < VE; e += 4) {
+        f4 w = {(float)v[e], (float)v[e + 1], (float)v[e + 2], (float)v[e + 3]};
+        *reinterpret_cast<f4*>(reinterpret_cast<float*>(dst) + e) = w;
+      }
+    } else {
+      typedef double d2 __attribute__((ext_vector_type(2)));
 #pragma unroll
-          for (int e = 0; e < VE; e += 2) {
-            d2 w = {(double)v[e], (double)v[e + 1]};
-            *reinterpret_cast<d2*>(reinterpret_cast<double*>(dst) + e) = w;
-          }
-        }
+      for (int e = 0; e < VE; e += 2) {
+        d2 w = {(double)v[e], (double)v[e + 1]};
+        *reinterpret_cast<d2*>(reinterpret_cast<double*>(dst) + e) = w;
       }
     }
+  }
+
+  __device__ __forceinline__ void store(T* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) store_slot(lds, tid, i);
   }
 };
 
@@ -274,18 +270,19 @@ struct WaveAcc {
         for (int v = 0; v < Mfma<T>::kAcc; ++v) c[i][j][v] = (T)0;
   }
 
-  // MFMA k-steps [S0, S1) of one LDS stage (kBK / kK steps in all) over the
-  // wave's NB x NB blocks.
+  // The MFMA k-steps of one LDS stage (kBK / kK steps) over the wave's
+  // NB x NB blocks.  hook(s) runs at k-step s, after the fragment reads of
+  // step s+1 are issued and before the MFMAs of step s.
   // SKIP: the wave's square sits on the diagonal of a symmetric output; its
   // MFMA blocks wholly below the diagonal (i > j) are never stored and are
   // skipped.
-  template <int LA, int LB, int LDPA, int LDPB, int S0 = 0, int S1 = Mfma<T>::kBK / Mfma<T>::kK, bool SKIP = false>
+  template <int LA, int LB, int LDPA, int LDPB, bool SKIP, typename Hook>
   __device__ __forceinline__ void stage(const T* __restrict__ a, const T* __restrict__ b, int wm0,
-                                        int wn0, int lane) {
+                                        int wn0, int lane, Hook&& hook) {
     constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;  // k-steps per stage
     constexpr int VP = 16 / (int)sizeof(T);         // elements per 16-byte LDS read
+    constexpr int S0 = 0, S1 = KS;
     static_assert(KS % VP == 0, "row fragments are read 16 bytes at a time");
-    static_assert(S0 % VP == 0 && S1 % VP == 0 && S0 < S1 && S1 <= KS, "k-step range of whole 16-byte reads");
     typedef T vec_t __attribute__((ext_vector_type(VP)));
     const int g = lane / Mfma<T>::kM;  // this lane's k group: k = g * KS + s at k-step s
     const int ml = lane % Mfma<T>::kM;
@@ -331,6 +328,7 @@ struct WaveAcc {
             for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[(s + 1) * LDPB + j * Mfma<T>::kM];
           }
         }
+        hook(s);
         if (LA == kLayoutK || LB == kLayoutK) __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int i = 0; i < NB; ++i)
@@ -346,78 +344,35 @@ struct WaveAcc {
   }
 };
 
-#ifndef SHP_LDS_DMA
-#define SHP_LDS_DMA 0
-#endif
-
-typedef __attribute__((address_space(3))) void* lds_vptr;
-
-// Direct global -> LDS copy of one k-layout stage (rows r0..r0+kBK of the
-// operand, columns c0..c0+128) with global_load_lds_dwordx4: lane i of a wave
-// instruction lands at LDS offset 16 i, so one instruction fills 1 KB =
-// 2 fp32 rows (or 1 fp64 row) of the unpadded [k][128] stage.  The caller
-// guarantees the stage is in bounds and 16-byte aligned.
-template <typename T>
-__device__ __forceinline__ void dma_stage(const Operand<T>& op, int r0, int c0, T* lds, int wave, int lane) {
-  constexpr int BK = Mfma<T>::kBK;
-  constexpr int EPL = 16 / (int)sizeof(T);  // elements per lane
-  constexpr int LPR = kTile / EPL;          // lanes per row
-  constexpr int RPI = 64 / LPR;             // rows per wave instruction
-  constexpr int NI = BK / RPI;              // instructions per stage
-  static_assert(NI % 4 == 0, "stage rows must split over 4 waves");
-  static_assert(Pitch<T, kLayoutK>::value == kTile, "DMA needs unpadded k-layout stages");
-  const int rr = lane / LPR, cc = (lane % LPR) * EPL;
-#pragma unroll
-  for (int q = 0; q < NI / 4; ++q) {
-    const int ins = wave + 4 * q;
-    const T* g = op.ptr + (int64_t)(r0 + ins * RPI + rr) * op.ld + (c0 + cc);
-    __builtin_amdgcn_global_load_lds(reinterpret_cast<const void*>(g), (lds_vptr)(lds + ins * RPI * kTile), 16, 0,
-                                     0);
-  }
-}
-
-// One operand's staging for one k-stage: DMA when the stage is a full,
-// aligned k-layout tile of an operand already in the compute type, else
-// register staging (bounds-checked loads, conversion, LDS stores).
-template <typename T, typename S, int LAYOUT>
-struct Stager {
-  Loader<T, S, LAYOUT> reg;
-  bool dma = false;
-  __device__ __forceinline__ void issue(const Operand<S>& op, int r0, int c0, T* lds, int tid) {
-    constexpr int BK = Mfma<T>::kBK;
-    dma = SHP_LDS_DMA && LAYOUT == kLayoutK && sizeof(S) == sizeof(T) && op.aligned &&
-          r0 + BK <= op.rows && c0 + kTile <= op.cols;
-    if (dma) {
-      if constexpr (LAYOUT == kLayoutK && sizeof(S) == sizeof(T))
-        dma_stage<T>(reinterpret_cast<const Operand<T>&>(op), r0, c0, lds, tid >> 6, tid & 63);
-    } else {
-      reg.load(op, r0, c0, tid);
-    }
-  }
-  __device__ __forceinline__ void finish(const Operand<S>& op, int r0, int c0, T* lds, int tid) {
-    if (!dma) reg.store(lds, op, r0, c0, tid);
-  }
-};
-
 // k-loop over LDS stages.  COMPUTE == false: the wave only helps to stage
-// operands (its MFMAs are skipped); the two variants are separate loops so the
+// operands (its MFMAs are skipped); the variants are separate loops so the
 // wave-uniform choice costs no registers inside the loop.  Stages alternate
-// between two static buffer pairs; the loop is unrolled by two so every LDS
-// access names its buffer at compile time (the wait for an in-flight DMA into
-// one buffer then does not hold back reads of the other).
+// between two buffer pairs; the staging of stage st+1 writes the pair that
+// stage st-1 read, which every wave left at the barrier ending stage st-1.
+//
+// Interior tiles (every stage of both operands full and aligned) stage with
+// plain 16-byte loads spread over the k-steps: a thread's i-th load of stage
+// st+1 is issued at k-step i of stage st and written to LDS at k-step
+// KS - PER + i, so the loads have most of a stage to arrive and the MFMA
+// stream carries no branches.  The last stage re-loads itself into the idle
+// buffer pair instead of testing for the end.  Other tiles (ragged edges, and
+// fp64, whose stages are too short to spread) load a whole stage at its start
+// and write it to LDS at its end.
 template <bool COMPUTE, typename T, typename SA, int LA, typename SB, int LB, bool SKIP = false>
 __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
                                           int n0, int K, T* a0, T* a1, T* b0, T* b1) {
   constexpr int BK = Mfma<T>::kBK;
+  constexpr int KS = BK / Mfma<T>::kK;
   typedef Loader<T, SA, LA> LdA;
   typedef Loader<T, SB, LB> LdB;
+  constexpr bool kSpread = 2 * LdA::PER <= KS && 2 * LdB::PER <= KS;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = tid >> 6;
   const int wm0 = (wave >> 1) * kWaveTile;
   const int wn0 = (wave & 1) * kWaveTile;
-  Stager<T, SA, LA> sa;
-  Stager<T, SB, LB> sb;
+  LdA la;
+  LdB lb;
   const int nst = (K + BK - 1) / BK;
   auto orgA = [&](int k0, int& r, int& c) {
     if (LA == kLayoutK) { r = k0; c = m0; } else { r = m0; c = k0; }
@@ -425,54 +380,53 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
   auto orgB = [&](int k0, int& r, int& c) {
     if (LB == kLayoutK) { r = k0; c = n0; } else { r = n0; c = k0; }
   };
-  int ar, ac, br, bc;
+  int ar, ac, br, bc, ar1, ac1, br1, bc1;
   orgA(0, ar, ac);
   orgB(0, br, bc);
-  sa.issue(A, ar, ac, a0, tid);
-  sb.issue(B, br, bc, b0, tid);
-  sa.finish(A, ar, ac, a0, tid);
-  sb.finish(B, br, bc, b0, tid);
-  __builtin_amdgcn_s_waitcnt(0);
+  orgA((nst - 1) * BK, ar1, ac1);
+  orgB((nst - 1) * BK, br1, bc1);
+  // stages are full from the first to the last one when both ends are
+  const bool interior = kSpread && COMPUTE && nst > 0 && LdA::full(A, ar, ac) && LdA::full(A, ar1, ac1) &&
+                        LdB::full(B, br, bc) && LdB::full(B, br1, bc1);
+  la.load(A, ar, ac, tid);
+  lb.load(B, br, bc, tid);
+  la.store(a0, tid);
+  lb.store(b0, tid);
   __syncthreads();
-  // one stage: prefetch st+1 into (na, nb) while computing on (ca, cb).
-  // SHP_SPLIT_STAGE: the LDS writes of st+1 go between the two halves of
-  // the stage's MFMAs (the buffer they fill was released by the previous
-  // barrier), so their latency hides under the second half instead of
-  // stalling every wave at the stage end.
-  constexpr int KSTEPS = Mfma<T>::kBK / Mfma<T>::kK;
-  constexpr int KH = SHP_SPLIT_STAGE ? KSTEPS / 2 : KSTEPS;
-  auto step = [&](int st, T* ca, T* cb, T* na, T* nb) {
+  if (interior) {
+    for (int st = 0; st < nst; ++st) {
+      const bool odd = st & 1;
+      const int nx = min(st + 1, nst - 1);
+      orgA(nx * BK, ar, ac);
+      orgB(nx * BK, br, bc);
+      T* na = odd ? a0 : a1;
+      T* nb = odd ? b0 : b1;
+      acc.template stage<LA, LB, LdA::LDP, LdB::LDP, SKIP>(odd ? a1 : a0, odd ? b1 : b0, wm0, wn0, lane, [&](int s) {
+        if (s < LdA::PER) la.load_slot(A, ar, ac, tid, s, true);
+        if (s < LdB::PER) lb.load_slot(B, br, bc, tid, s, true);
+        if (s >= KS - LdA::PER) la.store_slot(na, tid, s - (KS - LdA::PER));
+        if (s >= KS - LdB::PER) lb.store_slot(nb, tid, s - (KS - LdB::PER));
+      });
+      __syncthreads();
+    }
+    return;
+  }
+  for (int st = 0; st < nst; ++st) {
+    const bool odd = st & 1;
     const bool more = st + 1 < nst;
     if (more) {
       orgA((st + 1) * BK, ar, ac);
       orgB((st + 1) * BK, br, bc);
-      sa.issue(A, ar, ac, na, tid);
-      sb.issue(B, br, bc, nb, tid);
+      la.load(A, ar, ac, tid);
+      lb.load(B, br, bc, tid);
     }
-    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, 0, KH, SKIP>(ca, cb, wm0, wn0, lane);
+    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, SKIP>(odd ? a1 : a0, odd ? b1 : b0, wm0, wn0, lane, [](int) {});
     if (more) {
-      sa.finish(A, ar, ac, na, tid);
-      sb.finish(B, br, bc, nb, tid);
-      if (!SHP_SPLIT_STAGE) __builtin_amdgcn_s_waitcnt(0);
-    }
-    if constexpr (KH < KSTEPS) {
-      if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, KH, KSTEPS, SKIP>(ca, cb, wm0, wn0, lane);
+      la.store(odd ? a0 : a1, tid);
+      lb.store(odd ? b0 : b1, tid);
     }
     __syncthreads();
-  };
-#if SHP_LDS_DMA
-  for (int st = 0; st < nst; st += 2) {
-    step(st, a0, b0, a1, b1);
-    if (st + 1 < nst) step(st + 1, a1, b1, a0, b0);
   }
-#else
-  // register staging only: a select between the two static buffers keeps the
-  // LDS address space and avoids the larger two-way unrolled body
-  for (int st = 0; st < nst; ++st) {
-    const bool odd = st & 1;
-    step(st, odd ? a1 : a0, odd ? b1 : b0, odd ? a0 : a1, odd ? b0 : b1);
-  }
-#endif
 }
 
 
@@ -487,11 +441,8 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
 template <typename T, typename SA, int LA, typename SB, int LB>
 __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
                                          int n0, int K, T* a0, T* a1, T* b0, T* b1, bool lower_idle = false) {
-#ifndef SHP_IDLE_LOWER
-#define SHP_IDLE_LOWER 1
-#endif
   const int wave = threadIdx.x >> 6;
-  const bool idle = SHP_IDLE_LOWER && lower_idle && (wave >> 1) > (wave & 1);
+  const bool idle = lower_idle && (wave >> 1) > (wave & 1);
   const bool ondiag = lower_idle && (wave >> 1) == (wave & 1);
   if (idle)
     tile_loop<false, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);

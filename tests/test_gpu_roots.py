@@ -78,6 +78,27 @@ def test_scalings_against_transcript(env, scaling, p):
             assert abs(inf["iters"] - tr["iters"]) <= 1, (inf, tr["iters"])
 
 
+@pytest.mark.parametrize("scaling", ["frobenius", "power4"])
+def test_iterations_grow_with_condition(env, scaling):
+    """Property: with the eigenvectors and the relative spacing of the
+    log-eigenvalues held fixed, the fp32 iteration count does not decrease as
+    the condition number grows ten-fold at a time (the scaled smallest
+    eigenvalue, which the iteration lifts by a bounded factor per step, gets
+    smaller), and grows over the whole range; every root stays in its band."""
+    say("roots iterations vs condition", scaling)
+    torch, B, dev, h = env
+    code = B.SCALING_POWER4 if scaling == "power4" else B.SCALING_FROBENIUS
+    conds = [1e1, 1e2, 1e3, 1e4]
+    As = [spd(200, c, 7) for c in conds]
+    Xs, info = roots(env, As, p=4, eps=0.0, scaling=code, precision=0)
+    its = [i["iters"] for i in info]
+    assert all(i["status"] in (0, 1) for i in info), info
+    assert its == sorted(its) and its[-1] > its[0], its
+    for A, X in zip(As, Xs):
+        Xo, _, _ = O.inv_root(A, 4, 0.0)
+        assert rel(X, Xo) <= 1e-3, (its, rel(X, Xo))
+
+
 def test_closed_forms(env):
     say("roots closed forms")
     d = np.array([0.5, 2.0, 7.0, 30.0, 1.0, 3.0], dtype=np.float32)

@@ -101,6 +101,9 @@ def test_graft(env, beta1, use_shampoo):
         assert rel(host(dD), ref["D"]) <= 1e-6
         assert abs(nh[k, 0] - ref["norm_mg"]) <= 1e-5 * ref["norm_mg"]
         assert abs(nh[k, 2] - ref["eta"]) <= 1e-5 * max(ref["eta"], 1e-30)
+        # property of the graft: the step has the AdaGrad step's length, ||dW||_F = eta0 ||Mg||_F
+        dWn = float(np.linalg.norm(host(dW).astype(np.float64) - W0))
+        assert abs(dWn - 0.05 * nh[k, 0]) <= 1e-4 * dWn, (k, dWn, nh[k])
         if beta1:
             assert rel(host(dMg), ref["Mg"]) <= 1e-5
             if use_shampoo:
