@@ -194,8 +194,9 @@ size_t shampoo_inv_root_workspace_bytes(const shampoo_root_job* jobs, int njobs,
  * shampoo_inv_root_workspace_bytes(jobs, njobs, params->precision) bytes,
  * owned by the caller and used exclusively by this call until the stream
  * reaches its end.  `info` is a device array of njobs entries.
- * Errors: EINVAL (NULL pointers, n outside [1, 4096], eps < 0, tol < 0,
- * max_iters < 1), EUNSUPPORTED (p outside [1, 16]), ENOMEM (ws_bytes too small).
+ * Errors: EINVAL (NULL pointers, njobs above 2^22, n outside [1, 4096], eps < 0,
+ * tol < 0, max_iters < 1), EUNSUPPORTED (p outside [1, 16]), ENOMEM (ws_bytes
+ * too small).
  */
 shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jobs, int njobs,
                                         const shampoo_root_params* params, void* workspace,

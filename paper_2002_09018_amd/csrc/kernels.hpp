@@ -289,10 +289,17 @@ __device__ __forceinline__ T* newton_buf(const NewtonJob<T>* J, int par, int id)
   return J->S[id & 1];
 }
 
+// Upper tile t of a product launch, packed as job << 10 | ti << 5 | tj
+// (tile indices < 32: n <= 4096), so a workgroup finds its tile with one load.
+__host__ __device__ __forceinline__ uint32_t pack_tile(int j, int ti, int tj) {
+  return ((uint32_t)j << 10) | ((uint32_t)ti << 5) | (uint32_t)tj;
+}
+
 template <typename T>
 __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
-                                                               int njobs, RootState* __restrict__ st,
-                                                               int total_up, NewtonStage S) {
+                                                               const uint32_t* __restrict__ tmap, int njobs,
+                                                               RootState* __restrict__ st, int total_up,
+                                                               NewtonStage S) {
   __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutK>::value], sa1[StageElems<T, kLayoutK>::value];
   __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
   const int np = S.nprod;
@@ -300,12 +307,11 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
   if (l >= np * total_up) return;
   // the products of one tile run in neighbouring workgroups (shared operands)
   const int t = l / np, prod = l - t * np;
-  const int j = find_job_up(jobs, njobs, t);
+  const uint32_t code = tmap[t];
+  const int j = (int)(code >> 10), ti = (int)((code >> 5) & 31), tj = (int)(code & 31);
   if (st[j].status != kActive) return;
   const NewtonJob<T>* J = jobs + j;
   const int par = st[j].parity;
-  int ti, tj;
-  unrank_upper(t - J->up_begin, J->tiles_n, ti, tj);
   const int n = J->n;
   const int m0 = ti * kTile, n0 = tj * kTile;
 

@@ -24,6 +24,7 @@ using namespace shp;
 namespace {
 
 constexpr int kMaxDim = 4096;
+constexpr int kMaxRootJobs = 1 << 22;  // job index field of the packed tile map
 constexpr int kMaxRootOrder = 16;  // largest p of X = A^(-1/p)
 constexpr int kMaxEmbEntries = 1 << 26;  // lookup entries of one embedding call
 constexpr int kCountRing = 64;  // device/pinned slots (pairs) of per-iteration counts
@@ -549,7 +550,7 @@ NewtonStage drop_x(const NewtonStage& s0) {
 
 // One precision phase of the coupled Newton iteration.
 template <typename T>
-shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, RootState* st, int* dcount,
+shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t* tmap, int njobs, RootState* st, int* dcount,
                             int total_up, int total_full, const NewtonProgram& prog, int p, int scaling, float tol,
                             int cap, int poll, int cls, const float* esc_thr, int esc_n, hipStream_t s,
                             int* fails_out = nullptr) {
@@ -577,7 +578,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
     sq1.q[0] = make_prod(kBufS0, kBufS0, kBufNone, kBufS1, 1.0, 0.0, 0.0, 0);
     for (const NewtonStage* S : {&sq0, &sq1}) {
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, *S);
+        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tmap, njobs, st, total_up, *S);
       }));
     }
     const double a = 1.25, b = -0.25;
@@ -608,7 +609,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
         f.nprod = 1;
         f.q[0] = make_prod(kBufMc, kBufS1, kBufS0, kBufMn, 1.0, 1.0, 0.0, 1);
         STATUS_TRY(launch(h, cls, s, [&] {
-          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, f);
+          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tmap, njobs, st, total_up, f);
         }));
         break;  // the iteration's remaining stages are folded into this product
       }
@@ -621,7 +622,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, int njobs, Roo
         continue;
       }
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, njobs, st, total_up, S);
+        hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, tmap, njobs, st, total_up, S);
       }));
     }
     const int ring = 2 * (it % kCountRing);
@@ -886,6 +887,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
   if (!prm) return fail(h, SHAMPOO_EINVAL, "params is NULL");
   if (njobs < 0) return fail(h, SHAMPOO_EINVAL, "njobs < 0");
   if (njobs == 0) return SHAMPOO_OK;
+  if (njobs > kMaxRootJobs) return fail(h, SHAMPOO_EINVAL, "njobs = %d above %d", njobs, kMaxRootJobs);
   if (!jobs || !info || !workspace) return fail(h, SHAMPOO_EINVAL, "jobs, info or workspace is NULL");
   const int p = prm->p;
   if (p < 1 || p > kMaxRootOrder) return fail(h, SHAMPOO_EUNSUPPORTED, "p = %d outside [1, %d]", p, kMaxRootOrder);
@@ -929,6 +931,20 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
     const void* d = nullptr;
     STATUS_TRY(upload_table(h, t.data(), t.size() * sizeof(t[0]), s, &d));
     j64 = static_cast<const NewtonJob<double>*>(d);
+  }
+  // upper-tile map of the product launches: logical tile -> (job, ti, tj)
+  const uint32_t* tmap = nullptr;
+  {
+    std::vector<uint32_t> tm;
+    tm.reserve(up);
+    for (int j = 0; j < njobs; ++j) {
+      const int T = cdiv(jobs[j].n, kTile);
+      for (int ti = 0; ti < T; ++ti)
+        for (int tj = ti; tj < T; ++tj) tm.push_back(pack_tile(j, ti, tj));
+    }
+    const void* d = nullptr;
+    STATUS_TRY(upload_table(h, tm.data(), tm.size() * sizeof(uint32_t), s, &d));
+    tmap = static_cast<const uint32_t*>(d);
   }
   const int nb1 = cdiv(njobs, 64);
   const int tail_all = prec == SHAMPOO_PRECISION_FP64 ? 1 : 0;
@@ -1011,7 +1027,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       esc_n = cap;
     }
     int fails = -1;
-    STATUS_TRY(newton_phase<float>(h, j32, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap, prm->poll,
+    STATUS_TRY(newton_phase<float>(h, j32, tmap, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap, prm->poll,
                                    SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       int* esc_count = dcount + 2 * kCountRing + 2;
@@ -1039,7 +1055,7 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
         hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
       }));
     }
-    STATUS_TRY(newton_phase<double>(h, j64, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
+    STATUS_TRY(newton_phase<double>(h, j64, tmap, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
                                     SHAMPOO_KCLASS_NEWTON_F64, nullptr, 0, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);
