@@ -218,10 +218,16 @@ struct Loader {
     }
   }
 
+  // Whole stage: one branch for the stage (a branch per slot makes the
+  // compiler wait for each 16-byte load before issuing the next).
   __device__ __forceinline__ void load(const Operand<S>& op, int r0, int c0, int tid) {
-    const bool fast = full(op, r0, c0);
+    if (full(op, r0, c0)) {
 #pragma unroll
-    for (int i = 0; i < PER; ++i) load_slot(op, r0, c0, tid, i, fast);
+      for (int i = 0; i < PER; ++i) load_slot(op, r0, c0, tid, i, true);
+    } else {
+#pragma unroll
+      for (int i = 0; i < PER; ++i) load_slot(op, r0, c0, tid, i, false);
+    }
   }
 
   // Registers -> LDS stage, vector slot i (converted to the compute type).
