@@ -180,6 +180,9 @@ def run_c4(args, torch, B):
     ws = torch.empty(B.shampoo_inv_root_workspace_bytes([d] * len(As), prm.precision), dtype=torch.uint8,
                      device=dev)
     info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+    # one untimed call first (code-object loading, table allocation); the
+    # statistics are only read, so the timed call repeats the same work
+    B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info)
@@ -263,6 +266,9 @@ def run_c6(args, torch, B):
     prm = B.shampoo_root_params_default(p=2, eps=1e-6)
     rws = torch.empty(B.shampoo_inv_root_workspace_bytes([dim], prm.precision), dtype=torch.uint8, device=dev)
     info = torch.zeros(8, dtype=torch.int32, device=dev)
+    # one untimed call first (code-object loading, table allocation); R is
+    # only read, so the timed call repeats the same work
+    B.shampoo_inv_root_batched(h, [R], [Rr], prm, rws, info)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     B.shampoo_inv_root_batched(h, [R], [Rr], prm, rws, info)
