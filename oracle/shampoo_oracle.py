@@ -270,7 +270,10 @@ def coupled_newton_warm(A, p, X0, eps=0.0, tol=1e-10, max_iters=100,
     every iteration (R21): the warm start is aborted, and the root computed
     from the cold start instead, when max|XM - MX| exceeds
     comm_tol * max|X| * max|M|, when the residual grew in two consecutive
-    iterations, or when the warm iteration stops unconverged.  When X0
+    iterations, or when the warm iteration stops unconverged (divergence or
+    the iteration cap).  A residual that stops decreasing below STAG_GATE has
+    reached the rounding floor and is accepted as STAGNATED (R3, as in the
+    cold iteration).  When X0
     commutes with A_d the limit is A_d^{-1/p}; otherwise it is
     X0 (X0^p A_d)^{-1/p}, which differs from the root by an amount that
     grows with the commutator.
@@ -305,10 +308,16 @@ def coupled_newton_warm(A, p, X0, eps=0.0, tol=1e-10, max_iters=100,
         scale = float(np.max(np.abs(X))) * float(np.max(np.abs(M)))
         comm.append(c / scale if scale > 0 else np.inf)
         grew = grew + 1 if r_new > r else 0
-        r = r_new
         if not (c <= comm_tol * scale) or grew >= 2:
+            r = r_new
             aborted = True
             break
+        if r < STAG_GATE and r_new >= r and r_new > tol:
+            # R3's rounding floor, as in the cold iteration: accepted
+            r = r_new
+            status = STAGNATED
+            break
+        r = r_new
     if aborted:
         res = coupled_newton(A, p, eps=eps, tol=tol, max_iters=max_iters,
                              eps_relative=eps_relative, lam_max=lam,

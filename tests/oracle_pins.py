@@ -404,6 +404,11 @@ def pin_newton_warm(o):
     Bd = B + 1e-6 * np.eye(24)
     lim = X @ np.real(fractional_matrix_power(np.linalg.matrix_power(X, 4) @ Bd, -0.25))
     assert not res['warm_aborted'] and _relf(res['X'], lim) < 1e-8
+    # tol below the fp64 floor: the residual stops decreasing and the result
+    # is accepted as STAGNATED (R3), still the warm limit
+    res = o.coupled_newton_warm(B, 4, X, eps=1e-6, tol=0.0)
+    assert res['status'] == o.STAGNATED and not res['warm_aborted'] and res['resid'] < 1e-12
+    assert _relf(res['X'], lim) < 1e-8
     C = _spd(48, 1e6, 92)
     Xc, _, _ = o.inv_root(C, 4, eps=1e-6, eps_relative=True)
     C2 = C + 1e-3 * C.max() * _spd(48, 1e1, 93) / 48

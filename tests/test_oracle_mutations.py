@@ -42,6 +42,8 @@ MUTATIONS = [
     ("coupled_newton_warm", "M = np.linalg.matrix_power(X, p) @ Ad", "M = np.linalg.matrix_power(X, p - 1) @ Ad",
      [P.pin_newton_warm]),
     ("coupled_newton_warm", "X = X @ M1", "X = M1 @ X", [P.pin_newton_warm]),
+    ("coupled_newton_warm", "if r < STAG_GATE and r_new >= r and r_new > tol:",
+     "if False and r < STAG_GATE and r_new >= r and r_new > tol:", [P.pin_newton_warm]),
     ("coupled_newton_warm", "if not (c <= comm_tol * scale) or grew >= 2:",
      "if not (c <= 1e6 * comm_tol * scale) or grew >= 2:", [P.pin_newton_warm]),
     ("coupled_newton_warm", "    if aborted:\n        res = coupled_newton(", "    if False:\n        res = coupled_newton(",
