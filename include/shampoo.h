@@ -203,6 +203,39 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
                                         size_t ws_bytes, shampoo_root_info* info, void* stream);
 
 /*
+ * Warm-started batched inverse p-th roots (appendix "A coupled Newton
+ * iteration for computation of inverse p-th roots", warm start, with the
+ * commutator check it proposes for detecting divergence).  On entry jobs[j].X
+ * holds X0, the previous root of a nearby matrix (any n x n fp32 matrix with
+ * positive eigenvalues in exact arithmetic; typically the last call's result);
+ * then
+ *   M = X0^p A_d  (A_d = A_s + eps_eff I as in the cold call),  X = X0,
+ *   while max|M - I| > tol:  M1 = ((p + 1) I - M) / p;  X = X M1;  M = M1^p M;
+ *     after each iteration the warm start is given up when
+ *     max|XM - MX| > comm_tol * max|X| * max|M|, when the residual grew in two
+ *     consecutive iterations, or when it diverges or reaches max_iters.
+ * The iterates no longer commute with A, so every product is a full n x n
+ * product (twice the work of a cold product).  A residual that stops
+ * decreasing below 1e-3 is accepted (STAGNATED, the rounding floor).  When
+ * X0 commutes with A_d the limit is A_d^(-1/p); otherwise it is
+ * X0 (X0^p A_d)^(-1/p), close to the root only while the drift is small.
+ * Matrices whose warm start is given up are computed by the cold call's
+ * iteration in the same call (with its precision policy); the others keep the
+ * warm result.  The warm phase runs in fp64 under SHAMPOO_PRECISION_FP64 and
+ * in fp32 otherwise (under AUTO an fp32 warm result carries fp32 rounding
+ * amplified by the condition number: use FP64 for ill-conditioned factors).
+ * params, workspace, info: as shampoo_inv_root_batched (same workspace size;
+ * cond_est is 0 for a warm result).  warm_out (device, may be NULL): int32
+ * [njobs][2] = {outcome, warm iterations}, outcome 1 = warm result kept,
+ * 2 = warm start given up (cold result), 0 = not attempted (NOT_PD).
+ * Errors: as shampoo_inv_root_batched, and EINVAL for comm_tol <= 0.
+ */
+shampoo_status shampoo_inv_root_warm_batched(void* handle, const shampoo_root_job* jobs, int njobs,
+                                             const shampoo_root_params* params, float comm_tol, void* workspace,
+                                             size_t ws_bytes, shampoo_root_info* info, int32_t* warm_out,
+                                             void* stream);
+
+/*
  * Preconditioned gradient P = Lr G Rr (Preliminaries, Shampoo update rule;
  * one-sided forms of Lemma 1 when a root is NULL; P = G when both are).
  * Lr and Rr must be symmetric (inverse roots are).  G: g_dtype.

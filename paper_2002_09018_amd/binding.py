@@ -68,6 +68,8 @@ _sig = {
     "shampoo_inv_root_workspace_bytes": (_sz, [C.POINTER(shampoo_root_job), _i, _i]),
     "shampoo_inv_root_batched": (_i, [_vp, C.POINTER(shampoo_root_job), _i, C.POINTER(shampoo_root_params),
                                       _vp, _sz, _vp, _vp]),
+    "shampoo_inv_root_warm_batched": (_i, [_vp, C.POINTER(shampoo_root_job), _i, C.POINTER(shampoo_root_params),
+                                           _f, _vp, _sz, _vp, _vp, _vp]),
     "shampoo_precondition": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _vp]),
     "shampoo_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
     "shampoo_graft_lamb": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
@@ -199,6 +201,17 @@ def shampoo_inv_root_batched(handle, As, Xs, params, workspace, info, stream=Non
     _check(handle, _lib.shampoo_inv_root_batched(handle, arr, len(As), C.byref(params), _ptr(workspace),
                                                  int(workspace.numel() * workspace.element_size()),
                                                  _ptr(info), _stream(stream)))
+
+
+def shampoo_inv_root_warm_batched(handle, As, Xs, params, workspace, info, warm_out=None, comm_tol=1e-3,
+                                  stream=None):
+    """As shampoo_inv_root_batched; Xs hold the warm starts X0 on entry.
+    warm_out: None or an int32 device tensor of 2 * len(As)."""
+    arr = _jobs(As, Xs)
+    _check(handle, _lib.shampoo_inv_root_warm_batched(handle, arr, len(As), C.byref(params), float(comm_tol),
+                                                      _ptr(workspace),
+                                                      int(workspace.numel() * workspace.element_size()),
+                                                      _ptr(info), _ptr(warm_out), _stream(stream)))
 
 
 def shampoo_precondition(handle, blocks, stream=None):

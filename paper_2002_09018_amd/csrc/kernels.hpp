@@ -193,6 +193,8 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
 // ============================================================================
 enum : int { kActive = -1 };
 enum : int { kConverged = 0, kStagnated = 1, kMaxIter = 2, kDiverged = 3, kNotPD = 4 };
+// warm phase only: the warm start was given up, the matrix takes the cold start
+enum : int { kWarmAbort = 5 };
 
 constexpr float kStagGate = 1e-3f;  // stagnation is tested only below this residual
 constexpr float kDivergeAt = 1e6f;  // residual above this (or non-finite) diverged
@@ -214,6 +216,13 @@ struct RootState {
   double eps_eff;    // damping added
   double lam_max;    // MaxSV estimate (relative damping)
   double diag_min;   // smallest diagonal entry of A_d
+  // warm start (coupled-Newton appendix)
+  int warm;          // 0 not tried, 1 result from the warm iteration, 2 warm aborted (cold result)
+  int warm_iters;    // iterations of the warm phase
+  int grew;          // consecutive residual increases in the warm phase
+  unsigned xmax_bits;  // max|X| of the new iterate (float bits)
+  unsigned mmax_bits;  // max|M| of the new iterate
+  unsigned comm_bits;  // max|XM - MX| of the new iterates
 };
 
 // Buffers of one matrix in one precision.
@@ -264,9 +273,13 @@ __device__ __forceinline__ int find_job_full(const NewtonJob<T>* jobs, int njobs
 // symmetric and only upper tiles are computed.
 enum : int { kBufXc = 0, kBufXn = 1, kBufMc = 2, kBufMn = 3, kBufS0 = 4, kBufS1 = 5, kBufNone = -1 };
 
+// amax (full products of the warm start only): max|C| into the matrix's
+// monitor slot 1 xmax, 2 mmax or 3 comm.
+enum : int { kAmaxNone = 0, kAmaxX = 1, kAmaxM = 2, kAmaxComm = 3 };
+
 struct NewtonProd {
-  int a, b, e, dst;  // buffer ids (e = kBufNone: no affine E term)
-  int resid, pad;
+  int a, b, e, dst;  // buffer ids (e = kBufNone: no affine E term; dst = kBufNone: not stored)
+  int resid, amax;
   double ca, cb, cg;
 };
 
@@ -408,6 +421,219 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
   if (resid) {
     rmax = wave_max(rmax);
     if (lane == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+  }
+}
+
+// Warm start (coupled-Newton appendix: X0 = the previous root,
+// M0 = X0^p A_d).  X0 does not commute with the new statistics, so neither X
+// nor M stays symmetric: every product of the warm phase is a full n x n
+// product of general matrices, over the full tile grid of every active
+// matrix, with the program format of newton_stage_kernel:
+//   C[dst] = ca (B[a] B[b]) + cb B[e] + cg I
+// The left operand is staged in the row layout (its contraction index is
+// the storage column), the right one k-major.  dst == kBufNone stores
+// nothing (the commutator only needs its largest entry); q.amax adds max|C|
+// to a monitor slot, q.resid max|C - I| to the residual.
+template <typename T>
+__global__ __launch_bounds__(kThreads, kMinWaves) void newton_dense_kernel(const NewtonJob<T>* __restrict__ jobs,
+                                                                          const uint32_t* __restrict__ tmap,
+                                                                          int njobs, RootState* __restrict__ st,
+                                                                          int total_full, NewtonStage S) {
+  __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutRow>::value], sa1[StageElems<T, kLayoutRow>::value];
+  __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
+  const int np = S.nprod;
+  const int l = xcd_remap(blockIdx.x, gridDim.x);
+  if (l >= np * total_full) return;
+  const int t = l / np, prod = l - t * np;
+  const uint32_t code = tmap[t];
+  const int j = (int)(code >> 10), ti = (int)((code >> 5) & 31), tj = (int)(code & 31);
+  if (j >= njobs || st[j].status != kActive) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int par = st[j].parity;
+  const int n = J->n;
+  const int m0 = ti * kTile, n0 = tj * kTile;
+
+  const int ia = pick3(prod, S.q[0].a, S.q[1].a, S.q[2].a);
+  const int ib = pick3(prod, S.q[0].b, S.q[1].b, S.q[2].b);
+  const int ie = pick3(prod, S.q[0].e, S.q[1].e, S.q[2].e);
+  const int id = pick3(prod, S.q[0].dst, S.q[1].dst, S.q[2].dst);
+  const bool resid = pick3(prod, S.q[0].resid, S.q[1].resid, S.q[2].resid) != 0;
+  const int amax = pick3(prod, S.q[0].amax, S.q[1].amax, S.q[2].amax);
+  const T ca = (T)pick3(prod, S.q[0].ca, S.q[1].ca, S.q[2].ca);
+  const T cb = (T)pick3(prod, S.q[0].cb, S.q[1].cb, S.q[2].cb);
+  const T cg = (T)pick3(prod, S.q[0].cg, S.q[1].cg, S.q[2].cg);
+  const T* pa = newton_buf(J, par, ia);
+  const T* pb = newton_buf(J, par, ib);
+  T* pc = id >= 0 ? newton_buf(J, par, id) : nullptr;
+  const T* pe = ie >= 0 ? newton_buf(J, par, ie) : nullptr;
+  const bool al = (reinterpret_cast<uintptr_t>(pa) & 15) == 0 && (reinterpret_cast<uintptr_t>(pb) & 15) == 0 &&
+                  ((n * (int)sizeof(T)) & 15) == 0;
+  Operand<T> A{pa, n, n, n, al};
+  Operand<T> B{pb, n, n, n, al};
+
+  WaveAcc<T> acc;
+  acc.zero();
+  tile_mma<T, T, kLayoutRow, T, kLayoutK>(acc, A, B, m0, n0, n, sa0, sa1, sb0, sb1);
+
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
+  typedef Mfma<T> F;
+  float rmax = 0.f, cmax = 0.f;
+#pragma unroll
+  for (int i = 0; i < WaveAcc<T>::NB; ++i)
+#pragma unroll
+    for (int jj = 0; jj < WaveAcc<T>::NB; ++jj)
+#pragma unroll
+      for (int v = 0; v < F::kAcc; ++v) {
+        const int r = wm0 + i * F::kM + F::row(lane, v);
+        const int c = wn0 + jj * F::kM + F::col(lane);
+        if (r >= n || c >= n) continue;
+        T x = ca * acc.c[i][jj][v];
+        if (pe) x += cb * pe[(int64_t)r * n + c];
+        if (r == c) x += cg;
+        if (pc) gstore<T>(pc + (int64_t)r * n + c, x);
+        if (resid) {
+          float d = (float)fabs((double)x - (r == c ? 1.0 : 0.0));
+          if (!(d <= 3.0e38f)) d = INFINITY;  // NaN or overflow
+          rmax = rmax > d ? rmax : d;
+        }
+        if (amax) {
+          float d = (float)fabs((double)x);
+          if (!(d <= 3.0e38f)) d = INFINITY;
+          cmax = cmax > d ? cmax : d;
+        }
+      }
+  if (resid) {
+    rmax = wave_max(rmax);
+    if (lane == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
+  }
+  if (amax) {
+    cmax = wave_max(cmax);
+    unsigned* slot = amax == kAmaxX ? &st[j].xmax_bits : (amax == kAmaxM ? &st[j].mmax_bits : &st[j].comm_bits);
+    if (lane == 0 && cmax > 0.f) atomicMax(slot, __float_as_uint(cmax));
+  }
+}
+
+// Warm start, set-up pass over the full tile grid: A_d = A_s + eps_eff I
+// into the next-M buffer (the right factor of M0 = X0^p A_d); in fp64 the
+// caller's X0 (fp32) is also copied into the current-X buffer (in fp32 that
+// buffer is the caller's X itself).
+template <typename T>
+__global__ __launch_bounds__(kThreads) void warm_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                            const RootState* __restrict__ st, int total_full) {
+  __shared__ float lds[kTile * 33];
+  const int t = blockIdx.x;
+  if (t >= total_full) return;
+  const int j = find_job_full(jobs, njobs, t);
+  if (st[j].status != kActive) return;
+  const NewtonJob<T> J = jobs[j];
+  const int lt = t - J.full_begin;
+  const int ti = lt / J.tiles_n, tj = lt % J.tiles_n;
+  const double e = st[j].eps_eff;
+  const int n = J.n;
+  T* Ad = J.M[1];
+  sym_tile_pass(J.A, n, ti, tj, lds, [&](int r, int c, double s) {
+    Ad[(int64_t)r * n + c] = (T)(s + (r == c ? e : 0.0));
+  });
+  if (sizeof(T) == 8) {
+    const int r0 = ti * kTile, c0 = tj * kTile;
+    for (int q = threadIdx.x; q < kTile * kTile; q += kThreads) {
+      const int r = r0 + (q >> 7), c = c0 + (q & 127);
+      if (r < n && c < n) J.X[0][(int64_t)r * n + c] = (T)J.Xout[(int64_t)r * n + c];
+    }
+  }
+}
+
+// Warm-phase state machine, one workgroup (rules of the oracle's warm
+// iteration: Algorithm 1's stop test, R3's floor and divergence limits, and
+// the commutator monitor of the coupled-Newton appendix).  count[0]:
+// matrices still in the warm phase; count[1]: matrices whose warm start was
+// given up.
+//   init != 0: residual of M0 = X0^p A_d only.
+__global__ __launch_bounds__(kThreads) void root_warm_update_kernel(RootState* __restrict__ st, int njobs, int init,
+                                                                   float tol, float comm_tol, int max_iters,
+                                                                   int* __restrict__ count) {
+  __shared__ int red[2 * (kThreads / 64)];
+  int active = 0, aborted = 0;
+  for (int j = threadIdx.x; j < njobs; j += kThreads) {
+    RootState& s = st[j];
+    if (s.status != kActive) {
+      aborted += s.status == kWarmAbort;
+      continue;
+    }
+    const float r = __uint_as_float(s.resid_bits);
+    s.resid_bits = 0u;
+    bool abort = false;
+    if (init) {
+      s.resid = r;
+      if (r <= tol) s.status = kConverged;
+      else if (!(r <= kDivergeAt) || max_iters < 1) abort = true;
+    } else {
+      s.parity ^= 1;
+      s.iters += 1;
+      const float prev = s.resid;
+      s.resid = r;
+      const float c = __uint_as_float(s.comm_bits);
+      const float scale = __uint_as_float(s.xmax_bits) * __uint_as_float(s.mmax_bits);
+      s.comm_bits = s.xmax_bits = s.mmax_bits = 0u;
+      s.grew = r > prev ? s.grew + 1 : 0;
+      if (!(c <= comm_tol * scale) || s.grew >= 2) abort = true;
+      else if (r <= tol) s.status = kConverged;
+      else if (prev < kStagGate && r >= prev) s.status = kStagnated;
+      else if (!(r <= kDivergeAt) || s.iters >= max_iters) abort = true;
+    }
+    if (abort) s.status = kWarmAbort;
+    if (s.status == kActive) ++active;
+    else aborted += s.status == kWarmAbort;
+  }
+  int a = active, f = aborted;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    a += __shfl_xor(a, o, 64);
+    f += __shfl_xor(f, o, 64);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[threadIdx.x >> 6] = a;
+    red[kThreads / 64 + (threadIdx.x >> 6)] = f;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int sa = 0, sf = 0;
+    for (int w = 0; w < kThreads / 64; ++w) {
+      sa += red[w];
+      sf += red[kThreads / 64 + w];
+    }
+    count[0] = sa;
+    count[1] = sf;
+  }
+}
+
+// End of the warm phase: records its outcome (warm_out, device int32
+// [njobs][2] = {outcome, warm iterations}, may be NULL) and hands the
+// matrices whose warm start was given up to the cold start.
+__global__ void root_warm_finish_kernel(RootState* __restrict__ st, int njobs, int32_t* __restrict__ warm_out) {
+  const int j = blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= njobs) return;
+  RootState& s = st[j];
+  if (s.status == kNotPD) {
+    s.warm = 0;
+    s.warm_iters = 0;
+  } else if (s.status == kWarmAbort) {
+    s.warm = 2;
+    s.warm_iters = s.iters;
+    s.status = kActive;
+    s.iters = 0;
+    s.parity = 0;
+    s.resid_bits = 0u;
+    s.resid = INFINITY;
+    s.grew = 0;
+  } else {
+    s.warm = 1;
+    s.warm_iters = s.iters;
+  }
+  if (warm_out) {
+    warm_out[2 * j] = s.warm;
+    warm_out[2 * j + 1] = s.warm_iters;
   }
 }
 
@@ -967,6 +1193,12 @@ __global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int pha
   s.resid_bits = 0u;
   s.resid = INFINITY;
   s.precision = precision;
+  if (phase == 0) {
+    s.warm = 0;
+    s.warm_iters = 0;
+    s.grew = 0;
+    s.xmax_bits = s.mmax_bits = s.comm_bits = 0u;
+  }
 }
 
 // Per-iteration state machine, one workgroup.  count[0]: matrices still
@@ -1071,7 +1303,9 @@ __global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T
   if (phase_is_tail && !s.escalate) return;
   if (!phase_is_tail && s.escalate) return;
   if (s.status == kNotPD) return;
-  const bool ident = s.iters == 0;
+  // a warm result at zero iterations is X0 itself, already the caller's X
+  // (fp32) or in the current-X buffer (fp64)
+  const bool ident = s.iters == 0 && s.warm != 1;
   if (!ident && sizeof(T) == 4 && s.parity == 0) return;  // already in place
   const NewtonJob<T>* J = jobs + j;
   const T* src = J->X[s.parity];
@@ -1118,7 +1352,7 @@ __global__ void root_info_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
   const RootState& s = st[j];
   // condition estimate from the iteration count
   double kappa = 0.0;
-  if (s.status == kConverged || s.status == kStagnated) {
+  if ((s.status == kConverged || s.status == kStagnated) && s.warm != 1) {
     const double tl = fmax((double)tol, (double)s.resid);
     double lo = 1e-30, hi = 1.0;  // N(lo) > iters >= N(hi) (N decreasing on (0, 1])
     if (scalar_iters(lo, p, tl, 400) <= s.iters) {

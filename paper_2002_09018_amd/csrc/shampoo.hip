@@ -648,6 +648,95 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t
   return SHAMPOO_OK;
 }
 
+// Warm phase (coupled-Newton appendix, warm start): M0 = X0^p A_d from the
+// caller's X0, then Algorithm 1's iteration with full products and, after
+// every iteration, the commutator monitor max|XM - MX| <= comm_tol max|X|
+// max|M|.  X0^p A_d is formed right to left over the bits of p
+// (Y <- P_s Y for a set bit s, P_(s+1) = P_s P_s, P_0 = X0, Y_0 = A_d), so A_d
+// stays the rightmost factor; the Y products alternate between two buffers
+// so that the last one lands in the current M.  Sets *aborted_out to the
+// number of matrices handed to the cold start when the polled counts showed
+// the phase finished, else leaves it untouched.
+template <typename T>
+shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t* fmap, int njobs, RootState* st,
+                          int* dcount, int total_full, const NewtonProgram& prog, int p, float tol, float comm_tol,
+                          int cap, int poll, int cls, int32_t* warm_out, hipStream_t s, int* aborted_out) {
+  auto kdense = newton_dense_kernel<T>;
+  auto run = [&](const NewtonStage& S) {
+    return launch(h, cls, s, [&] {
+      hipLaunchKernelGGL(kdense, dim3(S.nprod * total_full), dim3(kThreads), 0, s, djobs, fmap, njobs, st,
+                         total_full, S);
+    });
+  };
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(warm_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full);
+  }));
+  int top = 0;
+  while ((p >> (top + 1)) != 0) ++top;
+  const int c = __builtin_popcount((unsigned)p);
+  int pb = kBufXc, yb = kBufMn, k = 0;
+  for (int b = 0; b <= top; ++b) {
+    NewtonStage S{};
+    int np = kBufNone, ny = kBufNone;
+    if ((p >> b) & 1) {
+      ++k;
+      ny = (c - k) % 2 == 0 ? kBufMc : kBufXn;
+      S.q[S.nprod++] = make_prod(pb, yb, kBufNone, ny, 1.0, 0.0, 0.0, k == c);
+    }
+    if (b < top) {
+      np = pb == kBufS0 ? kBufS1 : kBufS0;
+      S.q[S.nprod++] = make_prod(pb, pb, kBufNone, np, 1.0, 0.0, 0.0, 0);
+    }
+    STATUS_TRY(run(S));
+    if (ny != kBufNone) yb = ny;
+    if (np != kBufNone) pb = np;
+  }
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(root_warm_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, comm_tol, cap,
+                       dcount + 2 * kCountRing);
+  }));
+  // the iteration's program with the monitor reductions: max|X| on the X
+  // product, max|M| on the product that writes the next M
+  std::vector<NewtonStage> stages = prog.stages;
+  for (NewtonStage& S : stages)
+    for (int q = 0; q < S.nprod; ++q) {
+      if (S.q[q].dst == kBufXn) S.q[q].amax = kAmaxX;
+      if (S.q[q].dst == kBufMn) S.q[q].amax = kAmaxM;
+    }
+  NewtonStage xm{}, comm{};
+  xm.nprod = comm.nprod = 1;
+  xm.q[0] = make_prod(kBufXn, kBufMn, kBufNone, kBufS0, 1.0, 0.0, 0.0, 0);       // S0 = X' M'
+  comm.q[0] = make_prod(kBufMn, kBufXn, kBufS0, kBufNone, 1.0, -1.0, 0.0, 0);    // M' X' - S0
+  comm.q[0].amax = kAmaxComm;
+  for (int it = 0; it < cap; ++it) {
+    for (const NewtonStage& S : stages) STATUS_TRY(run(S));
+    STATUS_TRY(run(xm));
+    STATUS_TRY(run(comm));
+    const int ring = 2 * (it % kCountRing);
+    int* slot = dcount + ring;
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(root_warm_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, comm_tol, cap,
+                         slot);
+    }));
+    if (poll) {
+      HIP_TRY(h, hipMemcpyAsync(h->pinned + ring, slot, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
+      HIP_TRY(h, hipEventRecord(h->poll_ev[it & 1], s));
+      if (it >= 1) {
+        HIP_TRY(h, hipEventSynchronize(h->poll_ev[(it - 1) & 1]));
+        const int32_t* cnt = h->pinned + 2 * ((it - 1) % kCountRing);
+        if (cnt[0] == 0) {
+          *aborted_out = cnt[1];
+          break;
+        }
+      }
+    }
+  }
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(root_warm_finish_kernel, dim3(cdiv(njobs, 64)), dim3(64), 0, s, st, njobs, warm_out);
+  }));
+  return SHAMPOO_OK;
+}
+
 template <typename T>
 std::vector<NewtonJob<T>> newton_table(const shampoo_root_job* jobs, int njobs, char* ws, const RootLayout& L,
                                        int* total_up, int* total_full) {
@@ -878,13 +967,20 @@ size_t shampoo_inv_root_workspace_bytes(const shampoo_root_job* jobs, int njobs,
   return root_layout(jobs, njobs, precision).total;
 }
 
-shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jobs, int njobs,
-                                        const shampoo_root_params* prm, void* workspace, size_t ws_bytes,
-                                        shampoo_root_info* info, void* stream) {
-  Handle* h = static_cast<Handle*>(handle);
+}  // extern "C"
+
+namespace {
+// Both root entry points.  warm: the warm start of the coupled-Newton
+// appendix from the caller's X, in the precision the policy starts in (fp64
+// under FP64, else fp32), with the cold start for the matrices whose warm
+// start is given up.
+shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs, const shampoo_root_params* prm,
+                             int warm, float comm_tol, void* workspace, size_t ws_bytes, shampoo_root_info* info,
+                             int32_t* warm_out, void* stream) {
   if (!h) return SHAMPOO_EINVAL;
   h->err.clear();
   if (!prm) return fail(h, SHAMPOO_EINVAL, "params is NULL");
+  if (warm && !(comm_tol > 0.f)) return fail(h, SHAMPOO_EINVAL, "comm_tol must be > 0");
   if (njobs < 0) return fail(h, SHAMPOO_EINVAL, "njobs < 0");
   if (njobs == 0) return SHAMPOO_OK;
   if (njobs > kMaxRootJobs) return fail(h, SHAMPOO_EINVAL, "njobs = %d above %d", njobs, kMaxRootJobs);
@@ -946,6 +1042,20 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
     STATUS_TRY(upload_table(h, tm.data(), tm.size() * sizeof(uint32_t), s, &d));
     tmap = static_cast<const uint32_t*>(d);
   }
+  // full-grid tile map of the warm start's general products
+  const uint32_t* fmap = nullptr;
+  if (warm) {
+    std::vector<uint32_t> tm;
+    tm.reserve(full);
+    for (int j = 0; j < njobs; ++j) {
+      const int T = cdiv(jobs[j].n, kTile);
+      for (int ti = 0; ti < T; ++ti)
+        for (int tj = 0; tj < T; ++tj) tm.push_back(pack_tile(j, ti, tj));
+    }
+    const void* d = nullptr;
+    STATUS_TRY(upload_table(h, tm.data(), tm.size() * sizeof(uint32_t), s, &d));
+    fmap = static_cast<const uint32_t*>(d);
+  }
   const int nb1 = cdiv(njobs, 64);
   const int tail_all = prec == SHAMPOO_PRECISION_FP64 ? 1 : 0;
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -990,13 +1100,26 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
                          eps);
     }
   }));
+  // warm phase; -1: unknown number of matrices handed to the cold start
+  int warm_aborts = -1;
+  if (warm) {
+    if (j32)
+      STATUS_TRY(warm_phase<float>(h, j32, fmap, njobs, st, dcount, full, prog, p, prm->tol, comm_tol, prm->max_iters,
+                                   prm->poll, SHAMPOO_KCLASS_NEWTON_F32, warm_out, s, &warm_aborts));
+    else
+      STATUS_TRY(warm_phase<double>(h, j64, fmap, njobs, st, dcount, full, prog, p, prm->tol, comm_tol,
+                                    prm->max_iters, prm->poll, SHAMPOO_KCLASS_NEWTON_F64, warm_out, s, &warm_aborts));
+  }
   if (tail_all) {
-    // every matrix goes to the fp64 phase
+    // every matrix (after a warm phase: every matrix it handed on) goes to
+    // the fp64 phase
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + 2 * kCountRing + 2);
+      if (warm)  // results the warm phase accepted
+        hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 0, p);
     }));
   }
-  int run64 = tail_all;
+  int run64 = tail_all && !(warm && warm_aborts == 0);
   if (j32) {
     int cap = prm->max_iters;
     const float* esc = nullptr;
@@ -1027,8 +1150,11 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       esc_n = cap;
     }
     int fails = -1;
-    STATUS_TRY(newton_phase<float>(h, j32, tmap, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap, prm->poll,
-                                   SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
+    if (warm && warm_aborts == 0)
+      fails = 0;  // every warm result was accepted: no cold start
+    else
+      STATUS_TRY(newton_phase<float>(h, j32, tmap, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap,
+                                     prm->poll, SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       int* esc_count = dcount + 2 * kCountRing + 2;
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -1068,6 +1194,24 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
       hipLaunchKernelGGL(root_info_kernel<double>, dim3(nb1), dim3(64), 0, s, j64, njobs, st, p, prm->tol, (void*)info);
   }));
   return tables_done(h, s);
+}
+}  // namespace
+
+extern "C" {
+
+shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jobs, int njobs,
+                                        const shampoo_root_params* prm, void* workspace, size_t ws_bytes,
+                                        shampoo_root_info* info, void* stream) {
+  return inv_root_impl(static_cast<Handle*>(handle), jobs, njobs, prm, 0, 0.f, workspace, ws_bytes, info, nullptr,
+                       stream);
+}
+
+shampoo_status shampoo_inv_root_warm_batched(void* handle, const shampoo_root_job* jobs, int njobs,
+                                             const shampoo_root_params* prm, float comm_tol, void* workspace,
+                                             size_t ws_bytes, shampoo_root_info* info, int32_t* warm_out,
+                                             void* stream) {
+  return inv_root_impl(static_cast<Handle*>(handle), jobs, njobs, prm, 1, comm_tol, workspace, ws_bytes, info,
+                       warm_out, stream);
 }
 
 shampoo_status shampoo_timing_enable(void* handle, int enable) {
