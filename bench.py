@@ -136,6 +136,53 @@ def cpu_baseline(sample, n, k, p, eps, eta0, budget_s=12.0):
     return out
 
 
+def warm_measure(torch, B, h, As, X0s, prm, ws, ref=None, sample=4):
+    """Warm-started roots (coupled-Newton appendix, warm start) of As from
+    X0s: one untimed call (code-object loading), then a timed one with
+    kernel timing.  Full products counted as 2 n^3 each: at p = 4 the start
+    takes 3 (X0^2, X0^4, X0^4 A_d) and each warm iteration 6 (4 of the
+    iteration, 2 of the commutator monitor).  ref: cold roots of the same
+    As; the relative Frobenius distance of the warm result from them is
+    reported on a sample of matrices."""
+    dev = As[0].device
+    n_all = len(As)
+    info = torch.zeros(8 * n_all, dtype=torch.int32, device=dev)
+    wout = torch.zeros(2 * n_all, dtype=torch.int32, device=dev)
+    Xw = [x.clone() for x in X0s]
+    B.shampoo_inv_root_warm_batched(h, As, Xw, prm, ws, info, wout)
+    torch.cuda.synchronize()
+    for x, x0 in zip(Xw, X0s):
+        x.copy_(x0)
+    B.shampoo_timing_enable(h, True)
+    for c in range(len(B.KCLASS_NAMES)):
+        B.shampoo_timing_read(h, c)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    B.shampoo_inv_root_warm_batched(h, As, Xw, prm, ws, info, wout)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3
+    B.shampoo_timing_enable(h, False)
+    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
+    w = wout.cpu().numpy().reshape(-1, 2)
+    p = prm.p
+    prologue = (p.bit_length() - 1) + bin(p).count("1")
+    per_iter = (p.bit_length() - 1) + bin(p).count("1") + 1 + 2
+    flops = sum(2.0 * a.shape[0] ** 3 * (prologue + per_iter * int(k)) for a, k in zip(As, w[:, 1]))
+    wms = times["newton_warm"][0]
+    out = {"roots": n_all, "ms": ms, "roots_per_s": n_all / ms * 1e3,
+           "kept": int((w[:, 0] == 1).sum()), "given_up": int((w[:, 0] == 2).sum()),
+           "warm_iters_mean": float(w[:, 1].mean()),
+           "full_products_ms": wms, "full_products_tflops": flops / (wms * 1e-3) / 1e12 if wms else None,
+           "phases_ms": {c: v[0] for c, v in times.items() if v[1]}}
+    if ref is not None:
+        idx = np.linspace(0, n_all - 1, min(sample, n_all)).astype(int)
+        errs = [float(torch.linalg.norm(Xw[i].double() - ref[i].double()) / torch.linalg.norm(ref[i].double()))
+                for i in idx]
+        out["rel_dist_from_cold_root_max"] = max(errs)
+        out["rel_dist_sample"] = [int(i) for i in idx]
+    return out
+
+
 def run_c4(args, torch, B):
     """C4: 24 BERT-Large-shaped layers, 288 blocks of 1024 x 1024 (strided
     views of the Q, K, V, O, FFN-in and FFN-out tensors); a step is the
@@ -190,6 +237,23 @@ def run_c4(args, torch, B):
     root_ms = (time.perf_counter() - t0) * 1e3
     iters = [i["iters"] for i in B.decode_root_info(info)]
     log(f"root refresh: {len(As)} roots in {root_ms:.1f} ms")
+    # the next refresh (step 200) warm-started from these roots: 100 more
+    # gradients add an independent Wishart(1024, 102400 dof) draw
+    warm = None
+    if not args.no_warm:
+        As2 = [a + cfg.wishart_bartlett_device(d, 100 * d, 1e-3, torch, dev, cfg.C4, 8, b % nb, b // nb)
+               for b, a in enumerate(As)]
+        X2 = [torch.zeros(d, d, device=dev) for _ in As]
+        B.shampoo_inv_root_batched(h, As2, X2, prm, ws, info)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        B.shampoo_inv_root_batched(h, As2, X2, prm, ws, info)
+        torch.cuda.synchronize()
+        cold2_ms = (time.perf_counter() - t0) * 1e3
+        warm = warm_measure(torch, B, h, As2, Xs, prm, ws, ref=X2)
+        warm["cold_ms_same_matrices"] = cold2_ms
+        log(f"warm refresh: {warm['ms']:.1f} ms (cold {cold2_ms:.1f} ms), kept {warm['kept']}")
+        del As2, X2
 
     def step():
         B.shampoo_update_stats(h, blocks)
@@ -232,6 +296,7 @@ def run_c4(args, torch, B):
         "root_refresh": {"roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
                          "iters_mean": float(np.mean(iters)),
                          "newton_tflops": prods * d * d * (d + 1) / (root_ms * 1e-3) / 1e12},
+        "root_refresh_warm_step200": warm,
     }
     print(json.dumps(out), flush=True)
 
@@ -608,6 +673,8 @@ def main():
     ap.add_argument("--vocab", type=int, default=32768, help="c6: table rows")
     ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-warm", action="store_true",
+                    help="c2, c4: skip the warm-start roots measured after the timed steps")
     ap.add_argument("--no-kernel-timing", action="store_true",
                     help="c2: no per-launch HIP events in the timed steps (whole-step time only)")
     ap.add_argument("--calib-copy-mb", type=int, default=0,
@@ -708,6 +775,26 @@ def main():
         other_iters = float(np.mean([i["iters"] for i in B.decode_root_info(info)]))
         del Xo
 
+    # Warm start (coupled-Newton appendix): one more statistics update, then
+    # the roots of the new statistics from those of the last timed step,
+    # beside the cold call on the same statistics.
+    warm = None
+    if not args.no_warm:
+        X0 = [x.clone() for x in Lrs]
+        B.shampoo_update_stats(h, blocks)
+        Xc = [torch.zeros(n, n, device=dev) for _ in range(nb)]
+        info_c = torch.zeros(8 * nb, dtype=torch.int32, device=dev)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        B.shampoo_inv_root_batched(h, Ls, Xc, prm, ws, info_c)
+        torch.cuda.synchronize()
+        cold_ms = (time.perf_counter() - t1) * 1e3
+        warm = warm_measure(torch, B, h, Ls, X0, prm, ws, ref=Xc)
+        warm["cold_ms_same_matrices"] = cold_ms
+        warm["cold_iters_mean"] = float(np.mean([i["iters"] for i in B.decode_root_info(info_c)]))
+        log(f"warm roots: {warm['ms']:.1f} ms (cold {cold_ms:.1f} ms), kept {warm['kept']}")
+        del X0, Xc
+
     # algorithmic work
     # Products per matrix at p = 4: X M1, M1 M1, (M1^2)^2 and M1^4 M per
     # iteration, except the first, whose X product (X0 a multiple of I) is
@@ -782,6 +869,7 @@ def main():
         "other_scaling": None if other_ms is None else {
             "scaling": "frobenius" if scaling == B.SCALING_POWER4 else "power4",
             "roots_call_ms": other_ms, "roots_per_s_roots_call": nb / (other_ms * 1e-3), "iters_mean": other_iters},
+        "warm_start_next_step": warm,
     }
     # device copy bandwidth (a plain 1 GiB copy), the practical ceiling of
     # the HBM-bound graft passes

@@ -374,7 +374,8 @@ enum {
   SHAMPOO_KCLASS_GRAFT = 4,      /* graft reduction and update passes */
   SHAMPOO_KCLASS_ROOT_AUX = 5,   /* root prologue/epilogue/state kernels */
   SHAMPOO_KCLASS_EMB = 6,        /* embedding row compaction (sort, runs, segment sums) */
-  SHAMPOO_KCLASS_COUNT = 7
+  SHAMPOO_KCLASS_NEWTON_WARM = 7, /* full products of warm-started roots (fp32 or fp64 MFMA) */
+  SHAMPOO_KCLASS_COUNT = 8
 };
 shampoo_status shampoo_timing_enable(void* handle, int enable);
 shampoo_status shampoo_timing_read(void* handle, int kclass, double* total_ms, int64_t* launches);

@@ -36,7 +36,7 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
   (zero iterations), commuting diagonal starts (scalar recurrence, exact
   root), the non-commuting limit X0 (X0^p A)^{-1/p} from scipy's Schur-Pade
   fractional power, and the abort with cold fallback on an ill-conditioned
-  drift.  Not built on the GPU (measured: see the design notes).
+  drift.  The GPU counterpart is shampoo_inv_root_warm_batched.
 * ``precondition``      -- Preliminaries (Shampoo update) and Lemma 1's
   one-sided forms.  Pinned by brute force with the Kronecker product of the
   full-matrix AdaGrad preconditioner on tiny shapes.

@@ -27,8 +27,9 @@ SHAMPOO_F32, SHAMPOO_BF16 = 0, 1
 ROOT_CONVERGED, ROOT_STAGNATED, ROOT_MAXITER, ROOT_DIVERGED, ROOT_NOT_PD = 0, 1, 2, 3, 4
 PRECISION_FP32, PRECISION_AUTO, PRECISION_FP64 = 0, 1, 2
 SCALING_FROBENIUS, SCALING_POWER4 = 0, 1
-KCLASS_NEWTON_F32, KCLASS_NEWTON_F64, KCLASS_STATS, KCLASS_PRECOND, KCLASS_GRAFT, KCLASS_ROOT_AUX, KCLASS_EMB = range(7)
-KCLASS_NAMES = ["newton_f32", "newton_f64", "stats", "precond", "graft", "root_aux", "emb"]
+(KCLASS_NEWTON_F32, KCLASS_NEWTON_F64, KCLASS_STATS, KCLASS_PRECOND, KCLASS_GRAFT, KCLASS_ROOT_AUX, KCLASS_EMB,
+ KCLASS_NEWTON_WARM) = range(8)
+KCLASS_NAMES = ["newton_f32", "newton_f64", "stats", "precond", "graft", "root_aux", "emb", "newton_warm"]
 
 
 class shampoo_block(C.Structure):

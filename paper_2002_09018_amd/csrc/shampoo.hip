@@ -1105,10 +1105,10 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
   if (warm) {
     if (j32)
       STATUS_TRY(warm_phase<float>(h, j32, fmap, njobs, st, dcount, full, prog, p, prm->tol, comm_tol, prm->max_iters,
-                                   prm->poll, SHAMPOO_KCLASS_NEWTON_F32, warm_out, s, &warm_aborts));
+                                   prm->poll, SHAMPOO_KCLASS_NEWTON_WARM, warm_out, s, &warm_aborts));
     else
       STATUS_TRY(warm_phase<double>(h, j64, fmap, njobs, st, dcount, full, prog, p, prm->tol, comm_tol,
-                                    prm->max_iters, prm->poll, SHAMPOO_KCLASS_NEWTON_F64, warm_out, s, &warm_aborts));
+                                    prm->max_iters, prm->poll, SHAMPOO_KCLASS_NEWTON_WARM, warm_out, s, &warm_aborts));
   }
   if (tail_all) {
     // every matrix (after a warm phase: every matrix it handed on) goes to
