@@ -117,8 +117,11 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   tile_mma<float, SA, LA, SB, LB>(acc, A, B, m0, n0, K, sa0, sa1, sb0, sb1, P.sym && ti == tj);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
   const bool diag = P.sym && ti == tj;
+  // the squares of wave_role: on a diagonal tile waves 1 and 2 share the
+  // upper-right square (block rows of its top and bottom halves)
+  const bool helper = diag && wave == 2;
+  const int wm0 = m0 + (helper ? 0 : (wave >> 1) * kWaveTile), wn0 = n0 + (helper ? kWaveTile : (wave & 1) * kWaveTile);
   typedef Mfma<float> F;
 #if SHP_EPI_VEC
   // Symmetric output, off-diagonal full tile: mirrored values go out as
@@ -179,6 +182,8 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
       for (int v = 0; v < F::kAcc; ++v) {
         const int r = wm0 + i * F::kM + F::row(lane, v);
         const int c = wn0 + j * F::kM + F::col(lane);
+        if (diag && wave == 1 && i >= WaveAcc<float>::NB / 2) continue;
+        if (helper && i < WaveAcc<float>::NB / 2) continue;
         if (r >= P.M || c >= P.N) continue;
         if (diag && r > c) continue;
         float x = P.alpha * acc.c[i][j][v];
@@ -358,8 +363,11 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
   };
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm0 = m0 + (wave >> 1) * kWaveTile, wn0 = n0 + (wave & 1) * kWaveTile;
   const bool diag = ti == tj;
+  // the squares of wave_role (waves 1 and 2 share the upper-right square of
+  // a diagonal tile)
+  const bool helper = diag && wave == 2;
+  const int wm0 = m0 + (helper ? 0 : (wave >> 1) * kWaveTile), wn0 = n0 + (helper ? kWaveTile : (wave & 1) * kWaveTile);
   typedef Mfma<T> F;
   float rmax = 0.f;
   auto track = [&](T x, int r, int c) {
@@ -410,6 +418,8 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
         for (int v = 0; v < F::kAcc; ++v) {
           const int r = wm0 + i * F::kM + F::row(lane, v);
           const int c = wn0 + jj * F::kM + F::col(lane);
+          if (diag && wave == 1 && i >= WaveAcc<T>::NB / 2) continue;
+          if (helper && i < WaveAcc<T>::NB / 2) continue;
           if (r >= n || c >= n) continue;
           if (diag && r > c) continue;
           const T x = fin(acc.c[i][jj][v], r, c);

@@ -42,13 +42,14 @@ namespace shp {
 #define SHP_MIN_WAVES_F64 2
 #endif
 #ifndef SHP_MIN_WAVES_NEWTON_F32
-#define SHP_MIN_WAVES_NEWTON_F32 4
+#define SHP_MIN_WAVES_NEWTON_F32 2
 #endif
 // Minimum waves per SIMD requested from the register allocator
 // (__launch_bounds__ second argument).  Measured per kernel: the grouped
 // GEMMs run best at 2 (the allocator then reaches 3-4 waves without
-// spilling), the fp32 Newton products at 4 (a few epilogue spills, +3%),
-// fp64 at 2.
+// spilling), the fp32 Newton products at 2 as well (136 registers, 3 waves,
+// no spills: +1-2% over asking for 4, which spilled in the epilogue once
+// every wave of a diagonal tile computes), fp64 at 2.
 constexpr int kMinWaves = SHP_MIN_WAVES;
 template <typename T>
 struct MinWaves {
@@ -261,6 +262,33 @@ struct Loader {
   }
 };
 
+// Which MFMA blocks of its 64 x 64 square a wave computes.  On a diagonal
+// tile of a symmetric output only the upper triangle is stored: the two
+// waves on the diagonal skip their blocks below it, and the upper-right
+// square is split by block rows between its own wave and the wave of the
+// lower-left square (never stored), so no wave idles.
+enum : int { kBlocksAll = 0, kBlocksUpper = 1, kBlocksTopHalf = 2, kBlocksBottomHalf = 3 };
+
+template <int MODE, int NB>
+__host__ __device__ constexpr bool block_used(int i, int j) {
+  return MODE == kBlocksAll ? true
+         : MODE == kBlocksUpper ? i <= j
+         : MODE == kBlocksTopHalf ? i < NB / 2
+                                  : i >= NB / 2;
+}
+
+// The wave's square (row and column offsets inside the 128 x 128 tile) and
+// block set.
+struct WaveRole {
+  int wm, wn, mode;
+};
+__device__ __forceinline__ WaveRole wave_role(int wave, bool diag) {
+  if (!diag) return {(wave >> 1) * kWaveTile, (wave & 1) * kWaveTile, kBlocksAll};
+  if (wave == 0) return {0, 0, kBlocksUpper};
+  if (wave == 3) return {kWaveTile, kWaveTile, kBlocksUpper};
+  return {0, kWaveTile, wave == 1 ? kBlocksTopHalf : kBlocksBottomHalf};
+}
+
 // Accumulators of one wave: an NB x NB grid of MFMA blocks covering 64 x 64.
 template <typename T>
 struct WaveAcc {
@@ -279,10 +307,8 @@ struct WaveAcc {
   // The MFMA k-steps of one LDS stage (kBK / kK steps) over the wave's
   // NB x NB blocks.  hook(s) runs at k-step s, after the fragment reads of
   // step s+1 are issued and before the MFMAs of step s.
-  // SKIP: the wave's square sits on the diagonal of a symmetric output; its
-  // MFMA blocks wholly below the diagonal (i > j) are never stored and are
-  // skipped.
-  template <int LA, int LB, int LDPA, int LDPB, bool SKIP, typename Hook>
+  // MODE (kBlocks*): the blocks of the wave's square that are computed.
+  template <int LA, int LB, int LDPA, int LDPB, int MODE, typename Hook>
   __device__ __forceinline__ void stage(const T* __restrict__ a, const T* __restrict__ b, int wm0,
                                         int wn0, int lane, Hook&& hook) {
     constexpr int KS = Mfma<T>::kBK / Mfma<T>::kK;  // k-steps per stage
@@ -340,7 +366,7 @@ struct WaveAcc {
         for (int i = 0; i < NB; ++i)
 #pragma unroll
           for (int j = 0; j < NB; ++j) {
-            if (SKIP && i > j) continue;
+            if (!block_used<MODE, NB>(i, j)) continue;
             c[i][j] = Mfma<T>::mma(LA == kLayoutRow ? ra[i][e] : fa[cur][i], LB == kLayoutRow ? rb[j][e] : fb[cur][j],
                                    c[i][j]);
           }
@@ -350,10 +376,9 @@ struct WaveAcc {
   }
 };
 
-// k-loop over LDS stages.  COMPUTE == false: the wave only helps to stage
-// operands (its MFMAs are skipped); the variants are separate loops so the
-// wave-uniform choice costs no registers inside the loop.  Stages alternate
-// between two buffer pairs; the staging of stage st+1 writes the pair that
+// k-loop over LDS stages of one wave with square (wm0, wn0) and block set
+// MODE (each block set is a separate loop, so the wave-uniform choice costs
+// no registers inside the loop).  Stages alternate between two buffer pairs; the staging of stage st+1 writes the pair that
 // stage st-1 read, which every wave left at the barrier ending stage st-1.
 //
 // Interior tiles (every stage of both operands full and aligned) stage with
@@ -364,9 +389,9 @@ struct WaveAcc {
 // buffer pair instead of testing for the end.  Other tiles (ragged edges, and
 // fp64, whose stages are too short to spread) load a whole stage at its start
 // and write it to LDS at its end.
-template <bool COMPUTE, typename T, typename SA, int LA, typename SB, int LB, bool SKIP = false>
+template <int MODE, typename T, typename SA, int LA, typename SB, int LB>
 __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
-                                          int n0, int K, T* a0, T* a1, T* b0, T* b1) {
+                                          int n0, int K, T* a0, T* a1, T* b0, T* b1, int wm0, int wn0) {
   constexpr int BK = Mfma<T>::kBK;
   constexpr int KS = BK / Mfma<T>::kK;
   typedef Loader<T, SA, LA> LdA;
@@ -374,9 +399,6 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
   constexpr bool kSpread = 2 * LdA::PER <= KS && 2 * LdB::PER <= KS;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
-  const int wm0 = (wave >> 1) * kWaveTile;
-  const int wn0 = (wave & 1) * kWaveTile;
   LdA la;
   LdB lb;
   const int nst = (K + BK - 1) / BK;
@@ -392,7 +414,7 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
   orgA((nst - 1) * BK, ar1, ac1);
   orgB((nst - 1) * BK, br1, bc1);
   // stages are full from the first to the last one when both ends are
-  const bool interior = kSpread && COMPUTE && nst > 0 && LdA::full(A, ar, ac) && LdA::full(A, ar1, ac1) &&
+  const bool interior = kSpread && nst > 0 && LdA::full(A, ar, ac) && LdA::full(A, ar1, ac1) &&
                         LdB::full(B, br, bc) && LdB::full(B, br1, bc1);
   la.load(A, ar, ac, tid);
   lb.load(B, br, bc, tid);
@@ -407,7 +429,7 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
       orgB(nx * BK, br, bc);
       T* na = odd ? a0 : a1;
       T* nb = odd ? b0 : b1;
-      acc.template stage<LA, LB, LdA::LDP, LdB::LDP, SKIP>(odd ? a1 : a0, odd ? b1 : b0, wm0, wn0, lane, [&](int s) {
+      acc.template stage<LA, LB, LdA::LDP, LdB::LDP, MODE>(odd ? a1 : a0, odd ? b1 : b0, wm0, wn0, lane, [&](int s) {
         if (s < LdA::PER) la.load_slot(A, ar, ac, tid, s, true);
         if (s < LdB::PER) lb.load_slot(B, br, bc, tid, s, true);
         if (s >= KS - LdA::PER) la.store_slot(na, tid, s - (KS - LdA::PER));
@@ -426,7 +448,7 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
       la.load(A, ar, ac, tid);
       lb.load(B, br, bc, tid);
     }
-    if (COMPUTE) acc.template stage<LA, LB, LdA::LDP, LdB::LDP, SKIP>(odd ? a1 : a0, odd ? b1 : b0, wm0, wn0, lane, [](int) {});
+    acc.template stage<LA, LB, LdA::LDP, LdB::LDP, MODE>(odd ? a1 : a0, odd ? b1 : b0, wm0, wn0, lane, [](int) {});
     if (more) {
       la.store(odd ? a0 : a1, tid);
       lb.store(odd ? b0 : b1, tid);
@@ -441,21 +463,20 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
 //      reads storage rows m0.. (cols k).
 //   B: layout LB; kLayoutK reads storage rows k (cols n0..), kLayoutRow
 //      reads storage rows n0.. (cols k).
-// lower_idle: diagonal tile of a symmetric output, whose lower-left 64 x 64
-// quarter is never stored; that quarter's wave only stages operands, and the
-// two waves on the diagonal skip their MFMA blocks below it.
+// diag: diagonal tile of a symmetric output; the waves take the squares and
+// block sets of wave_role (the epilogue must use the same roles).
 template <typename T, typename SA, int LA, typename SB, int LB>
 __device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
-                                         int n0, int K, T* a0, T* a1, T* b0, T* b1, bool lower_idle = false) {
-  const int wave = threadIdx.x >> 6;
-  const bool idle = lower_idle && (wave >> 1) > (wave & 1);
-  const bool ondiag = lower_idle && (wave >> 1) == (wave & 1);
-  if (idle)
-    tile_loop<false, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
-  else if (ondiag)
-    tile_loop<true, T, SA, LA, SB, LB, true>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
+                                         int n0, int K, T* a0, T* a1, T* b0, T* b1, bool diag = false) {
+  const WaveRole ro = wave_role(threadIdx.x >> 6, diag);
+  if (ro.mode == kBlocksAll)
+    tile_loop<kBlocksAll, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+  else if (ro.mode == kBlocksUpper)
+    tile_loop<kBlocksUpper, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+  else if (ro.mode == kBlocksTopHalf)
+    tile_loop<kBlocksTopHalf, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
   else
-    tile_loop<true, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1);
+    tile_loop<kBlocksBottomHalf, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
 }
 
 // Workgroup id -> logical tile index so that consecutive logical tiles land
