@@ -86,7 +86,17 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   int ti, tj;
   const int lt = t - P.tile_begin;
   if (P.sym) unrank_upper(lt, P.tiles_n, ti, tj);
-  else { ti = lt / P.tiles_n; tj = lt % P.tiles_n; }
+  else if (!LIM) {
+    // column-major over the output tiles: neighbouring workgroups (one XCD,
+    // one L2) share the column block of B and walk the row blocks of A
+    // (preconditioning Lr G: G's 128-column slab is fetched once per matrix)
+    const int tm = (P.M + kTile - 1) / kTile;
+    tj = lt / tm;
+    ti = lt - tj * tm;
+  } else {
+    ti = lt / P.tiles_n;
+    tj = lt % P.tiles_n;
+  }
   const int m0 = ti * kTile, n0 = tj * kTile;
   if (LIM && P.mcount && m0 >= *P.mcount) return;
 

@@ -139,3 +139,40 @@ def test_rejects_bad_comm_tol(env):
     with pytest.raises(B.ShampooError) as e:
         warm_roots(env, [A], [np.eye(16, dtype=np.float32)], comm_tol=0.0)
     assert e.value.code == B.SHAMPOO_EINVAL
+
+
+def test_c2_size_warm_sampled(env):
+    """The C2 size in the benchmark's launch configuration: 96 statistics
+    1024 x 1024 (Wishart, 19 x 4096 degrees of freedom), cold roots, one
+    statistics update with a new gradient (1024 x 4096, N(0, 1/4096)), then
+    the 96 roots warm-started from the previous ones in one call.  Sampled
+    matrices against the oracle's warm iteration on the same fp32 inputs."""
+    torch, B, dev, h = env
+    say("warm C2 size: 96 x 1024^2")
+    from synth import configs as cfg
+    nb, n, k = 96, 1024, 4096
+    gen = torch.Generator(device=dev).manual_seed(5)
+    Ls = [cfg.wishart_bartlett_device(n, 19 * k, 1.0 / k, torch, dev, cfg.C2, b, 9) for b in range(nb)]
+    Gs = [torch.randn(n, k, device=dev, generator=gen) / k ** 0.5 for _ in range(nb)]
+    Xs = [torch.zeros(n, n, device=dev) for _ in range(nb)]
+    prm = B.shampoo_root_params_default(p=4, eps=1e-6)
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([n] * nb, prm.precision), dtype=torch.uint8, device=dev)
+    info = torch.zeros(8 * nb, dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_batched(h, Ls, Xs, prm, ws, info)
+    B.shampoo_update_stats(h, [B.Block(G=Gs[b], L=Ls[b]) for b in range(nb)])
+    torch.cuda.synchronize()
+    samples = (0, 95)
+    X0 = {b: host(Xs[b]) for b in samples}
+    A1 = {b: host(Ls[b]) for b in samples}
+    wout = torch.full((2 * nb,), -1, dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_warm_batched(h, Ls, Xs, prm, ws, info, wout)
+    torch.cuda.synchronize()
+    w = host(wout).reshape(-1, 2)
+    assert (w[:, 0] == 1).all(), w[:4]
+    infos = B.decode_root_info(info)
+    assert all(i["status"] in (0, 1) for i in infos)
+    for b in samples:
+        ref = O.coupled_newton_warm(A1[b], 4, X0[b], eps=1e-6, tol=1e-6)
+        assert not ref["warm_aborted"]
+        assert abs(int(w[b, 1]) - ref["warm_iters"]) <= 1, (w[b], ref["warm_iters"])
+        assert rel(host(Xs[b]), ref["X"]) <= 1e-3, b
