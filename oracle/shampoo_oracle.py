@@ -37,6 +37,12 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
   root), the non-commuting limit X0 (X0^p A)^{-1/p} from scipy's Schur-Pade
   fractional power, and the abort with cold fallback on an ill-conditioned
   drift.  The GPU counterpart is shampoo_inv_root_warm_batched.
+* ``tensor_stats``, ``tensor_precondition`` -- tensors of order k
+  (Preliminaries: the design holds for any order; the K-FAC comparison
+  appendix: exponent -1/(2k)).  Pinned by pure-Python brute force of the
+  per-mode statistics, the trace identity, a rank-1 tensor's closed form, the
+  Kronecker identity vec(G x_1 H_1 x_2 H_2 x_3 H_3) = (H_1 (x) H_2 (x) H_3)
+  vec(G) with non-symmetric H, and the order-2 case L G R^T.
 * ``precondition``      -- Preliminaries (Shampoo update) and Lemma 1's
   one-sided forms.  Pinned by brute force with the Kronecker product of the
   full-matrix AdaGrad preconditioner on tiny shapes.
@@ -390,6 +396,40 @@ def precondition(G, Lr=None, Rr=None):
         P = _f64(Lr) @ P
     if Rr is not None:
         P = P @ _f64(Rr)
+    return P
+
+
+# --------------------------------------------------------------------------
+# Tensors of any order (Preliminaries: the design holds for tensors of any
+# order; K-FAC comparison appendix: the exponent is -1/(2k) for a tensor of
+# order k).  Mode i of an order-k tensor G has its own statistic over the
+# mode-i unfolding G_(i) (rows indexed by mode i, columns by all the other
+# modes in order), and the preconditioned gradient multiplies every mode by
+# its root.
+# --------------------------------------------------------------------------
+def tensor_stats(stats, G, beta2=1.0):
+    """H_i = beta2 H_i + c G_(i) G_(i)^T for every mode i (c as in
+    stats_update); stats: list of k matrices or None (start from zero)."""
+    G = _f64(G)
+    k = G.ndim
+    c = 1.0 if beta2 == 1.0 else 1.0 - beta2
+    out = []
+    for i in range(k):
+        Gi = np.moveaxis(G, i, 0).reshape(G.shape[i], -1)
+        S = c * (Gi @ Gi.T)
+        if stats is not None and stats[i] is not None:
+            S = beta2 * _f64(stats[i]) + S
+        out.append(S)
+    return out
+
+
+def tensor_precondition(G, roots):
+    """G x_1 H_1 x_2 H_2 ... x_k H_k: the mode-i product contracts mode i of
+    the tensor with the second index of H_i (a None root is the identity)."""
+    P = _f64(G)
+    for i, H in enumerate(roots):
+        if H is not None:
+            P = np.moveaxis(np.tensordot(_f64(H), P, axes=(1, i)), 0, i)
     return P
 
 

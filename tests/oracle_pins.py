@@ -557,4 +557,58 @@ def pin_lamb_worked(o):
     assert abs(s2['eta'] - 0.4) < 1e-15 and abs(s2['W'][0, 0] - 3.0) < 1e-14
 
 
+# ------------------------------------------------------------------ order-k tensors
+def pin_tensor_stats_bruteforce(o):
+    """Per-mode statistics of a 2 x 3 x 4 tensor by pure-Python loops over
+    the other two indices; every mode's trace is ||G||_F^2; a rank-1 tensor
+    u (x) v (x) w has H_1 = |v|^2 |w|^2 u u^T (and likewise per mode)."""
+    r = np.random.default_rng(70)
+    G = r.standard_normal((2, 3, 4))
+    H = o.tensor_stats(None, G)
+    d = G.shape
+    for i in range(3):
+        want = [[0.0] * d[i] for _ in range(d[i])]
+        for a in range(d[i]):
+            for b in range(d[i]):
+                acc = 0.0
+                for x in range(d[(i + 1) % 3]):
+                    for y in range(d[(i + 2) % 3]):
+                        ia, ib = [0] * 3, [0] * 3
+                        ia[i], ib[i] = a, b
+                        ia[(i + 1) % 3] = ib[(i + 1) % 3] = x
+                        ia[(i + 2) % 3] = ib[(i + 2) % 3] = y
+                        acc += G[tuple(ia)] * G[tuple(ib)]
+                want[a][b] = acc
+        assert np.allclose(H[i], np.array(want), rtol=1e-13, atol=1e-13)
+        assert abs(np.trace(H[i]) - float(np.sum(G * G))) < 1e-12
+    u, v, w = r.standard_normal(5), r.standard_normal(6), r.standard_normal(7)
+    T = np.einsum('a,b,c->abc', u, v, w)
+    H = o.tensor_stats(None, T)
+    nu, nv, nw = u @ u, v @ v, w @ w
+    assert np.allclose(H[0], nv * nw * np.outer(u, u), rtol=1e-12, atol=1e-12)
+    assert np.allclose(H[1], nu * nw * np.outer(v, v), rtol=1e-12, atol=1e-12)
+    assert np.allclose(H[2], nu * nv * np.outer(w, w), rtol=1e-12, atol=1e-12)
+    # EMA: beta2 H + (1 - beta2) G_(i) G_(i)^T
+    H2 = o.tensor_stats(H, T, beta2=0.5)
+    assert np.allclose(H2[1], 0.5 * H[1] + 0.5 * nu * nw * np.outer(v, v), rtol=1e-12, atol=1e-12)
+
+
+def pin_tensor_precondition_kronecker(o):
+    """vec(G x_1 H_1 x_2 H_2 x_3 H_3) = (H_1 (x) H_2 (x) H_3) vec(G) with
+    row-major vec and non-symmetric H (numpy's kron); for an order-2 tensor
+    the mode products are H_1 G H_2^T."""
+    r = np.random.default_rng(71)
+    G = r.standard_normal((2, 3, 4))
+    Hs = [r.standard_normal((n, n)) for n in G.shape]
+    P = o.tensor_precondition(G, Hs)
+    K = np.kron(np.kron(Hs[0], Hs[1]), Hs[2])
+    assert np.allclose(P.reshape(-1), K @ G.reshape(-1), rtol=1e-12, atol=1e-12)
+    P = o.tensor_precondition(G, [None, Hs[1], None])
+    assert np.allclose(P.reshape(-1), np.kron(np.kron(np.eye(2), Hs[1]), np.eye(4)) @ G.reshape(-1),
+                       rtol=1e-12, atol=1e-12)
+    M = r.standard_normal((3, 5))
+    A, B = r.standard_normal((3, 3)), r.standard_normal((5, 5))
+    assert np.allclose(o.tensor_precondition(M, [A, B]), A @ M @ B.T, rtol=1e-12, atol=1e-12)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith('pin_')]

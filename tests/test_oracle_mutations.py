@@ -42,6 +42,14 @@ MUTATIONS = [
     ("coupled_newton_warm", "M = np.linalg.matrix_power(X, p) @ Ad", "M = np.linalg.matrix_power(X, p - 1) @ Ad",
      [P.pin_newton_warm]),
     ("coupled_newton_warm", "X = X @ M1", "X = M1 @ X", [P.pin_newton_warm]),
+    ("tensor_stats", "Gi = np.moveaxis(G, i, 0).reshape(G.shape[i], -1)",
+     "Gi = G.reshape(G.shape[i], -1)", [P.pin_tensor_stats_bruteforce]),
+    ("tensor_stats", "S = beta2 * _f64(stats[i]) + S", "S = _f64(stats[i]) + S", [P.pin_tensor_stats_bruteforce]),
+    ("tensor_precondition", "np.tensordot(_f64(H), P, axes=(1, i))", "np.tensordot(_f64(H), P, axes=(0, i))",
+     [P.pin_tensor_precondition_kronecker]),
+    ("tensor_precondition", "P = np.moveaxis(np.tensordot(_f64(H), P, axes=(1, i)), 0, i)",
+     "P = np.tensordot(_f64(H), P, axes=(1, i))",
+     [P.pin_tensor_precondition_kronecker]),
     ("coupled_newton_warm", "if r < STAG_GATE and r_new >= r and r_new > tol:",
      "if False and r < STAG_GATE and r_new >= r and r_new > tol:", [P.pin_newton_warm]),
     ("coupled_newton_warm", "if not (c <= comm_tol * scale) or grew >= 2:",
