@@ -131,6 +131,18 @@ def test_asynchronous_call_matches_polled(env):
     for xa, xb in zip(a[0], b[0]):
         assert np.array_equal(xa, xb)
     assert np.array_equal(a[2], b[2])
+    # warm_out is optional (NULL)
+    torch, B, dev, h = env
+    prm = B.shampoo_root_params_default(p=4, eps=1e-6, max_iters=30)
+    dA = [to_dev(torch, x, dev) for x in As]
+    dX = [to_dev(torch, x, dev) for x in X0s]
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([x.shape[0] for x in As], prm.precision),
+                     dtype=torch.uint8, device=dev)
+    info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_warm_batched(h, dA, dX, prm, ws, info, None)
+    torch.cuda.synchronize()
+    for xa, xc in zip(a[0], dX):
+        assert np.array_equal(xa, host(xc))
 
 
 def test_rejects_bad_comm_tol(env):
