@@ -471,7 +471,14 @@ def run_c5(args, torch, B):
     statistics steps build the factors; one grouped call then roots all 464
     factors (p = 4, per-matrix early exit); the call is timed, and each size
     class is also rooted alone.  A step is the statistics, the two-sided
-    preconditioning and the graft over the 232 blocks."""
+    preconditioning and the graft over the 232 blocks.
+
+    --emb-lookups N > 0: the embedding's gradient is row-sparse instead of
+    dense, the rows read by N lookups per step from a Zipf(1.1) token stream
+    (embedding appendix: only the looked-up rows carry gradient), so its 64
+    factors are rank-deficient and damping-dominated (condition ~1e9) and
+    take the fp64 tail while the 400 others stop after a few fp32
+    iterations: the case per-matrix early exit is for."""
     from synth import configs as cfg
     dev = torch.device("cuda:0")
     nemb = cfg.C5_EMB_ROWS // cfg.C5_D
@@ -497,18 +504,32 @@ def run_c5(args, torch, B):
                       Rr=Rrs[b]) for b in range(nb)]
     h = B.shampoo_create(0)
 
-    def fill_grads():
-        for t in tensors:
-            t.copy_((torch.randn(t.shape, device=dev, generator=gen) * 1e-3 ** 0.5).to(torch.bfloat16))
+    sparse = args.emb_lookups > 0
+    emb32 = torch.zeros(emb.shape, device=dev) if sparse else None
 
-    log(f"C5: {nb} blocks, 10 statistics steps")
+    def fill_grads(step):
+        for t in tensors[1:] if sparse else tensors:
+            t.copy_((torch.randn(t.shape, device=dev, generator=gen) * 1e-3 ** 0.5).to(torch.bfloat16))
+        if sparse:
+            idx = torch.from_numpy(cfg.zipf_rows(args.emb_lookups, emb.shape[0], 1.1, cfg.C5, 3, step)).to(dev)
+            dy = torch.randn(args.emb_lookups, emb.shape[1], device=dev, generator=gen) * 1e-3 ** 0.5
+            emb32.zero_()
+            emb32.index_add_(0, idx.long(), dy)
+            emb.copy_(emb32.to(torch.bfloat16))
+
+    log(f"C5: {nb} blocks, 10 statistics steps" + (f", embedding row-sparse ({args.emb_lookups} Zipf lookups/step)"
+                                                    if sparse else ""))
     for t in range(10):
-        fill_grads()
+        fill_grads(t)
         B.shampoo_update_stats(h, blocks)
     torch.cuda.synchronize()
     As, Xs = Ls + Rs, Lrs + Rrs
     ns = [a.shape[0] for a in As]
-    prm = B.shampoo_root_params_default(p=4, eps=1e-6)
+    # the row-sparse variant's factors have many zero eigenvalues, and fp32
+    # rounding of the statistics leaves them near +-1e-7 lambda_max, far
+    # above an absolute 1e-6 ridge: they take the scaled damping
+    # eps * lambda_max of Algorithm 1 (MaxSV) instead
+    prm = B.shampoo_root_params_default(p=4, eps=1e-6, eps_relative=1 if sparse else 0)
     ws = torch.empty(B.shampoo_inv_root_workspace_bytes(ns, prm.precision), dtype=torch.uint8, device=dev)
     info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
     B.shampoo_inv_root_batched(h, As[:2], Xs[:2], prm, ws, info)     # warm-up
@@ -525,10 +546,16 @@ def run_c5(args, torch, B):
     inf = B.decode_root_info(info)
     log(f"grouped roots: {len(As)} in {root_ms:.1f} ms")
     sym = [n * n * (n + 1) for n in ns]
-    prods = [newton_products(i["iters"], 4, True) for i in inf]
-    executed = sum(pq * s for pq, s in zip(prods, sym))
-    kmax = max(i["iters"] for i in inf)
-    no_exit = newton_products(kmax, 4, True) * sum(sym)
+    # executed products: every matrix's fp32 iterations, plus the fp64 tail of
+    # the escalated ones; without early exit every matrix of a phase would run
+    # that phase's largest iteration count
+    prods = [newton_products(i["iters_fp32"], 4, True) for i in inf]
+    prods64 = [newton_products(i["iters"], 4, True) if i["precision"] == 64 else 0 for i in inf]
+    executed = sum((pq + pq64) * s for pq, pq64, s in zip(prods, prods64, sym))
+    esc = [j for j, i in enumerate(inf) if i["precision"] == 64]
+    no_exit = newton_products(max(i["iters_fp32"] for i in inf), 4, True) * sum(sym)
+    if esc:
+        no_exit += newton_products(max(inf[j]["iters"] for j in esc), 4, True) * sum(sym[j] for j in esc)
     classes = {}
     for k in sorted(set(ns)):
         sel = [j for j, n in enumerate(ns) if n == k]
@@ -540,11 +567,11 @@ def run_c5(args, torch, B):
         B.shampoo_inv_root_batched(h, a_k, x_k, prm, ws, info_k)
         torch.cuda.synchronize()
         ms_k = (time.perf_counter() - t1) * 1e3
-        it_k = [inf[j]["iters"] for j in sel]
+        it_k = [inf[j]["iters"] + (inf[j]["iters_fp32"] if inf[j]["precision"] == 64 else 0) for j in sel]
         classes[str(k)] = {"roots": len(sel), "iters_min": min(it_k), "iters_max": max(it_k),
                            "iters_mean": float(np.mean(it_k)), "alone_ms": ms_k,
                            "alone_roots_per_s": len(sel) / ms_k * 1e3,
-                           "alone_newton_tflops": sum(prods[j] * sym[j] for j in sel) / (ms_k * 1e-3) / 1e12}
+                           "alone_newton_tflops": sum((prods[j] + prods64[j]) * sym[j] for j in sel) / (ms_k * 1e-3) / 1e12}
         log(f"  class {k}: {len(sel)} roots alone in {ms_k:.2f} ms")
 
     def step():
@@ -580,7 +607,9 @@ def run_c5(args, torch, B):
         "dtype": "f32 (bf16-stored G)", "data": "synthetic",
         "config": {"workload": "C5: embedding 32768x1024 as 32 row blocks + 200 square blocks k in "
                                "{128,256,512,1024,2048}; G ~ N(0,1e-3) stored bf16; 10 stats steps; p=4, "
-                               "eps 1e-6", "blocks": nb, "factors": len(As)},
+                               "eps 1e-6" + (f"; embedding gradient row-sparse, {args.emb_lookups} Zipf(1.1) "
+                                             "lookups/step; damping eps * lambda_max" if sparse else ""),
+                   "blocks": nb, "factors": len(As), "emb_lookups": args.emb_lookups},
         "phase_roofline_ms": roof_ms, "frac_of_phase_roofline": roof_ms / ms_step,
         "phases_ms_per_step": {c: v[0] / K for c, v in times.items()},
         "kernels": {"stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12,
@@ -590,8 +619,14 @@ def run_c5(args, torch, B):
             "roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
             "newton_ms": ms_newton, "root_aux_ms": rt["root_aux"][0],
             "newton_tflops": executed / (ms_newton * 1e-3) / 1e12 if ms_newton else None,
+            "newton_f32_tflops": (sum(pq * s for pq, s in zip(prods, sym)) / (rt["newton_f32"][0] * 1e-3) / 1e12
+                                  if rt["newton_f32"][0] else None),
+            "newton_f64_tflops": (sum(pq * s for pq, s in zip(prods64, sym)) / (rt["newton_f64"][0] * 1e-3) / 1e12
+                                  if rt["newton_f64"][0] else None),
             "statuses": sorted(set(i["status"] for i in inf)),
-            "n_fp64": sum(1 for i in inf if i["precision"] == 64),
+            "n_fp64": len(esc),
+            "iters_fp32_max": max(i["iters_fp32"] for i in inf),
+            "iters_fp64_max": max((inf[j]["iters"] for j in esc), default=0),
             "executed_gflop": executed / 1e9, "no_early_exit_gflop": no_exit / 1e9,
             "early_exit_saving": 1.0 - executed / no_exit,
             "by_size": classes,
@@ -671,6 +706,8 @@ def main():
     ap.add_argument("--no-compare-scaling", action="store_true",
                     help="skip the comparison roots call under the other scaling (for profiling runs)")
     ap.add_argument("--vocab", type=int, default=32768, help="c6: table rows")
+    ap.add_argument("--emb-lookups", type=int, default=0,
+                    help="c5: row-sparse embedding gradient from this many Zipf lookups per step (0: dense)")
     ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-warm", action="store_true",

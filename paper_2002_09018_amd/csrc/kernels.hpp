@@ -323,19 +323,25 @@ __host__ __device__ __forceinline__ uint32_t pack_tile(int j, int ti, int tj) {
   return ((uint32_t)j << 10) | ((uint32_t)ti << 5) | (uint32_t)tj;
 }
 
+// tlist / tcount: the compact upper-tile list of the matrices still active
+// (build_tile_list); the grid is sized for every upper tile, and the
+// workgroups past S.nprod * *tcount return at once.  The workgroup -> tile
+// remap is taken over the active part only, so the work of a few remaining
+// matrices still spreads over every XCD.
 template <typename T>
 __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
-                                                               const uint32_t* __restrict__ tmap, int njobs,
-                                                               RootState* __restrict__ st, int total_up,
-                                                               NewtonStage S) {
+                                                               const uint32_t* __restrict__ tlist,
+                                                               const int* __restrict__ tcount, int njobs,
+                                                               RootState* __restrict__ st, NewtonStage S) {
   __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutK>::value], sa1[StageElems<T, kLayoutK>::value];
   __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
   const int np = S.nprod;
-  const int l = xcd_remap(blockIdx.x, gridDim.x);
-  if (l >= np * total_up) return;
+  const int nwork = np * *tcount;
+  if ((int)blockIdx.x >= nwork) return;
+  const int l = xcd_remap(blockIdx.x, nwork);
   // the products of one tile run in neighbouring workgroups (shared operands)
   const int t = l / np, prod = l - t * np;
-  const uint32_t code = tmap[t];
+  const uint32_t code = tlist[t];
   const int j = (int)(code >> 10), ti = (int)((code >> 5) & 31), tj = (int)(code & 31);
   if (st[j].status != kActive) return;
   const NewtonJob<T>* J = jobs + j;
@@ -1186,6 +1192,46 @@ __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob
   if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
 }
 
+// Compact list of the upper tiles of the matrices still active, in job
+// order: tlist[0, *tcount).  tmap holds every upper tile (job-major) and
+// ubegin[j] the first of job j (ubegin[njobs] = their number).  Called by one
+// whole workgroup; st must be final for every job (the caller's threads have
+// passed a barrier since they last wrote it).
+__device__ __forceinline__ void build_tile_list(const RootState* __restrict__ st, int njobs,
+                                                const uint32_t* __restrict__ tmap, const int* __restrict__ ubegin,
+                                                uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
+  __shared__ int scan[kThreads];
+  __shared__ int base;
+  if (threadIdx.x == 0) base = 0;
+  __syncthreads();
+  for (int j0 = 0; j0 < njobs; j0 += kThreads) {
+    const int j = j0 + (int)threadIdx.x;
+    const int b = j < njobs ? ubegin[j] : 0;
+    const int n = (j < njobs && st[j].status == kActive) ? ubegin[j + 1] - b : 0;
+    scan[threadIdx.x] = n;
+    __syncthreads();
+    for (int o = 1; o < kThreads; o <<= 1) {  // inclusive scan
+      const int v = (int)threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
+      __syncthreads();
+      scan[threadIdx.x] += v;
+      __syncthreads();
+    }
+    const int off = base + scan[threadIdx.x] - n;
+    for (int k = 0; k < n; ++k) tlist[off + k] = tmap[b + k];
+    __syncthreads();
+    if (threadIdx.x == 0) base += scan[kThreads - 1];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *tcount = base;
+}
+
+__global__ __launch_bounds__(kThreads) void tile_list_kernel(const RootState* __restrict__ st, int njobs,
+                                                            const uint32_t* __restrict__ tmap,
+                                                            const int* __restrict__ ubegin,
+                                                            uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
+  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
+}
+
 // Resets the state of the matrices that take part in a phase.
 //   phase 0: every matrix (fresh call), phase 1: fp64 tail of AUTO, only
 //   matrices flagged `escalate`.
@@ -1229,9 +1275,13 @@ __global__ void root_reset_kernel(RootState* __restrict__ st, int njobs, int pha
 // esc_thr (AUTO fp32 phase, else NULL): esc_thr[k-1] is the largest residual
 // after k iterations of a matrix that can still converge within the phase's
 // cap; a matrix above it leaves the phase at once (MAXITER, escalated).
+// Ends by building the compact tile list of the matrices still active.
 __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __restrict__ st, int njobs, int init,
                                                               float tol, int max_iters, int* __restrict__ count,
-                                                              const float* __restrict__ esc_thr, int esc_n) {
+                                                              const float* __restrict__ esc_thr, int esc_n,
+                                                              const uint32_t* __restrict__ tmap,
+                                                              const int* __restrict__ ubegin,
+                                                              uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
   __shared__ int red[2 * (kThreads / 64)];
   int active = 0, fails = 0;
   for (int j = threadIdx.x; j < njobs; j += kThreads) {
@@ -1281,6 +1331,8 @@ __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __rest
     count[0] = sa;
     count[1] = sf;
   }
+  // the next iteration's tiles (every thread's matrices are final here)
+  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
 }
 
 // End of the fp32 phase under AUTO: flag matrices whose fp32 result is not

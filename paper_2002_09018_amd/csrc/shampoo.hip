@@ -401,7 +401,7 @@ shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float 
 
 // ---------------------------------------------------------------- roots
 struct RootLayout {
-  size_t state = 0, counts = 0, total = 0;
+  size_t state = 0, counts = 0, tlist = 0, tcount = 0, total = 0;
   std::vector<size_t> part, vec, f32, f64;  // per job offsets
 };
 
@@ -412,6 +412,16 @@ RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
   off += align256((size_t)njobs * sizeof(RootState));
   L.counts = off;
   off += align256(kCountInts * sizeof(int));
+  // compact tile list of the product launches (one entry per upper tile)
+  size_t up = 0;
+  for (int j = 0; j < njobs; ++j) {
+    const size_t T = (size_t)cdiv(jobs[j].n, kTile);
+    up += T * (T + 1) / 2;
+  }
+  L.tlist = off;
+  off += align256(up * sizeof(uint32_t));
+  L.tcount = off;
+  off += 256;
   for (int j = 0; j < njobs; ++j) {
     const size_t n = (size_t)jobs[j].n;
     const size_t T = (size_t)cdiv(jobs[j].n, kTile);
@@ -548,9 +558,19 @@ NewtonStage drop_x(const NewtonStage& s0) {
   return r;
 }
 
+// Tiles of the product launches: every upper tile (tmap, job-major, job j's
+// from ubegin[j]) and the compact list of the matrices still active (tlist,
+// *tcount), rebuilt at the start of a phase and after every iteration.
+struct TileLists {
+  const uint32_t* tmap;
+  const int* ubegin;
+  uint32_t* tlist;
+  int* tcount;
+};
+
 // One precision phase of the coupled Newton iteration.
 template <typename T>
-shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t* tmap, int njobs, RootState* st, int* dcount,
+shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileLists& tl, int njobs, RootState* st, int* dcount,
                             int total_up, int total_full, const NewtonProgram& prog, int p, int scaling, float tol,
                             int cap, int poll, int cls, const float* esc_thr, int esc_n, hipStream_t s,
                             int* fails_out = nullptr) {
@@ -561,7 +581,12 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t
   auto kstage = newton_stage_kernel<T>;
   const bool power = scaling == SHAMPOO_SCALING_POWER4;
   const int nb1 = cdiv(njobs, 64);
-  // M0 (and, with the Frobenius scaling, X1 and the residual of M0)
+  // M0 (and, with the Frobenius scaling, X1 and the residual of M0); the
+  // tiles of the matrices that take part in this phase
+  STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+    hipLaunchKernelGGL(tile_list_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, tl.tmap, tl.ubegin, tl.tlist,
+                       tl.tcount);
+  }));
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p,
                        power ? 0 : 1);
@@ -578,7 +603,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t
     sq1.q[0] = make_prod(kBufS0, kBufS0, kBufNone, kBufS1, 1.0, 0.0, 0.0, 0);
     for (const NewtonStage* S : {&sq0, &sq1}) {
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tmap, njobs, st, total_up, *S);
+        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs, st, *S);
       }));
     }
     const double a = 1.25, b = -0.25;
@@ -596,7 +621,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
-                       dcount + 2 * kCountRing, (const float*)nullptr, 0);
+                       dcount + 2 * kCountRing, (const float*)nullptr, 0, tl.tmap, tl.ubegin, tl.tlist, tl.tcount);
   }));
   const NewtonStage first0 = drop_x(prog.stages[0]);
   for (int it = 0; it < cap; ++it) {
@@ -609,7 +634,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t
         f.nprod = 1;
         f.q[0] = make_prod(kBufMc, kBufS1, kBufS0, kBufMn, 1.0, 1.0, 0.0, 1);
         STATUS_TRY(launch(h, cls, s, [&] {
-          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tmap, njobs, st, total_up, f);
+          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs, st, f);
         }));
         break;  // the iteration's remaining stages are folded into this product
       }
@@ -622,14 +647,15 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t
         continue;
       }
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, tmap, njobs, st, total_up, S);
+        hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs,
+                           st, S);
       }));
     }
     const int ring = 2 * (it % kCountRing);
     int* slot = dcount + ring;
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, cap, slot, esc_thr,
-                         esc_n);
+                         esc_n, tl.tmap, tl.ubegin, tl.tlist, tl.tcount);
     }));
     if (poll) {
       HIP_TRY(h, hipMemcpyAsync(h->pinned + ring, slot, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
@@ -1029,18 +1055,26 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     j64 = static_cast<const NewtonJob<double>*>(d);
   }
   // upper-tile map of the product launches: logical tile -> (job, ti, tj)
-  const uint32_t* tmap = nullptr;
+  TileLists tl{};
   {
     std::vector<uint32_t> tm;
+    std::vector<int> ub;
     tm.reserve(up);
+    ub.reserve(njobs + 1);
     for (int j = 0; j < njobs; ++j) {
+      ub.push_back((int)tm.size());
       const int T = cdiv(jobs[j].n, kTile);
       for (int ti = 0; ti < T; ++ti)
         for (int tj = ti; tj < T; ++tj) tm.push_back(pack_tile(j, ti, tj));
     }
+    ub.push_back((int)tm.size());
     const void* d = nullptr;
     STATUS_TRY(upload_table(h, tm.data(), tm.size() * sizeof(uint32_t), s, &d));
-    tmap = static_cast<const uint32_t*>(d);
+    tl.tmap = static_cast<const uint32_t*>(d);
+    STATUS_TRY(upload_table(h, ub.data(), ub.size() * sizeof(int), s, &d));
+    tl.ubegin = static_cast<const int*>(d);
+    tl.tlist = reinterpret_cast<uint32_t*>(ws + L.tlist);
+    tl.tcount = reinterpret_cast<int*>(ws + L.tcount);
   }
   // full-grid tile map of the warm start's general products
   const uint32_t* fmap = nullptr;
@@ -1153,7 +1187,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     if (warm && warm_aborts == 0)
       fails = 0;  // every warm result was accepted: no cold start
     else
-      STATUS_TRY(newton_phase<float>(h, j32, tmap, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap,
+      STATUS_TRY(newton_phase<float>(h, j32, tl, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap,
                                      prm->poll, SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       int* esc_count = dcount + 2 * kCountRing + 2;
@@ -1181,7 +1215,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
         hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
       }));
     }
-    STATUS_TRY(newton_phase<double>(h, j64, tmap, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
+    STATUS_TRY(newton_phase<double>(h, j64, tl, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
                                     SHAMPOO_KCLASS_NEWTON_F64, nullptr, 0, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);
