@@ -75,12 +75,13 @@ __device__ __forceinline__ void epi_rows(const float* epi, float* dst, int64_t l
 // instantiation, so the plain kernels carry no extra registers).
 template <typename SA, int LA, typename SB, int LB, bool LIM = false>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
-                                                               int nprob, int total_tiles) {
+                                                               int nprob, int total_tiles, int mixed) {
   __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
   __shared__ __attribute__((aligned(16))) float sb0[StageElems<float, LB>::value], sb1[StageElems<float, LB>::value];
   // LIM: work depends on device-side counts and sits in the first logical
   // tiles; dispatch order (round robin over the XCDs) spreads it evenly.
-  const int t = LIM ? (int)blockIdx.x : xcd_remap(blockIdx.x, gridDim.x);
+  // mixed: problems of different sizes, tiles dealt in chunks (deal_chunks).
+  const int t = LIM ? (int)blockIdx.x : (mixed ? deal_chunks(blockIdx.x) : xcd_remap(blockIdx.x, gridDim.x));
   if (t >= total_tiles) return;
   const GemmProblem P = probs[find_problem_gemm(probs, nprob, t)];
   int ti, tj;
@@ -332,13 +333,20 @@ template <typename T>
 __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
                                                                const uint32_t* __restrict__ tlist,
                                                                const int* __restrict__ tcount, int njobs,
-                                                               RootState* __restrict__ st, NewtonStage S) {
+                                                               RootState* __restrict__ st, NewtonStage S,
+                                                               int mixed) {
   __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutK>::value], sa1[StageElems<T, kLayoutK>::value];
   __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
   const int np = S.nprod;
   const int nwork = np * *tcount;
-  if ((int)blockIdx.x >= nwork) return;
-  const int l = xcd_remap(blockIdx.x, nwork);
+  int l;
+  if (mixed) {  // matrices of different sizes: chunks dealt over the XCDs
+    l = deal_chunks(blockIdx.x);
+    if (l >= nwork) return;
+  } else {
+    if ((int)blockIdx.x >= nwork) return;
+    l = xcd_remap(blockIdx.x, nwork);
+  }
   // the products of one tile run in neighbouring workgroups (shared operands)
   const int t = l / np, prod = l - t * np;
   const uint32_t code = tlist[t];

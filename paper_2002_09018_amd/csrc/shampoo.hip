@@ -215,19 +215,23 @@ shampoo_status set_lds(Handle* h, K kernel, int bytes) {
 template <typename SA, int LA, typename SB, int LB, bool LIM = false>
 shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t s, int cls) {
   if (probs.empty()) return SHAMPOO_OK;
-  int total = 0;
+  int total = 0, mixed = 0;
   for (auto& p : probs) {
     p.tiles_n = cdiv(p.N, kTile);
     p.tile_begin = total;
     total += p.sym ? p.tiles_n * (p.tiles_n + 1) / 2 : cdiv(p.M, kTile) * p.tiles_n;
+    mixed |= p.M != probs[0].M || p.N != probs[0].N || p.K != probs[0].K;
   }
+  // problems of different sizes: tiles dealt in chunks over the XCDs (grid
+  // padded to a multiple of 8 chunks); the LIM instantiation keeps dispatch order
+  const int grid = mixed && !LIM ? cdiv(total, 8 * kDealChunk) * 8 * kDealChunk : total;
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
   auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM>;
   const int lds = 0;  // static LDS
   const int np = (int)probs.size();
   STATUS_TRY(launch(h, cls, s, [&] {
-    hipLaunchKernelGGL(k, dim3(total), dim3(kThreads), lds, s, (const GemmProblem*)d, np, total);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, s, (const GemmProblem*)d, np, total, mixed);
   }));
   return SHAMPOO_OK;
 }
@@ -566,6 +570,7 @@ struct TileLists {
   const int* ubegin;
   uint32_t* tlist;
   int* tcount;
+  int mixed;  // matrices of different sizes (tiles dealt in chunks over the XCDs)
 };
 
 // One precision phase of the coupled Newton iteration.
@@ -581,6 +586,11 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
   auto kstage = newton_stage_kernel<T>;
   const bool power = scaling == SHAMPOO_SCALING_POWER4;
   const int nb1 = cdiv(njobs, 64);
+  // grid of a product launch of np products per tile (padded for the
+  // chunked deal of matrices of different sizes)
+  auto pgrid = [&](int np) {
+    return tl.mixed ? cdiv(np * total_up, 8 * kDealChunk) * 8 * kDealChunk : np * total_up;
+  };
   // M0 (and, with the Frobenius scaling, X1 and the residual of M0); the
   // tiles of the matrices that take part in this phase
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -603,7 +613,8 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
     sq1.q[0] = make_prod(kBufS0, kBufS0, kBufNone, kBufS1, 1.0, 0.0, 0.0, 0);
     for (const NewtonStage* S : {&sq0, &sq1}) {
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs, st, *S);
+        hipLaunchKernelGGL(kstage, dim3(pgrid(1)), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs, st, *S,
+                           tl.mixed);
       }));
     }
     const double a = 1.25, b = -0.25;
@@ -634,7 +645,8 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
         f.nprod = 1;
         f.q[0] = make_prod(kBufMc, kBufS1, kBufS0, kBufMn, 1.0, 1.0, 0.0, 1);
         STATUS_TRY(launch(h, cls, s, [&] {
-          hipLaunchKernelGGL(kstage, dim3(total_up), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs, st, f);
+          hipLaunchKernelGGL(kstage, dim3(pgrid(1)), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs, st, f,
+                             tl.mixed);
         }));
         break;  // the iteration's remaining stages are folded into this product
       }
@@ -647,8 +659,8 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
         continue;
       }
       STATUS_TRY(launch(h, cls, s, [&] {
-        hipLaunchKernelGGL(kstage, dim3(S.nprod * total_up), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs,
-                           st, S);
+        hipLaunchKernelGGL(kstage, dim3(pgrid(S.nprod)), dim3(kThreads), lds, s, djobs, tl.tlist, tl.tcount, njobs,
+                           st, S, tl.mixed);
       }));
     }
     const int ring = 2 * (it % kCountRing);
@@ -1075,6 +1087,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     tl.ubegin = static_cast<const int*>(d);
     tl.tlist = reinterpret_cast<uint32_t*>(ws + L.tlist);
     tl.tcount = reinterpret_cast<int*>(ws + L.tcount);
+    for (int j = 1; j < njobs; ++j) tl.mixed |= jobs[j].n != jobs[0].n;
   }
   // full-grid tile map of the warm start's general products
   const uint32_t* fmap = nullptr;

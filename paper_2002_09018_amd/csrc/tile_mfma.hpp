@@ -489,6 +489,18 @@ __device__ __forceinline__ int xcd_remap(int b, int nwg) {
   return x * q + (x < r ? x : r) + s;
 }
 
+// Workgroup id -> logical index for launches whose tiles differ in cost
+// (grouped problems of mixed sizes): chunks of kDealChunk consecutive
+// indices are dealt round-robin over the 8 XCDs, so every XCD gets an even
+// share of the work while its L2 still sees runs of neighbouring tiles.  A
+// bijection on [0, 8 kDealChunk m) for every m: such launches pad their grid
+// to a multiple of 8 kDealChunk, and ids mapped past the work return.
+constexpr int kDealChunk = 8;
+__device__ __forceinline__ int deal_chunks(int b) {
+  const int x = b & 7, s = b >> 3;
+  return ((s / kDealChunk) * 8 + x) * kDealChunk + (s % kDealChunk);
+}
+
 // Index t of the upper-triangular tile list of a T x T tile grid (row-major
 // over ti, tj >= ti) -> (ti, tj).
 __device__ __forceinline__ void unrank_upper(int t, int T, int& ti, int& tj) {
