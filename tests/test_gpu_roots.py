@@ -289,3 +289,23 @@ def test_argument_errors(env):
     assert e.value.code == B.SHAMPOO_ENOMEM
     with pytest.raises(B.ShampooError):
         B.shampoo_inv_root_batched(h, [A], [X], B.shampoo_root_params_default(eps=-1.0), ws, info)
+
+
+def test_early_exit_mixed_sizes_and_precisions(env):
+    """One grouped AUTO call over matrices of different sizes and condition
+    numbers: some stop after a few fp32 iterations, others run on alone (the
+    product launches then cover only the active matrices' tiles), two take
+    the fp64 tail.  Every result agrees with eigh to its band and is bit for
+    bit the result of a call with that matrix alone."""
+    say("roots early exit, mixed sizes and precisions")
+    spec = [(130, 10.0), (512, 1e3), (256, 1e7), (384, 2.0), (64, 1e5), (200, 50.0), (129, 3e3)]
+    As = [spd(n, c, 40 + i) for i, (n, c) in enumerate(spec)]
+    Xs, info = roots(env, As, p=4, eps=0.0)
+    assert sorted(i["precision"] for i in info).count(64) >= 2, info
+    assert len(set(i["iters"] for i in info)) >= 3, info
+    for A, X, inf in zip(As, Xs, info):
+        Xo, _, _ = O.inv_root(A, 4, 0.0)
+        assert inf["status"] in (0, 1), inf
+        assert rel(X, Xo) <= band(O.cond_damped(A, 0.0)), (A.shape, inf, rel(X, Xo))
+        X1, i1 = roots(env, [A], p=4, eps=0.0)
+        assert np.array_equal(X1[0], X) and i1[0] == inf, (A.shape, inf, i1[0])
