@@ -183,6 +183,36 @@ def warm_measure(torch, B, h, As, X0s, prm, ws, ref=None, sample=4):
     return out
 
 
+def time_steps(torch, B, h, step, K, kernel_timing=True):
+    """Times K steps (per-launch HIP events when kernel_timing): elapsed
+    seconds and {kernel class: (ms, launches)}."""
+    B.shampoo_timing_enable(h, kernel_timing)
+    for c in range(len(B.KCLASS_NAMES)):
+        B.shampoo_timing_read(h, c)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(K):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    B.shampoo_timing_enable(h, False)
+    return elapsed, {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
+
+
+def step_report(K, el_f, t_f, el_s, t_s, flops_stats, flops_prec, bytes_graft, bytes_pass2):
+    """Per-kernel rates from the run with separate preconditioning and graft
+    calls (their classes hold exactly those kernels); the whole-step time and
+    phases of the fused run beside it."""
+    return {
+        "phases_ms_per_step": {c: v[0] / K for c, v in t_f.items()},
+        "kernels": {"stats_tflops": flops_stats / (t_s["stats"][0] * 1e-3) / 1e12,
+                    "precond_tflops": flops_prec / (t_s["precond"][0] * 1e-3) / 1e12,
+                    "graft_gbs": bytes_graft / (t_s["graft"][0] * 1e-3) / 1e9,
+                    "fused_graft_pass2_gbs": bytes_pass2 / (t_f["graft"][0] * 1e-3) / 1e9 if t_f["graft"][0] else None},
+        "split_calls_phases_ms_per_step": {c: v[0] / K for c, v in t_s.items()},
+    }
+
+
 def run_c4(args, torch, B):
     """C4: 24 BERT-Large-shaped layers, 288 blocks of 1024 x 1024 (strided
     views of the Q, K, V, O, FFN-in and FFN-out tensors); a step is the
@@ -255,26 +285,23 @@ def run_c4(args, torch, B):
         log(f"warm refresh: {warm['ms']:.1f} ms (cold {cold2_ms:.1f} ms), kept {warm['kept']}")
         del As2, X2
 
-    def step():
+    def step_fused():
+        B.shampoo_update_stats(h, blocks)
+        B.shampoo_precondition_graft(h, blocks, 6e-3)
+
+    def step_split():
         B.shampoo_update_stats(h, blocks)
         B.shampoo_precondition(h, blocks)
         B.shampoo_graft(h, blocks, 6e-3)
 
+    main_step = step_split if args.split_graft else step_fused
     for _ in range(args.warmup):
-        step()
+        main_step()
     torch.cuda.synchronize()
-    B.shampoo_timing_enable(h, True)
-    for c in range(len(B.KCLASS_NAMES)):
-        B.shampoo_timing_read(h, c)
-    t0 = time.perf_counter()
-    for s_ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    B.shampoo_timing_enable(h, False)
-    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
-    B.shampoo_destroy(h)
     K = args.steps
+    elapsed, times = time_steps(torch, B, h, main_step, K)
+    el_s, t_s = time_steps(torch, B, h, step_split, K)
+    B.shampoo_destroy(h)
     flops_stats = K * nb * 2 * d * d * (d + 1)
     flops_prec = K * nb * 4 * d ** 3
     bytes_graft = K * nb * d * d * 28
@@ -287,12 +314,10 @@ def run_c4(args, torch, B):
         "ms_per_step": ms_step, "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
         "dtype": "f32", "data": "synthetic",
         "config": {"workload": "C4: 24 layers x 12 blocks of 1024x1024 (BERT-Large shapes), G ~ N(0,1e-3) fp32, "
-                               "stats L,R + L^-1/4 G R^-1/4 + AdaGrad graft per step", "blocks": nb},
+                               "stats L,R + L^-1/4 G R^-1/4 + AdaGrad graft per step",
+                   "blocks": nb, "graft": "separate calls" if args.split_graft else "fused into preconditioning"},
         "phase_roofline_ms": roof_ms, "frac_of_phase_roofline": roof_ms / ms_step,
-        "phases_ms_per_step": {c: v[0] / K for c, v in times.items()},
-        "kernels": {"stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12,
-                    "precond_tflops": flops_prec / (times["precond"][0] * 1e-3) / 1e12,
-                    "graft_gbs": bytes_graft / (times["graft"][0] * 1e-3) / 1e9},
+        **step_report(K, elapsed, times, el_s, t_s, flops_stats, flops_prec, bytes_graft, K * nb * d * d * 12),
         "root_refresh": {"roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
                          "iters_mean": float(np.mean(iters)),
                          "newton_tflops": prods * d * d * (d + 1) / (root_ms * 1e-3) / 1e12},
@@ -574,26 +599,23 @@ def run_c5(args, torch, B):
                            "alone_newton_tflops": sum((prods[j] + prods64[j]) * sym[j] for j in sel) / (ms_k * 1e-3) / 1e12}
         log(f"  class {k}: {len(sel)} roots alone in {ms_k:.2f} ms")
 
-    def step():
+    def step_fused():
+        B.shampoo_update_stats(h, blocks)
+        B.shampoo_precondition_graft(h, blocks, 1e-2)
+
+    def step_split():
         B.shampoo_update_stats(h, blocks)
         B.shampoo_precondition(h, blocks)
         B.shampoo_graft(h, blocks, 1e-2)
 
+    main_step = step_split if args.split_graft else step_fused
     for _ in range(args.warmup):
-        step()
+        main_step()
     torch.cuda.synchronize()
-    B.shampoo_timing_enable(h, True)
-    for c in range(len(B.KCLASS_NAMES)):
-        B.shampoo_timing_read(h, c)
-    t0 = time.perf_counter()
-    for s_ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    B.shampoo_timing_enable(h, False)
-    times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
-    B.shampoo_destroy(h)
     K = args.steps
+    elapsed, times = time_steps(torch, B, h, main_step, K)
+    el_s, t_s = time_steps(torch, B, h, step_split, K)
+    B.shampoo_destroy(h)
     flops_stats = K * sum(m * (m + 1) * n + n * (n + 1) * m for m, n in shp)
     flops_prec = K * sum(2 * m * m * n + 2 * m * n * n for m, n in shp)
     bytes_graft = K * sum(m * n for m, n in shp) * 26     # bf16 G: 2 + 3 * 4 B pass 1, 3 * 4 B pass 2
@@ -609,12 +631,11 @@ def run_c5(args, torch, B):
                                "{128,256,512,1024,2048}; G ~ N(0,1e-3) stored bf16; 10 stats steps; p=4, "
                                "eps 1e-6" + (f"; embedding gradient row-sparse, {args.emb_lookups} Zipf(1.1) "
                                              "lookups/step; damping eps * lambda_max" if sparse else ""),
-                   "blocks": nb, "factors": len(As), "emb_lookups": args.emb_lookups},
+                   "blocks": nb, "factors": len(As), "emb_lookups": args.emb_lookups,
+                   "graft": "separate calls" if args.split_graft else "fused into preconditioning"},
         "phase_roofline_ms": roof_ms, "frac_of_phase_roofline": roof_ms / ms_step,
-        "phases_ms_per_step": {c: v[0] / K for c, v in times.items()},
-        "kernels": {"stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12,
-                    "precond_tflops": flops_prec / (times["precond"][0] * 1e-3) / 1e12,
-                    "graft_gbs": bytes_graft / (times["graft"][0] * 1e-3) / 1e9},
+        **step_report(K, elapsed, times, el_s, t_s, flops_stats, flops_prec, bytes_graft,
+                      K * sum(m * n for m, n in shp) * 12),
         "grouped_roots": {
             "roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
             "newton_ms": ms_newton, "root_aux_ms": rt["root_aux"][0],
@@ -710,6 +731,9 @@ def main():
                     help="c5: row-sparse embedding gradient from this many Zipf lookups per step (0: dense)")
     ap.add_argument("--lookups", type=int, default=65536, help="c6: lookups per step")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--split-graft", action="store_true",
+                    help="c2, c4, c5: separate preconditioning and graft calls instead of the fused "
+                         "shampoo_precondition_graft")
     ap.add_argument("--no-warm", action="store_true",
                     help="c2, c4: skip the warm-start roots measured after the timed steps")
     ap.add_argument("--no-kernel-timing", action="store_true",
@@ -771,13 +795,16 @@ def main():
     info = torch.zeros(8 * nb, dtype=torch.int32, device=dev)
     infos = []
 
-    def step(record):
+    def step(record, split=args.split_graft):
         B.shampoo_update_stats(h, blocks)
         B.shampoo_inv_root_batched(h, Ls, Lrs, prm, ws, info)
         if record:
             infos.append(info.clone())
-        B.shampoo_precondition(h, blocks)
-        B.shampoo_graft(h, blocks, eta0)
+        if split:
+            B.shampoo_precondition(h, blocks)
+            B.shampoo_graft(h, blocks, eta0)
+        else:  # graft pass 1 runs in the preconditioning GEMM's epilogue
+            B.shampoo_precondition_graft(h, blocks, eta0)
 
     for w in range(args.warmup):
         step(False)
@@ -795,8 +822,11 @@ def main():
     elapsed = time.perf_counter() - t0
     B.shampoo_timing_enable(h, False)
     times = {B.KCLASS_NAMES[c]: B.shampoo_timing_read(h, c) for c in range(len(B.KCLASS_NAMES))}
-
-    # The same roots under the other scaling, for comparison (roots call only).
+    # The same steps with separate preconditioning and graft calls: the
+    # statistics + preconditioning half of the metric and the per-kernel
+    # rates (the fused call's preconditioning time also carries graft pass 1).
+    el_s, t_s = time_steps(torch, B, h, lambda: step(False, True), args.steps)
+    log("split-call steps done")
     other = B.SCALING_FROBENIUS if scaling == B.SCALING_POWER4 else B.SCALING_POWER4
     other_ms, other_iters = None, None
     if not args.no_compare_scaling:
@@ -856,7 +886,7 @@ def main():
     ms_newton, launches_newton = times["newton_f32"]
     achieved = flops_newton32 / (ms_newton * 1e-3) / 1e12 if ms_newton > 0 else 0.0
     ms_step = elapsed * 1e3 / args.steps
-    stats_prec_ms = (times["stats"][0] + times["precond"][0]) / args.steps
+    stats_prec_ms = (t_s["stats"][0] + t_s["precond"][0]) / args.steps
     out = {
         "metric": METRIC,
         "value": nb * args.steps / elapsed,
@@ -873,7 +903,8 @@ def main():
         "config": {"workload": "C2 step: 96 blocks, L 1024x1024 (Wishart, 19x4096 dof) + G 1024x4096 "
                                "N(0,1/4096); stats + 96 inverse 4th roots (grouped coupled Newton, eps 1e-6, "
                                "tol 1e-6, AUTO precision) + L^-1/4 G + AdaGrad graft",
-                   "blocks": nb, "n": n, "k": k, "p": p, "eps": eps, "root_scaling": args.scaling},
+                   "blocks": nb, "n": n, "k": k, "p": p, "eps": eps, "root_scaling": args.scaling,
+                   "graft": "separate calls" if args.split_graft else "fused into preconditioning"},
         "roofline": {
             "kernel": "newton_stage_kernel<float> (grouped fp32-MFMA Newton products)",
             "bound": "mfma", "achieved": achieved, "peak": PEAK_F32_MFMA, "unit": "TFLOP/s",
@@ -891,10 +922,13 @@ def main():
         "fp32_mfma_util": achieved / PEAK_F32_MFMA,
         "phases_ms_per_step": {c: v[0] / args.steps for c, v in times.items()},
         "launches_per_step": {c: v[1] / args.steps for c, v in times.items()},
+        "split_calls_phases_ms_per_step": {c: v[0] / args.steps for c, v in t_s.items()},
         "kernels": {
-            "stats_tflops": flops_stats / (times["stats"][0] * 1e-3) / 1e12 if times["stats"][0] else None,
-            "precond_tflops": flops_prec / (times["precond"][0] * 1e-3) / 1e12 if times["precond"][0] else None,
-            "graft_gbs": graft_bytes / (times["graft"][0] * 1e-3) / 1e9 if times["graft"][0] else None,
+            "stats_tflops": flops_stats / (t_s["stats"][0] * 1e-3) / 1e12 if t_s["stats"][0] else None,
+            "precond_tflops": flops_prec / (t_s["precond"][0] * 1e-3) / 1e12 if t_s["precond"][0] else None,
+            "graft_gbs": graft_bytes / (t_s["graft"][0] * 1e-3) / 1e9 if t_s["graft"][0] else None,
+            "fused_graft_pass2_gbs": (args.steps * nb * n * k * 12 / (times["graft"][0] * 1e-3) / 1e9
+                                      if times["graft"][0] and not args.split_graft else None),
             "newton_f64_tflops": (flops_newton64 / (times["newton_f64"][0] * 1e-3) / 1e12
                                   if times["newton_f64"][0] else None),
         },

@@ -262,6 +262,24 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
                              float eta0, float beta1, int use_shampoo, float* norms, void* stream);
 
 /*
+ * Preconditioning and the AdaGrad-grafted update in one call: the same
+ * result as shampoo_precondition followed by shampoo_graft with beta1 = 0 and
+ * use_shampoo = 1 (Preliminaries, Shampoo update rule; Algorithm 2 with the
+ * graft of "Layer wise learning rates"):
+ *   P = Lr G Rr;  D = D + G o G;
+ *   eta = eta0 ||D^(-1/2) o G||_F / ||P||_F  (0 when ||P||_F == 0);  W = W - eta P
+ * The GEMM that writes each block's P also updates D and sums the two squared
+ * norms per output tile, so G, D and P are not read by a separate pass; the
+ * norms are then reduced per block in a fixed order (deterministic, but in
+ * another order than shampoo_graft's, so eta may differ in the last bits).
+ * Every block needs W, D, P and at least one root; G: g_dtype.  norms:
+ * as shampoo_graft.  Errors: as shampoo_graft, and EINVAL for a block with
+ * both roots NULL.
+ */
+shampoo_status shampoo_precondition_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                          float eta0, float* norms, void* stream);
+
+/*
  * Grafted update with the LARS/LAMB layer-wise magnitude of the same appendix
  * paragraph ("Layer wise learning rates": learning rate ||W||_F / ||G||_F per
  * layer, applied per block here): the step is eta0 ||W||_F long, W taken

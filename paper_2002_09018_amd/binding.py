@@ -74,6 +74,7 @@ _sig = {
     "shampoo_precondition": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _vp]),
     "shampoo_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
     "shampoo_graft_lamb": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
+    "shampoo_precondition_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _vp, _vp]),
     "shampoo_embedding_workspace_bytes": (_sz, [_i, _i]),
     "shampoo_embedding_rows": (_i, [_vp, _vp, _vp, _vp, _i, _i64, _vp, _i, _i, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
     "shampoo_embedding_stats": (_i, [_vp, _vp, _vp, _i, _i, _vp, _f, _vp, _sz, _vp]),
@@ -263,6 +264,12 @@ def shampoo_embedding_graft(handle, rows, count, U, P, W, D, eta0, use_shampoo=T
     _check(handle, _lib.shampoo_embedding_graft(handle, _ptr(rows), _ptr(count), nnz, dim, _ptr(U), _ptr(P),
                                                 _ptr(W), _ptr(D), int(W.shape[0]), int(W.stride(0)), float(eta0),
                                                 int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+
+
+def shampoo_precondition_graft(handle, blocks, eta0, norms=None, stream=None):
+    arr = _blocks(blocks)
+    _check(handle, _lib.shampoo_precondition_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
+                                                   _ptr(norms), _stream(stream)))
 
 
 def shampoo_graft_lamb(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):

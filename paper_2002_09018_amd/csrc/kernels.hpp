@@ -5,6 +5,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "tile_mfma.hpp"
 
 #ifndef SHP_EPI_VEC
@@ -14,6 +16,49 @@
 namespace shp {
 
 typedef float f4v __attribute__((ext_vector_type(4)));
+
+// Sum over the workgroup (fixed order: waves, then the per-wave partials).
+__device__ __forceinline__ double block_sum(double v, double* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+#pragma unroll
+  for (int w = 0; w < kThreads / 64; ++w) s += red[w];
+  return s;
+}
+
+template <typename SG>
+__device__ __forceinline__ float load_g(const void* G, int64_t i) {
+  return cvt<float, SG>(reinterpret_cast<const SG*>(G)[i]);
+}
+
+// D^{-1/2} o G with 0 where D == 0.
+__device__ __forceinline__ float ada_dir(float g, float d) { return d > 0.f ? g / sqrtf(d) : 0.f; }
+
+// Element access of the graft passes: 4 consecutive elements of a row.
+template <typename SG>
+struct G4;
+template <>
+struct G4<float> {
+  static __device__ __forceinline__ void load(const void* G, int64_t i, float g[4]) {
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const f4 v = gload<f4>(reinterpret_cast<const float*>(G) + i);
+    g[0] = v[0]; g[1] = v[1]; g[2] = v[2]; g[3] = v[3];
+  }
+};
+template <>
+struct G4<uint16_t> {
+  static __device__ __forceinline__ void load(const void* G, int64_t i, float g[4]) {
+    typedef uint16_t u4 __attribute__((ext_vector_type(4)));
+    const u4 v = gload<u4>(reinterpret_cast<const uint16_t*>(G) + i);
+    g[0] = cvt<float, uint16_t>(v[0]); g[1] = cvt<float, uint16_t>(v[1]);
+    g[2] = cvt<float, uint16_t>(v[2]); g[3] = cvt<float, uint16_t>(v[3]);
+  }
+};
+
 
 // ============================================================================
 // Grouped GEMM for statistics and preconditioning.
@@ -45,6 +90,16 @@ struct GemmProblem {
   const int* kcount;
   const int* mcount;
   int koff, ksplit;
+  // Graft pass 1 fused into the preconditioning GEMM that writes P (graft
+  // instantiation, gD != NULL): for every output element (r, c),
+  // D = D + G o G, and per output tile the sums of (D^{-1/2} o G)^2 and P^2
+  // into gpart[2 (part_base + tile)] and gpart[2 (part_base + tile) + 1].
+  // G and D are the block's views (row stride ldg, the same as P's).
+  const void* gG;
+  float* gD;
+  int64_t ldg;
+  double* gpart;
+  int part_base;
 };
 
 __device__ __forceinline__ int find_problem_gemm(const GemmProblem* probs, int nprob, int t) {
@@ -73,7 +128,9 @@ __device__ __forceinline__ void epi_rows(const float* epi, float* dst, int64_t l
 
 // LIM: honour the device-side limits kcount / mcount (a separate
 // instantiation, so the plain kernels carry no extra registers).
-template <typename SA, int LA, typename SB, int LB, bool LIM = false>
+// SGG (not void): element type of G for the fused graft pass 1 (problems
+// with gD set; a separate instantiation as well).
+template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
                                                                int nprob, int total_tiles, int mixed) {
   __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
@@ -134,6 +191,87 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   const bool helper = diag && wave == 2;
   const int wm0 = m0 + (helper ? 0 : (wave >> 1) * kWaveTile), wn0 = n0 + (helper ? kWaveTile : (wave & 1) * kWaveTile);
   typedef Mfma<float> F;
+  if constexpr (!std::is_same<SGG, void>::value) {
+    // plain outputs only (preconditioning); P.gD set: P with the fused graft
+    // pass 1, else a plain store (the intermediate G Rr of two-sided blocks)
+    const bool graft = P.gD != nullptr;
+    {
+      __shared__ double gred[kThreads / 64];
+      float smg = 0.f, sps = 0.f;
+      const bool vec = m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 && (P.ldg & 3) == 0 &&
+                       (reinterpret_cast<uintptr_t>(P.C) & 15) == 0 && (reinterpret_cast<uintptr_t>(P.gD) & 15) == 0 &&
+                       (reinterpret_cast<uintptr_t>(P.gG) & (4 * sizeof(SGG) - 1)) == 0;
+      const bool rows16 = m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
+                          (reinterpret_cast<uintptr_t>(P.C) & 15) == 0;
+      // a block row of the wave's accumulators goes through the wave's own
+      // LDS slice; the graft work then walks it row by row (rolled loops,
+      // so the epilogue keeps the main loop's register budget)
+      float* epi = reinterpret_cast<float*>(wave == 0 ? sa0 : (wave == 1 ? sa1 : (wave == 2 ? sb0 : sb1)));
+#pragma unroll
+      for (int i = 0; i < WaveAcc<float>::NB; ++i) {
+#pragma unroll
+        for (int j = 0; j < WaveAcc<float>::NB; ++j)
+#pragma unroll
+          for (int v = 0; v < F::kAcc; ++v)
+            epi[F::row(lane, v) * kWaveTile + j * F::kM + F::col(lane)] = P.alpha * acc.c[i][j][v];
+        const int r0 = wm0 + i * F::kM;
+        if (!graft && rows16) {
+          epi_rows(epi, P.C + (int64_t)r0 * P.ldc + wn0, P.ldc, lane);
+        } else if (!graft) {
+#pragma unroll 1
+          for (int idx = lane; idx < F::kM * kWaveTile; idx += 64) {
+            const int r = r0 + idx / kWaveTile, c = wn0 + idx % kWaveTile;
+            if (r < P.M && c < P.N) gstore<float>(P.C + (int64_t)r * P.ldc + c, epi[idx]);
+          }
+        } else if (vec) {
+          constexpr int kSeg = kWaveTile / 4;
+#pragma unroll 1
+          for (int k = 0; k < F::kM * kSeg / 64; ++k) {
+            const int idx = lane + 64 * k, rr = idx / kSeg, c4 = (idx % kSeg) * 4;
+            const f4v pv = *reinterpret_cast<const f4v*>(epi + rr * kWaveTile + c4);
+            const int64_t gi = (int64_t)(r0 + rr) * P.ldg + wn0 + c4;
+            gstore<f4v>(P.C + (int64_t)(r0 + rr) * P.ldc + wn0 + c4, pv);
+            float g[4];
+            G4<SGG>::load(P.gG, gi, g);
+            f4v d = gload<f4v>(P.gD + gi);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              d[e] += g[e] * g[e];
+              const float u = ada_dir(g[e], d[e]);
+              smg += u * u;
+              sps += pv[e] * pv[e];
+            }
+            gstore<f4v>(P.gD + gi, d);
+          }
+        } else {
+#pragma unroll 1
+          for (int idx = lane; idx < F::kM * kWaveTile; idx += 64) {
+            const int rr = idx / kWaveTile, cc = idx % kWaveTile;
+            const int r = r0 + rr, c = wn0 + cc;
+            if (r >= P.M || c >= P.N) continue;
+            const float x = epi[rr * kWaveTile + cc];
+            gstore<float>(P.C + (int64_t)r * P.ldc + c, x);
+            const int64_t gi = (int64_t)r * P.ldg + c;
+            const float g = load_g<SGG>(P.gG, gi);
+            const float d = gload<float>(P.gD + gi) + g * g;
+            gstore<float>(P.gD + gi, d);
+            const float u = ada_dir(g, d);
+            smg += u * u;
+            sps += x * x;
+          }
+        }
+      }
+      if (graft) {
+        const double a = block_sum((double)smg, gred);
+        const double b = block_sum((double)sps, gred);
+        if (threadIdx.x == 0) {
+          P.gpart[2 * (P.part_base + lt) + 0] = a;
+          P.gpart[2 * (P.part_base + lt) + 1] = b;
+        }
+      }
+      return;
+    }
+  }
 #if SHP_EPI_VEC
   // Symmetric output, off-diagonal full tile: mirrored values go out as
   // 16-byte stores (a lane's 4 consecutive rows are 4 consecutive columns of
@@ -676,18 +814,6 @@ __global__ void root_warm_finish_kernel(RootState* __restrict__ st, int njobs, i
 // fp64 arithmetic, one workgroup per matrix, v0 = ones, Rayleigh quotient,
 // relative stop.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ double block_sum(double v, double* red) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __syncthreads();
-  if (lane == 0) red[wave] = v;
-  __syncthreads();
-  double s = 0.0;
-#pragma unroll
-  for (int w = 0; w < kThreads / 64; ++w) s += red[w];
-  return s;
-}
-
 // MaxSV, one power step over all matrices, in two launches.  Tile pass:
 // workgroup (matrix, ti, tj) stages tile A[ti, tj] in LDS and writes its
 // row partials (A vh)_rows and column partials (A^T vh)_cols.  Reduce pass
@@ -1481,6 +1607,11 @@ struct GraftBlock {
   const int* count;
   int64_t ldw;
   int64_t wlimit;  // rows of the W/D tensor (a wrows entry outside is skipped)
+  // pass 2 reduces the block's norm partials partial[2 (part_begin + q)],
+  // q < nparts: pass 1's chunks, or the preconditioning GEMM's output tiles
+  // when pass 1 is fused into it
+  int part_begin;
+  int nparts;
 };
 
 __device__ __forceinline__ int find_block_graft(const GraftBlock* b, int nb, int t) {
@@ -1492,34 +1623,6 @@ __device__ __forceinline__ int find_block_graft(const GraftBlock* b, int nb, int
   return lo;
 }
 
-template <typename SG>
-__device__ __forceinline__ float load_g(const void* G, int64_t i) {
-  return cvt<float, SG>(reinterpret_cast<const SG*>(G)[i]);
-}
-
-// D^{-1/2} o G with 0 where D == 0.
-__device__ __forceinline__ float ada_dir(float g, float d) { return d > 0.f ? g / sqrtf(d) : 0.f; }
-
-// Element access of the graft passes: 4 consecutive elements of a row.
-template <typename SG>
-struct G4;
-template <>
-struct G4<float> {
-  static __device__ __forceinline__ void load(const void* G, int64_t i, float g[4]) {
-    typedef float f4 __attribute__((ext_vector_type(4)));
-    const f4 v = gload<f4>(reinterpret_cast<const float*>(G) + i);
-    g[0] = v[0]; g[1] = v[1]; g[2] = v[2]; g[3] = v[3];
-  }
-};
-template <>
-struct G4<uint16_t> {
-  static __device__ __forceinline__ void load(const void* G, int64_t i, float g[4]) {
-    typedef uint16_t u4 __attribute__((ext_vector_type(4)));
-    const u4 v = gload<u4>(reinterpret_cast<const uint16_t*>(G) + i);
-    g[0] = cvt<float, uint16_t>(v[0]); g[1] = cvt<float, uint16_t>(v[1]);
-    g[2] = cvt<float, uint16_t>(v[2]); g[3] = cvt<float, uint16_t>(v[3]);
-  }
-};
 // Calls f(ig, iw, w) for the elements of a chunk (rows r0..r1 of a block):
 // ig is the offset in G and P, iw the offset in W, D, Mg and Ps; 4-wide
 // (w = 4) where the block allows vector access, else scalar (w = 1).  Whole
@@ -1650,9 +1753,9 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
   // the block's norms from its chunk partials, reduced cooperatively in a
   // fixed order (every workgroup of the block gets the same bits)
   double smg = 0.0, sps = 0.0;
-  for (int q = threadIdx.x; q < B.nchunks; q += kThreads) {
-    smg += partial[2 * (B.chunk_begin + q) + 0];
-    sps += partial[2 * (B.chunk_begin + q) + 1];
+  for (int q = threadIdx.x; q < B.nparts; q += kThreads) {
+    smg += partial[2 * (B.part_begin + q) + 0];
+    sps += partial[2 * (B.part_begin + q) + 1];
   }
   smg = block_sum(smg, red);
   sps = block_sum(sps, red);

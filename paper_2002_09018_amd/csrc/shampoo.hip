@@ -212,7 +212,7 @@ shampoo_status set_lds(Handle* h, K kernel, int bytes) {
 }
 
 // ---------------------------------------------------------------- GEMM
-template <typename SA, int LA, typename SB, int LB, bool LIM = false>
+template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void>
 shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t s, int cls) {
   if (probs.empty()) return SHAMPOO_OK;
   int total = 0, mixed = 0;
@@ -227,7 +227,7 @@ shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t 
   const int grid = mixed && !LIM ? cdiv(total, 8 * kDealChunk) * 8 * kDealChunk : total;
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
-  auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM>;
+  auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM, SGG>;
   const int lds = 0;  // static LDS
   const int np = (int)probs.size();
   STATUS_TRY(launch(h, cls, s, [&] {
@@ -307,6 +307,8 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
     g.vec4 = al && a16(b.W) && a16(b.D) && a16(b.P) && a16(b.Mg) && a16(b.Ps) &&
              (reinterpret_cast<uintptr_t>(b.G) & 15) == 0;
     g.chunk_begin = t;
+    g.part_begin = t;
+    g.nparts = g.nchunks;
     t += g.nchunks;
     v.push_back(g);
   }
@@ -314,10 +316,32 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
   return v;
 }
 
+// fuse_graft: the GEMM that writes a block's P also runs graft pass 1 on it
+// (D += G o G and the norm partials of every output tile into h->partial),
+// and graft pass 2 follows (AdaGrad graft, beta1 = 0, Shampoo direction);
+// every block must have a root.
 template <typename SG>
-shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipStream_t s) {
+shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipStream_t s, bool fuse_graft = false,
+                            float eta0 = 0.f, float* norms = nullptr) {
   const int ve = 16 / (int)sizeof(SG);
   std::vector<GemmProblem> g_rr, lr_z, lr_g;
+  // graft: per block, the first and the number of norm partials (the P
+  // GEMM's output tiles)
+  std::vector<int> pbegin(nb), pcount(nb);
+  int ptotal = 0;
+  if (fuse_graft) {
+    for (int i = 0; i < nb; ++i) {
+      pbegin[i] = ptotal;
+      pcount[i] = cdiv(blocks[i].rows, kTile) * cdiv(blocks[i].cols, kTile);
+      ptotal += pcount[i];
+    }
+    STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)std::max(ptotal, 1) * 2 * sizeof(double)));
+  }
+  double* gpart = static_cast<double*>(h->partial);
+  auto with_graft = [&](GemmProblem& q, const shampoo_block& b, int i) {
+    if (!fuse_graft) return;
+    q.gG = b.G; q.gD = b.D; q.ldg = b.ld; q.gpart = gpart; q.part_base = pbegin[i];
+  };
   std::vector<shampoo_block> copy;
   size_t zbytes = 0;
   for (int i = 0; i < nb; ++i) {
@@ -345,6 +369,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       q.B = Z; q.ldb = b.cols; q.b_rows = b.rows; q.b_cols = b.cols; q.b_aligned = (b.cols % 4) == 0;
       q.C = b.P; q.ldc = b.ld; q.M = b.rows; q.N = b.cols; q.K = b.rows;
       q.alpha = 1.f; q.beta = 0.f;
+      with_graft(q, b, i);
       lr_z.push_back(q);
     } else if (b.Rr) {
       GemmProblem p{};  // P = G Rr
@@ -353,6 +378,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       p.b_aligned = aligned16(b.Rr) && (b.cols % 4) == 0;
       p.C = b.P; p.ldc = b.ld; p.M = b.rows; p.N = b.cols; p.K = b.cols;
       p.alpha = 1.f; p.beta = 0.f;
+      with_graft(p, b, i);
       g_rr.push_back(p);
     } else if (b.Lr) {
       GemmProblem q{};  // P = Lr G
@@ -361,10 +387,31 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       q.B = b.G; q.ldb = b.ld; q.b_rows = b.rows; q.b_cols = b.cols; q.b_aligned = gal;
       q.C = b.P; q.ldc = b.ld; q.M = b.rows; q.N = b.cols; q.K = b.rows;
       q.alpha = 1.f; q.beta = 0.f;
+      with_graft(q, b, i);
       lr_g.push_back(q);
     } else {
       copy.push_back(b);
     }
+  }
+  if (fuse_graft) {
+    STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK, false, SG>(h, g_rr, s, SHAMPOO_KCLASS_PRECOND)));
+    STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK, false, SG>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
+    STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK, false, SG>(h, lr_g, s, SHAMPOO_KCLASS_PRECOND)));
+    // graft pass 2 over the row chunks of every block, with the GEMM's
+    // per-tile norm partials
+    int total = 0;
+    std::vector<GraftBlock> tb = graft_table(blocks, nb, &total);
+    for (int i = 0; i < nb; ++i) {
+      tb[i].part_begin = pbegin[i];
+      tb[i].nparts = pcount[i];
+    }
+    const void* d = nullptr;
+    STATUS_TRY(upload_table(h, tb.data(), tb.size() * sizeof(GraftBlock), s, &d));
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
+      hipLaunchKernelGGL((graft_pass2_kernel<SG, false>), dim3(total), dim3(kThreads), 0, s, (const GraftBlock*)d, nb,
+                         total, eta0, 0.f, 1, (const double*)gpart, norms);
+    }));
+    return tables_done(h, s);
   }
   STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK>(h, g_rr, s, SHAMPOO_KCLASS_PRECOND)));
   STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
@@ -992,6 +1039,25 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
   return graft_entry(handle, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, norms, stream, false);
 }
 
+shampoo_status shampoo_precondition_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                         float eta0, float* norms, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
+  if (!isfinite(eta0)) return fail(h, SHAMPOO_EINVAL, "eta0 is not finite");
+  for (int i = 0; i < nblocks; ++i) {
+    const shampoo_block& b = blocks[i];
+    if (!b.P || !b.W || !b.D) return fail(h, SHAMPOO_EINVAL, "block %d: P, W or D is NULL", i);
+    if (!b.Lr && !b.Rr) return fail(h, SHAMPOO_EINVAL, "block %d: no root (use shampoo_graft)", i);
+  }
+  if (nblocks == 0) return SHAMPOO_OK;
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (g_dtype == SHAMPOO_BF16) return precond_impl<uint16_t>(h, blocks, nblocks, s, true, eta0, norms);
+  return precond_impl<float>(h, blocks, nblocks, s, true, eta0, norms);
+}
+
 shampoo_status shampoo_graft_lamb(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
                                   float beta1, int use_shampoo, float* norms, void* stream) {
   return graft_entry(handle, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, norms, stream, true);
@@ -1459,6 +1525,8 @@ shampoo_status shampoo_embedding_graft(void* handle, const int32_t* rows, const 
   b.rows_per_chunk = std::max(1, 16384 / dim);
   b.nchunks = cdiv(nnz, b.rows_per_chunk);
   b.chunk_begin = 0;
+  b.part_begin = 0;
+  b.nparts = b.nchunks;
   b.vec4 = (dim % 4) == 0 && (ldw % 4) == 0 && aligned16(U) && aligned16(W) && aligned16(D) &&
            (!b.P || aligned16(b.P));
   const int total = b.nchunks;
