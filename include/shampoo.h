@@ -239,7 +239,8 @@ shampoo_status shampoo_inv_root_warm_batched(void* handle, const shampoo_root_jo
  * Preconditioned gradient P = Lr G Rr (Preliminaries, Shampoo update rule;
  * one-sided forms of Lemma 1 when a root is NULL; P = G when both are).
  * Lr and Rr must be symmetric (inverse roots are).  G: g_dtype.
- * Errors: as shampoo_update_stats; P must be non-NULL.
+ * Errors: as shampoo_update_stats; EINVAL when P is NULL or is the same
+ * buffer as G, Lr or Rr.
  */
 shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, int nblocks,
                                     int g_dtype, void* stream);
@@ -274,7 +275,8 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
  * another order than shampoo_graft's, so eta may differ in the last bits).
  * Every block needs W, D, P and at least one root; G: g_dtype.  norms:
  * as shampoo_graft.  Errors: as shampoo_graft, and EINVAL for a block with
- * both roots NULL.
+ * both roots NULL, or whose P, W, D are not distinct or coincide with G or a
+ * root.
  */
 shampoo_status shampoo_precondition_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
                                           float eta0, float* norms, void* stream);

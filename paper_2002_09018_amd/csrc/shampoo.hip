@@ -1025,8 +1025,13 @@ shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, i
   if (!h) return SHAMPOO_EINVAL;
   h->err.clear();
   STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
-  for (int i = 0; i < nblocks; ++i)
-    if (!blocks[i].P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
+  for (int i = 0; i < nblocks; ++i) {
+    const shampoo_block& b = blocks[i];
+    if (!b.P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
+    // the GEMMs read G and the roots while other workgroups write P
+    if (b.P == b.G || (const float*)b.P == b.Lr || (const float*)b.P == b.Rr)
+      return fail(h, SHAMPOO_EINVAL, "block %d: P aliases G or a root", i);
+  }
   if (nblocks == 0) return SHAMPOO_OK;
   DeviceGuard g(h->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -1050,6 +1055,12 @@ shampoo_status shampoo_precondition_graft(void* handle, const shampoo_block* blo
     const shampoo_block& b = blocks[i];
     if (!b.P || !b.W || !b.D) return fail(h, SHAMPOO_EINVAL, "block %d: P, W or D is NULL", i);
     if (!b.Lr && !b.Rr) return fail(h, SHAMPOO_EINVAL, "block %d: no root (use shampoo_graft)", i);
+    const void* outs[3] = {b.P, b.W, b.D};
+    for (const void* o : outs)
+      if (o == b.G || o == (const void*)b.Lr || o == (const void*)b.Rr)
+        return fail(h, SHAMPOO_EINVAL, "block %d: P, W or D aliases G or a root", i);
+    if (b.P == b.W || b.P == b.D || b.W == b.D)
+      return fail(h, SHAMPOO_EINVAL, "block %d: P, W and D must be distinct", i);
   }
   if (nblocks == 0) return SHAMPOO_OK;
   DeviceGuard g(h->device);

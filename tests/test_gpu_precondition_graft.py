@@ -123,3 +123,18 @@ def test_fused_rejects_rootless_block(env):
     with pytest.raises(B.ShampooError) as e:
         B.shampoo_precondition_graft(h, [B.Block(G=x, W=x.clone(), D=x.clone(), P=x.clone())], 0.05)
     assert e.value.code == B.SHAMPOO_EINVAL
+
+
+def test_aliasing_is_rejected(env):
+    torch, B, dev, h = env
+    x = torch.zeros(8, 8, device=dev)
+    r = torch.eye(8, device=dev)
+    for kw in (dict(G=x, P=x, Lr=r), dict(G=x, P=r, Lr=r)):
+        with pytest.raises(B.ShampooError) as e:
+            B.shampoo_precondition(h, [B.Block(**kw)])
+        assert e.value.code == B.SHAMPOO_EINVAL
+    W, D, P = (torch.zeros(8, 8, device=dev) for _ in range(3))
+    for kw in (dict(G=x, W=W, D=D, P=x, Lr=r), dict(G=x, W=W, D=W, P=P, Lr=r), dict(G=x, W=W, D=D, P=P, Lr=P)):
+        with pytest.raises(B.ShampooError) as e:
+            B.shampoo_precondition_graft(h, [B.Block(**kw)], 0.05)
+        assert e.value.code == B.SHAMPOO_EINVAL
