@@ -167,9 +167,9 @@ void shampoo_root_params_default(shampoo_root_params* params);
  * For every block with non-NULL L (resp. R).  L and R stay exactly symmetric:
  * the upper triangle is computed and mirrored.  The ridge eps*I is not added
  * here; shampoo_inv_root_batched adds it once.  G: g_dtype.
- * Errors: EINVAL for nblocks < 0, NULL blocks with nblocks > 0, a block with
- * both L and R NULL is skipped, sizes outside [1, 4096], ld < cols, beta2
- * outside (0, 1].
+ * Errors: EINVAL for nblocks < 0, NULL blocks with nblocks > 0, sizes
+ * outside [1, 4096], ld < cols, beta2 outside (0, 1], L, R and G not
+ * distinct buffers (a block with both L and R NULL is skipped).
  */
 shampoo_status shampoo_update_stats(void* handle, const shampoo_block* blocks, int nblocks,
                                     int g_dtype, float beta2, void* stream);
@@ -257,7 +257,8 @@ shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, i
  * With beta1 == 0, Mg and Ps are not stored (may be NULL) and P is used as Ps.
  * norms (device, may be NULL): per block {||Mg||_F, ||Ps||_F, eta} as 3 floats.
  * Errors: EINVAL as above, non-finite eta0, beta1 outside [0, 1), NULL
- * W/D, P NULL with use_shampoo, Mg/Ps NULL with beta1 > 0.
+ * W/D, P NULL with use_shampoo, Mg/Ps NULL with beta1 > 0, and an updated
+ * state (W, D, Mg, Ps) that is the same buffer as G, P or another state.
  */
 shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
                              float eta0, float beta1, int use_shampoo, float* norms, void* stream);

@@ -920,6 +920,17 @@ shampoo_status graft_entry(void* handle, const shampoo_block* blocks, int nblock
     if (use_shampoo && !b.P) return fail(h, SHAMPOO_EINVAL, "block %d: P is NULL", i);
     if (beta1 > 0.f && (!b.Mg || (use_shampoo && !b.Ps)))
       return fail(h, SHAMPOO_EINVAL, "block %d: Mg/Ps needed when beta1 > 0", i);
+    // the states written (W, D, and Mg, Ps with momentum) are distinct from
+    // each other and from the inputs G and P
+    const void* outs[4] = {b.W, lamb ? nullptr : b.D, beta1 > 0.f ? b.Mg : nullptr,
+                           beta1 > 0.f && use_shampoo ? b.Ps : nullptr};
+    for (int a = 0; a < 4; ++a) {
+      if (!outs[a]) continue;
+      if (outs[a] == b.G || (use_shampoo && outs[a] == b.P))
+        return fail(h, SHAMPOO_EINVAL, "block %d: an updated state aliases G or P", i);
+      for (int c = a + 1; c < 4; ++c)
+        if (outs[a] == outs[c]) return fail(h, SHAMPOO_EINVAL, "block %d: updated states alias", i);
+    }
   }
   if (nblocks == 0) return SHAMPOO_OK;
   DeviceGuard g(h->device);
@@ -1012,6 +1023,11 @@ shampoo_status shampoo_update_stats(void* handle, const shampoo_block* blocks, i
   h->err.clear();
   STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
   if (!(beta2 > 0.f && beta2 <= 1.f)) return fail(h, SHAMPOO_EINVAL, "beta2 %g outside (0, 1]", (double)beta2);
+  for (int i = 0; i < nblocks; ++i) {
+    const shampoo_block& b = blocks[i];
+    if ((b.L && (b.L == b.G || b.L == b.R)) || (b.R && b.R == b.G))
+      return fail(h, SHAMPOO_EINVAL, "block %d: L, R and G must be distinct", i);
+  }
   if (nblocks == 0) return SHAMPOO_OK;
   DeviceGuard g(h->device);
   hipStream_t s = static_cast<hipStream_t>(stream);

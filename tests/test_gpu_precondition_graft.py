@@ -138,3 +138,15 @@ def test_aliasing_is_rejected(env):
         with pytest.raises(B.ShampooError) as e:
             B.shampoo_precondition_graft(h, [B.Block(**kw)], 0.05)
         assert e.value.code == B.SHAMPOO_EINVAL
+
+
+def test_aliasing_in_stats_and_graft_is_rejected(env):
+    torch, B, dev, h = env
+    x = torch.zeros(8, 8, device=dev)
+    W, D, P = (torch.zeros(8, 8, device=dev) for _ in range(3))
+    with pytest.raises(B.ShampooError):
+        B.shampoo_update_stats(h, [B.Block(G=x, L=x)])
+    for kw in (dict(G=x, W=x, D=D, P=P), dict(G=x, W=W, D=P, P=P), dict(G=x, W=W, D=W, P=P)):
+        with pytest.raises(B.ShampooError) as e:
+            B.shampoo_graft(h, [B.Block(**kw)], 0.05)
+        assert e.value.code == B.SHAMPOO_EINVAL
