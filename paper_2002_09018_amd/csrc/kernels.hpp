@@ -827,9 +827,13 @@ __global__ void root_warm_finish_kernel(RootState* __restrict__ st, int njobs, i
 template <typename T>
 __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
                                                              const RootState* __restrict__ st, int total_full) {
-  __shared__ float tile[kTile * (kTile + 1)];
+  // the tile is staged in two halves of 64 rows (33 KB of LDS, so four
+  // workgroups share a CU and hide each other's loads)
+  constexpr int kHalf = kTile / 2;
+  __shared__ float tile[kHalf * (kTile + 1)];
   __shared__ double vr[kTile], vc[kTile];       // v on the tile's rows and columns
-  __shared__ double half_sum[2][kTile];
+  __shared__ double rsum[4][kHalf];             // row partials of a half, by column quarter
+  __shared__ double csum[2][kTile];             // column partials, by row half of a half
   const int t = blockIdx.x;
   if (t >= total_full) return;
   const int j = find_job_full(jobs, njobs, t);
@@ -848,48 +852,68 @@ __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>
     vc[i] = c0 + i < n ? vh[c0 + i] : 0.0;
     vr[i] = r0 + i < n ? vh[r0 + i] : 0.0;
   }
-  if ((n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n && (reinterpret_cast<uintptr_t>(A) & 15) == 0) {
-    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
-      const int r = e >> 5, c = (e & 31) * 4;
-      const f4v v = gload<f4v>(A + (int64_t)(r0 + r) * n + c0 + c);
-      float* d = tile + r * (kTile + 1) + c;
-      d[0] = v[0]; d[1] = v[1]; d[2] = v[2]; d[3] = v[3];
+  const bool vec = (n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n && (reinterpret_cast<uintptr_t>(A) & 15) == 0;
+  const int rq = threadIdx.x & (kHalf - 1), quarter = threadIdx.x >> 6;  // row dots: 4 column quarters
+  const int cq = threadIdx.x & (kTile - 1), rh = threadIdx.x >> 7;       // column dots: 2 row halves
+  double cacc = 0.0;
+  for (int h = 0; h < 2; ++h) {
+    const int hr0 = r0 + h * kHalf;
+    __syncthreads();  // the previous half's tile has been read
+    if (vec) {
+      for (int e = threadIdx.x; e < kHalf * kTile / 4; e += kThreads) {
+        const int r = e >> 5, c = (e & 31) * 4;
+        const f4v v = gload<f4v>(A + (int64_t)(hr0 + r) * n + c0 + c);
+        float* d = tile + r * (kTile + 1) + c;
+        d[0] = v[0]; d[1] = v[1]; d[2] = v[2]; d[3] = v[3];
+      }
+    } else {
+      for (int e = threadIdx.x; e < kHalf * kTile; e += kThreads) {
+        const int r = e >> 7, c = e & 127;
+        tile[r * (kTile + 1) + c] = (hr0 + r < n && c0 + c < n) ? A[(int64_t)(hr0 + r) * n + c0 + c] : 0.f;
+      }
     }
-  } else {
-    for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-      const int r = e >> 7, c = e & 127;
-      tile[r * (kTile + 1) + c] = (r0 + r < n && c0 + c < n) ? A[(int64_t)(r0 + r) * n + c0 + c] : 0.f;
-    }
+    __syncthreads();
+    // (A v) on the half's rows, each dot product over four column quarters
+    double racc = 0.0;
+#pragma unroll 8
+    for (int c = quarter * 32; c < quarter * 32 + 32; ++c) racc += (double)tile[rq * (kTile + 1) + c] * vc[c];
+    rsum[quarter][rq] = racc;
+    // (A^T v) on the tile's columns, accumulated over both halves
+#pragma unroll 8
+    for (int r = rh * 32; r < rh * 32 + 32; ++r) cacc += (double)tile[r * (kTile + 1) + cq] * vr[h * kHalf + r];
+    __syncthreads();
+    if (threadIdx.x < kHalf && hr0 + threadIdx.x < n)
+      prow[(int64_t)tj * n + hr0 + threadIdx.x] =
+          rsum[0][threadIdx.x] + rsum[1][threadIdx.x] + rsum[2][threadIdx.x] + rsum[3][threadIdx.x];
   }
+  csum[rh][cq] = cacc;
   __syncthreads();
-  // (A v) on the tile's rows and (A^T v) on its columns, each dot product
-  // split over the two halves of the workgroup
-  const int qi = threadIdx.x & 127, hf = threadIdx.x >> 7;
-  {
-    double acc = 0.0;
-    for (int c = hf * 64; c < hf * 64 + 64; ++c) acc += (double)tile[qi * (kTile + 1) + c] * vc[c];
-    half_sum[hf][qi] = acc;
-  }
-  __syncthreads();
-  if (hf == 0 && r0 + qi < n) prow[(int64_t)tj * n + r0 + qi] = half_sum[0][qi] + half_sum[1][qi];
-  __syncthreads();
-  {
-    double acc = 0.0;
-    for (int r = hf * 64; r < hf * 64 + 64; ++r) acc += (double)tile[r * (kTile + 1) + qi] * vr[r];
-    half_sum[hf][qi] = acc;
-  }
-  __syncthreads();
-  if (hf == 0 && c0 + qi < n) pcol[(int64_t)ti * n + c0 + qi] = half_sum[0][qi] + half_sum[1][qi];
+  if (threadIdx.x < kTile && c0 + threadIdx.x < n)
+    pcol[(int64_t)ti * n + c0 + threadIdx.x] = csum[0][threadIdx.x] + csum[1][threadIdx.x];
 }
 
 // MaxSV reduction, one workgroup per matrix: v = (A v + A^T v) / 2 from the
 // tile partials (fixed order), lambda = vh . v, vh = v / ||v||.  The kernel
 // boundary after the tile pass makes every partial visible.
+constexpr int kSvThreads = 1024;  // threads of the MaxSV reduction (one workgroup per matrix)
+
+__device__ __forceinline__ double sv_block_sum(double v, double* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  double s = 0.0;
+#pragma unroll
+  for (int w = 0; w < kSvThreads / 64; ++w) s += red[w];
+  return s;
+}
+
 template <typename T>
-__global__ __launch_bounds__(kThreads) void maxsv_reduce_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                               RootState* __restrict__ st, double tol, double eps,
-                                                               int last_step) {
-  __shared__ double red[kThreads / 64];
+__global__ __launch_bounds__(kSvThreads) void maxsv_reduce_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                                 RootState* __restrict__ st, double tol, double eps,
+                                                                 int last_step) {
+  __shared__ double red[kSvThreads / 64];
   const int j = blockIdx.x;
   if (j >= njobs || st[j].status != kActive || st[j].sv_done) return;
   const NewtonJob<T>* J = jobs + j;
@@ -898,7 +922,7 @@ __global__ __launch_bounds__(kThreads) void maxsv_reduce_kernel(const NewtonJob<
   double* prow = J->vec + n;
   double* pcol = J->vec + n + (int64_t)TN * n;
   double q = 0.0, s2 = 0.0;
-  for (int i = threadIdx.x; i < n; i += kThreads) {
+  for (int i = threadIdx.x; i < n; i += kSvThreads) {
     double a = 0.0, b = 0.0;
     for (int k = 0; k < TN; ++k) {
       a += prow[(int64_t)k * n + i];
@@ -909,10 +933,10 @@ __global__ __launch_bounds__(kThreads) void maxsv_reduce_kernel(const NewtonJob<
     s2 += v * v;
     prow[i] = v;  // row partials of tile column 0 are consumed: reuse as v
   }
-  const double lam = block_sum(q, red);
-  const double nrm = sqrt(block_sum(s2, red));
+  const double lam = sv_block_sum(q, red);
+  const double nrm = sqrt(sv_block_sum(s2, red));
   const double lam_old = st[j].lam_max;
-  for (int i = threadIdx.x; i < n; i += kThreads) vh[i] = nrm > 0.0 ? prow[i] / nrm : 0.0;
+  for (int i = threadIdx.x; i < n; i += kSvThreads) vh[i] = nrm > 0.0 ? prow[i] / nrm : 0.0;
   if (threadIdx.x == 0) {
     st[j].lam_max = lam;
     st[j].eps_eff = eps * lam;

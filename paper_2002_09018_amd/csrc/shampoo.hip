@@ -1219,12 +1219,12 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
         if (j32) {
           hipLaunchKernelGGL(maxsv_step_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs,
                              (const RootState*)st, full);
-          hipLaunchKernelGGL(maxsv_reduce_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, njobs, st, mtol,
+          hipLaunchKernelGGL(maxsv_reduce_kernel<float>, dim3(njobs), dim3(kSvThreads), 0, s, j32, njobs, st, mtol,
                              eps, last);
         } else {
           hipLaunchKernelGGL(maxsv_step_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs,
                              (const RootState*)st, full);
-          hipLaunchKernelGGL(maxsv_reduce_kernel<double>, dim3(njobs), dim3(kThreads), 0, s, j64, njobs, st, mtol,
+          hipLaunchKernelGGL(maxsv_reduce_kernel<double>, dim3(njobs), dim3(kSvThreads), 0, s, j64, njobs, st, mtol,
                              eps, last);
         }
       }));
