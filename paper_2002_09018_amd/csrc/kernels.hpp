@@ -462,6 +462,47 @@ __host__ __device__ __forceinline__ uint32_t pack_tile(int j, int ti, int tj) {
   return ((uint32_t)j << 10) | ((uint32_t)ti << 5) | (uint32_t)tj;
 }
 
+// Compact list of the tiles of the matrices still active, in job order:
+// tlist[0, *tcount).  tmap holds every tile of a launch (job-major: the
+// upper tiles of the symmetric products, or the full grid of the warm
+// start's) and ubegin[j] the first of job j (ubegin[njobs] = their number).  Called by one
+// whole workgroup; st must be final for every job (the caller's threads have
+// passed a barrier since they last wrote it).
+__device__ __forceinline__ void build_tile_list(const RootState* __restrict__ st, int njobs,
+                                                const uint32_t* __restrict__ tmap, const int* __restrict__ ubegin,
+                                                uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
+  __shared__ int scan[kThreads];
+  __shared__ int base;
+  if (threadIdx.x == 0) base = 0;
+  __syncthreads();
+  for (int j0 = 0; j0 < njobs; j0 += kThreads) {
+    const int j = j0 + (int)threadIdx.x;
+    const int b = j < njobs ? ubegin[j] : 0;
+    const int n = (j < njobs && st[j].status == kActive) ? ubegin[j + 1] - b : 0;
+    scan[threadIdx.x] = n;
+    __syncthreads();
+    for (int o = 1; o < kThreads; o <<= 1) {  // inclusive scan
+      const int v = (int)threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
+      __syncthreads();
+      scan[threadIdx.x] += v;
+      __syncthreads();
+    }
+    const int off = base + scan[threadIdx.x] - n;
+    for (int k = 0; k < n; ++k) tlist[off + k] = tmap[b + k];
+    __syncthreads();
+    if (threadIdx.x == 0) base += scan[kThreads - 1];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) *tcount = base;
+}
+
+__global__ __launch_bounds__(kThreads) void tile_list_kernel(const RootState* __restrict__ st, int njobs,
+                                                            const uint32_t* __restrict__ tmap,
+                                                            const int* __restrict__ ubegin,
+                                                            uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
+  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
+}
+
 // tlist / tcount: the compact upper-tile list of the matrices still active
 // (build_tile_list); the grid is sized for every upper tile, and the
 // workgroups past S.nprod * *tcount return at once.  The workgroup -> tile
@@ -606,18 +647,27 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
 // the storage column), the right one k-major.  dst == kBufNone stores
 // nothing (the commutator only needs its largest entry); q.amax adds max|C|
 // to a monitor slot, q.resid max|C - I| to the residual.
+// tlist / tcount / mixed: as newton_stage_kernel, over the full tile grid.
 template <typename T>
 __global__ __launch_bounds__(kThreads, kMinWaves) void newton_dense_kernel(const NewtonJob<T>* __restrict__ jobs,
-                                                                          const uint32_t* __restrict__ tmap,
+                                                                          const uint32_t* __restrict__ tlist,
+                                                                          const int* __restrict__ tcount,
                                                                           int njobs, RootState* __restrict__ st,
-                                                                          int total_full, NewtonStage S) {
+                                                                          NewtonStage S, int mixed) {
   __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutRow>::value], sa1[StageElems<T, kLayoutRow>::value];
   __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
   const int np = S.nprod;
-  const int l = xcd_remap(blockIdx.x, gridDim.x);
-  if (l >= np * total_full) return;
+  const int nwork = np * *tcount;
+  int l;
+  if (mixed) {
+    l = deal_chunks(blockIdx.x);
+    if (l >= nwork) return;
+  } else {
+    if ((int)blockIdx.x >= nwork) return;
+    l = xcd_remap(blockIdx.x, nwork);
+  }
   const int t = l / np, prod = l - t * np;
-  const uint32_t code = tmap[t];
+  const uint32_t code = tlist[t];
   const int j = (int)(code >> 10), ti = (int)((code >> 5) & 31), tj = (int)(code & 31);
   if (j >= njobs || st[j].status != kActive) return;
   const NewtonJob<T>* J = jobs + j;
@@ -724,7 +774,11 @@ __global__ __launch_bounds__(kThreads) void warm_init_kernel(const NewtonJob<T>*
 //   init != 0: residual of M0 = X0^p A_d only.
 __global__ __launch_bounds__(kThreads) void root_warm_update_kernel(RootState* __restrict__ st, int njobs, int init,
                                                                    float tol, float comm_tol, int max_iters,
-                                                                   int* __restrict__ count) {
+                                                                   int* __restrict__ count,
+                                                                   const uint32_t* __restrict__ tmap,
+                                                                   const int* __restrict__ ubegin,
+                                                                   uint32_t* __restrict__ tlist,
+                                                                   int* __restrict__ tcount) {
   __shared__ int red[2 * (kThreads / 64)];
   int active = 0, aborted = 0;
   for (int j = threadIdx.x; j < njobs; j += kThreads) {
@@ -778,6 +832,8 @@ __global__ __launch_bounds__(kThreads) void root_warm_update_kernel(RootState* _
     count[0] = sa;
     count[1] = sf;
   }
+  // the next iteration's tiles (full grid) of the matrices still in the phase
+  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
 }
 
 // End of the warm phase: records its outcome (warm_out, device int32
@@ -1348,46 +1404,6 @@ __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob
   }
   rmax = wave_max(rmax);
   if ((threadIdx.x & 63) == 0 && rmax > 0.f) atomicMax(&st[j].resid_bits, __float_as_uint(rmax));
-}
-
-// Compact list of the upper tiles of the matrices still active, in job
-// order: tlist[0, *tcount).  tmap holds every upper tile (job-major) and
-// ubegin[j] the first of job j (ubegin[njobs] = their number).  Called by one
-// whole workgroup; st must be final for every job (the caller's threads have
-// passed a barrier since they last wrote it).
-__device__ __forceinline__ void build_tile_list(const RootState* __restrict__ st, int njobs,
-                                                const uint32_t* __restrict__ tmap, const int* __restrict__ ubegin,
-                                                uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
-  __shared__ int scan[kThreads];
-  __shared__ int base;
-  if (threadIdx.x == 0) base = 0;
-  __syncthreads();
-  for (int j0 = 0; j0 < njobs; j0 += kThreads) {
-    const int j = j0 + (int)threadIdx.x;
-    const int b = j < njobs ? ubegin[j] : 0;
-    const int n = (j < njobs && st[j].status == kActive) ? ubegin[j + 1] - b : 0;
-    scan[threadIdx.x] = n;
-    __syncthreads();
-    for (int o = 1; o < kThreads; o <<= 1) {  // inclusive scan
-      const int v = (int)threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
-      __syncthreads();
-      scan[threadIdx.x] += v;
-      __syncthreads();
-    }
-    const int off = base + scan[threadIdx.x] - n;
-    for (int k = 0; k < n; ++k) tlist[off + k] = tmap[b + k];
-    __syncthreads();
-    if (threadIdx.x == 0) base += scan[kThreads - 1];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) *tcount = base;
-}
-
-__global__ __launch_bounds__(kThreads) void tile_list_kernel(const RootState* __restrict__ st, int njobs,
-                                                            const uint32_t* __restrict__ tmap,
-                                                            const int* __restrict__ ubegin,
-                                                            uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
-  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
 }
 
 // Resets the state of the matrices that take part in a phase.

@@ -452,7 +452,7 @@ shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float 
 
 // ---------------------------------------------------------------- roots
 struct RootLayout {
-  size_t state = 0, counts = 0, tlist = 0, tcount = 0, total = 0;
+  size_t state = 0, counts = 0, tlist = 0, tcount = 0, tlistf = 0, tcountf = 0, total = 0;
   std::vector<size_t> part, vec, f32, f64;  // per job offsets
 };
 
@@ -464,14 +464,20 @@ RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
   L.counts = off;
   off += align256(kCountInts * sizeof(int));
   // compact tile list of the product launches (one entry per upper tile)
-  size_t up = 0;
+  size_t up = 0, full = 0;
   for (int j = 0; j < njobs; ++j) {
     const size_t T = (size_t)cdiv(jobs[j].n, kTile);
     up += T * (T + 1) / 2;
+    full += T * T;
   }
   L.tlist = off;
   off += align256(up * sizeof(uint32_t));
   L.tcount = off;
+  off += 256;
+  // and of the warm start's full-grid products
+  L.tlistf = off;
+  off += align256(full * sizeof(uint32_t));
+  L.tcountf = off;
   off += 256;
   for (int j = 0; j < njobs; ++j) {
     const size_t n = (size_t)jobs[j].n;
@@ -743,18 +749,21 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
 // number of matrices handed to the cold start when the polled counts showed
 // the phase finished, else leaves it untouched.
 template <typename T>
-shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t* fmap, int njobs, RootState* st,
+shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const TileLists& tf, int njobs, RootState* st,
                           int* dcount, int total_full, const NewtonProgram& prog, int p, float tol, float comm_tol,
                           int cap, int poll, int cls, int32_t* warm_out, hipStream_t s, int* aborted_out) {
   auto kdense = newton_dense_kernel<T>;
   auto run = [&](const NewtonStage& S) {
+    const int np = S.nprod;
+    const int grid = tf.mixed ? cdiv(np * total_full, 8 * kDealChunk) * 8 * kDealChunk : np * total_full;
     return launch(h, cls, s, [&] {
-      hipLaunchKernelGGL(kdense, dim3(S.nprod * total_full), dim3(kThreads), 0, s, djobs, fmap, njobs, st,
-                         total_full, S);
+      hipLaunchKernelGGL(kdense, dim3(grid), dim3(kThreads), 0, s, djobs, tf.tlist, tf.tcount, njobs, st, S, tf.mixed);
     });
   };
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(warm_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full);
+    hipLaunchKernelGGL(tile_list_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, tf.tmap, tf.ubegin, tf.tlist,
+                       tf.tcount);
   }));
   int top = 0;
   while ((p >> (top + 1)) != 0) ++top;
@@ -778,7 +787,7 @@ shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t* 
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_warm_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, comm_tol, cap,
-                       dcount + 2 * kCountRing);
+                       dcount + 2 * kCountRing, tf.tmap, tf.ubegin, tf.tlist, tf.tcount);
   }));
   // the iteration's program with the monitor reductions: max|X| on the X
   // product, max|M| on the product that writes the next M
@@ -801,7 +810,7 @@ shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const uint32_t* 
     int* slot = dcount + ring;
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_warm_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, comm_tol, cap,
-                         slot);
+                         slot, tf.tmap, tf.ubegin, tf.tlist, tf.tcount);
     }));
     if (poll) {
       HIP_TRY(h, hipMemcpyAsync(h->pinned + ring, slot, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
@@ -1182,19 +1191,28 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     tl.tcount = reinterpret_cast<int*>(ws + L.tcount);
     for (int j = 1; j < njobs; ++j) tl.mixed |= jobs[j].n != jobs[0].n;
   }
-  // full-grid tile map of the warm start's general products
-  const uint32_t* fmap = nullptr;
+  // full-grid tiles of the warm start's general products
+  TileLists tf{};
   if (warm) {
     std::vector<uint32_t> tm;
+    std::vector<int> fb;
     tm.reserve(full);
+    fb.reserve(njobs + 1);
     for (int j = 0; j < njobs; ++j) {
+      fb.push_back((int)tm.size());
       const int T = cdiv(jobs[j].n, kTile);
       for (int ti = 0; ti < T; ++ti)
         for (int tj = 0; tj < T; ++tj) tm.push_back(pack_tile(j, ti, tj));
     }
+    fb.push_back((int)tm.size());
     const void* d = nullptr;
     STATUS_TRY(upload_table(h, tm.data(), tm.size() * sizeof(uint32_t), s, &d));
-    fmap = static_cast<const uint32_t*>(d);
+    tf.tmap = static_cast<const uint32_t*>(d);
+    STATUS_TRY(upload_table(h, fb.data(), fb.size() * sizeof(int), s, &d));
+    tf.ubegin = static_cast<const int*>(d);
+    tf.tlist = reinterpret_cast<uint32_t*>(ws + L.tlistf);
+    tf.tcount = reinterpret_cast<int*>(ws + L.tcountf);
+    tf.mixed = tl.mixed;
   }
   const int nb1 = cdiv(njobs, 64);
   const int tail_all = prec == SHAMPOO_PRECISION_FP64 ? 1 : 0;
@@ -1244,10 +1262,10 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
   int warm_aborts = -1;
   if (warm) {
     if (j32)
-      STATUS_TRY(warm_phase<float>(h, j32, fmap, njobs, st, dcount, full, prog, p, prm->tol, comm_tol, prm->max_iters,
+      STATUS_TRY(warm_phase<float>(h, j32, tf, njobs, st, dcount, full, prog, p, prm->tol, comm_tol, prm->max_iters,
                                    prm->poll, SHAMPOO_KCLASS_NEWTON_WARM, warm_out, s, &warm_aborts));
     else
-      STATUS_TRY(warm_phase<double>(h, j64, fmap, njobs, st, dcount, full, prog, p, prm->tol, comm_tol,
+      STATUS_TRY(warm_phase<double>(h, j64, tf, njobs, st, dcount, full, prog, p, prm->tol, comm_tol,
                                     prm->max_iters, prm->poll, SHAMPOO_KCLASS_NEWTON_WARM, warm_out, s, &warm_aborts));
   }
   if (tail_all) {
