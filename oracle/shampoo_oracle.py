@@ -60,6 +60,22 @@ Functions and what pins them (tests under ``tests/test_oracle_*.py``):
   rates" (AdaGrad magnitude, Shampoo direction).  Pinned by the step-norm
   identity ||dW||_F = eta0 ||D^{-1/2} o G||_F and the t=1 closed form
   eta0 * sqrt(nnz(G)).
+* ``cond_damped``       -- condition number of the damped matrix, which picks
+  the tolerance band of a root comparison (Section 3.2: the loss of
+  precision grows with the condition number).  Pinned by the closed form
+  (max d + eps_eff) / (min d + eps_eff) on rotated diagonal inputs, with
+  absolute and relative damping, and infinity for an indefinite input.
+* ``shampoo_step``      -- one step of Algorithm 2 for a block.  Pinned as a
+  whole, independently of its parts: statistics by loops, the direction from
+  one eigendecomposition of the Kronecker product of the damped statistics
+  (the full-matrix form of the Preliminaries), the AdaGrad magnitude from the
+  explicit sum of squares (t=1: eta0 sqrt(nnz(G))), stale roots between
+  refreshes, the one-sided form, the fallback before the first roots and
+  momentum unrolled from M_0 = P_0 = 0.
+* ``bf16_bits_to_f64``  -- exact decode of bfloat16 inputs.  Pinned on all
+  65536 bit patterns against the binary32 layout (sign, 8-bit exponent with
+  bias 127, 7 fraction bits) and on fixed values (1, -2, the smallest
+  subnormal, the largest finite value, +-inf, -0).
 
 Readings of the paper where it is silent or ambiguous (each is listed in the
 design notes of the repository as well):

@@ -53,11 +53,6 @@ def f32_to_bf16_bits(x):
     return (rounded >> np.uint32(16)).astype(np.uint16)
 
 
-def bf16_bits_to_f32(bits):
-    """Exact decode of bfloat16 bit patterns to fp32."""
-    return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
-
-
 # ---------------------------------------------------------------- C1
 def c1_weight(seed=0, n=128):
     return gaussian((n, n), 1.0, C1, seed, 0, 0)

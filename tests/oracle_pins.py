@@ -301,6 +301,32 @@ def pin_root_asymmetric_input(o):
     assert _relf(X1, X0) < 1e-13
 
 
+def pin_cond_damped(o):
+    """Condition number of the damped matrix A + eps_eff I: for a rotated
+    diagonal d it is (max d + eps_eff) / (min d + eps_eff), with eps_eff = eps
+    (absolute) or eps * max d (relative, MaxSV of an isolated top eigenvalue);
+    an indefinite damped matrix has no finite condition number."""
+    r = rng(18)
+    Q, _ = np.linalg.qr(r.standard_normal((9, 9)))
+    d = np.array([1e-6, 3e-5, 0.01, 0.2, 0.5, 0.9, 1.0, 1.3, 40.0])
+    A = (Q * d) @ Q.T
+    for eps in (0.0, 1e-6, 1e-3):
+        want = (d.max() + eps) / (d.min() + eps)
+        assert abs(o.cond_damped(A, eps) - want) < 1e-6 * want
+    for eps in (1e-6, 1e-8):
+        e = eps * d.max()
+        want = (d.max() + e) / (d.min() + e)
+        assert abs(o.cond_damped(A, eps, eps_relative=True) - want) < 1e-6 * want
+        # the lambda_max the GPU reports may be passed in instead of MaxSV's
+        assert abs(o.cond_damped(A, eps, eps_relative=True, lam_max=2.0 * d.max())
+                   - (d.max() + 2 * e) / (d.min() + 2 * e)) < 1e-6 * want
+    # a slightly asymmetric input: condition of its symmetric part
+    S = r.standard_normal((9, 9))
+    want = (d.max() + 1e-3) / (d.min() + 1e-3)
+    assert abs(o.cond_damped(A + 1e-7 * (S - S.T), 1e-3) - want) < 1e-6 * want
+    assert o.cond_damped(np.diag([1.0, 2.0, -0.5]), 0.1) == np.inf
+
+
 # ------------------------------------------------------------------ MaxSV
 def pin_maxsv(o):
     """Power iteration converges to the top eigenvalue when it is isolated."""
@@ -609,6 +635,118 @@ def pin_tensor_precondition_kronecker(o):
     M = r.standard_normal((3, 5))
     A, B = r.standard_normal((3, 3)), r.standard_normal((5, 5))
     assert np.allclose(o.tensor_precondition(M, [A, B]), A @ M @ B.T, rtol=1e-12, atol=1e-12)
+
+
+
+# ------------------------------------------------------------------ whole step (Algorithm 2)
+def _stats_loops(Gs, m, n):
+    """L_t = sum_s G_s G_s^T and R_t = sum_s G_s^T G_s by pure-Python loops."""
+    L = [[sum(float(G[i, k]) * float(G[j, k]) for G in Gs for k in range(n)) for j in range(m)] for i in range(m)]
+    R = [[sum(float(G[k, i]) * float(G[k, j]) for G in Gs for k in range(m)) for j in range(n)] for i in range(n)]
+    return np.array(L), np.array(R)
+
+
+def _kron_root_apply(Ld, Rd, G, p):
+    """(Ld (x) Rd)^{-1/p} vec(G) from one eigendecomposition of the mn x mn
+    Kronecker product (row-stacking vec): the full-matrix preconditioner of
+    the Preliminaries, of which L^{-1/p} G R^{-1/p} is the factored form."""
+    w, V = np.linalg.eigh(np.kron(Ld, Rd))
+    return ((V * w ** (-1.0 / p)) @ V.T @ G.reshape(-1)).reshape(G.shape)
+
+
+def pin_shampoo_step_kronecker(o):
+    """Three steps of Algorithm 2 (beta1 = 0, beta2 = 1) on a non-square and
+    a square block, against an independent route: statistics by loops, the
+    direction from one eigh of the mn x mn Kronecker product of the damped
+    statistics, the AdaGrad magnitude from the explicit sum of squares.
+    Step 2 keeps step 1's roots (no refresh), step 3 refreshes them.  The
+    step is eta0 ||D_t^{-1/2} o G_t||_F long along -dir / ||dir||; at t = 1
+    D^{-1/2} o G = sign(G), so its length is eta0 sqrt(nnz(G))."""
+    eps, p, eta0 = 1e-3, 4, 0.1
+    for seed, (m, n) in ((60, (3, 2)), (61, (3, 3))):
+        r = rng(seed)
+        Gs = [r.standard_normal((m, n)) for _ in range(3)]
+        W0 = r.standard_normal((m, n))
+        s = dict(W=W0.copy(), D=np.zeros((m, n)), L=np.zeros((m, m)), R=np.zeros((n, n)))
+        W = W0.copy()
+        Ld = Rd = None
+        for t, refresh in ((1, True), (2, False), (3, True)):
+            G = Gs[t - 1]
+            s = o.shampoo_step(s, G, p=p, eps=eps, eta0=eta0, refresh_roots=refresh)
+            if refresh:
+                L, R = _stats_loops(Gs[:t], m, n)
+                Ld, Rd = L + eps * np.eye(m), R + eps * np.eye(n)
+            dirn = _kron_root_apply(Ld, Rd, G, p)
+            Dt = sum(g * g for g in Gs[:t])
+            mag = eta0 * np.linalg.norm(G / np.sqrt(Dt))
+            if t == 1:
+                assert abs(mag - eta0 * np.sqrt(m * n)) < 1e-12
+            W = W - mag * dirn / np.linalg.norm(dirn)
+            assert _relf(s['W'], W) < 1e-10, (m, n, t)
+            assert _relf(s['D'], Dt) < 1e-14
+
+
+def pin_shampoo_step_variants(o):
+    """The step's other branches against the same independent routes:
+    the AdaGrad fallback before the first roots (W -= eta0 M_t, at t = 1
+    eta0 sign(G)); a one-sided block (right side not tracked: the Kronecker
+    factor on that side is the identity); and heavy-ball momentum beta1 =
+    1/2 over two steps, unrolled from M_0 = P_0 = 0 as Algorithm 2 states."""
+    eps, p = 1e-3, 4
+    r = rng(62)
+    G1, G2, W0 = r.standard_normal((3, 4)), r.standard_normal((3, 4)), r.standard_normal((3, 4))
+    s0 = dict(W=W0, D=np.zeros((3, 4)), L=np.zeros((3, 3)), R=np.zeros((4, 4)))
+    s = o.shampoo_step(s0, G1, p=p, eps=eps, eta0=0.2, use_shampoo=False)
+    assert _relf(s['W'], W0 - 0.2 * np.sign(G1)) < 1e-15
+    # one-sided
+    s = o.shampoo_step(dict(W=W0, D=np.zeros((3, 4)), L=np.zeros((3, 3))), G1, p=p, eps=eps, eta0=0.2,
+                       right=False)
+    L, _ = _stats_loops([G1], 3, 4)
+    dirn = _kron_root_apply(L + eps * np.eye(3), np.eye(4), G1, p)
+    assert _relf(s['W'], W0 - 0.2 * np.sqrt(12) * dirn / np.linalg.norm(dirn)) < 1e-10
+    assert s.get('R') is None and s.get('Rr') is None
+    # momentum
+    b1 = 0.5
+    s = dict(W=W0, D=np.zeros((3, 4)), L=np.zeros((3, 3)), R=np.zeros((4, 4)), Mg=np.zeros((3, 4)),
+             Ps=np.zeros((3, 4)))
+    M, P, W = np.zeros((3, 4)), np.zeros((3, 4)), W0.copy()
+    for t, G in ((1, G1), (2, G2)):
+        s = o.shampoo_step(s, G, p=p, eps=eps, eta0=0.2, beta1=b1)
+        L, R = _stats_loops([G1, G2][:t], 3, 4)
+        Dt = sum(g * g for g in [G1, G2][:t])
+        M = b1 * M + (1 - b1) * G / np.sqrt(Dt)
+        P = b1 * P + (1 - b1) * _kron_root_apply(L + eps * np.eye(3), R + eps * np.eye(4), G, p)
+        W = W - 0.2 * np.linalg.norm(M) / np.linalg.norm(P) * P
+        assert _relf(s['W'], W) < 1e-10, t
+
+
+# ------------------------------------------------------------------ bf16 inputs
+def pin_bf16_decode(o):
+    """bfloat16 is the top half of an IEEE binary32: sign, 8 exponent bits
+    (bias 127), 7 fraction bits.  Every one of the 65536 patterns against
+    that definition evaluated with exact integer scaling (math.ldexp), plus
+    fixed values: 0x3F80 = 1, 0xC000 = -2, 0x4049 = 3.140625, 0x0001 =
+    2^-133 (smallest subnormal), 0x7F7F = (2 - 2^-7) 2^127 (largest finite),
+    0x7F80 / 0xFF80 = +-inf, 0x8000 = -0."""
+    import math
+    bits = np.arange(65536, dtype=np.uint32).astype(np.uint16)
+    with np.errstate(invalid="ignore"):      # NaN patterns
+        got = o.bf16_bits_to_f64(bits)
+    assert got.dtype == np.float64
+    for b in range(65536):
+        sgn = -1.0 if b >> 15 else 1.0
+        e, f = (b >> 7) & 0xFF, b & 0x7F
+        v = got[b]
+        if e == 0xFF:
+            assert (np.isinf(v) and np.sign(v) == sgn) if f == 0 else np.isnan(v), hex(b)
+            continue
+        want = sgn * (math.ldexp(f, -133) if e == 0 else math.ldexp(128 + f, e - 134))
+        assert v == want and math.copysign(1.0, v) == sgn, hex(b)
+    fixed = {0x3F80: 1.0, 0xC000: -2.0, 0x4049: 3.140625, 0x0001: 2.0 ** -133,
+             0x7F7F: (2.0 - 2.0 ** -7) * 2.0 ** 127, 0x7F80: np.inf, 0xFF80: -np.inf}
+    for b, v in fixed.items():
+        assert got[b] == v, hex(b)
+    assert got[0x8000] == 0.0 and math.copysign(1.0, got[0x8000]) == -1.0
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith('pin_')]

@@ -65,7 +65,7 @@ def test_c5_full_grouped():
             picks.append(32 + [s[0] for s in shp[32:]].index(k))
         for b in picks:
             m, n = shp[b]
-            Gs = [cfg.bf16_bits_to_f32(cfg.c5_grad_bf16(b, t, (m, n))) for t in range(1, STEPS + 1)]
+            Gs = [O.bf16_bits_to_f64(cfg.c5_grad_bf16(b, t, (m, n))) for t in range(1, STEPS + 1)]
             Lo, Ro = np.zeros((m, m)), np.zeros((n, n))
             for g in Gs:
                 Lo, Ro = O.stats_update(Lo, Ro, g)

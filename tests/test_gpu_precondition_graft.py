@@ -33,7 +33,7 @@ def _case(torch, dev, m, n, sides, pad, seed, bf16=False):
     r = np.random.default_rng(seed)
     if bf16:
         bits = cfg.c5_grad_bf16(seed, 1, (m, n))
-        G = cfg.bf16_bits_to_f32(bits)
+        G = O.bf16_bits_to_f64(bits)
     else:
         G = r.standard_normal((m, n)).astype(np.float32)
         G[r.random((m, n)) < 0.05] = 0.0

@@ -46,7 +46,7 @@ def _oracle(Gs, beta2=1.0, bf16=False):
     m, n = Gs[0].shape
     L, R = np.zeros((m, m)), np.zeros((n, n))
     for G in Gs:
-        g = cfg.bf16_bits_to_f32(cfg.f32_to_bf16_bits(G)) if bf16 else G
+        g = O.bf16_bits_to_f64(cfg.f32_to_bf16_bits(G)) if bf16 else G
         L, R = O.stats_update(L, R, g, beta2)
     return L, R
 

@@ -62,7 +62,7 @@ def test_precondition_bf16_grouped(env):
         Lr, Rr = _roots(m, n, 40 + k)
         P = torch.zeros(m, n, device=dev)
         blocks.append(B.Block(G=g, P=P, Lr=to_dev(torch, Lr, dev), Rr=to_dev(torch, Rr, dev)))
-        refs.append(O.precondition(cfg.bf16_bits_to_f32(bits), Lr, Rr))
+        refs.append(O.precondition(O.bf16_bits_to_f64(bits), Lr, Rr))
         Ps.append(P)
     B.shampoo_precondition(h, blocks)
     torch.cuda.synchronize()
@@ -201,7 +201,7 @@ def test_graft_lamb_bf16_and_c1_steps(env):
     W = to_dev(torch, W0, dev)
     B.shampoo_graft_lamb(h, [B.Block(G=g, W=W)], 0.1, use_shampoo=False)
     torch.cuda.synchronize()
-    ref = O.lamb_graft_update(W0, cfg.bf16_bits_to_f32(bits), None, 0.1, use_shampoo=False)
+    ref = O.lamb_graft_update(W0, O.bf16_bits_to_f64(bits), None, 0.1, use_shampoo=False)
     assert rel(host(W) - W0, ref["W"] - W0) <= TOL
     n, p, eps, eta0 = 128, 4, 1e-6, 1e-2
     W0 = cfg.c1_weight()

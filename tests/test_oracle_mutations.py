@@ -84,6 +84,30 @@ MUTATIONS = [
      [P.pin_embedding_lookup_matrix, P.pin_embedding_worked_example]),
     ("embedding_rows", "rows = np.array(sorted(acc), dtype=np.int64)", "rows = np.array(list(acc), dtype=np.int64)",
      [P.pin_embedding_lookup_matrix, P.pin_embedding_worked_example]),
+    ("cond_damped", "w = np.linalg.eigvalsh(As) + eps_eff", "w = np.linalg.eigvalsh(As)", [P.pin_cond_damped]),
+    ("cond_damped", "eps_eff, _ = damping(As, eps, eps_relative, lam_max)", "eps_eff, _ = damping(As, eps, False, lam_max)",
+     [P.pin_cond_damped]),
+    ("cond_damped", "float(w.max() / w.min())", "float(w.max() / abs(w).max())", [P.pin_cond_damped]),
+    ("cond_damped", "np.linalg.eigvalsh(As)", "np.linalg.eigvalsh(np.triu(A) + np.triu(A, 1).T)", [P.pin_cond_damped]),
+    ("cond_damped", "if w.min() > 0 else np.inf", "if w.min() != 0 else np.inf", [P.pin_cond_damped]),
+    ("shampoo_step", "s['Lr'], st, _ = inv_root(L, p, eps, eps_relative)",
+     "s['Lr'], st, _ = inv_root(state['L'] + 0.0 * L, p, eps, eps_relative)",
+     [P.pin_shampoo_step_kronecker, P.pin_shampoo_step_variants]),
+    ("shampoo_step", "s['Rr'], st, _ = inv_root(R, p, eps, eps_relative)",
+     "s['Rr'], st, _ = inv_root(R, p, 0.0, eps_relative)", [P.pin_shampoo_step_kronecker]),
+    ("shampoo_step", "P = precondition(G, s.get('Lr') if left else None,\n                     s.get('Rr') if right else None)",
+     "P = precondition(G, s.get('Rr') if right else None,\n                     s.get('Lr') if left else None)",
+     [P.pin_shampoo_step_kronecker]),
+    ("shampoo_step", "    if refresh_roots:", "    if True:", [P.pin_shampoo_step_kronecker]),
+    ("shampoo_step", "out = graft_update(s['W'], s['D'], G, P, eta0, beta1,", "out = graft_update(s['W'], s['D'], G, P, eta0, 0.0,",
+     [P.pin_shampoo_step_variants]),
+    ("shampoo_step", "s.update(W=out['W'], D=out['D'],", "s.update(W=out['W'], D=s['D'],",
+     [P.pin_shampoo_step_kronecker]),
+    ("bf16_bits_to_f64", "<< 16", "<< 15", [P.pin_bf16_decode]),
+    ("bf16_bits_to_f64", "return bits.view(np.float32).astype(np.float64)",
+     "return bits.astype(np.float32).astype(np.float64)", [P.pin_bf16_decode]),
+    ("bf16_bits_to_f64", "return bits.view(np.float32).astype(np.float64)",
+     "return bits.view(np.float32).astype(np.float16).astype(np.float64)", [P.pin_bf16_decode]),
 ]
 
 
