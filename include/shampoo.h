@@ -58,6 +58,12 @@ enum {
   SHAMPOO_ROOT_DIVERGED = 3,  /* residual non-finite or above 1e6 */
   SHAMPOO_ROOT_NOT_PD = 4     /* damped matrix has a non-positive diagonal entry or zero norm */
 };
+/* NOT_PD is a cheap necessary test only (a positive definite matrix has a
+ * positive diagonal), not an eigenvalue test.  An indefinite damped matrix
+ * whose diagonal is positive is not flagged up front: its negative
+ * eigenvalues make the iteration fail, and it comes back DIVERGED (or
+ * MAXITER).  Either status means that no root exists or none was found; X
+ * then holds the last iterate and must not be used. */
 
 /* Arithmetic used for roots (shampoo_root_params.precision). */
 enum {

@@ -101,6 +101,136 @@ def _ptr(t):
     return None if t is None else t.data_ptr()
 
 
+# ------------------------------------------------------------------ argument checks
+# The C side cannot see shapes, strides, element types or devices: it gets
+# raw pointers.  Every entry point below therefore checks its tensors against
+# the layout include/shampoo.h states and raises ValueError before any C call.
+# Device placement is checked last, so that a layout mistake is reported as
+# such whatever the device.
+_handle_device = {}
+
+
+def _is_dtype(t, *names):
+    return str(t.dtype).replace("torch.", "") in names
+
+
+def _need(cond, msg):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _fp32(t, what):
+    _need(_is_dtype(t, "float32"), f"{what}: dtype {t.dtype}, expected float32")
+
+
+def _int32(t, what):
+    _need(_is_dtype(t, "int32"), f"{what}: dtype {t.dtype}, expected int32")
+
+
+def _contig(t, what):
+    _need(t.is_contiguous(), f"{what}: must be contiguous (row-major, no gaps)")
+
+
+def _square(t, n, what):
+    _need(t.dim() == 2 and tuple(t.shape) == (n, n), f"{what}: shape {tuple(t.shape)}, expected ({n}, {n})")
+
+
+def _min_numel(t, k, what):
+    _need(t.numel() >= k, f"{what}: {t.numel()} elements, at least {k} needed")
+
+
+def _devices(handle, tensors):
+    """Every tensor must be a GPU tensor on the handle's device (one device
+    for the call when the handle's device is not known)."""
+    want = _handle_device.get(getattr(handle, "value", handle))
+    for what, t in tensors:
+        if t is None:
+            continue
+        _need(t.device.type == "cuda", f"{what}: on {t.device}, expected a GPU tensor")
+        if want is None:
+            want = t.device.index
+        _need(t.device.index == want, f"{what}: on cuda:{t.device.index}, expected cuda:{want}")
+
+
+_STATE_FIELDS = ("W", "D", "P", "Mg", "Ps")
+
+
+def _check_blocks(handle, blocks, norms=None):
+    tensors = []
+    g_dtype = None
+    for i, b in enumerate(blocks):
+        g = b.G
+        _need(g is not None, f"block {i}: G is required")
+        _need(g.dim() == 2, f"block {i}: G has {g.dim()} dimensions, expected 2")
+        _need(_is_dtype(g, "float32", "bfloat16"), f"block {i}: G dtype {g.dtype}, expected float32 or bfloat16")
+        if g_dtype is None:
+            g_dtype = g.dtype
+        _need(g.dtype == g_dtype, f"block {i}: G dtype {g.dtype} differs from block 0's {g_dtype}: one call "
+                                  f"takes one gradient type")
+        m, n = int(g.shape[0]), int(g.shape[1])
+        _need(n == 1 or g.stride(1) == 1, f"block {i}: G columns must be adjacent (stride(1) == 1)")
+        ld = int(g.stride(0)) if m > 1 else n
+        tensors.append((f"block {i}: G", g))
+        for name in _STATE_FIELDS:
+            t = getattr(b, name)
+            if t is None:
+                continue
+            what = f"block {i}: {name}"
+            _fp32(t, what)
+            _need(tuple(t.shape) == (m, n), f"{what}: shape {tuple(t.shape)}, expected G's {(m, n)}")
+            _need((n == 1 or t.stride(1) == 1) and (m == 1 or int(t.stride(0)) == ld),
+                  f"{what}: strides {tuple(t.stride())}, expected G's row stride ({ld}, 1): the views of a "
+                  f"block share one ld")
+            tensors.append((what, t))
+        for name, k in (("L", m), ("R", n), ("Lr", m), ("Rr", n)):
+            t = getattr(b, name)
+            if t is None:
+                continue
+            what = f"block {i}: {name}"
+            _fp32(t, what)
+            _square(t, k, what)
+            _contig(t, what)
+            tensors.append((what, t))
+    _check_norms(handle, norms, len(blocks), tensors)
+
+
+def _check_norms(handle, norms, nblocks, tensors=()):
+    tensors = list(tensors)
+    if norms is not None:
+        _fp32(norms, "norms")
+        _contig(norms, "norms")
+        _min_numel(norms, 3 * nblocks, "norms")
+        tensors.append(("norms", norms))
+    _devices(handle, tensors)
+
+
+def _check_jobs(handle, As, Xs, workspace, info, warm_out=None):
+    As, Xs = list(As), list(Xs)
+    _need(len(As) == len(Xs), f"{len(As)} statistics but {len(Xs)} outputs")
+    tensors = []
+    for i, (a, x) in enumerate(zip(As, Xs)):
+        _need(a.dim() == 2, f"job {i}: A has {a.dim()} dimensions, expected 2")
+        n = int(a.shape[0])
+        for what, t in ((f"job {i}: A", a), (f"job {i}: X", x)):
+            _fp32(t, what)
+            _square(t, n, what)
+            _contig(t, what)
+            tensors.append((what, t))
+        _need(a.data_ptr() != x.data_ptr() or n == 0, f"job {i}: A and X must be distinct buffers")
+    _need(workspace is not None, "workspace is required")
+    _contig(workspace, "workspace")
+    _int32(info, "info")
+    _contig(info, "info")
+    _min_numel(info, 8 * len(As), "info (8 int32 per job)")
+    tensors += [("workspace", workspace), ("info", info)]
+    if warm_out is not None:
+        _int32(warm_out, "warm_out")
+        _contig(warm_out, "warm_out")
+        _min_numel(warm_out, 2 * len(As), "warm_out (2 int32 per job)")
+        tensors.append(("warm_out", warm_out))
+    _devices(handle, tensors)
+
+
 def _stream(stream):
     if stream is not None:
         return stream if isinstance(stream, int) else stream.cuda_stream
@@ -134,7 +264,7 @@ def _blocks(blocks: Sequence[Block]):
     for i, b in enumerate(blocks):
         g = b.G
         arr[i].rows, arr[i].cols = int(g.shape[0]), int(g.shape[1])
-        arr[i].ld = int(g.stride(0))
+        arr[i].ld = int(g.stride(0)) if g.shape[0] > 1 else int(g.shape[1])   # one row: no stride used
         for name in ("G", "W", "D", "P", "Mg", "Ps", "L", "R", "Lr", "Rr"):
             setattr(arr[i], name, _ptr(getattr(b, name)))
     return arr
@@ -166,14 +296,17 @@ def shampoo_create(device=0):
     code = _lib.shampoo_create(C.byref(h), int(device))
     if code != SHAMPOO_OK:
         raise ShampooError(code, f"shampoo_create(device={device}) failed")
+    _handle_device[h.value] = int(device)
     return h
 
 
 def shampoo_destroy(handle):
     _check(handle, _lib.shampoo_destroy(handle))
+    _handle_device.pop(getattr(handle, "value", handle), None)
 
 
 def shampoo_update_stats(handle, blocks, beta2=1.0, stream=None):
+    _check_blocks(handle, blocks)
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_update_stats(handle, arr, len(blocks), _dtype_code(blocks), float(beta2),
                                              _stream(stream)))
@@ -199,6 +332,7 @@ def shampoo_inv_root_workspace_bytes(ns, precision=PRECISION_AUTO):
 def shampoo_inv_root_batched(handle, As, Xs, params, workspace, info, stream=None):
     """As, Xs: lists of contiguous n x n fp32 device tensors; workspace: a
     uint8 device tensor; info: an int32 device tensor of 8 * len(As)."""
+    _check_jobs(handle, As, Xs, workspace, info)
     arr = _jobs(As, Xs)
     _check(handle, _lib.shampoo_inv_root_batched(handle, arr, len(As), C.byref(params), _ptr(workspace),
                                                  int(workspace.numel() * workspace.element_size()),
@@ -209,6 +343,7 @@ def shampoo_inv_root_warm_batched(handle, As, Xs, params, workspace, info, warm_
                                   stream=None):
     """As shampoo_inv_root_batched; Xs hold the warm starts X0 on entry.
     warm_out: None or an int32 device tensor of 2 * len(As)."""
+    _check_jobs(handle, As, Xs, workspace, info, warm_out)
     arr = _jobs(As, Xs)
     _check(handle, _lib.shampoo_inv_root_warm_batched(handle, arr, len(As), C.byref(params), float(comm_tol),
                                                       _ptr(workspace),
@@ -217,11 +352,13 @@ def shampoo_inv_root_warm_batched(handle, As, Xs, params, workspace, info, warm_
 
 
 def shampoo_precondition(handle, blocks, stream=None):
+    _check_blocks(handle, blocks)
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_precondition(handle, arr, len(blocks), _dtype_code(blocks), _stream(stream)))
 
 
 def shampoo_graft(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
+    _check_blocks(handle, blocks, norms)
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0), float(beta1),
                                       int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
@@ -235,44 +372,100 @@ def shampoo_embedding_workspace_bytes(nnz, dim):
     return int(_lib.shampoo_embedding_workspace_bytes(int(nnz), int(dim)))
 
 
+def _check_vec(t, k, what, kind):
+    (_int32 if kind == "int32" else _fp32)(t, what)
+    _contig(t, what)
+    _min_numel(t, k, what)
+
+
+def _check_compact(U, what="U"):
+    _need(U.dim() == 2, f"{what}: {U.dim()} dimensions, expected nnz x dim")
+    _fp32(U, what)
+    _contig(U, what)
+    return int(U.shape[0]), int(U.shape[1])
+
+
 def shampoo_embedding_rows(handle, idx, feat, weight, vocab, dy, rows, U, count, workspace, stream=None):
     """idx, feat (or None): int32 [nnz]; weight: fp32 [nnz] or None; dy: m x dim
     fp32 (row-major view); rows int32 [nnz], U fp32 nnz x dim (contiguous),
     count int32 [2]; workspace: uint8 device tensor."""
     nnz = int(idx.numel())
+    _check_vec(idx, nnz, "idx", "int32")
+    if feat is not None:
+        _need(feat.numel() == nnz, f"feat: {feat.numel()} entries, idx has {nnz}")
+        _check_vec(feat, nnz, "feat", "int32")
+    if weight is not None:
+        _need(weight.numel() == nnz, f"weight: {weight.numel()} entries, idx has {nnz}")
+        _check_vec(weight, nnz, "weight", "float32")
+    _need(dy.dim() == 2, f"dy: {dy.dim()} dimensions, expected 2")
+    _fp32(dy, "dy")
+    _need(dy.shape[1] == 1 or dy.stride(1) == 1, "dy: columns must be adjacent (stride(1) == 1)")
     m, dim = int(dy.shape[0]), int(dy.shape[1])
+    _check_vec(rows, nnz, "rows", "int32")
+    _need(_check_compact(U) == (nnz, dim), f"U: shape {tuple(U.shape)}, expected ({nnz}, {dim})")
+    _check_vec(count, 2, "count", "int32")
+    _need(workspace is not None, "workspace is required")
+    _contig(workspace, "workspace")
+    _devices(handle, [("idx", idx), ("feat", feat), ("weight", weight), ("dy", dy), ("rows", rows), ("U", U),
+                      ("count", count), ("workspace", workspace)])
     _check(handle, _lib.shampoo_embedding_rows(handle, _ptr(idx), _ptr(feat), _ptr(weight), nnz, int(vocab),
                                                _ptr(dy), m, dim, int(dy.stride(0)), _ptr(rows), _ptr(U),
                                                _ptr(count), _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def shampoo_embedding_stats(handle, U, count, R, beta2=1.0, workspace=None, stream=None):
-    nnz, dim = int(U.shape[0]), int(U.shape[1])
+    nnz, dim = _check_compact(U)
+    _check_vec(count, 2, "count", "int32")
+    _fp32(R, "R")
+    _square(R, dim, "R")
+    _contig(R, "R")
+    _need(workspace is not None, "workspace is required")
+    _contig(workspace, "workspace")
+    _devices(handle, [("U", U), ("count", count), ("R", R), ("workspace", workspace)])
     _check(handle, _lib.shampoo_embedding_stats(handle, _ptr(U), _ptr(count), nnz, dim, _ptr(R), float(beta2),
                                                 _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def shampoo_embedding_precondition(handle, U, count, Rr, P, stream=None):
-    nnz, dim = int(U.shape[0]), int(U.shape[1])
+    nnz, dim = _check_compact(U)
+    _check_vec(count, 2, "count", "int32")
+    _fp32(Rr, "Rr")
+    _square(Rr, dim, "Rr")
+    _contig(Rr, "Rr")
+    _need(_check_compact(P, "P") == (nnz, dim), f"P: shape {tuple(P.shape)}, expected U's ({nnz}, {dim})")
+    _devices(handle, [("U", U), ("count", count), ("Rr", Rr), ("P", P)])
     _check(handle, _lib.shampoo_embedding_precondition(handle, _ptr(U), _ptr(count), nnz, dim, _ptr(Rr), _ptr(P),
                                                        _stream(stream)))
 
 
 def shampoo_embedding_graft(handle, rows, count, U, P, W, D, eta0, use_shampoo=True, norms=None, stream=None):
     """W, D: vocab x dim fp32 tables (same row stride)."""
-    nnz, dim = int(U.shape[0]), int(U.shape[1])
+    nnz, dim = _check_compact(U)
+    _check_vec(rows, nnz, "rows", "int32")
+    _check_vec(count, 2, "count", "int32")
+    _need(_check_compact(P, "P") == (nnz, dim), f"P: shape {tuple(P.shape)}, expected U's ({nnz}, {dim})")
+    for what, t in (("W", W), ("D", D)):
+        _fp32(t, what)
+        _need(t.dim() == 2 and int(t.shape[1]) == dim, f"{what}: shape {tuple(t.shape)}, expected (vocab, {dim})")
+        _need(dim == 1 or t.stride(1) == 1, f"{what}: columns must be adjacent (stride(1) == 1)")
+    _need(tuple(W.shape) == tuple(D.shape) and (W.shape[0] == 1 or W.stride(0) == D.stride(0)),
+          f"W {tuple(W.shape)} / {tuple(W.stride())} and D {tuple(D.shape)} / {tuple(D.stride())} must share "
+          f"shape and row stride")
+    _check_norms(handle, norms, 1, [("rows", rows), ("count", count), ("U", U), ("P", P), ("W", W), ("D", D)])
     _check(handle, _lib.shampoo_embedding_graft(handle, _ptr(rows), _ptr(count), nnz, dim, _ptr(U), _ptr(P),
                                                 _ptr(W), _ptr(D), int(W.shape[0]), int(W.stride(0)), float(eta0),
                                                 int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
 
 
 def shampoo_precondition_graft(handle, blocks, eta0, norms=None, stream=None):
+    _check_blocks(handle, blocks, norms)
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_precondition_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
                                                    _ptr(norms), _stream(stream)))
 
 
 def shampoo_graft_lamb(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
+    _check_blocks(handle, blocks, norms)
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_graft_lamb(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
                                            float(beta1), int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
