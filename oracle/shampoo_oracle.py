@@ -193,18 +193,28 @@ def damping(A, eps, eps_relative=False, lam_max=None, maxsv_steps=100,
     return float(eps) * float(lam_max), float(lam_max)
 
 
-def inv_root(A, p, eps=0.0, eps_relative=False, lam_max=None):
+def sym_eig(A):
+    """Symmetric part A_s = (A + A^T) / 2 of an input (R10) and its
+    eigendecomposition A_s = Q diag(w) Q^T.  Returns (A_s, w, Q).  The root
+    and condition-number functions below take it as ``eig`` so that one
+    decomposition can serve several root orders and dampings of one input."""
+    A = _f64(A)
+    As = 0.5 * (A + A.T)
+    w, Q = np.linalg.eigh(As)
+    return As, w, Q
+
+
+def inv_root(A, p, eps=0.0, eps_relative=False, lam_max=None, eig=None):
     """(A_s + eps_eff I)^(-1/p) by symmetric eigendecomposition.
 
     Definition of A^alpha through A = U D U^T (Preliminaries, notation
     paragraph): A^alpha = U D^alpha U^T, defined for alpha < 0 only when
-    every eigenvalue is positive.  Returns (X, status, eps_eff) with status
-    CONVERGED (root defined) or NOT_PD (X is None).
+    every eigenvalue is positive.  ``eig``: sym_eig(A), if already computed.
+    Returns (X, status, eps_eff) with status CONVERGED (root defined) or
+    NOT_PD (X is None).
     """
-    A = _f64(A)
-    As = 0.5 * (A + A.T)                                   # R10
+    As, w, Q = sym_eig(A) if eig is None else eig
     eps_eff, _ = damping(As, eps, eps_relative, lam_max)
-    w, Q = np.linalg.eigh(As)
     w = w + eps_eff
     if not np.all(w > 0.0):
         return None, NOT_PD, eps_eff
@@ -212,12 +222,12 @@ def inv_root(A, p, eps=0.0, eps_relative=False, lam_max=None):
     return 0.5 * (X + X.T), CONVERGED, eps_eff
 
 
-def cond_damped(A, eps=0.0, eps_relative=False, lam_max=None):
-    """Condition number of the damped matrix A_s + eps_eff I (eigh)."""
-    A = _f64(A)
-    As = 0.5 * (A + A.T)
+def cond_damped(A, eps=0.0, eps_relative=False, lam_max=None, eig=None):
+    """Condition number of the damped matrix A_s + eps_eff I (eigh);
+    ``eig``: sym_eig(A), if already computed."""
+    As, w, _ = sym_eig(A) if eig is None else eig
     eps_eff, _ = damping(As, eps, eps_relative, lam_max)
-    w = np.linalg.eigvalsh(As) + eps_eff
+    w = w + eps_eff
     return float(w.max() / w.min()) if w.min() > 0 else np.inf
 
 

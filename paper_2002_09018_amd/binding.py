@@ -402,7 +402,8 @@ def shampoo_embedding_rows(handle, idx, feat, weight, vocab, dy, rows, U, count,
     _need(dy.shape[1] == 1 or dy.stride(1) == 1, "dy: columns must be adjacent (stride(1) == 1)")
     m, dim = int(dy.shape[0]), int(dy.shape[1])
     _check_vec(rows, nnz, "rows", "int32")
-    _need(_check_compact(U) == (nnz, dim), f"U: shape {tuple(U.shape)}, expected ({nnz}, {dim})")
+    u_rows, u_dim = _check_compact(U)
+    _need(u_rows >= nnz and u_dim == dim, f"U: shape {tuple(U.shape)}, expected at least ({nnz}, {dim})")
     _check_vec(count, 2, "count", "int32")
     _need(workspace is not None, "workspace is required")
     _contig(workspace, "workspace")

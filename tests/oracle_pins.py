@@ -327,6 +327,18 @@ def pin_cond_damped(o):
     assert o.cond_damped(np.diag([1.0, 2.0, -0.5]), 0.1) == np.inf
 
 
+def pin_root_shared_eig(o):
+    """One eigendecomposition reused for several orders and dampings gives
+    exactly the results of separate calls (roots and condition numbers)."""
+    A = _spd(30, 1e5, 19)
+    eig = o.sym_eig(A)
+    for p, eps, relative in ((2, 1e-6, True), (4, 1e-8, True), (4, 1e-3, False)):
+        X0, s0, e0 = o.inv_root(A, p, eps, relative)
+        X1, s1, e1 = o.inv_root(A, p, eps, relative, eig=eig)
+        assert s0 == s1 and e0 == e1 and np.array_equal(X0, X1)
+        assert o.cond_damped(A, eps, relative) == o.cond_damped(A, eps, relative, eig=eig)
+
+
 # ------------------------------------------------------------------ MaxSV
 def pin_maxsv(o):
     """Power iteration converges to the top eigenvalue when it is isolated."""

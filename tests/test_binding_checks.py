@@ -108,6 +108,8 @@ def test_embedding_checks():
     _raises(rows_call(weight=w.double()), "float32")
     _raises(rows_call(dy=torch.zeros(m, 2 * dim)[:, ::2]), "stride")
     _raises(rows_call(U=torch.zeros(nnz, dim + 1)), "expected")
+    _raises(rows_call(U=torch.zeros(nnz - 1, dim)), "at least")
+    _raises(rows_call(U=torch.zeros(nnz + 5, dim)), "expected a GPU tensor")   # a larger buffer is fine
     _raises(rows_call(U=torch.zeros(nnz, dim + 2)[:, :dim]), "contiguous")
     _raises(rows_call(count=torch.zeros(1, **i32)), "at least 2")
     _raises(rows_call(rows=torch.zeros(nnz - 1, **i32)), "at least")

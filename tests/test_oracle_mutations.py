@@ -19,8 +19,8 @@ MUTATIONS = [
     ("inv_root", "w ** (-1.0 / p)", "w ** (1.0 / p)", [P.pin_root_diagonal]),
     ("inv_root", "w = w + eps_eff", "w = w + 0.0 * eps_eff", [P.pin_root_diagonal]),
     ("inv_root", "(Q * w ** (-1.0 / p)) @ Q.T", "(Q * w ** (-1.0 / p)) @ Q", [P.pin_root_mpmath_4x4]),
-    ("inv_root", "As = 0.5 * (A + A.T)", "As = np.triu(A) + np.triu(A, 1).T",
-     [P.pin_root_asymmetric_input]),
+    ("sym_eig", "As = 0.5 * (A + A.T)", "As = np.triu(A) + np.triu(A, 1).T",
+     [P.pin_root_asymmetric_input, P.pin_cond_damped]),
     ("damping", "return float(eps) * float(lam_max), float(lam_max)",
      "return float(eps), float(lam_max)", [P.pin_root_scaled_identity]),
     ("stats_update", "c * (G @ G.T)", "c * (G.T @ G) if G.shape[0] == G.shape[1] else c * (G @ G.T)",
@@ -84,11 +84,12 @@ MUTATIONS = [
      [P.pin_embedding_lookup_matrix, P.pin_embedding_worked_example]),
     ("embedding_rows", "rows = np.array(sorted(acc), dtype=np.int64)", "rows = np.array(list(acc), dtype=np.int64)",
      [P.pin_embedding_lookup_matrix, P.pin_embedding_worked_example]),
-    ("cond_damped", "w = np.linalg.eigvalsh(As) + eps_eff", "w = np.linalg.eigvalsh(As)", [P.pin_cond_damped]),
+    ("cond_damped", "w = w + eps_eff", "w = w + 0.0 * eps_eff", [P.pin_cond_damped]),
     ("cond_damped", "eps_eff, _ = damping(As, eps, eps_relative, lam_max)", "eps_eff, _ = damping(As, eps, False, lam_max)",
      [P.pin_cond_damped]),
     ("cond_damped", "float(w.max() / w.min())", "float(w.max() / abs(w).max())", [P.pin_cond_damped]),
-    ("cond_damped", "np.linalg.eigvalsh(As)", "np.linalg.eigvalsh(np.triu(A) + np.triu(A, 1).T)", [P.pin_cond_damped]),
+    ("cond_damped", "As, w, _ = sym_eig(A) if eig is None else eig", "As, w, _ = sym_eig(np.triu(A)) if eig is None else eig",
+     [P.pin_cond_damped]),
     ("cond_damped", "if w.min() > 0 else np.inf", "if w.min() != 0 else np.inf", [P.pin_cond_damped]),
     ("shampoo_step", "s['Lr'], st, _ = inv_root(L, p, eps, eps_relative)",
      "s['Lr'], st, _ = inv_root(state['L'] + 0.0 * L, p, eps, eps_relative)",
