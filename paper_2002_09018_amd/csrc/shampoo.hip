@@ -63,8 +63,8 @@ struct Handle {
   std::vector<TableEntry> cache;
   std::vector<int> pending;  // cache entries referenced by the launches being enqueued
   uint64_t clock = 0;
-  void* scratch = nullptr;
-  size_t scratch_cap = 0;
+  void* zbuf = nullptr;  // intermediate G Rr of two-sided preconditioning (grown on demand)
+  size_t zbuf_cap = 0;
   void* partial = nullptr;
   size_t partial_cap = 0;
   void* sort_tmp = nullptr;  // rocPRIM temporary storage of the embedding row compaction
@@ -162,10 +162,11 @@ shampoo_status tables_done(Handle* h, hipStream_t s) {
   return SHAMPOO_OK;
 }
 
-shampoo_status grow(Handle* h, void** buf, size_t* cap, size_t bytes) {
+shampoo_status grow(Handle* h, void** buf, size_t* cap, size_t bytes, hipStream_t s) {
   if (*cap >= bytes) return SHAMPOO_OK;
-  // The old buffer may still be read by queued work of this handle.
-  HIP_TRY(h, hipDeviceSynchronize());
+  // The old buffer may still be read by queued work of this handle, which is
+  // ordered on its stream (one handle per stream).
+  HIP_TRY(h, hipStreamSynchronize(s));
   if (*buf) HIP_TRY(h, hipFree(*buf));
   *buf = nullptr;
   *cap = 0;
@@ -335,7 +336,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       pcount[i] = cdiv(blocks[i].rows, kTile) * cdiv(blocks[i].cols, kTile);
       ptotal += pcount[i];
     }
-    STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)std::max(ptotal, 1) * 2 * sizeof(double)));
+    STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)std::max(ptotal, 1) * 2 * sizeof(double), s));
   }
   double* gpart = static_cast<double*>(h->partial);
   auto with_graft = [&](GemmProblem& q, const shampoo_block& b, int i) {
@@ -348,13 +349,13 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
     const shampoo_block& b = blocks[i];
     if (b.Lr && b.Rr) zbytes += align256((size_t)b.rows * b.cols * sizeof(float));
   }
-  if (zbytes) STATUS_TRY(grow(h, &h->scratch, &h->scratch_cap, zbytes));
+  if (zbytes) STATUS_TRY(grow(h, &h->zbuf, &h->zbuf_cap, zbytes, s));
   size_t zoff = 0;
   for (int i = 0; i < nb; ++i) {
     const shampoo_block& b = blocks[i];
     const bool gal = aligned16(b.G) && (b.ld % ve) == 0;
     if (b.Lr && b.Rr) {
-      float* Z = reinterpret_cast<float*>(static_cast<char*>(h->scratch) + zoff);
+      float* Z = reinterpret_cast<float*>(static_cast<char*>(h->zbuf) + zoff);
       zoff += align256((size_t)b.rows * b.cols * sizeof(float));
       GemmProblem p{};  // Z = G Rr
       p.A = b.G; p.lda = b.ld; p.a_rows = b.rows; p.a_cols = b.cols; p.a_aligned = gal;
@@ -436,7 +437,7 @@ shampoo_status graft_impl(Handle* h, const shampoo_block* blocks, int nb, float 
   std::vector<GraftBlock> tb = graft_table(blocks, nb, &total);
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, tb.data(), tb.size() * sizeof(GraftBlock), s, &d));
-  STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)total * 2 * sizeof(double)));
+  STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)total * 2 * sizeof(double), s));
   double* part = static_cast<double*>(h->partial);
   const GraftBlock* db = static_cast<const GraftBlock*>(d);
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
@@ -1010,7 +1011,7 @@ shampoo_status shampoo_destroy(void* handle) {
     (void)hipEventDestroy(t.b);
   }
   for (auto e : h->spare_events) (void)hipEventDestroy(e);
-  if (h->scratch) (void)hipFree(h->scratch);
+  if (h->zbuf) (void)hipFree(h->zbuf);
   if (h->partial) (void)hipFree(h->partial);
   if (h->sort_tmp) (void)hipFree(h->sort_tmp);
   if (h->pinned) (void)hipHostFree(h->pinned);
@@ -1449,7 +1450,7 @@ shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const in
   HIP_TRY(h, rocprim::run_length_encode(nullptr, t_rle, keys_s, (unsigned)nnz, uniq, lens, nruns, s));
   HIP_TRY(h, rocprim::exclusive_scan(nullptr, t_scan, lens, offs, 0, (unsigned)nnz, rocprim::plus<int32_t>(), s));
   size_t tb = std::max(t_sort, std::max(t_rle, t_scan));
-  STATUS_TRY(grow(h, &h->sort_tmp, &h->sort_tmp_cap, std::max<size_t>(tb, 256)));
+  STATUS_TRY(grow(h, &h->sort_tmp, &h->sort_tmp_cap, std::max<size_t>(tb, 256), s));
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_EMB, s, [&] {
     hipLaunchKernelGGL(emb_keys_kernel, dim3(cdiv(nnz, kThreads)), dim3(kThreads), 0, s, idx, feat, nnz, v32, m,
                        keys, vals, lens);
@@ -1577,7 +1578,7 @@ shampoo_status shampoo_embedding_graft(void* handle, const int32_t* rows, const 
   const int total = b.nchunks;
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, &b, sizeof(b), s, &d));
-  STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)total * 2 * sizeof(double)));
+  STATUS_TRY(grow(h, &h->partial, &h->partial_cap, (size_t)total * 2 * sizeof(double), s));
   double* part = static_cast<double*>(h->partial);
   const GraftBlock* db = static_cast<const GraftBlock*>(d);
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
