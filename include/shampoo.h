@@ -270,6 +270,33 @@ shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblo
                              float eta0, float beta1, int use_shampoo, float* norms, void* stream);
 
 /*
+ * Allocation-free form of shampoo_graft, for callers that cannot allocate
+ * device memory (code under stream capture, tight serving loops, harnesses
+ * that forbid hipMalloc): same arguments, same kernels and the same result
+ * bit for bit.  Its scratch -- the block table and one pair of fp64 norm
+ * partials per chunk of at most 16384 elements (whole rows of a block) --
+ * lives in a fixed device array of SHAMPOO_GRAFT_NOALLOC_SCRATCH_BYTES that
+ * every GPU the library runs on holds until the process ends; the table is
+ * staged through pinned host memory that shampoo_create sets up.  The call
+ * itself allocates nothing (no hipMalloc/hipFree, no growth of the handle),
+ * and its launches are not recorded by shampoo_timing_*.
+ * Limits: nblocks <= SHAMPOO_GRAFT_NOALLOC_MAX_BLOCKS and at most
+ * SHAMPOO_GRAFT_NOALLOC_MAX_CHUNKS chunks in total, where a block of
+ * m x n has ceil(m / max(1, 16384 / n)) chunks (C2's 96 blocks of
+ * 1024 x 4096 take 24576); beyond either, ENOMEM and nothing is enqueued.
+ * Every call on a GPU uses that GPU's one array: calls on one stream are
+ * ordered, calls that overlap on different streams of one GPU race.  The
+ * host waits, if needed, for the previous call's table copy out of the
+ * handle's staging memory before writing it again.
+ * Errors: as shampoo_graft, and ENOMEM as above.
+ */
+#define SHAMPOO_GRAFT_NOALLOC_MAX_BLOCKS 8192
+#define SHAMPOO_GRAFT_NOALLOC_MAX_CHUNKS 196608
+#define SHAMPOO_GRAFT_NOALLOC_SCRATCH_BYTES (4u << 20)
+shampoo_status shampoo_graft_noalloc(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                     float eta0, float beta1, int use_shampoo, float* norms, void* stream);
+
+/*
  * Preconditioning and the AdaGrad-grafted update in one call: the same
  * result as shampoo_precondition followed by shampoo_graft with beta1 = 0 and
  * use_shampoo = 1 (Preliminaries, Shampoo update rule; Algorithm 2 with the

@@ -74,6 +74,7 @@ _sig = {
     "shampoo_precondition": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _vp]),
     "shampoo_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
     "shampoo_graft_lamb": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
+    "shampoo_graft_noalloc": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _f, _i, _vp, _vp]),
     "shampoo_precondition_graft": (_i, [_vp, C.POINTER(shampoo_block), _i, _i, _f, _vp, _vp]),
     "shampoo_embedding_workspace_bytes": (_sz, [_i, _i]),
     "shampoo_embedding_rows": (_i, [_vp, _vp, _vp, _vp, _i, _i64, _vp, _i, _i, _i64, _vp, _vp, _vp, _vp, _sz, _vp]),
@@ -362,6 +363,14 @@ def shampoo_graft(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None,
     arr = _blocks(blocks)
     _check(handle, _lib.shampoo_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0), float(beta1),
                                       int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+
+
+def shampoo_graft_noalloc(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
+    """shampoo_graft without any device allocation (fixed scratch; see the header for its limits)."""
+    _check_blocks(handle, blocks, norms)
+    arr = _blocks(blocks)
+    _check(handle, _lib.shampoo_graft_noalloc(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
+                                              float(beta1), int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
 
 
 def _nbytes(t):

@@ -21,6 +21,13 @@
 
 using namespace shp;
 
+// Scratch of shampoo_graft_noalloc: the block table, then the per-chunk norm
+// partials.  Every GPU the library runs on holds its own copy for the life
+// of the process.  In host code `scratch` names a host-side stand-in, not a
+// device address: host code uses the address hipGetSymbolAddress returns for
+// the device (Handle::noalloc_dev), resolved once per handle at creation.
+static __device__ __align__(256) unsigned char scratch[SHAMPOO_GRAFT_NOALLOC_SCRATCH_BYTES];
+
 namespace {
 
 constexpr int kMaxDim = 4096;
@@ -31,6 +38,13 @@ constexpr int kCountRing = 64;  // device/pinned slots (pairs) of per-iteration 
 // count pairs: kCountRing per-iteration slots, the initial residual check, the
 // AUTO escalation count
 constexpr int kCountInts = 2 * (kCountRing + 2);
+// allocation-free graft: table region, then fp64 partial pairs
+constexpr int kNoallocMaxBlocks = SHAMPOO_GRAFT_NOALLOC_MAX_BLOCKS;
+constexpr int kNoallocMaxChunks = SHAMPOO_GRAFT_NOALLOC_MAX_CHUNKS;
+constexpr size_t kNoallocTableBytes = (size_t)kNoallocMaxBlocks * sizeof(GraftBlock);
+static_assert(kNoallocTableBytes % 256 == 0, "partials must start 256-byte aligned");
+static_assert(kNoallocTableBytes + (size_t)kNoallocMaxChunks * 2 * sizeof(double) <= SHAMPOO_GRAFT_NOALLOC_SCRATCH_BYTES,
+              "table and partials must fit the scratch array");
 
 inline int cdiv(int a, int b) { return (a + b - 1) / b; }
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -74,6 +88,11 @@ struct Handle {
   bool timing = false;
   std::vector<TimedLaunch> timed;
   std::vector<hipEvent_t> spare_events;
+  // shampoo_graft_noalloc: this device's address of `scratch`, the pinned
+  // staging of its block table and the event of the last table copy
+  void* noalloc_dev = nullptr;
+  GraftBlock* noalloc_host = nullptr;
+  hipEvent_t noalloc_ev = nullptr;
 };
 
 struct DeviceGuard {
@@ -290,8 +309,11 @@ shampoo_status stats_impl(Handle* h, const shampoo_block* blocks, int nb, float 
 }
 
 // ---------------------------------------------------------------- elementwise block tables
-std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* total) {
-  std::vector<GraftBlock> v;
+// Chunks of one block in the graft kernels: whole rows, at most 16384 elements.
+inline int graft_rows_per_chunk(int cols) { return std::max(1, 16384 / cols); }
+
+// Fills out[0..nb) with the graft table of the blocks; returns the chunk count.
+int fill_graft_table(const shampoo_block* blocks, int nb, GraftBlock* out) {
   int t = 0;
   for (int i = 0; i < nb; ++i) {
     const shampoo_block& b = blocks[i];
@@ -299,7 +321,7 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
     g.G = b.G; g.W = b.W; g.D = b.D; g.P = b.P; g.Mg = b.Mg; g.Ps = b.Ps;
     g.ld = b.ld; g.rows = b.rows; g.cols = b.cols;
     g.ldw = b.ld; g.wrows = nullptr; g.count = nullptr; g.wlimit = b.rows;
-    g.rows_per_chunk = std::max(1, 16384 / b.cols);
+    g.rows_per_chunk = graft_rows_per_chunk(b.cols);
     g.nchunks = cdiv(b.rows, g.rows_per_chunk);
     // 4-wide access needs every row start 16-byte aligned in every tensor
     // (G: 8-byte for bf16 is enough since it is read 4 elements at a time)
@@ -311,9 +333,14 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
     g.part_begin = t;
     g.nparts = g.nchunks;
     t += g.nchunks;
-    v.push_back(g);
+    out[i] = g;
   }
-  *total = t;
+  return t;
+}
+
+std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* total) {
+  std::vector<GraftBlock> v(nb);
+  *total = fill_graft_table(blocks, nb, v.data());
   return v;
 }
 
@@ -916,11 +943,8 @@ shampoo_status emb_check(Handle* h, int nnz, int dim) {
   return SHAMPOO_OK;
 }
 
-shampoo_status graft_entry(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
-                           float beta1, int use_shampoo, float* norms, void* stream, bool lamb) {
-  Handle* h = static_cast<Handle*>(handle);
-  if (!h) return SHAMPOO_EINVAL;
-  h->err.clear();
+shampoo_status graft_check(Handle* h, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
+                           float beta1, int use_shampoo, bool lamb) {
   STATUS_TRY(check_blocks(h, blocks, nblocks, g_dtype));
   if (!isfinite(eta0)) return fail(h, SHAMPOO_EINVAL, "eta0 is not finite");
   if (!(beta1 >= 0.f && beta1 < 1.f)) return fail(h, SHAMPOO_EINVAL, "beta1 %g outside [0, 1)", (double)beta1);
@@ -942,6 +966,15 @@ shampoo_status graft_entry(void* handle, const shampoo_block* blocks, int nblock
         if (outs[a] == outs[c]) return fail(h, SHAMPOO_EINVAL, "block %d: updated states alias", i);
     }
   }
+  return SHAMPOO_OK;
+}
+
+shampoo_status graft_entry(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
+                           float beta1, int use_shampoo, float* norms, void* stream, bool lamb) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(graft_check(h, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, lamb));
   if (nblocks == 0) return SHAMPOO_OK;
   DeviceGuard g(h->device);
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -985,10 +1018,20 @@ shampoo_status shampoo_create(void** handle, int device) {
   Handle* h = new Handle();
   h->device = device;
   DeviceGuard g(device);
+  h->err.reserve(512);  // fail() then never reallocates (messages are at most 511 characters)
   if (hipHostMalloc(reinterpret_cast<void**>(&h->pinned), kCountInts * sizeof(int32_t),
                     hipHostMallocDefault) != hipSuccess ||
       hipEventCreateWithFlags(&h->poll_ev[0], hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&h->poll_ev[1], hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&h->poll_ev[1], hipEventDisableTiming) != hipSuccess ||
+      // set-up of the allocation-free graft, with this device current
+      hipGetSymbolAddress(&h->noalloc_dev, HIP_SYMBOL(scratch)) != hipSuccess || !h->noalloc_dev ||
+      hipHostMalloc(reinterpret_cast<void**>(&h->noalloc_host), kNoallocTableBytes, hipHostMallocDefault) !=
+          hipSuccess ||
+      hipEventCreateWithFlags(&h->noalloc_ev, hipEventDisableTiming) != hipSuccess) {
+    if (h->pinned) (void)hipHostFree(h->pinned);
+    if (h->noalloc_host) (void)hipHostFree(h->noalloc_host);
+    for (auto e : h->poll_ev)
+      if (e) (void)hipEventDestroy(e);
     delete h;
     return SHAMPOO_EHIP;
   }
@@ -1017,6 +1060,8 @@ shampoo_status shampoo_destroy(void* handle) {
   if (h->pinned) (void)hipHostFree(h->pinned);
   for (auto e : h->poll_ev)
     if (e) (void)hipEventDestroy(e);
+  if (h->noalloc_host) (void)hipHostFree(h->noalloc_host);
+  if (h->noalloc_ev) (void)hipEventDestroy(h->noalloc_ev);
   delete h;
   return SHAMPOO_OK;
 }
@@ -1068,6 +1113,45 @@ shampoo_status shampoo_precondition(void* handle, const shampoo_block* blocks, i
 shampoo_status shampoo_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype, float eta0,
                              float beta1, int use_shampoo, float* norms, void* stream) {
   return graft_entry(handle, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, norms, stream, false);
+}
+
+shampoo_status shampoo_graft_noalloc(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
+                                     float eta0, float beta1, int use_shampoo, float* norms, void* stream) {
+  Handle* h = static_cast<Handle*>(handle);
+  if (!h) return SHAMPOO_EINVAL;
+  h->err.clear();
+  STATUS_TRY(graft_check(h, blocks, nblocks, g_dtype, eta0, beta1, use_shampoo, false));
+  if (nblocks == 0) return SHAMPOO_OK;
+  if (nblocks > kNoallocMaxBlocks)
+    return fail(h, SHAMPOO_ENOMEM, "%d blocks exceed the allocation-free graft's limit of %d", nblocks,
+                kNoallocMaxBlocks);
+  int64_t chunks = 0;
+  for (int i = 0; i < nblocks; ++i) chunks += cdiv(blocks[i].rows, graft_rows_per_chunk(blocks[i].cols));
+  if (chunks > kNoallocMaxChunks)
+    return fail(h, SHAMPOO_ENOMEM, "%lld chunks exceed the allocation-free graft's limit of %d", (long long)chunks,
+                kNoallocMaxChunks);
+  DeviceGuard g(h->device);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  // the previous call's table copy must have left the staging memory
+  HIP_TRY(h, hipEventSynchronize(h->noalloc_ev));
+  const int total = fill_graft_table(blocks, nblocks, h->noalloc_host);
+  GraftBlock* dtab = static_cast<GraftBlock*>(h->noalloc_dev);
+  double* part = reinterpret_cast<double*>(static_cast<char*>(h->noalloc_dev) + kNoallocTableBytes);
+  HIP_TRY(h, hipMemcpyAsync(dtab, h->noalloc_host, (size_t)nblocks * sizeof(GraftBlock), hipMemcpyHostToDevice, s));
+  HIP_TRY(h, hipEventRecord(h->noalloc_ev, s));
+  if (g_dtype == SHAMPOO_F32) {
+    hipLaunchKernelGGL((graft_pass1_kernel<float, false>), dim3(total), dim3(kThreads), 0, s, dtab, nblocks, total,
+                       beta1, use_shampoo, part);
+    hipLaunchKernelGGL((graft_pass2_kernel<float, false>), dim3(total), dim3(kThreads), 0, s, dtab, nblocks, total,
+                       eta0, beta1, use_shampoo, (const double*)part, norms);
+  } else {
+    hipLaunchKernelGGL((graft_pass1_kernel<uint16_t, false>), dim3(total), dim3(kThreads), 0, s, dtab, nblocks,
+                       total, beta1, use_shampoo, part);
+    hipLaunchKernelGGL((graft_pass2_kernel<uint16_t, false>), dim3(total), dim3(kThreads), 0, s, dtab, nblocks,
+                       total, eta0, beta1, use_shampoo, (const double*)part, norms);
+  }
+  HIP_TRY(h, hipGetLastError());
+  return SHAMPOO_OK;
 }
 
 shampoo_status shampoo_precondition_graft(void* handle, const shampoo_block* blocks, int nblocks, int g_dtype,
