@@ -146,6 +146,18 @@ def test_c2_full_size_grouped_all(env):
     assert worst_res <= 4e-3
 
 
+@pytest.mark.skip(reason="stage-chain Newton launches (one persistent launch per iteration with per-matrix "
+                         "dependency counters, per-XCD work queues) stalled on C2's 96 matrices twice on MI355X, the "
+                         "second time after its counter poll was changed to an atomic compare-and-swap; the path was "
+                         "taken out of the library (see the design notes, Newton kernel), so this case has no code "
+                         "to run until a design whose cause is understood replaces it")
+def test_c2_stage_chain_grouped():
+    """C2's 96 roots through the stage-chain launches, against the per-stage
+    launches bit for bit (the same products, tiles and epilogues)."""
+    torch, B, dev = gpu_env()
+    pytest.fail("the stage-chain launches are not built")
+
+
 @pytest.mark.parametrize("p", [2, 4])
 def test_c3_ill_conditioned_reduced(env, p):
     """C3 recipe at n = 256 (spectrum log-uniform in [1e-6, 1e2], relative
