@@ -230,6 +230,14 @@ shampoo_status shampoo_inv_root_batched(void* handle, const shampoo_root_job* jo
  * warm result.  The warm phase runs in fp64 under SHAMPOO_PRECISION_FP64 and
  * in fp32 otherwise (under AUTO an fp32 warm result carries fp32 rounding
  * amplified by the condition number: use FP64 for ill-conditioned factors).
+ * A kept warm result is that limit, not the root: its distance from
+ * A_d^(-1/p) grows with the drift of the statistics since X0 and is NOT held
+ * to the tolerance of the cold call.  The monitor only guards against
+ * divergence; it does not bound that distance (measured: 2.5e-4 to 6e-4 from
+ * the cold roots one gradient after X0 on 1024 x 1024 statistics of ~20
+ * gradients, 1.1e-3 when the statistics doubled since X0, every result kept
+ * at comm_tol = 1e-3).  Callers that need the root to a stated tolerance use
+ * shampoo_inv_root_batched.
  * params, workspace, info: as shampoo_inv_root_batched (same workspace size;
  * cond_est is 0 for a warm result).  warm_out (device, may be NULL): int32
  * [njobs][2] = {outcome, warm iterations}, outcome 1 = warm result kept,
