@@ -365,6 +365,10 @@ struct RootState {
   int precision;     // 32 or 64: phase that produced the result
   int sv_done;       // MaxSV stopped
   int sv_steps;      // MaxSV power steps taken
+  int lz_done;       // Lanczos condition witness stopped (AUTO pre-escalation)
+  int lz_steps;      // Lanczos steps taken
+  double lz_beta;    // last off-diagonal of the Lanczos tridiagonal
+  double lz_theta;   // its smallest Ritz value after the last step
   double z;          // scaling of M0 = z A_d: (1 + p) / (2 ||A_d||_F), times zc
   double zc;         // tightening factor of the power-bound scaling (1: Frobenius)
   double eps_eff;    // damping added
@@ -880,9 +884,12 @@ __global__ void root_warm_finish_kernel(RootState* __restrict__ st, int njobs, i
 // fence per workgroup would write back and invalidate the XCD L2s).
 // Vector layout per matrix (doubles): [0, n) vh, [n, n + T n) row partials
 // by tile column, [n + T n, n + 2 T n) column partials by tile row.
+// lanczos: the same pass for a Lanczos step (lanczos_reduce_kernel), gated
+// by that iteration's own stop flag.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                             const RootState* __restrict__ st, int total_full) {
+                                                             const RootState* __restrict__ st, int total_full,
+                                                             int lanczos) {
   // the tile is staged in two halves of 64 rows (33 KB of LDS, so four
   // workgroups share a CU and hide each other's loads)
   constexpr int kHalf = kTile / 2;
@@ -893,7 +900,7 @@ __global__ __launch_bounds__(kThreads) void maxsv_step_kernel(const NewtonJob<T>
   const int t = blockIdx.x;
   if (t >= total_full) return;
   const int j = find_job_full(jobs, njobs, t);
-  if (st[j].status != kActive || st[j].sv_done) return;
+  if (st[j].status != kActive || (lanczos ? st[j].lz_done : st[j].sv_done)) return;
   const NewtonJob<T>* J = jobs + j;
   const int n = J->n, TN = J->tiles_n;
   const int lt = t - J->full_begin;
@@ -1012,6 +1019,155 @@ __global__ void maxsv_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njo
     st[j].lam_max = 0.0;
     st[j].sv_done = 0;
     st[j].sv_steps = 0;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// AUTO pre-escalation: a Lanczos witness of the condition number.  k steps
+// of the Lanczos iteration on A_d = A_s + eps_eff I (fp64 arithmetic, start
+// ones / sqrt(n)) give a k x k tridiagonal T whose Ritz values lie inside
+// [lambda_min(A_d), lambda_max(A_d)]; with the MaxSV Rayleigh quotient
+// lambda_hat + eps_eff <= lambda_max(A_d),
+//   kappa(A_d) >= kappa_lb = (lambda_hat + eps_eff) / theta_min(T).
+// After the cold start the smallest scaled eigenvalue is at most
+// (p + 1) / (2 kappa), so once (p + 1) / (2 kappa_lb) < m1, the smallest
+// scaled eigenvalue that still converges within the fp32 cap, the fp32 phase
+// is certain to end unaccepted for this matrix: it goes straight to fp64
+// (status MAXITER, 0 fp32 iterations).  A matrix stops when that is shown,
+// when theta_min has settled (relative change below 1e-2), when the Krylov
+// space is exhausted, or after kmax steps; it then takes the fp32 phase as
+// before.  Vector layout after MaxSV's: [n + 2 T n, 2 n + 2 T n) the previous
+// Lanczos vector, then alpha[kLanczosMax], beta[kLanczosMax].
+// ---------------------------------------------------------------------------
+constexpr int kLanczosMax = 96;
+
+template <typename T>
+__global__ void lanczos_init_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs, RootState* __restrict__ st) {
+  const int j = blockIdx.x;
+  if (j >= njobs) return;
+  const int n = jobs[j].n, TN = jobs[j].tiles_n;
+  double* v = jobs[j].vec;
+  double* vp = jobs[j].vec + n + 2 * (int64_t)TN * n;
+  for (int i = threadIdx.x; i < n; i += blockDim.x) {
+    v[i] = 1.0 / sqrt((double)n);
+    vp[i] = 0.0;
+  }
+  if (threadIdx.x == 0) {
+    st[j].lz_done = st[j].status != kActive;
+    st[j].lz_steps = 0;
+    st[j].lz_beta = 0.0;
+    st[j].lz_theta = INFINITY;
+  }
+}
+
+// Number of eigenvalues of the symmetric tridiagonal (a[0..m), b[0..m-1))
+// below x: negative pivots of the LDL^T factorisation of T - x I (Sturm).
+__device__ inline int sturm_below(const double* a, const double* b, int m, double x) {
+  int c = 0;
+  double d = 1.0;
+  for (int i = 0; i < m; ++i) {
+    d = a[i] - x - (i > 0 ? b[i - 1] * b[i - 1] / d : 0.0);
+    if (d == 0.0) d = -1e-300;  // an exact zero pivot counts as negative
+    c += d < 0.0;
+  }
+  return c;
+}
+
+// One Lanczos step per matrix from the tile pass's partials: w = A_d v -
+// beta_prev v_prev, alpha = w . v, w -= alpha v, beta = |w|, next v = w /
+// beta; then the witness test above.  mthr: m1 of the fp32 cap.
+template <typename T>
+__global__ __launch_bounds__(kSvThreads) void lanczos_reduce_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
+                                                                   RootState* __restrict__ st, int p, double mthr,
+                                                                   int kmax) {
+  __shared__ double red[kSvThreads / 64];
+  __shared__ double sa[kLanczosMax], sb[kLanczosMax];
+  const int j = blockIdx.x;
+  if (j >= njobs || st[j].status != kActive || st[j].lz_done) return;
+  const NewtonJob<T>* J = jobs + j;
+  const int n = J->n, TN = J->tiles_n;
+  double* v = J->vec;
+  double* prow = J->vec + n;
+  double* pcol = J->vec + n + (int64_t)TN * n;
+  double* vp = J->vec + n + 2 * (int64_t)TN * n;
+  double* al = vp + n;
+  double* be = al + kLanczosMax;
+  const double e = st[j].eps_eff, bprev = st[j].lz_beta;
+  const int k = st[j].lz_steps;
+  double q = 0.0;
+  for (int i = threadIdx.x; i < n; i += kSvThreads) {
+    double a = 0.0, b = 0.0;
+    for (int c = 0; c < TN; ++c) {
+      a += prow[(int64_t)c * n + i];
+      b += pcol[(int64_t)c * n + i];
+    }
+    const double w = 0.5 * (a + b) + e * v[i] - bprev * vp[i];
+    prow[i] = w;  // row partials of tile column 0 are consumed: reuse as w
+    q += w * v[i];
+  }
+  const double alpha = sv_block_sum(q, red);
+  double s2 = 0.0;
+  for (int i = threadIdx.x; i < n; i += kSvThreads) {
+    const double w = prow[i] - alpha * v[i];
+    prow[i] = w;
+    s2 += w * w;
+  }
+  const double beta = sqrt(sv_block_sum(s2, red));
+  for (int i = threadIdx.x; i < n; i += kSvThreads) {
+    vp[i] = v[i];
+    v[i] = beta > 0.0 ? prow[i] / beta : 0.0;
+  }
+  for (int i = threadIdx.x; i < k; i += kSvThreads) {
+    sa[i] = al[i];
+    sb[i] = be[i];
+  }
+  __shared__ double slo, shi;
+  __shared__ int sfirst;
+  if (threadIdx.x == 0) {
+    sa[k] = alpha;
+    al[k] = alpha;
+    be[k] = beta;
+  }
+  __syncthreads();
+  const int m = k + 1;
+  // smallest Ritz value: the Gershgorin interval, narrowed by three rounds of
+  // multisection (every thread counts the eigenvalues below its own point)
+  if (threadIdx.x == 0) {
+    double lo = INFINITY, hi = -INFINITY;
+    for (int i = 0; i < m; ++i) {
+      const double r = (i > 0 ? fabs(sb[i - 1]) : 0.0) + (i + 1 < m ? fabs(sb[i]) : 0.0);
+      lo = fmin(lo, sa[i] - r);
+      hi = fmax(hi, sa[i] + r);
+    }
+    slo = lo;
+    shi = hi;
+  }
+  for (int round = 0; round < 3; ++round) {
+    if (threadIdx.x == 0) sfirst = kSvThreads;
+    __syncthreads();
+    const double lo = slo, w = (shi - slo) / kSvThreads;
+    const double x = lo + w * (threadIdx.x + 1);
+    if (sturm_below(sa, sb, m, x) >= 1) atomicMin(&sfirst, (int)threadIdx.x);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      const int f = sfirst < kSvThreads ? sfirst : kSvThreads - 1;
+      slo = lo + w * f;
+      shi = lo + w * (f + 1);
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x != 0) return;
+  const double theta = shi;
+  const double top = st[j].lam_max + e;
+  const double prev = st[j].lz_theta;
+  st[j].lz_steps = m;
+  st[j].lz_beta = beta;
+  st[j].lz_theta = theta;
+  if (theta > 0.0 && top > 0.0 && (p + 1.0) * theta / (2.0 * top) < mthr) {
+    st[j].status = kMaxIter;  // certain to end unaccepted in fp32: straight to fp64
+    st[j].lz_done = 1;
+  } else if (!(theta > 0.0) || beta <= 1e-12 * top || m >= kmax || fabs(prev - theta) <= 1e-2 * theta) {
+    st[j].lz_done = 1;
   }
 }
 

@@ -513,7 +513,9 @@ RootLayout root_layout(const shampoo_root_job* jobs, int njobs, int precision) {
     L.part.push_back(off);
     off += align256(3 * T * T * sizeof(double));
     L.vec.push_back(off);
-    off += align256((2 * T + 1) * n * sizeof(double));
+    // MaxSV: v and the tile partials; the Lanczos witness: its previous
+    // vector and the tridiagonal
+    off += align256(((2 * T + 2) * n + 2 * kLanczosMax) * sizeof(double));
     L.f32.push_back(off);
     if (precision != SHAMPOO_PRECISION_FP64) off += 5 * align256(n * n * sizeof(float));
     L.f64.push_back(off);
@@ -1321,12 +1323,12 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
         if (j32) {
           hipLaunchKernelGGL(maxsv_step_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs,
-                             (const RootState*)st, full);
+                             (const RootState*)st, full, 0);
           hipLaunchKernelGGL(maxsv_reduce_kernel<float>, dim3(njobs), dim3(kSvThreads), 0, s, j32, njobs, st, mtol,
                              eps, last);
         } else {
           hipLaunchKernelGGL(maxsv_step_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs,
-                             (const RootState*)st, full);
+                             (const RootState*)st, full, 0);
           hipLaunchKernelGGL(maxsv_reduce_kernel<double>, dim3(njobs), dim3(kSvThreads), 0, s, j64, njobs, st, mtol,
                              eps, last);
         }
@@ -1343,6 +1345,38 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
                          eps);
     }
   }));
+  // AUTO: the fp32 phase's cap, from the scalar recurrence for the
+  // smallest scaled eigenvalue (p + 1) / (2 kappa32), and m1, the smallest
+  // scaled eigenvalue that still converges within it
+  int cap32 = prm->max_iters;
+  double m1 = 0.0;
+  if (prec == SHAMPOO_PRECISION_AUTO) {
+    const double tl = std::max((double)prm->tol, 1e-6);
+    const double m0 = std::min(1.0, (p + 1.0) / (2.0 * (double)prm->kappa32));
+    const int k32 = host_scalar_iters(m0, p, tl, 1000) + 1;
+    cap32 = std::min(cap32, std::max(k32, 1));
+    double lo = 1e-300, hi = 1.0;
+    for (int b = 0; b < 200; ++b) {
+      const double mid = sqrt(lo * hi);
+      if (host_scalar_iters(mid, p, tl, cap32 + 1) <= cap32) hi = mid; else lo = mid;
+    }
+    m1 = hi;
+  }
+  // AUTO with scaled damping (MaxSV ran): the Lanczos condition witness
+  // sends matrices that the fp32 cap would certainly reject straight to fp64
+  if (prec == SHAMPOO_PRECISION_AUTO && prm->eps_relative && !warm && j32) {
+    STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+      hipLaunchKernelGGL(lanczos_init_kernel<float>, dim3(njobs), dim3(kThreads), 0, s, j32, njobs, st);
+    }));
+    for (int k = 0; k < kLanczosMax; ++k) {
+      STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
+        hipLaunchKernelGGL(maxsv_step_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs,
+                           (const RootState*)st, full, 1);
+        hipLaunchKernelGGL(lanczos_reduce_kernel<float>, dim3(njobs), dim3(kSvThreads), 0, s, j32, njobs, st, p, m1,
+                           kLanczosMax);
+      }));
+    }
+  }
   // warm phase; -1: unknown number of matrices handed to the cold start
   int warm_aborts = -1;
   if (warm) {
@@ -1364,25 +1398,16 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
   }
   int run64 = tail_all && !(warm && warm_aborts == 0);
   if (j32) {
-    int cap = prm->max_iters;
+    const int cap = cap32;
     const float* esc = nullptr;
     int esc_n = 0;
     if (prec == SHAMPOO_PRECISION_AUTO) {
-      const double tl = std::max((double)prm->tol, 1e-6);
-      const double m0 = std::min(1.0, (p + 1.0) / (2.0 * (double)prm->kappa32));
-      const int k32 = host_scalar_iters(m0, p, tl, 1000) + 1;
-      cap = std::min(cap, std::max(k32, 1));
       // Early escalation: m1 is the smallest scaled eigenvalue that still
       // converges within the cap; after k iterations it has reached f^k(m1)
       // (f(m) = ((p+1-m)/p)^p m), so a residual above 1 - f^k(m1) means the
       // matrix would reach the cap unconverged.
-      double lo = 1e-300, hi = 1.0;
-      for (int b = 0; b < 200; ++b) {
-        const double mid = sqrt(lo * hi);
-        if (host_scalar_iters(mid, p, tl, cap + 1) <= cap) hi = mid; else lo = mid;
-      }
       std::vector<float> thr(cap);
-      double m = hi;
+      double m = m1;
       for (int k = 0; k < cap; ++k) {
         m = pow((p + 1.0 - m) / p, p) * m;
         thr[k] = (float)(1.0 - m);  // escalating a borderline matrix early is harmless

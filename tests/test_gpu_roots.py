@@ -234,7 +234,8 @@ def test_c3_full_size_grouped_all(env, c3_full, p):
         kap = [r[1] for r in res]
         say(f"C3 p={p} eps_d={epsd:g}: damped condition {min(kap):.3g}..{max(kap):.3g}, fp64 iterations "
             f"{min(i['iters'] for i in info)}..{max(i['iters'] for i in info)}, fp32 attempt "
-            f"{min(i['iters_fp32'] for i in info)}..{max(i['iters_fp32'] for i in info)}")
+            f"{min(i['iters_fp32'] for i in info)}..{max(i['iters_fp32'] for i in info)} (0: sent to fp64 by "
+            f"the Lanczos witness)")
         _, worst, frac = summarize(f"C3 p={p} eps_d={epsd:g} roots (all 32)", [r[0] for r in res],
                                    [r[2] for r in res])
         assert frac == 1.0, worst
@@ -268,6 +269,30 @@ def test_auto_escalates_early(env):
     for A, X, inf in zip((A_ok, A_bad), Xs, info):
         Xo, _, _ = O.inv_root(A, 4, 0.0)
         assert rel(X, Xo) <= band(O.cond_damped(A, 0.0)), (inf, rel(X, Xo))
+
+
+def test_auto_lanczos_preescalation(env):
+    """AUTO with scaled damping: a Lanczos witness (its smallest Ritz value
+    bounds lambda_min from above) sends a matrix straight to fp64 only when
+    the fp32 cap would certainly reject it.  Well-conditioned matrices stay
+    in fp32; a C3-like spectrum (log-uniform over 8 decades, damped
+    condition ~5e7) goes to fp64 with no fp32 iteration; every root matches
+    eigh within its band."""
+    say("roots Lanczos pre-escalation")
+    ok = [spd(300, 30.0, 41), spd(256, 1e3, 42), cfg.wishart_bartlett(384, 40 * 384, 1.0 / 384, 43, 0)
+          .astype(np.float32)]
+    bad = [cfg.c3_matrix(i, n=256)[0] for i in range(3)]
+    for p in (2, 4):
+        Xs, info = roots(env, ok + bad, p=p, eps=1e-8, eps_relative=1)
+        for A, X, inf in zip(ok + bad, Xs, info):
+            Xo, _, _ = O.inv_root(A, p, 1e-8, eps_relative=True, lam_max=inf["lambda_max"])
+            kappa = O.cond_damped(A, 1e-8, True, lam_max=inf["lambda_max"])
+            assert inf["status"] in (0, 1), inf
+            assert rel(X, Xo) <= band(kappa), (p, kappa, inf, rel(X, Xo))
+        for inf in info[:len(ok)]:
+            assert inf["precision"] == 32 and inf["iters_fp32"] > 0, inf
+        for inf in info[len(ok):]:
+            assert inf["precision"] == 64 and inf["iters_fp32"] == 0, inf
 
 
 def test_status_paths_and_isolation(env):
