@@ -156,7 +156,78 @@ def _devices(handle, tensors):
 _STATE_FIELDS = ("W", "D", "P", "Mg", "Ps")
 
 
+_torch_mod = None
+
+
+def _torch():
+    global _torch_mod
+    if _torch_mod is None:
+        import torch
+        _torch_mod = torch
+    return _torch_mod
+
+
 def _check_blocks(handle, blocks, norms=None):
+    """Fast pass over the blocks (cheap accessors, no per-check calls); the
+    detailed checker below runs only when something fails, to raise with the
+    exact reason."""
+    torch = _torch()
+    f32, bf16 = torch.float32, torch.bfloat16
+    want = _handle_device.get(getattr(handle, "value", handle))
+    dev0 = None
+    ok = True
+    g_dtype = None
+    for b in blocks:
+        g = b.G
+        if g is None or g.dim() != 2:
+            ok = False
+            break
+        gd = g.dtype
+        if g_dtype is None:
+            g_dtype = gd
+        if gd is not g_dtype or (gd is not f32 and gd is not bf16):
+            ok = False
+            break
+        gs = g.size()
+        m, n = gs[0], gs[1]
+        gst = g.stride()
+        ld = gst[0] if m > 1 else n
+        dev = g.get_device()
+        if dev0 is None:
+            dev0 = dev
+        if (n != 1 and gst[1] != 1) or dev != dev0:
+            ok = False
+            break
+        for t in (b.W, b.D, b.P, b.Mg, b.Ps):
+            if t is None:
+                continue
+            st = t.stride()
+            if (t.dtype is not f32 or t.size() != gs or t.get_device() != dev0 or (n != 1 and st[1] != 1)
+                    or (m != 1 and st[0] != ld)):
+                ok = False
+                break
+        if not ok:
+            break
+        for t, k in ((b.L, m), (b.R, n), (b.Lr, m), (b.Rr, n)):
+            if t is None:
+                continue
+            if t.dtype is not f32 or t.size() != (k, k) or not t.is_contiguous() or t.get_device() != dev0:
+                ok = False
+                break
+        if not ok:
+            break
+    if ok and norms is not None:
+        ok = (norms.dtype is f32 and norms.is_contiguous() and norms.numel() >= 3 * len(blocks)
+              and (dev0 is None or norms.get_device() == dev0))
+    if ok and (dev0 is None or (dev0 >= 0 and (want is None or dev0 == want))):
+        if dev0 is None and norms is not None:
+            _devices(handle, [("norms", norms)])
+        return
+    _check_blocks_detailed(handle, blocks, norms)
+    raise ValueError("tensors of one call must all be on one GPU, the handle's")
+
+
+def _check_blocks_detailed(handle, blocks, norms=None):
     tensors = []
     g_dtype = None
     for i, b in enumerate(blocks):
@@ -206,6 +277,39 @@ def _check_norms(handle, norms, nblocks, tensors=()):
 
 
 def _check_jobs(handle, As, Xs, workspace, info, warm_out=None):
+    """Fast pass (see _check_blocks); the detailed checks raise the reason."""
+    torch = _torch()
+    f32 = torch.float32
+    want = _handle_device.get(getattr(handle, "value", handle))
+    ok = len(As) == len(Xs) and workspace is not None
+    dev0 = None
+    if ok:
+        for a, x in zip(As, Xs):
+            sz = a.size()
+            dev = a.get_device()
+            if dev0 is None:
+                dev0 = dev
+            if (len(sz) != 2 or sz[0] != sz[1] or a.dtype is not f32 or x.dtype is not f32 or x.size() != sz
+                    or not a.is_contiguous() or not x.is_contiguous() or dev != dev0 or x.get_device() != dev0
+                    or a.data_ptr() == x.data_ptr()):
+                ok = False
+                break
+    if ok:
+        ok = (workspace.is_contiguous() and info.dtype is torch.int32 and info.is_contiguous()
+              and info.numel() >= 8 * len(As) and (warm_out is None or (warm_out.dtype is torch.int32 and
+                                                                        warm_out.is_contiguous() and
+                                                                        warm_out.numel() >= 2 * len(As))))
+        devs = [workspace.get_device(), info.get_device()] + ([] if warm_out is None else [warm_out.get_device()])
+        if dev0 is None:
+            dev0 = devs[0]
+        ok = ok and all(d == dev0 for d in devs) and dev0 >= 0 and (want is None or dev0 == want)
+    if ok:
+        return
+    _check_jobs_detailed(handle, As, Xs, workspace, info, warm_out)
+    raise ValueError("tensors of one call must all be on one GPU, the handle's")
+
+
+def _check_jobs_detailed(handle, As, Xs, workspace, info, warm_out=None):
     As, Xs = list(As), list(Xs)
     _need(len(As) == len(Xs), f"{len(As)} statistics but {len(Xs)} outputs")
     tensors = []
@@ -260,15 +364,30 @@ class Block:
     Rr: Optional[object] = None
 
 
+_BLOCK_PTRS = ("G", "W", "D", "P", "Mg", "Ps", "L", "R", "Lr", "Rr")
+
+
 def _blocks(blocks: Sequence[Block]):
-    arr = (shampoo_block * max(1, len(blocks)))()
-    for i, b in enumerate(blocks):
+    """The shampoo_block array of a call, packed as 12 int64 words per block
+    (rows | cols << 32, ld, then the ten pointers), as a ctypes pointer into a
+    numpy buffer that the caller keeps alive over the C call."""
+    import numpy as np
+    rec = []
+    for b in blocks:
         g = b.G
-        arr[i].rows, arr[i].cols = int(g.shape[0]), int(g.shape[1])
-        arr[i].ld = int(g.stride(0)) if g.shape[0] > 1 else int(g.shape[1])   # one row: no stride used
-        for name in ("G", "W", "D", "P", "Mg", "Ps", "L", "R", "Lr", "Rr"):
-            setattr(arr[i], name, _ptr(getattr(b, name)))
-    return arr
+        m, n = g.size()
+        ld = g.stride(0) if m > 1 else n   # one row: no stride used
+        rec.append([m | (n << 32), ld] + [0 if t is None else t.data_ptr() for t in
+                                          (b.G, b.W, b.D, b.P, b.Mg, b.Ps, b.L, b.R, b.Lr, b.Rr)])
+    buf = np.array(rec if rec else [[0] * 12], dtype=np.uint64)
+    assert buf.shape[1] * 8 == C.sizeof(shampoo_block)
+    return _Packed(buf, buf.ctypes.data_as(C.POINTER(shampoo_block)))
+
+
+class _Packed:
+    """A packed host table and its ctypes pointer (the table lives as long as this object)."""
+    def __init__(self, buf, ptr):
+        self._buf, self._as_parameter_ = buf, ptr
 
 
 def _dtype_code(blocks):
@@ -314,13 +433,12 @@ def shampoo_update_stats(handle, blocks, beta2=1.0, stream=None):
 
 
 def _jobs(As, Xs):
-    arr = (shampoo_root_job * max(1, len(As)))()
-    for i, (a, x) in enumerate(zip(As, Xs)):
-        arr[i].n = int(a.shape[0])
-        arr[i].reserved = 0
-        arr[i].A = _ptr(a)
-        arr[i].X = _ptr(x)
-    return arr
+    """The shampoo_root_job array, packed as 3 int64 words per job (n, A, X)."""
+    import numpy as np
+    rec = [[a.size(0), a.data_ptr(), x.data_ptr()] for a, x in zip(As, Xs)]
+    buf = np.array(rec if rec else [[0] * 3], dtype=np.uint64)
+    assert buf.shape[1] * 8 == C.sizeof(shampoo_root_job)
+    return _Packed(buf, buf.ctypes.data_as(C.POINTER(shampoo_root_job)))
 
 
 def shampoo_inv_root_workspace_bytes(ns, precision=PRECISION_AUTO):
