@@ -171,8 +171,10 @@ void shampoo_root_params_default(shampoo_root_params* params);
  *   beta2 == 1:  L += G G^T,  R += G^T G
  *   beta2 <  1:  L = beta2 L + (1 - beta2) G G^T  (same for R)
  * For every block with non-NULL L (resp. R).  L and R stay exactly symmetric:
- * the upper triangle is computed and mirrored.  The ridge eps*I is not added
- * here; shampoo_inv_root_batched adds it once.  G: g_dtype.
+ * the upper triangle is computed and mirrored.  They must be symmetric on
+ * entry as well (zero, or the output of earlier updates): the old value of an
+ * off-diagonal element may be read from its mirror.  The ridge eps*I is not
+ * added here; shampoo_inv_root_batched adds it once.  G: g_dtype.
  * Errors: EINVAL for nblocks < 0, NULL blocks with nblocks > 0, sizes
  * outside [1, 4096], ld < cols, beta2 outside (0, 1], L, R and G not
  * distinct buffers (a block with both L and R NULL is skipped).
@@ -392,7 +394,8 @@ shampoo_status shampoo_embedding_rows(void* handle, const int32_t* idx, const in
 /*
  * R = beta2 R + c U^T U over the first count[0] rows of U (c = 1 if
  * beta2 == 1 else 1 - beta2): the statistic of the table, dim x dim, kept
- * exactly symmetric.  The active rows are split into a fixed number of
+ * exactly symmetric (and required symmetric on entry, as for
+ * shampoo_update_stats).  The active rows are split into a fixed number of
  * equal parts (set from nnz and dim); their partial products are added in
  * part order (deterministic).
  * Errors: EINVAL (NULL pointers, sizes, beta2 outside (0, 1]), ENOMEM.

@@ -275,7 +275,9 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
 #if SHP_EPI_VEC
   // Symmetric output, off-diagonal full tile: mirrored values go out as
   // 16-byte stores (a lane's 4 consecutive rows are 4 consecutive columns of
-  // the transposed tile).
+  // the transposed tile).  The old output is symmetric too, so the four old
+  // values of rows r..r+3, column c are one 16-byte load of row c (the
+  // mirror this lane then overwrites; no other lane or workgroup touches it).
   if (P.sym && !diag && m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
       (reinterpret_cast<uintptr_t>(P.C) & 15) == 0) {
 #pragma unroll
@@ -287,11 +289,12 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
           const int r = wm0 + i * F::kM + F::row(lane, 4 * g);
           const int c = wn0 + j * F::kM + F::col(lane);
           typedef float f4 __attribute__((ext_vector_type(4)));
-          f4 w;
+          f4 w, old = {0.f, 0.f, 0.f, 0.f};
+          if (P.beta != 0.f) old = gload<f4>(P.C + (int64_t)c * P.ldc + r);
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
             float x = P.alpha * acc.c[i][j][4 * g + q];
-            if (P.beta != 0.f) x += P.beta * gload<float>(P.C + (int64_t)(r + q) * P.ldc + c);
+            if (P.beta != 0.f) x += P.beta * old[q];
             gstore<float>(P.C + (int64_t)(r + q) * P.ldc + c, x);
             w[q] = x;
           }
