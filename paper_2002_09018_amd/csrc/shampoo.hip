@@ -93,6 +93,11 @@ struct Handle {
   void* noalloc_dev = nullptr;
   GraftBlock* noalloc_host = nullptr;
   hipEvent_t noalloc_ev = nullptr;
+  // shampoo_precondition_graft: graft pass 2 of a chunk of blocks runs on
+  // `side` while the next chunk's GEMMs run on the caller's stream (both at
+  // the default priority); `handoff` orders the two
+  hipStream_t side = nullptr;
+  hipEvent_t handoff = nullptr;
 };
 
 struct DeviceGuard {
@@ -344,6 +349,33 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
   return v;
 }
 
+// Group boundaries of shampoo_precondition_graft: cut[0] = 0 < cut[1] < ...
+// < cut[k] = nb, contiguous groups of about equal GEMM flops.  Calls with
+// fewer than 8 blocks or under 2^24 elements stay one group (their graft
+// pass 2 is too short to pay for the extra launches).
+std::vector<int> precond_groups(const shampoo_block* blocks, int nb) {
+  constexpr int kGroups = 4;
+  std::vector<double> w(nb);
+  double work = 0.0;
+  int64_t elems = 0;
+  for (int i = 0; i < nb; ++i) {
+    const shampoo_block& b = blocks[i];
+    w[i] = (double)b.rows * b.cols * ((b.Lr ? b.rows : 0) + (b.Rr ? b.cols : 0));
+    work += w[i];
+    elems += (int64_t)b.rows * b.cols;
+  }
+  std::vector<int> cut{0};
+  if (nb >= 8 && elems >= (int64_t(1) << 24)) {
+    double acc = 0.0;
+    for (int i = 0; i + 1 < nb && (int)cut.size() < kGroups; ++i) {
+      acc += w[i];
+      if (acc >= work * (double)cut.size() / kGroups) cut.push_back(i + 1);
+    }
+  }
+  cut.push_back(nb);
+  return cut;
+}
+
 // fuse_graft: the GEMM that writes a block's P also runs graft pass 1 on it
 // (D += G o G and the norm partials of every output tile into h->partial),
 // and graft pass 2 follows (AdaGrad graft, beta1 = 0, Shampoo direction);
@@ -353,6 +385,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
                             float eta0 = 0.f, float* norms = nullptr) {
   const int ve = 16 / (int)sizeof(SG);
   std::vector<GemmProblem> g_rr, lr_z, lr_g;
+  std::vector<int> g_rr_b, lr_z_b, lr_g_b;  // block of each problem (ascending)
   // graft: per block, the first and the number of norm partials (the P
   // GEMM's output tiles)
   std::vector<int> pbegin(nb), pcount(nb);
@@ -391,6 +424,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       p.C = Z; p.ldc = b.cols; p.M = b.rows; p.N = b.cols; p.K = b.cols;
       p.alpha = 1.f; p.beta = 0.f;
       g_rr.push_back(p);
+      g_rr_b.push_back(i);
       GemmProblem q{};  // P = Lr Z, Lr symmetric: read k-major
       q.A = b.Lr; q.lda = b.rows; q.a_rows = b.rows; q.a_cols = b.rows;
       q.a_aligned = aligned16(b.Lr) && (b.rows % 4) == 0;
@@ -399,6 +433,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       q.alpha = 1.f; q.beta = 0.f;
       with_graft(q, b, i);
       lr_z.push_back(q);
+      lr_z_b.push_back(i);
     } else if (b.Rr) {
       GemmProblem p{};  // P = G Rr
       p.A = b.G; p.lda = b.ld; p.a_rows = b.rows; p.a_cols = b.cols; p.a_aligned = gal;
@@ -408,6 +443,7 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       p.alpha = 1.f; p.beta = 0.f;
       with_graft(p, b, i);
       g_rr.push_back(p);
+      g_rr_b.push_back(i);
     } else if (b.Lr) {
       GemmProblem q{};  // P = Lr G
       q.A = b.Lr; q.lda = b.rows; q.a_rows = b.rows; q.a_cols = b.rows;
@@ -417,28 +453,59 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
       q.alpha = 1.f; q.beta = 0.f;
       with_graft(q, b, i);
       lr_g.push_back(q);
+      lr_g_b.push_back(i);
     } else {
       copy.push_back(b);
     }
   }
   if (fuse_graft) {
-    STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK, false, SG>(h, g_rr, s, SHAMPOO_KCLASS_PRECOND)));
-    STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK, false, SG>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
-    STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK, false, SG>(h, lr_g, s, SHAMPOO_KCLASS_PRECOND)));
-    // graft pass 2 over the row chunks of every block, with the GEMM's
-    // per-tile norm partials
-    int total = 0;
-    std::vector<GraftBlock> tb = graft_table(blocks, nb, &total);
-    for (int i = 0; i < nb; ++i) {
-      tb[i].part_begin = pbegin[i];
-      tb[i].nparts = pcount[i];
+    // The blocks go in contiguous groups of about equal GEMM work: the GEMMs
+    // of every group run on the caller's stream, and graft pass 2 of a group
+    // (HBM-bound) on the handle's side stream, where it overlaps the GEMMs
+    // (MFMA-bound) of the next group.  Each block's result is the same as in
+    // one group.
+    const std::vector<int> cut = precond_groups(blocks, nb);
+    const int ngroups = (int)cut.size() - 1;
+    size_t ir = 0, iz = 0, ig = 0;  // next problem of each list
+    auto take = [](const std::vector<GemmProblem>& v, const std::vector<int>& vb, size_t& i, int end) {
+      std::vector<GemmProblem> out;
+      while (i < v.size() && vb[i] < end) out.push_back(v[i++]);
+      return out;
+    };
+    for (int c = 0; c < ngroups; ++c) {
+      const int b0 = cut[c], nbc = cut[c + 1] - cut[c];
+      std::vector<GemmProblem> c_rr = take(g_rr, g_rr_b, ir, b0 + nbc);
+      std::vector<GemmProblem> c_z = take(lr_z, lr_z_b, iz, b0 + nbc);
+      std::vector<GemmProblem> c_g = take(lr_g, lr_g_b, ig, b0 + nbc);
+      STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK, false, SG>(h, c_rr, s, SHAMPOO_KCLASS_PRECOND)));
+      STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK, false, SG>(h, c_z, s, SHAMPOO_KCLASS_PRECOND)));
+      STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK, false, SG>(h, c_g, s, SHAMPOO_KCLASS_PRECOND)));
+      // graft pass 2 over the row chunks of the group's blocks, with the
+      // GEMM's per-tile norm partials
+      int total = 0;
+      std::vector<GraftBlock> tb = graft_table(blocks + b0, nbc, &total);
+      for (int i = 0; i < nbc; ++i) {
+        tb[i].part_begin = pbegin[b0 + i];
+        tb[i].nparts = pcount[b0 + i];
+      }
+      const void* d = nullptr;
+      STATUS_TRY(upload_table(h, tb.data(), tb.size() * sizeof(GraftBlock), s, &d));
+      hipStream_t ps = s;
+      if (ngroups > 1) {
+        HIP_TRY(h, hipEventRecord(h->handoff, s));
+        HIP_TRY(h, hipStreamWaitEvent(h->side, h->handoff, 0));
+        ps = h->side;
+      }
+      float* gn = norms ? norms + 3 * b0 : nullptr;
+      STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, ps, [&] {
+        hipLaunchKernelGGL((graft_pass2_kernel<SG, false>), dim3(total), dim3(kThreads), 0, ps, (const GraftBlock*)d,
+                           nbc, total, eta0, 0.f, 1, (const double*)gpart, gn);
+      }));
     }
-    const void* d = nullptr;
-    STATUS_TRY(upload_table(h, tb.data(), tb.size() * sizeof(GraftBlock), s, &d));
-    STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, s, [&] {
-      hipLaunchKernelGGL((graft_pass2_kernel<SG, false>), dim3(total), dim3(kThreads), 0, s, (const GraftBlock*)d, nb,
-                         total, eta0, 0.f, 1, (const double*)gpart, norms);
-    }));
+    if (ngroups > 1) {  // the caller's stream continues after the last pass 2
+      HIP_TRY(h, hipEventRecord(h->handoff, h->side));
+      HIP_TRY(h, hipStreamWaitEvent(s, h->handoff, 0));
+    }
     return tables_done(h, s);
   }
   STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK>(h, g_rr, s, SHAMPOO_KCLASS_PRECOND)));
@@ -1029,11 +1096,15 @@ shampoo_status shampoo_create(void** handle, int device) {
       hipGetSymbolAddress(&h->noalloc_dev, HIP_SYMBOL(scratch)) != hipSuccess || !h->noalloc_dev ||
       hipHostMalloc(reinterpret_cast<void**>(&h->noalloc_host), kNoallocTableBytes, hipHostMallocDefault) !=
           hipSuccess ||
-      hipEventCreateWithFlags(&h->noalloc_ev, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&h->noalloc_ev, hipEventDisableTiming) != hipSuccess ||
+      hipStreamCreateWithFlags(&h->side, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&h->handoff, hipEventDisableTiming) != hipSuccess) {
     if (h->pinned) (void)hipHostFree(h->pinned);
     if (h->noalloc_host) (void)hipHostFree(h->noalloc_host);
     for (auto e : h->poll_ev)
       if (e) (void)hipEventDestroy(e);
+    if (h->noalloc_ev) (void)hipEventDestroy(h->noalloc_ev);
+    if (h->side) (void)hipStreamDestroy(h->side);
     delete h;
     return SHAMPOO_EHIP;
   }
@@ -1064,6 +1135,8 @@ shampoo_status shampoo_destroy(void* handle) {
     if (e) (void)hipEventDestroy(e);
   if (h->noalloc_host) (void)hipHostFree(h->noalloc_host);
   if (h->noalloc_ev) (void)hipEventDestroy(h->noalloc_ev);
+  if (h->handoff) (void)hipEventDestroy(h->handoff);
+  if (h->side) (void)hipStreamDestroy(h->side);
   delete h;
   return SHAMPOO_OK;
 }

@@ -2,7 +2,9 @@
 BERT-Large-shaped layers (288 blocks of 1024 x 1024, strided views of the Q,
 K, V, O, FFN-in and FFN-out tensors), one grouped root refresh of all 576
 factors (statistics of 100 earlier gradients), then one step: statistics,
-two-sided preconditioning and the AdaGrad graft over all 288 blocks.
+then two-sided preconditioning and the AdaGrad graft over all 288 blocks in
+one shampoo_precondition_graft call (grouped, graft pass 2 of a group
+overlapping the next group's GEMMs).
 
 Every factor's root against eigh (damped condition number ~1.5: the 1e-3
 band), and every block's step against the fp64 oracle, which takes the same
@@ -71,8 +73,7 @@ def c4_run():
         B.shampoo_inv_root_batched(h, Ls + Rs, Lrs + Rrs, prm, ws, info)
         say("C4 full: stats + precondition + graft over 288 blocks")
         B.shampoo_update_stats(h, blocks)
-        B.shampoo_precondition(h, blocks)
-        B.shampoo_graft(h, blocks, ETA0)
+        B.shampoo_precondition_graft(h, blocks, ETA0)   # as the benchmark times the step
         torch.cuda.synchronize()
         del ws
     finally:
