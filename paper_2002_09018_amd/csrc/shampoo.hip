@@ -350,22 +350,27 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
 }
 
 // Group boundaries of shampoo_precondition_graft: cut[0] = 0 < cut[1] < ...
-// < cut[k] = nb, contiguous groups of about equal GEMM flops.  Calls with
-// fewer than 8 blocks or under 2^24 elements stay one group (their graft
-// pass 2 is too short to pay for the extra launches).
+// < cut[k] = nb, contiguous groups of about equal GEMM flops.  Only calls
+// whose blocks all have one shape and one root layout are grouped, with at
+// least 8 blocks and 2^24 elements: smaller calls have too short a graft
+// pass 2 to pay for the extra launches, and with blocks of mixed sizes every
+// group's launches end in a longer tail (measured: C5's step 0.5 ms slower).
 std::vector<int> precond_groups(const shampoo_block* blocks, int nb) {
   constexpr int kGroups = 4;
   std::vector<double> w(nb);
   double work = 0.0;
   int64_t elems = 0;
+  bool uniform = true;
   for (int i = 0; i < nb; ++i) {
     const shampoo_block& b = blocks[i];
     w[i] = (double)b.rows * b.cols * ((b.Lr ? b.rows : 0) + (b.Rr ? b.cols : 0));
     work += w[i];
     elems += (int64_t)b.rows * b.cols;
+    uniform = uniform && b.rows == blocks[0].rows && b.cols == blocks[0].cols &&
+              !b.Lr == !blocks[0].Lr && !b.Rr == !blocks[0].Rr;
   }
   std::vector<int> cut{0};
-  if (nb >= 8 && elems >= (int64_t(1) << 24)) {
+  if (uniform && nb >= 8 && elems >= (int64_t(1) << 24)) {
     double acc = 0.0;
     for (int i = 0; i + 1 < nb && (int)cut.size() < kGroups; ++i) {
       acc += w[i];

@@ -8,10 +8,10 @@ the step size sums the same squares in another order, so W agrees to 1e-5
 of the step; against the oracle the bars of the update tests (2e-3 on P and
 dW, 1e-6 on D, 1e-5 on the norms).  Cases: left, right and two-sided roots,
 ragged shapes on padded (strided) views, one launch over mixed sizes, bf16
-gradients, a zero gradient block, and a call large enough to be split into
-groups (graft pass 2 of a group on the handle's side stream, overlapping
-the next group's GEMMs), which must give every block bit for bit what a
-call with that block alone gives.
+gradients, a zero gradient block, and calls large and uniform enough to be
+split into groups (graft pass 2 of a group on the handle's side stream,
+overlapping the next group's GEMMs), which must give every block bit for
+bit what a call with that block alone gives.
 """
 import numpy as np
 import pytest
@@ -120,37 +120,37 @@ def test_fused_mixed_sizes_bf16_and_zero_block(env):
     assert np.array_equal(host(t["W"]), W0) and host(norms)[2] == 0.0
 
 
-def test_fused_groups_match_single_block_calls(env):
-    """12 blocks, 18.5M elements: the call runs in groups; P, D, W and the
-    norms of every block equal those of a call with that block alone (one
-    group), and agree with the oracle."""
+@pytest.mark.parametrize("nb,m,n,sides,bf16", [(8, 512, 4096, "L", False), (8, 512, 4096, "L", True),
+                                                (16, 1024, 1024, "LR", False)])
+def test_fused_groups_match_single_block_calls(env, nb, m, n, sides, bf16):
+    """Calls of 8+ blocks of one shape and 2^24 elements run in groups; P, D,
+    W and the norms of every block equal those of a call with that block
+    alone (one group), and agree with the oracle."""
     torch, B, dev, h = env
-    shapes = [(1024, 4096, "L"), (512, 512, "LR"), (1024, 1024, "LR"), (640, 1024, "R")] * 3
-    for bf16 in (False, True):
-        say("precondition_graft groups: 12 blocks, bf16", bf16)
-        cases = [_case(torch, dev, m, n, s, 0, 101 + i, bf16) for i, (m, n, s) in enumerate(shapes)]
-        grouped = [mk() for _, mk in cases]
-        single = [mk() for _, mk in cases]
-        ng = torch.zeros(3 * len(cases), device=dev)
-        ns = torch.zeros(3 * len(cases), device=dev)
-        B.shampoo_precondition_graft(h, [B.Block(**t) for t in grouped], 0.05, norms=ng)
-        for k, t in enumerate(single):
-            B.shampoo_precondition_graft(h, [B.Block(**t)], 0.05, norms=ns[3 * k:3 * k + 3])
-        torch.cuda.synchronize()
-        for k in range(len(cases)):
-            for key in ("P", "D", "W"):
-                assert np.array_equal(host(grouped[k][key]), host(single[k][key])), (bf16, k, key)
-        assert np.array_equal(host(ng), host(ns))
-        nf = host(ng).reshape(-1, 3)
-        for k in range(4):
-            ref = cases[k][0]
-            W0 = ref["W"].astype(np.float64)
-            Po = O.precondition(ref["G"], ref["Lr"], ref["Rr"])
-            out = O.graft_update(ref["W"], ref["D"], ref["G"], Po, 0.05)
-            assert rel(host(grouped[k]["P"]), Po) <= TOL, k
-            assert rel(host(grouped[k]["W"]) - W0, out["W"] - W0) <= TOL, k
-            assert rel(host(grouped[k]["D"]), out["D"]) <= 1e-6, k
-            assert abs(nf[k, 0] - out["norm_mg"]) <= 1e-5 * out["norm_mg"], k
+    say("precondition_graft groups:", nb, m, n, sides, "bf16", bf16)
+    cases = [_case(torch, dev, m, n, sides, 0, 101 + i, bf16) for i in range(nb)]
+    grouped = [mk() for _, mk in cases]
+    single = [mk() for _, mk in cases]
+    ng = torch.zeros(3 * nb, device=dev)
+    ns = torch.zeros(3 * nb, device=dev)
+    B.shampoo_precondition_graft(h, [B.Block(**t) for t in grouped], 0.05, norms=ng)
+    for k, t in enumerate(single):
+        B.shampoo_precondition_graft(h, [B.Block(**t)], 0.05, norms=ns[3 * k:3 * k + 3])
+    torch.cuda.synchronize()
+    for k in range(nb):
+        for key in ("P", "D", "W"):
+            assert np.array_equal(host(grouped[k][key]), host(single[k][key])), (k, key)
+    assert np.array_equal(host(ng), host(ns))
+    nf = host(ng).reshape(-1, 3)
+    for k in (0, nb // 2, nb - 1):
+        ref = cases[k][0]
+        W0 = ref["W"].astype(np.float64)
+        Po = O.precondition(ref["G"], ref["Lr"], ref["Rr"])
+        out = O.graft_update(ref["W"], ref["D"], ref["G"], Po, 0.05)
+        assert rel(host(grouped[k]["P"]), Po) <= TOL, k
+        assert rel(host(grouped[k]["W"]) - W0, out["W"] - W0) <= TOL, k
+        assert rel(host(grouped[k]["D"]), out["D"]) <= 1e-6, k
+        assert abs(nf[k, 0] - out["norm_mg"]) <= 1e-5 * out["norm_mg"], k
 
 
 def test_fused_rejects_rootless_block(env):
