@@ -130,11 +130,16 @@ __device__ __forceinline__ void epi_rows(const float* epi, float* dst, int64_t l
 // instantiation, so the plain kernels carry no extra registers).
 // SGG (not void): element type of G for the fused graft pass 1 (problems
 // with gD set; a separate instantiation as well).
-template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void>
+// WN = 2: 128 x 256 output tiles (plain outputs, both operands k-major;
+// tiles_n counts 256-wide tile columns).
+template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void, int WN = 1>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
                                                                int nprob, int total_tiles, int mixed) {
+  static_assert(WN == 1 || (!LIM && LA == kLayoutK && LB == kLayoutK), "wide tiles: plain k-major products");
+  constexpr int TN = kTile * WN;  // output tile width
   __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
-  __shared__ __attribute__((aligned(16))) float sb0[StageElems<float, LB>::value], sb1[StageElems<float, LB>::value];
+  __shared__ __attribute__((aligned(16))) float sb0[StageElems<float, LB, TN>::value],
+      sb1[StageElems<float, LB, TN>::value];
   // LIM: work depends on device-side counts and sits in the first logical
   // tiles; dispatch order (round robin over the XCDs) spreads it evenly.
   // mixed: problems of different sizes, tiles dealt in chunks (deal_chunks).
@@ -155,7 +160,7 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
     ti = lt / P.tiles_n;
     tj = lt % P.tiles_n;
   }
-  const int m0 = ti * kTile, n0 = tj * kTile;
+  const int m0 = ti * kTile, n0 = tj * TN;
   if (LIM && P.mcount && m0 >= *P.mcount) return;
 
   Operand<SA> A{reinterpret_cast<const SA*>(P.A), P.lda, P.a_rows, P.a_cols, P.a_aligned != 0};
@@ -180,16 +185,17 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
     if (LA == kLayoutK) A.rows = min(A.rows, K); else A.cols = min(A.cols, K);
     if (LB == kLayoutK) B.rows = min(B.rows, K); else B.cols = min(B.cols, K);
   }
-  WaveAcc<float> acc;
+  WaveAcc<float, WN> acc;
   acc.zero();
-  tile_mma<float, SA, LA, SB, LB>(acc, A, B, m0, n0, K, sa0, sa1, sb0, sb1, P.sym && ti == tj);
+  tile_mma<float, SA, LA, SB, LB, WN>(acc, A, B, m0, n0, K, sa0, sa1, sb0, sb1, P.sym && ti == tj);
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const bool diag = P.sym && ti == tj;
   // the squares of wave_role: on a diagonal tile waves 1 and 2 share the
   // upper-right square (block rows of its top and bottom halves)
   const bool helper = diag && wave == 2;
-  const int wm0 = m0 + (helper ? 0 : (wave >> 1) * kWaveTile), wn0 = n0 + (helper ? kWaveTile : (wave & 1) * kWaveTile);
+  const int wm0 = m0 + (helper ? 0 : (wave >> 1) * kWaveTile),
+            wn0 = n0 + (helper ? kWaveTile : (wave & 1) * kWaveTile * WN);
   typedef Mfma<float> F;
   if constexpr (!std::is_same<SGG, void>::value) {
     // plain outputs only (preconditioning); P.gD set: P with the fused graft
@@ -198,29 +204,31 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
     {
       __shared__ double gred[kThreads / 64];
       float smg = 0.f, sps = 0.f;
-      const bool vec = m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 && (P.ldg & 3) == 0 &&
+      const bool vec = m0 + kTile <= P.M && n0 + TN <= P.N && (P.ldc & 3) == 0 && (P.ldg & 3) == 0 &&
                        (reinterpret_cast<uintptr_t>(P.C) & 15) == 0 && (reinterpret_cast<uintptr_t>(P.gD) & 15) == 0 &&
                        (reinterpret_cast<uintptr_t>(P.gG) & (4 * sizeof(SGG) - 1)) == 0;
-      const bool rows16 = m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
+      const bool rows16 = m0 + kTile <= P.M && n0 + TN <= P.N && (P.ldc & 3) == 0 &&
                           (reinterpret_cast<uintptr_t>(P.C) & 15) == 0;
-      // a block row of the wave's accumulators goes through the wave's own
-      // LDS slice; the graft work then walks it row by row (rolled loops,
-      // so the epilogue keeps the main loop's register budget)
+      // a block row of the wave's accumulators (64 columns at a time) goes
+      // through the wave's own LDS slice; the graft work then walks it row by
+      // row (rolled loops, so the epilogue keeps the main loop's register
+      // budget)
       float* epi = reinterpret_cast<float*>(wave == 0 ? sa0 : (wave == 1 ? sa1 : (wave == 2 ? sb0 : sb1)));
 #pragma unroll
-      for (int i = 0; i < WaveAcc<float>::NB; ++i) {
+      for (int ih = 0; ih < WaveAcc<float>::NB * WN; ++ih) {
+        const int i = ih / WN, h = ih % WN;
 #pragma unroll
         for (int j = 0; j < WaveAcc<float>::NB; ++j)
 #pragma unroll
           for (int v = 0; v < F::kAcc; ++v)
-            epi[F::row(lane, v) * kWaveTile + j * F::kM + F::col(lane)] = P.alpha * acc.c[i][j][v];
-        const int r0 = wm0 + i * F::kM;
+            epi[F::row(lane, v) * kWaveTile + j * F::kM + F::col(lane)] = P.alpha * acc.c[i][h * WaveAcc<float>::NB + j][v];
+        const int r0 = wm0 + i * F::kM, c0 = wn0 + h * kWaveTile;
         if (!graft && rows16) {
-          epi_rows(epi, P.C + (int64_t)r0 * P.ldc + wn0, P.ldc, lane);
+          epi_rows(epi, P.C + (int64_t)r0 * P.ldc + c0, P.ldc, lane);
         } else if (!graft) {
 #pragma unroll 1
           for (int idx = lane; idx < F::kM * kWaveTile; idx += 64) {
-            const int r = r0 + idx / kWaveTile, c = wn0 + idx % kWaveTile;
+            const int r = r0 + idx / kWaveTile, c = c0 + idx % kWaveTile;
             if (r < P.M && c < P.N) gstore<float>(P.C + (int64_t)r * P.ldc + c, epi[idx]);
           }
         } else if (vec) {
@@ -229,8 +237,8 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
           for (int k = 0; k < F::kM * kSeg / 64; ++k) {
             const int idx = lane + 64 * k, rr = idx / kSeg, c4 = (idx % kSeg) * 4;
             const f4v pv = *reinterpret_cast<const f4v*>(epi + rr * kWaveTile + c4);
-            const int64_t gi = (int64_t)(r0 + rr) * P.ldg + wn0 + c4;
-            gstore<f4v>(P.C + (int64_t)(r0 + rr) * P.ldc + wn0 + c4, pv);
+            const int64_t gi = (int64_t)(r0 + rr) * P.ldg + c0 + c4;
+            gstore<f4v>(P.C + (int64_t)(r0 + rr) * P.ldc + c0 + c4, pv);
             float g[4];
             G4<SGG>::load(P.gG, gi, g);
             f4v d = gload<f4v>(P.gD + gi);
@@ -247,7 +255,7 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
 #pragma unroll 1
           for (int idx = lane; idx < F::kM * kWaveTile; idx += 64) {
             const int rr = idx / kWaveTile, cc = idx % kWaveTile;
-            const int r = r0 + rr, c = wn0 + cc;
+            const int r = r0 + rr, c = c0 + cc;
             if (r >= P.M || c >= P.N) continue;
             const float x = epi[rr * kWaveTile + cc];
             gstore<float>(P.C + (int64_t)r * P.ldc + c, x);
@@ -278,6 +286,7 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   // the transposed tile).  The old output is symmetric too, so the four old
   // values of rows r..r+3, column c are one 16-byte load of row c (the
   // mirror this lane then overwrites; no other lane or workgroup touches it).
+  if constexpr (WN == 1)
   if (P.sym && !diag && m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
       (reinterpret_cast<uintptr_t>(P.C) & 15) == 0) {
 #pragma unroll
@@ -306,22 +315,24 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
   // (not compiled into the row x row instantiation, which only forms
   // symmetric statistics and would lose an occupancy step to it).
   if constexpr (!(LA == kLayoutRow && LB == kLayoutRow))
-  if (!P.sym && m0 + kTile <= P.M && n0 + kTile <= P.N && (P.ldc & 3) == 0 &&
+  if (!P.sym && m0 + kTile <= P.M && n0 + TN <= P.N && (P.ldc & 3) == 0 &&
       (reinterpret_cast<uintptr_t>(P.C) & 15) == 0) {
     float* epi = reinterpret_cast<float*>(wave == 0 ? sa0 : (wave == 1 ? sa1 : (wave == 2 ? sb0 : sb1)));
 #pragma unroll
-    for (int i = 0; i < WaveAcc<float>::NB; ++i) {
+    for (int ih = 0; ih < WaveAcc<float>::NB * WN; ++ih) {
+      const int i = ih / WN, h = ih % WN;
+      const int c0 = wn0 + h * kWaveTile;
 #pragma unroll
       for (int j = 0; j < WaveAcc<float>::NB; ++j)
 #pragma unroll
         for (int v = 0; v < F::kAcc; ++v) {
           const int r = wm0 + i * F::kM + F::row(lane, v);
-          const int c = wn0 + j * F::kM + F::col(lane);
-          float x = P.alpha * acc.c[i][j][v];
+          const int c = c0 + j * F::kM + F::col(lane);
+          float x = P.alpha * acc.c[i][h * WaveAcc<float>::NB + j][v];
           if (P.beta != 0.f) x += P.beta * gload<float>(P.C + (int64_t)r * P.ldc + c);
           epi[F::row(lane, v) * kWaveTile + j * F::kM + F::col(lane)] = x;
         }
-      epi_rows(epi, P.C + (int64_t)(wm0 + i * F::kM) * P.ldc + wn0, P.ldc, lane);
+      epi_rows(epi, P.C + (int64_t)(wm0 + i * F::kM) * P.ldc + c0, P.ldc, lane);
     }
     return;
   }
@@ -329,7 +340,7 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
 #pragma unroll
   for (int i = 0; i < WaveAcc<float>::NB; ++i)
 #pragma unroll
-    for (int j = 0; j < WaveAcc<float>::NB; ++j)
+    for (int j = 0; j < WaveAcc<float, WN>::NBJ; ++j)
 #pragma unroll
       for (int v = 0; v < F::kAcc; ++v) {
         const int r = wm0 + i * F::kM + F::row(lane, v);

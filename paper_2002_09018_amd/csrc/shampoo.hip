@@ -237,12 +237,12 @@ shampoo_status set_lds(Handle* h, K kernel, int bytes) {
 }
 
 // ---------------------------------------------------------------- GEMM
-template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void>
+template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void, int WN = 1>
 shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t s, int cls) {
   if (probs.empty()) return SHAMPOO_OK;
   int total = 0, mixed = 0;
   for (auto& p : probs) {
-    p.tiles_n = cdiv(p.N, kTile);
+    p.tiles_n = cdiv(p.N, kTile * WN);  // WN = 2: 256-wide tile columns (plain outputs only)
     p.tile_begin = total;
     total += p.sym ? p.tiles_n * (p.tiles_n + 1) / 2 : cdiv(p.M, kTile) * p.tiles_n;
     mixed |= p.M != probs[0].M || p.N != probs[0].N || p.K != probs[0].K;
@@ -252,7 +252,7 @@ shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t 
   const int grid = mixed && !LIM ? cdiv(total, 8 * kDealChunk) * 8 * kDealChunk : total;
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
-  auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM, SGG>;
+  auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM, SGG, WN>;
   const int lds = 0;  // static LDS
   const int np = (int)probs.size();
   STATUS_TRY(launch(h, cls, s, [&] {
@@ -395,6 +395,15 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
   // GEMM's output tiles)
   std::vector<int> pbegin(nb), pcount(nb);
   int ptotal = 0;
+  // Without the fused graft, the products by Lr (P = Lr G, or Lr Z) run on
+  // 128 x 256 tiles when every block with Lr has a width that is a multiple
+  // of 256 (C2: 126 -> 132 TFLOP/s; fewer operand bytes per flop).  G Rr, and
+  // every GEMM with the fused graft, keep 128 x 128: the wide kernel runs two
+  // workgroups per CU, which hides the graft epilogue less than four
+  // (measured: no gain).
+  bool wide = !fuse_graft;
+  for (int i = 0; i < nb; ++i)
+    if (blocks[i].Lr && blocks[i].cols % (2 * kTile) != 0) wide = false;
   if (fuse_graft) {
     for (int i = 0; i < nb; ++i) {
       pbegin[i] = ptotal;
@@ -514,8 +523,13 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
     return tables_done(h, s);
   }
   STATUS_TRY((run_gemm<SG, kLayoutRow, float, kLayoutK>(h, g_rr, s, SHAMPOO_KCLASS_PRECOND)));
-  STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
-  STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK>(h, lr_g, s, SHAMPOO_KCLASS_PRECOND)));
+  if (wide) {
+    STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK, false, void, 2>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
+    STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK, false, void, 2>(h, lr_g, s, SHAMPOO_KCLASS_PRECOND)));
+  } else {
+    STATUS_TRY((run_gemm<float, kLayoutK, float, kLayoutK>(h, lr_z, s, SHAMPOO_KCLASS_PRECOND)));
+    STATUS_TRY((run_gemm<float, kLayoutK, SG, kLayoutK>(h, lr_g, s, SHAMPOO_KCLASS_PRECOND)));
+  }
   if (!copy.empty()) {
     int total = 0;
     std::vector<GraftBlock> tb = graft_table(copy.data(), (int)copy.size(), &total);

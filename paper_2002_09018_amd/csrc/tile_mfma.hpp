@@ -4,7 +4,9 @@
 // Workgroup: 256 threads = 4 wave64s arranged 2 x 2, each owning a 64 x 64
 // sub-tile as a grid of MFMA blocks (fp32: 2 x 2 blocks of 32 x 32 with
 // v_mfma_f32_32x32x2_f32; fp64: 4 x 4 blocks of 16 x 16 with
-// v_mfma_f64_16x16x4_f64).  The k dimension is streamed through LDS in stages
+// v_mfma_f64_16x16x4_f64).  Wide tiles (WN = 2, plain fp32 products with both
+// operands k-major) are 128 x 256: each wave owns 64 x 128 (2 x 4 blocks),
+// and B's stage is 256 columns wide.  The k dimension is streamed through LDS in stages
 // of kBK = 16, double-buffered: the global loads of stage s+1 are in flight in
 // registers while the MFMAs of stage s run (on interior tiles spread over the
 // stage's k-steps, see tile_loop).
@@ -104,16 +106,17 @@ struct Mfma<double> {
 // contiguous runs (no pad needed: measured conflict-free).  kLayoutRow:
 // [128][kBK] rows padded by 16 bytes, so the 16-byte fragment reads of 8
 // consecutive rows fall in distinct banks and every row stays 16-byte aligned.
-template <typename T, int LAYOUT>
+template <typename T, int LAYOUT, int TW = kTile>
 struct Pitch {
   static constexpr int value =
-      LAYOUT == kLayoutK ? kTile : Mfma<T>::kBK + 16 / (int)sizeof(T);
+      LAYOUT == kLayoutK ? TW : Mfma<T>::kBK + 16 / (int)sizeof(T);
 };
 
-// Elements of one operand stage in LDS.
-template <typename T, int LAYOUT>
+// Elements of one operand stage in LDS (TW: the operand's tile width, 128,
+// or 256 for B of a wide tile).
+template <typename T, int LAYOUT, int TW = kTile>
 struct StageElems {
-  static constexpr int value = (LAYOUT == kLayoutK ? Mfma<T>::kBK : kTile) * Pitch<T, LAYOUT>::value;
+  static constexpr int value = (LAYOUT == kLayoutK ? Mfma<T>::kBK : TW) * Pitch<T, LAYOUT, TW>::value;
   static_assert(value * (int)sizeof(T) % 16 == 0, "stages must stay 16-byte aligned");
 };
 
@@ -168,15 +171,15 @@ struct Operand {
   bool aligned;  // ptr and ld allow 16-byte vector loads
 };
 
-// Per-thread staging registers for one operand stage.
-template <typename T, typename S, int LAYOUT>
+// Per-thread staging registers for one operand stage (TW: tile width).
+template <typename T, typename S, int LAYOUT, int TW = kTile>
 struct Loader {
   typedef typename SrcVec<S>::type V;
   static constexpr int VE = SrcVec<S>::n;
   static constexpr int BK = Mfma<T>::kBK;
-  static constexpr int NVEC = BK * kTile / VE;
+  static constexpr int NVEC = BK * TW / VE;
   static constexpr int PER = NVEC / kThreads;
-  static constexpr int LDP = Pitch<T, LAYOUT>::value;
+  static constexpr int LDP = Pitch<T, LAYOUT, TW>::value;
   static_assert(NVEC % kThreads == 0, "stage must split evenly over the workgroup");
   V buf[PER];
 
@@ -184,7 +187,7 @@ struct Loader {
   static __device__ __forceinline__ void slot(int tid, int i, int& sr, int& sc) {
     const int v = tid + i * kThreads;
     if (LAYOUT == kLayoutK) {
-      constexpr int VPR = kTile / VE;
+      constexpr int VPR = TW / VE;
       sr = v / VPR;
       sc = (v % VPR) * VE;
     } else {
@@ -197,8 +200,8 @@ struct Loader {
   // Whether the stage with storage origin (r0, c0) lies inside the operand
   // and is 16-byte aligned (plain 16-byte loads, no bounds checks).
   static __device__ __forceinline__ bool full(const Operand<S>& op, int r0, int c0) {
-    constexpr int SR = LAYOUT == kLayoutK ? BK : kTile;
-    constexpr int SC = LAYOUT == kLayoutK ? kTile : BK;
+    constexpr int SR = LAYOUT == kLayoutK ? BK : TW;
+    constexpr int SC = LAYOUT == kLayoutK ? TW : BK;
     return op.aligned && (r0 + SR <= op.rows) && (c0 + SC <= op.cols);
   }
 
@@ -282,30 +285,32 @@ __host__ __device__ constexpr bool block_used(int i, int j) {
 struct WaveRole {
   int wm, wn, mode;
 };
-__device__ __forceinline__ WaveRole wave_role(int wave, bool diag) {
-  if (!diag) return {(wave >> 1) * kWaveTile, (wave & 1) * kWaveTile, kBlocksAll};
+__device__ __forceinline__ WaveRole wave_role(int wave, bool diag, int wn = 1) {
+  if (!diag) return {(wave >> 1) * kWaveTile, (wave & 1) * kWaveTile * wn, kBlocksAll};
   if (wave == 0) return {0, 0, kBlocksUpper};
   if (wave == 3) return {kWaveTile, kWaveTile, kBlocksUpper};
   return {0, kWaveTile, wave == 1 ? kBlocksTopHalf : kBlocksBottomHalf};
 }
 
-// Accumulators of one wave: an NB x NB grid of MFMA blocks covering 64 x 64.
-template <typename T>
+// Accumulators of one wave: an NB x NBJ grid of MFMA blocks covering
+// 64 x 64 WN.
+template <typename T, int WN = 1>
 struct WaveAcc {
   static constexpr int NB = kWaveTile / Mfma<T>::kM;
-  typename Mfma<T>::acc_t c[NB][NB];
+  static constexpr int NBJ = NB * WN;
+  typename Mfma<T>::acc_t c[NB][NBJ];
 
   __device__ __forceinline__ void zero() {
 #pragma unroll
     for (int i = 0; i < NB; ++i)
 #pragma unroll
-      for (int j = 0; j < NB; ++j)
+      for (int j = 0; j < NBJ; ++j)
 #pragma unroll
         for (int v = 0; v < Mfma<T>::kAcc; ++v) c[i][j][v] = (T)0;
   }
 
   // The MFMA k-steps of one LDS stage (kBK / kK steps) over the wave's
-  // NB x NB blocks.  hook(s) runs at k-step s, after the fragment reads of
+  // NB x NBJ blocks.  hook(s) runs at k-step s, after the fragment reads of
   // step s+1 are issued and before the MFMAs of step s.
   // MODE (kBlocks*): the blocks of the wave's square that are computed.
   template <int LA, int LB, int LDPA, int LDPB, int MODE, typename Hook>
@@ -320,7 +325,7 @@ struct WaveAcc {
     const int ml = lane % Mfma<T>::kM;
     // kLayoutK fragments: one element per k-step, double-buffered in
     // registers so the reads of step s+1 are issued before the MFMAs of s.
-    T fa[2][NB], fb[2][NB];
+    T fa[2][NB], fb[2][NBJ];
     const T* pa = a + g * KS * LDPA + wm0 + ml;
     const T* pb = b + g * KS * LDPB + wn0 + ml;
     if (LA == kLayoutK) {
@@ -329,13 +334,13 @@ struct WaveAcc {
     }
     if (LB == kLayoutK) {
 #pragma unroll
-      for (int j = 0; j < NB; ++j) fb[S0 & 1][j] = pb[S0 * LDPB + j * Mfma<T>::kM];
+      for (int j = 0; j < NBJ; ++j) fb[S0 & 1][j] = pb[S0 * LDPB + j * Mfma<T>::kM];
     }
     // kLayoutRow fragments: VP k-steps per 16-byte read, read per chunk of
     // VP steps (the registers of one chunk only)
 #pragma unroll
     for (int cch = S0 / VP; cch < S1 / VP; ++cch) {
-      vec_t ra[LA == kLayoutRow ? NB : 1], rb[LB == kLayoutRow ? NB : 1];
+      vec_t ra[LA == kLayoutRow ? NB : 1], rb[LB == kLayoutRow ? NBJ : 1];
       if (LA == kLayoutRow) {
 #pragma unroll
         for (int i = 0; i < NB; ++i)
@@ -343,7 +348,7 @@ struct WaveAcc {
       }
       if (LB == kLayoutRow) {
 #pragma unroll
-        for (int j = 0; j < NB; ++j)
+        for (int j = 0; j < NBJ; ++j)
           rb[j] = *reinterpret_cast<const vec_t*>(b + (wn0 + j * Mfma<T>::kM + ml) * LDPB + g * KS + cch * VP);
       }
 #pragma unroll
@@ -357,7 +362,7 @@ struct WaveAcc {
           }
           if (LB == kLayoutK) {
 #pragma unroll
-            for (int j = 0; j < NB; ++j) fb[cur ^ 1][j] = pb[(s + 1) * LDPB + j * Mfma<T>::kM];
+            for (int j = 0; j < NBJ; ++j) fb[cur ^ 1][j] = pb[(s + 1) * LDPB + j * Mfma<T>::kM];
           }
         }
         hook(s);
@@ -365,7 +370,7 @@ struct WaveAcc {
 #pragma unroll
         for (int i = 0; i < NB; ++i)
 #pragma unroll
-          for (int j = 0; j < NB; ++j) {
+          for (int j = 0; j < NBJ; ++j) {
             if (!block_used<MODE, NB>(i, j)) continue;
             c[i][j] = Mfma<T>::mma(LA == kLayoutRow ? ra[i][e] : fa[cur][i], LB == kLayoutRow ? rb[j][e] : fb[cur][j],
                                    c[i][j]);
@@ -389,13 +394,13 @@ struct WaveAcc {
 // buffer pair instead of testing for the end.  Other tiles (ragged edges, and
 // fp64, whose stages are too short to spread) load a whole stage at its start
 // and write it to LDS at its end.
-template <int MODE, typename T, typename SA, int LA, typename SB, int LB>
-__device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
+template <int MODE, typename T, typename SA, int LA, typename SB, int LB, int WN = 1>
+__device__ __forceinline__ void tile_loop(WaveAcc<T, WN>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
                                           int n0, int K, T* a0, T* a1, T* b0, T* b1, int wm0, int wn0) {
   constexpr int BK = Mfma<T>::kBK;
   constexpr int KS = BK / Mfma<T>::kK;
   typedef Loader<T, SA, LA> LdA;
-  typedef Loader<T, SB, LB> LdB;
+  typedef Loader<T, SB, LB, kTile * WN> LdB;
   constexpr bool kSpread = 2 * LdA::PER <= KS && 2 * LdB::PER <= KS;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -458,25 +463,29 @@ __device__ __forceinline__ void tile_loop(WaveAcc<T>& acc, const Operand<SA>& A,
 }
 
 
-// Full k-loop of one 128 x 128 output tile.
+// Full k-loop of one 128 x (128 WN) output tile.
 //   A: layout LA; kLayoutK reads storage rows k (cols m0..), kLayoutRow
 //      reads storage rows m0.. (cols k).
 //   B: layout LB; kLayoutK reads storage rows k (cols n0..), kLayoutRow
 //      reads storage rows n0.. (cols k).
-// diag: diagonal tile of a symmetric output; the waves take the squares and
-// block sets of wave_role (the epilogue must use the same roles).
-template <typename T, typename SA, int LA, typename SB, int LB>
-__device__ __forceinline__ void tile_mma(WaveAcc<T>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
+// diag: diagonal tile of a symmetric output (WN = 1 only); the waves take
+// the squares and block sets of wave_role (the epilogue must use the same
+// roles).
+template <typename T, typename SA, int LA, typename SB, int LB, int WN = 1>
+__device__ __forceinline__ void tile_mma(WaveAcc<T, WN>& acc, const Operand<SA>& A, const Operand<SB>& B, int m0,
                                          int n0, int K, T* a0, T* a1, T* b0, T* b1, bool diag = false) {
-  const WaveRole ro = wave_role(threadIdx.x >> 6, diag);
-  if (ro.mode == kBlocksAll)
-    tile_loop<kBlocksAll, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
-  else if (ro.mode == kBlocksUpper)
-    tile_loop<kBlocksUpper, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
-  else if (ro.mode == kBlocksTopHalf)
-    tile_loop<kBlocksTopHalf, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
-  else
-    tile_loop<kBlocksBottomHalf, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+  static_assert(WN == 1 || WN == 2, "tile width 128 or 256");
+  const WaveRole ro = wave_role(threadIdx.x >> 6, WN == 1 && diag, WN);
+  if (WN > 1 || ro.mode == kBlocksAll)
+    tile_loop<kBlocksAll, T, SA, LA, SB, LB, WN>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+  else if constexpr (WN == 1) {
+    if (ro.mode == kBlocksUpper)
+      tile_loop<kBlocksUpper, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+    else if (ro.mode == kBlocksTopHalf)
+      tile_loop<kBlocksTopHalf, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+    else
+      tile_loop<kBlocksBottomHalf, T, SA, LA, SB, LB>(acc, A, B, m0, n0, K, a0, a1, b0, b1, ro.wm, ro.wn);
+  }
 }
 
 // Workgroup id -> logical tile index so that consecutive logical tiles land
