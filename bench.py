@@ -280,7 +280,10 @@ def run_c4(args, torch, B):
     torch.cuda.synchronize()
     root_ms = (time.perf_counter() - t0) * 1e3
     iters = [i["iters"] for i in B.decode_root_info(info)]
-    log(f"root refresh: {len(As)} roots in {root_ms:.1f} ms")
+    # the same call once more with per-launch events: the Newton products' own time
+    _, rtimes = time_steps(torch, B, h, lambda: B.shampoo_inv_root_batched(h, As, Xs, prm, ws, info), 1)
+    root_newton_ms = rtimes["newton_f32"][0]
+    log(f"root refresh: {len(As)} roots in {root_ms:.1f} ms (Newton products {root_newton_ms:.1f} ms)")
     # the next refresh (step 200) warm-started from these roots: 100 more
     # gradients add an independent Wishart(1024, 102400 dof) draw
     warm = None
@@ -334,7 +337,9 @@ def run_c4(args, torch, B):
         **step_report(K, elapsed, times, el_s, t_s, flops_stats, flops_prec, bytes_graft, K * nb * d * d * 12),
         "root_refresh": {"roots": len(As), "ms": root_ms, "roots_per_s": len(As) / root_ms * 1e3,
                          "iters_mean": float(np.mean(iters)),
-                         "newton_tflops": prods * d * d * (d + 1) / (root_ms * 1e-3) / 1e12},
+                         "newton_ms": root_newton_ms,
+                         "newton_tflops": prods * d * d * (d + 1) / (root_newton_ms * 1e-3) / 1e12,
+                         "call_tflops": prods * d * d * (d + 1) / (root_ms * 1e-3) / 1e12},
         "root_refresh_warm_step200": warm,
     }
     kr = out["kernels"]
