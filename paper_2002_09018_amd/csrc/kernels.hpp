@@ -1771,12 +1771,14 @@ __global__ void root_info_kernel(const NewtonJob<T>* __restrict__ jobs, int njob
   if ((s.status == kConverged || s.status == kStagnated) && s.warm != 1) {
     const double tl = fmax((double)tol, (double)s.resid);
     double lo = 1e-30, hi = 1.0;  // N(lo) > iters >= N(hi) (N decreasing on (0, 1])
-    if (scalar_iters(lo, p, tl, 400) <= s.iters) {
+    // only N(m) <= iters is asked: counting stops at iters + 1
+    const int cap = s.iters + 1;
+    if (scalar_iters(lo, p, tl, cap) <= s.iters) {
       kappa = 1.0;
     } else {
       for (int b = 0; b < 40; ++b) {  // hi / lo = 1e30^(2^-40) < 1 + 1e-10
         const double mid = sqrt(lo * hi);
-        if (scalar_iters(mid, p, tl, 400) <= s.iters) hi = mid; else lo = mid;
+        if (scalar_iters(mid, p, tl, cap) <= s.iters) hi = mid; else lo = mid;
       }
       kappa = (1.0 + p) / (2.0 * hi);
     }

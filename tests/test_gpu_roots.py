@@ -144,6 +144,34 @@ def test_c2_full_size_grouped_all(env):
         worst_res = max(worst_res, float(torch.linalg.norm(Rm)))
     say(f"C2 true residual ||X^4 A_d - I||_F max over 96: {worst_res:.3e}")
     assert worst_res <= 4e-3
+    # the condition estimate of the info record: the kappa whose cold-start
+    # eigenvalue (p+1)/(2 kappa) takes exactly the reported iterations in the
+    # scalar recurrence (a bisection on the host, with the same 40 steps)
+    for inf in info[::7]:
+        est = _cond_from_iters(4, max(1e-6, inf["resid"]), inf["iters"])
+        assert abs(inf["cond_est"] - est) <= 1e-5 * est, (inf, est)
+
+
+def _cond_from_iters(p, tol, iters):
+    def count(m):
+        k = 0
+        while abs(m - 1.0) > tol and k <= iters:
+            f, fp = (p + 1.0 - m) / p, 1.0
+            for _ in range(p):
+                fp *= f
+            m = fp * m
+            k += 1
+        return k
+    lo, hi = 1e-30, 1.0
+    if count(lo) <= iters:
+        return 1.0
+    for _ in range(40):
+        mid = (lo * hi) ** 0.5
+        if count(mid) <= iters:
+            hi = mid
+        else:
+            lo = mid
+    return (1.0 + p) / (2.0 * hi)
 
 
 @pytest.mark.skip(reason="stage-chain Newton launches (one persistent launch per iteration with per-matrix "
