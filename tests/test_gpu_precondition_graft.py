@@ -3,7 +3,9 @@ the GEMM that writes P, then graft pass 2) against the two separate calls
 shampoo_precondition + shampoo_graft(beta1 = 0, use_shampoo) and against the
 oracle (precondition, graft_update).
 
-P and D are the same arithmetic in both routes and must agree bit for bit;
+P and D are the same arithmetic in both routes and must agree bit for bit
+(also where the separate call runs 128 x 256 tiles and the fused one
+128 x 128);
 the step size sums the same squares in another order, so W agrees to 1e-5
 of the step; against the oracle the bars of the update tests (2e-3 on P and
 dW, 1e-6 on D, 1e-5 on the norms).  Cases: left, right and two-sided roots,
@@ -91,7 +93,10 @@ def _check(cases, fused, split, nf, ns, eta0=0.05):
 
 @pytest.mark.parametrize("m,n,sides,pad", [(1024, 4096, "L", 0), (256, 384, "R", 0), (512, 512, "LR", 0),
                                            (200, 96, "LR", 3), (129, 257, "L", 2), (77, 45, "R", 1),
-                                           (1, 1, "LR", 0), (300, 130, "LR", 4)])
+                                           (1, 1, "LR", 0), (300, 130, "LR", 4),
+                                           # widths that are multiples of 256: the separate call takes
+                                           # 128 x 256 tiles, on ragged rows and unaligned row strides
+                                           (300, 768, "LR", 5), (129, 512, "L", 3)])
 def test_fused_matches_two_calls(env, m, n, sides, pad):
     torch, B, dev, h = env
     say("precondition_graft", m, n, sides, pad)
