@@ -49,7 +49,7 @@ namespace shp {
 // Minimum waves per SIMD requested from the register allocator
 // (__launch_bounds__ second argument).  Measured per kernel: the grouped
 // GEMMs run best at 2 (the allocator then reaches 3-4 waves without
-// spilling), the fp32 Newton products at 2 as well (136 registers, 3 waves,
+// spilling), the fp32 Newton products at 2 as well (138 registers, 3 waves,
 // no spills: +1-2% over asking for 4, which spilled in the epilogue once
 // every wave of a diagonal tile computes), fp64 at 2.
 constexpr int kMinWaves = SHP_MIN_WAVES;
