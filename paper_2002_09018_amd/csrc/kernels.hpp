@@ -480,52 +480,102 @@ __host__ __device__ __forceinline__ uint32_t pack_tile(int j, int ti, int tj) {
   return ((uint32_t)j << 10) | ((uint32_t)ti << 5) | (uint32_t)tj;
 }
 
-// Compact list of the tiles of the matrices still active, in job order:
-// tlist[0, *tcount).  tmap holds every tile of a launch (job-major: the
-// upper tiles of the symmetric products, or the full grid of the warm
-// start's) and ubegin[j] the first of job j (ubegin[njobs] = their number).  Called by one
-// whole workgroup; st must be final for every job (the caller's threads have
-// passed a barrier since they last wrote it).
+// Compact list of the tiles of the matrices still active, in two parts:
+// tlist[0, tcount[1]) the early tiles, then tlist[tcount[1], tcount[0]) the
+// late ones, each part in job order.  tmap holds every tile of a launch
+// (job-major: the upper tiles of the symmetric products, row-major, or the
+// full grid of the warm start's) and ubegin[j] the first of job j
+// (ubegin[njobs] = their number).  diag_last (upper tiles only): the
+// diagonal tiles, which cost less than the others, form the late part, and
+// the launch runs each XCD's share of them last; else every tile is early.
+// A job's upper tiles end with its last diagonal tile (T-1, T-1), so it has
+// that tile's row + 1 of them.  Called by one whole workgroup; st must be
+// final for every job (the caller's threads have passed a barrier since they
+// last wrote it).
 __device__ __forceinline__ void build_tile_list(const RootState* __restrict__ st, int njobs,
                                                 const uint32_t* __restrict__ tmap, const int* __restrict__ ubegin,
-                                                uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
-  __shared__ int scan[kThreads];
-  __shared__ int base;
-  if (threadIdx.x == 0) base = 0;
+                                                int diag_last, uint32_t* __restrict__ tlist,
+                                                int* __restrict__ tcount) {
+  __shared__ int scan[2][kThreads];
+  __shared__ int base[2];
+  __shared__ int red[2][kThreads / 64];
+  auto ndiag = [&](int j) { return (int)((tmap[ubegin[j + 1] - 1] >> 5) & 31) + 1; };
+  // tiles of the active matrices and their late ones: where the late part starts
+  int all = 0, late = 0;
+  for (int j = threadIdx.x; j < njobs; j += kThreads)
+    if (st[j].status == kActive) {
+      all += ubegin[j + 1] - ubegin[j];
+      if (diag_last) late += ndiag(j);
+    }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    all += __shfl_xor(all, o, 64);
+    late += __shfl_xor(late, o, 64);
+  }
+  if ((threadIdx.x & 63) == 0) {
+    red[0][threadIdx.x >> 6] = all;
+    red[1][threadIdx.x >> 6] = late;
+  }
+  if (threadIdx.x == 0) base[0] = base[1] = 0;
   __syncthreads();
+  int early = 0;
+  for (int w = 0; w < kThreads / 64; ++w) early += red[0][w] - red[1][w];
   for (int j0 = 0; j0 < njobs; j0 += kThreads) {
     const int j = j0 + (int)threadIdx.x;
-    const int b = j < njobs ? ubegin[j] : 0;
-    const int n = (j < njobs && st[j].status == kActive) ? ubegin[j + 1] - b : 0;
-    scan[threadIdx.x] = n;
+    const bool on = j < njobs && st[j].status == kActive;
+    const bool mv = on && diag_last;
+    const int b = on ? ubegin[j] : 0, n = on ? ubegin[j + 1] - b : 0;
+    const int n1 = mv ? ndiag(j) : 0, n0 = n - n1;
+    scan[0][threadIdx.x] = n0;
+    scan[1][threadIdx.x] = n1;
     __syncthreads();
-    for (int o = 1; o < kThreads; o <<= 1) {  // inclusive scan
-      const int v = (int)threadIdx.x >= o ? scan[threadIdx.x - o] : 0;
+    for (int o = 1; o < kThreads; o <<= 1) {  // inclusive scans
+      const int v0 = (int)threadIdx.x >= o ? scan[0][threadIdx.x - o] : 0;
+      const int v1 = (int)threadIdx.x >= o ? scan[1][threadIdx.x - o] : 0;
       __syncthreads();
-      scan[threadIdx.x] += v;
+      scan[0][threadIdx.x] += v0;
+      scan[1][threadIdx.x] += v1;
       __syncthreads();
     }
-    const int off = base + scan[threadIdx.x] - n;
-    for (int k = 0; k < n; ++k) tlist[off + k] = tmap[b + k];
+    int o0 = base[0] + scan[0][threadIdx.x] - n0;
+    int o1 = early + base[1] + scan[1][threadIdx.x] - n1;
+    if (mv) {
+      for (int k = 0; k < n; ++k) {
+        const uint32_t c = tmap[b + k];
+        if (((c >> 5) & 31) == (c & 31)) tlist[o1++] = c;
+        else tlist[o0++] = c;
+      }
+    } else {
+      for (int k = 0; k < n; ++k) tlist[o0 + k] = tmap[b + k];
+    }
     __syncthreads();
-    if (threadIdx.x == 0) base += scan[kThreads - 1];
+    if (threadIdx.x == 0) {
+      base[0] += scan[0][kThreads - 1];
+      base[1] += scan[1][kThreads - 1];
+    }
     __syncthreads();
   }
-  if (threadIdx.x == 0) *tcount = base;
+  if (threadIdx.x == 0) {
+    tcount[0] = early + base[1];
+    tcount[1] = early;
+  }
 }
 
 __global__ __launch_bounds__(kThreads) void tile_list_kernel(const RootState* __restrict__ st, int njobs,
                                                             const uint32_t* __restrict__ tmap,
-                                                            const int* __restrict__ ubegin,
+                                                            const int* __restrict__ ubegin, int diag_last,
                                                             uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
-  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
+  build_tile_list(st, njobs, tmap, ubegin, diag_last, tlist, tcount);
 }
 
 // tlist / tcount: the compact upper-tile list of the matrices still active
-// (build_tile_list); the grid is sized for every upper tile, and the
-// workgroups past S.nprod * *tcount return at once.  The workgroup -> tile
-// remap is taken over the active part only, so the work of a few remaining
-// matrices still spreads over every XCD.
+// (build_tile_list: early tiles, then any late diagonal ones); the grid is
+// sized for every upper tile (plus the slack of xcd_split_remap), and the
+// workgroups past the work return at once.  The workgroup -> tile remap is
+// taken over the active part only, so the work of a few remaining matrices
+// still spreads over every XCD.  Each XCD runs its share of the early tiles
+// before its share of the late, cheaper diagonal ones (of the matrices of
+// its own range), which evens out when its compute units finish.
 template <typename T>
 __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_kernel(const NewtonJob<T>* __restrict__ jobs,
                                                                const uint32_t* __restrict__ tlist,
@@ -535,14 +585,14 @@ __global__ __launch_bounds__(kThreads, MinWaves<T>::value) void newton_stage_ker
   __shared__ __attribute__((aligned(16))) T sa0[StageElems<T, kLayoutK>::value], sa1[StageElems<T, kLayoutK>::value];
   __shared__ __attribute__((aligned(16))) T sb0[StageElems<T, kLayoutK>::value], sb1[StageElems<T, kLayoutK>::value];
   const int np = S.nprod;
-  const int nwork = np * *tcount;
+  const int nt = tcount[0], ne = tcount[1];
   int l;
   if (mixed) {  // matrices of different sizes: chunks dealt over the XCDs
     l = deal_chunks(blockIdx.x);
-    if (l >= nwork) return;
+    if (l >= np * nt) return;
   } else {
-    if ((int)blockIdx.x >= nwork) return;
-    l = xcd_remap(blockIdx.x, nwork);
+    l = xcd_split_remap(blockIdx.x, np * ne, np * (nt - ne));
+    if (l < 0) return;
   }
   // the products of one tile run in neighbouring workgroups (shared operands)
   const int t = l / np, prod = l - t * np;
@@ -851,7 +901,7 @@ __global__ __launch_bounds__(kThreads) void root_warm_update_kernel(RootState* _
     count[1] = sf;
   }
   // the next iteration's tiles (full grid) of the matrices still in the phase
-  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
+  build_tile_list(st, njobs, tmap, ubegin, 0, tlist, tcount);
 }
 
 // End of the warm phase: records its outcome (warm_out, device int32
@@ -1624,7 +1674,7 @@ __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __rest
                                                               float tol, int max_iters, int* __restrict__ count,
                                                               const float* __restrict__ esc_thr, int esc_n,
                                                               const uint32_t* __restrict__ tmap,
-                                                              const int* __restrict__ ubegin,
+                                                              const int* __restrict__ ubegin, int diag_last,
                                                               uint32_t* __restrict__ tlist, int* __restrict__ tcount) {
   __shared__ int red[2 * (kThreads / 64)];
   int active = 0, fails = 0;
@@ -1676,7 +1726,7 @@ __global__ __launch_bounds__(kThreads) void root_update_kernel(RootState* __rest
     count[1] = sf;
   }
   // the next iteration's tiles (every thread's matrices are final here)
-  build_tile_list(st, njobs, tmap, ubegin, tlist, tcount);
+  build_tile_list(st, njobs, tmap, ubegin, diag_last, tlist, tcount);
 }
 
 // End of the fp32 phase under AUTO: flag matrices whose fp32 result is not

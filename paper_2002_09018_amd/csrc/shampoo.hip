@@ -731,12 +731,26 @@ NewtonStage drop_x(const NewtonStage& s0) {
   return r;
 }
 
+// Diagonal tiles of a symmetric product launch run last (build_tile_list)
+// when each XCD has at most this many of them: the cheaper tiles then end
+// each XCD's run and even out when its compute units finish, worth a
+// fraction of a tile's time per launch.  Measured on uniform launches: with
+// up to about 100 per XCD (96 or 62 matrices of 1024 or 512) the launches
+// ran 1.8-2.8% faster; from about 150 per XCD on (150 or 576 of 1024, 384
+// of 512) they ran up to 2% slower, since each moved tile reads its panels
+// again long after the tiles of its row read them, and that cost grows with
+// the launch while the gain at its end does not.  Launches of matrices of
+// different sizes keep one part.
+constexpr int kDiagLastMaxPerXcd = 128;
+
 // Tiles of the product launches: every upper tile (tmap, job-major, job j's
-// from ubegin[j]) and the compact list of the matrices still active (tlist,
-// *tcount), rebuilt at the start of a phase and after every iteration.
+// from ubegin[j]) and the compact list of the matrices still active (tlist;
+// tcount[0] tiles, any late diagonal ones after the first tcount[1]),
+// rebuilt at the start of a phase and after every iteration.
 struct TileLists {
   const uint32_t* tmap;
   const int* ubegin;
+  int diag_last;
   uint32_t* tlist;
   int* tcount;
   int mixed;  // matrices of different sizes (tiles dealt in chunks over the XCDs)
@@ -758,13 +772,13 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
   // grid of a product launch of np products per tile (padded for the
   // chunked deal of matrices of different sizes)
   auto pgrid = [&](int np) {
-    return tl.mixed ? cdiv(np * total_up, 8 * kDealChunk) * 8 * kDealChunk : np * total_up;
+    return tl.mixed ? cdiv(np * total_up, 8 * kDealChunk) * 8 * kDealChunk : 8 * (cdiv(np * total_up, 8) + 1);
   };
   // M0 (and, with the Frobenius scaling, X1 and the residual of M0); the
   // tiles of the matrices that take part in this phase
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-    hipLaunchKernelGGL(tile_list_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, tl.tmap, tl.ubegin, tl.tlist,
-                       tl.tcount);
+    hipLaunchKernelGGL(tile_list_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, tl.tmap, tl.ubegin,
+                       tl.diag_last, tl.tlist, tl.tcount);
   }));
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full, p,
@@ -801,7 +815,8 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 1, tol, cap,
-                       dcount + 2 * kCountRing, (const float*)nullptr, 0, tl.tmap, tl.ubegin, tl.tlist, tl.tcount);
+                       dcount + 2 * kCountRing, (const float*)nullptr, 0, tl.tmap, tl.ubegin, tl.diag_last,
+                       tl.tlist, tl.tcount);
   }));
   const NewtonStage first0 = drop_x(prog.stages[0]);
   for (int it = 0; it < cap; ++it) {
@@ -836,7 +851,7 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
     int* slot = dcount + ring;
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_update_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, 0, tol, cap, slot, esc_thr,
-                         esc_n, tl.tmap, tl.ubegin, tl.tlist, tl.tcount);
+                         esc_n, tl.tmap, tl.ubegin, tl.diag_last, tl.tlist, tl.tcount);
     }));
     if (poll) {
       HIP_TRY(h, hipMemcpyAsync(h->pinned + ring, slot, 2 * sizeof(int), hipMemcpyDeviceToHost, s));
@@ -878,7 +893,7 @@ shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const TileLists&
   };
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
     hipLaunchKernelGGL(warm_init_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st, total_full);
-    hipLaunchKernelGGL(tile_list_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, tf.tmap, tf.ubegin, tf.tlist,
+    hipLaunchKernelGGL(tile_list_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, tf.tmap, tf.ubegin, 0, tf.tlist,
                        tf.tcount);
   }));
   int top = 0;
@@ -1354,11 +1369,13 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     std::vector<int> ub;
     tm.reserve(up);
     ub.reserve(njobs + 1);
+    int ndiag = 0;
     for (int j = 0; j < njobs; ++j) {
       ub.push_back((int)tm.size());
       const int T = cdiv(jobs[j].n, kTile);
       for (int ti = 0; ti < T; ++ti)
         for (int tj = ti; tj < T; ++tj) tm.push_back(pack_tile(j, ti, tj));
+      ndiag += T;
     }
     ub.push_back((int)tm.size());
     const void* d = nullptr;
@@ -1369,6 +1386,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     tl.tlist = reinterpret_cast<uint32_t*>(ws + L.tlist);
     tl.tcount = reinterpret_cast<int*>(ws + L.tcount);
     for (int j = 1; j < njobs; ++j) tl.mixed |= jobs[j].n != jobs[0].n;
+    tl.diag_last = !tl.mixed && ndiag <= 8 * kDiagLastMaxPerXcd;
   }
   // full-grid tiles of the warm start's general products
   TileLists tf{};

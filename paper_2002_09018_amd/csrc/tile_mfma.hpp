@@ -498,6 +498,23 @@ __device__ __forceinline__ int xcd_remap(int b, int nwg) {
   return x * q + (x < r ? x : r) + s;
 }
 
+// Workgroup id -> logical index over two consecutive parts, [0, n1) and
+// [n1, n1 + n2): XCD x runs its contiguous share of the first part (as
+// xcd_remap), then its contiguous share of the second; -1 past both.  A
+// launch needs 8 (ceil((n1 + n2) / 8) + 1) workgroups, since the two
+// shares of one XCD round up separately.
+__device__ __forceinline__ int xcd_split_remap(int b, int n1, int n2) {
+  const int x = b & 7;
+  int s = b >> 3;
+  const int q1 = n1 >> 3, r1 = n1 & 7;
+  const int c1 = q1 + (x < r1 ? 1 : 0);
+  if (s < c1) return x * q1 + (x < r1 ? x : r1) + s;
+  s -= c1;
+  const int q2 = n2 >> 3, r2 = n2 & 7;
+  if (s >= q2 + (x < r2 ? 1 : 0)) return -1;
+  return n1 + x * q2 + (x < r2 ? x : r2) + s;
+}
+
 // Workgroup id -> logical index for launches whose tiles differ in cost
 // (grouped problems of mixed sizes): chunks of kDealChunk consecutive
 // indices are dealt round-robin over the 8 XCDs, so every XCD gets an even
