@@ -132,9 +132,10 @@ __device__ __forceinline__ void epi_rows(const float* epi, float* dst, int64_t l
 // with gD set; a separate instantiation as well).
 // WN = 2: 128 x 256 output tiles (plain outputs, both operands k-major;
 // tiles_n counts 256-wide tile columns).
+// map: how workgroups find their tiles (kMapXcd, kMapDeal, kMapDiagLast).
 template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void, int WN = 1>
 __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const GemmProblem* __restrict__ probs,
-                                                               int nprob, int total_tiles, int mixed) {
+                                                               int nprob, int total_tiles, int map) {
   static_assert(WN == 1 || (!LIM && LA == kLayoutK && LB == kLayoutK), "wide tiles: plain k-major products");
   constexpr int TN = kTile * WN;  // output tile width
   __shared__ __attribute__((aligned(16))) float sa0[StageElems<float, LA>::value], sa1[StageElems<float, LA>::value];
@@ -142,24 +143,42 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
       sb1[StageElems<float, LB, TN>::value];
   // LIM: work depends on device-side counts and sits in the first logical
   // tiles; dispatch order (round robin over the XCDs) spreads it evenly.
-  // mixed: problems of different sizes, tiles dealt in chunks (deal_chunks).
-  const int t = LIM ? (int)blockIdx.x : (mixed ? deal_chunks(blockIdx.x) : xcd_remap(blockIdx.x, gridDim.x));
-  if (t >= total_tiles) return;
-  const GemmProblem P = probs[find_problem_gemm(probs, nprob, t)];
-  int ti, tj;
-  const int lt = t - P.tile_begin;
-  if (P.sym) unrank_upper(lt, P.tiles_n, ti, tj);
-  else if (!LIM) {
-    // column-major over the output tiles: neighbouring workgroups (one XCD,
-    // one L2) share the column block of B and walk the row blocks of A
-    // (preconditioning Lr G: G's 128-column slab is fetched once per matrix)
-    const int tm = (P.M + kTile - 1) / kTile;
-    tj = lt / tm;
-    ti = lt - tj * tm;
+  int pi, ti, tj, lt = 0;  // lt: the tile's index in its problem (graft partial slots)
+  if (!LIM && map == kMapDiagLast) {
+    // symmetric problems of one size: every problem's off-diagonal tiles,
+    // then the diagonal ones, each XCD running its share of the second part
+    // last
+    const int T = probs[0].tiles_n, od = T * (T - 1) / 2, n1 = nprob * od;
+    const int l = xcd_split_remap(blockIdx.x, n1, nprob * T);
+    if (l < 0) return;
+    if (l < n1) {
+      pi = l / od;
+      unrank_strict_upper(l - pi * od, T, ti, tj);
+    } else {
+      pi = (l - n1) / T;
+      ti = tj = l - n1 - pi * T;
+    }
   } else {
-    ti = lt / P.tiles_n;
-    tj = lt % P.tiles_n;
+    // kMapDeal: problems of different sizes, tiles dealt in chunks
+    const int t = LIM ? (int)blockIdx.x : (map == kMapDeal ? deal_chunks(blockIdx.x) : xcd_remap(blockIdx.x, gridDim.x));
+    if (t >= total_tiles) return;
+    pi = find_problem_gemm(probs, nprob, t);
+    lt = t - probs[pi].tile_begin;
+    const int tn = probs[pi].tiles_n;
+    if (probs[pi].sym) unrank_upper(lt, tn, ti, tj);
+    else if (!LIM) {
+      // column-major over the output tiles: neighbouring workgroups (one XCD,
+      // one L2) share the column block of B and walk the row blocks of A
+      // (preconditioning Lr G: G's 128-column slab is fetched once per matrix)
+      const int tm = (probs[pi].M + kTile - 1) / kTile;
+      tj = lt / tm;
+      ti = lt - tj * tm;
+    } else {
+      ti = lt / tn;
+      tj = lt % tn;
+    }
   }
+  const GemmProblem P = probs[pi];
   const int m0 = ti * kTile, n0 = tj * TN;
   if (LIM && P.mcount && m0 >= *P.mcount) return;
 

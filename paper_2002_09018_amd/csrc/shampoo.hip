@@ -237,26 +237,47 @@ shampoo_status set_lds(Handle* h, K kernel, int bytes) {
 }
 
 // ---------------------------------------------------------------- GEMM
+// Diagonal tiles of a symmetric product launch (the Newton products through
+// build_tile_list, the statistics GEMM through kMapDiagLast) run last when
+// each XCD has at most this many of them: the cheaper tiles then end
+// each XCD's run and even out when its compute units finish, worth a
+// fraction of a tile's time per launch.  Measured on uniform launches: with
+// up to about 100 per XCD (96 or 62 matrices of 1024 or 512) the launches
+// ran 1.8-2.8% faster; from about 150 per XCD on (150 or 576 of 1024, 384
+// of 512) they ran up to 2% slower, since each moved tile reads its panels
+// again long after the tiles of its row read them, and that cost grows with
+// the launch while the gain at its end does not.  Launches of matrices of
+// different sizes keep one part.
+constexpr int kDiagLastMaxPerXcd = 128;
+
 template <typename SA, int LA, typename SB, int LB, bool LIM = false, typename SGG = void, int WN = 1>
 shampoo_status run_gemm(Handle* h, std::vector<GemmProblem>& probs, hipStream_t s, int cls) {
   if (probs.empty()) return SHAMPOO_OK;
-  int total = 0, mixed = 0;
+  int total = 0, mixed = 0, sym = 1;
   for (auto& p : probs) {
     p.tiles_n = cdiv(p.N, kTile * WN);  // WN = 2: 256-wide tile columns (plain outputs only)
     p.tile_begin = total;
     total += p.sym ? p.tiles_n * (p.tiles_n + 1) / 2 : cdiv(p.M, kTile) * p.tiles_n;
     mixed |= p.M != probs[0].M || p.N != probs[0].N || p.K != probs[0].K;
+    sym &= p.sym;
   }
   // problems of different sizes: tiles dealt in chunks over the XCDs (grid
-  // padded to a multiple of 8 chunks); the LIM instantiation keeps dispatch order
-  const int grid = mixed && !LIM ? cdiv(total, 8 * kDealChunk) * 8 * kDealChunk : total;
+  // padded to a multiple of 8 chunks); the LIM instantiation keeps dispatch
+  // order; symmetric problems of one size with few diagonal tiles: those last
+  const int ndiag = (int)probs.size() * probs[0].tiles_n;
+  const int map = LIM ? kMapXcd
+                  : mixed ? kMapDeal
+                  : (sym && ndiag <= 8 * kDiagLastMaxPerXcd) ? kMapDiagLast : kMapXcd;
+  const int grid = map == kMapDeal       ? cdiv(total, 8 * kDealChunk) * 8 * kDealChunk
+                   : map == kMapDiagLast ? 8 * (cdiv(total, 8) + 1)
+                                         : total;
   const void* d = nullptr;
   STATUS_TRY(upload_table(h, probs.data(), probs.size() * sizeof(GemmProblem), s, &d));
   auto k = gemm_grouped_kernel<SA, LA, SB, LB, LIM, SGG, WN>;
   const int lds = 0;  // static LDS
   const int np = (int)probs.size();
   STATUS_TRY(launch(h, cls, s, [&] {
-    hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, s, (const GemmProblem*)d, np, total, mixed);
+    hipLaunchKernelGGL(k, dim3(grid), dim3(kThreads), lds, s, (const GemmProblem*)d, np, total, map);
   }));
   return SHAMPOO_OK;
 }
@@ -730,18 +751,6 @@ NewtonStage drop_x(const NewtonStage& s0) {
   for (int i = 1; i < s0.nprod; ++i) r.q[r.nprod++] = s0.q[i];
   return r;
 }
-
-// Diagonal tiles of a symmetric product launch run last (build_tile_list)
-// when each XCD has at most this many of them: the cheaper tiles then end
-// each XCD's run and even out when its compute units finish, worth a
-// fraction of a tile's time per launch.  Measured on uniform launches: with
-// up to about 100 per XCD (96 or 62 matrices of 1024 or 512) the launches
-// ran 1.8-2.8% faster; from about 150 per XCD on (150 or 576 of 1024, 384
-// of 512) they ran up to 2% slower, since each moved tile reads its panels
-// again long after the tiles of its row read them, and that cost grows with
-// the launch while the gain at its end does not.  Launches of matrices of
-// different sizes keep one part.
-constexpr int kDiagLastMaxPerXcd = 128;
 
 // Tiles of the product launches: every upper tile (tmap, job-major, job j's
 // from ubegin[j]) and the compact list of the matrices still active (tlist;

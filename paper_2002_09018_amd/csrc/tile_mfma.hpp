@@ -522,6 +522,10 @@ __device__ __forceinline__ int xcd_split_remap(int b, int n1, int n2) {
 // bijection on [0, 8 kDealChunk m) for every m: such launches pad their grid
 // to a multiple of 8 kDealChunk, and ids mapped past the work return.
 constexpr int kDealChunk = 8;
+// Workgroup -> tile maps of the grouped GEMM: xcd_remap, deal_chunks, or
+// (symmetric problems of one size) xcd_split_remap with the diagonal tiles
+// last.
+enum { kMapXcd = 0, kMapDeal = 1, kMapDiagLast = 2 };
 __device__ __forceinline__ int deal_chunks(int b) {
   const int x = b & 7, s = b >> 3;
   return ((s / kDealChunk) * 8 + x) * kDealChunk + (s % kDealChunk);
@@ -537,6 +541,18 @@ __device__ __forceinline__ void unrank_upper(int t, int T, int& ti, int& tj) {
   }
   ti = i;
   tj = i + t;
+}
+
+// Index t of the strictly upper tile list of a T x T tile grid (row-major
+// over ti, tj > ti) -> (ti, tj).
+__device__ __forceinline__ void unrank_strict_upper(int t, int T, int& ti, int& tj) {
+  int i = 0;
+  while (t >= T - 1 - i) {
+    t -= T - 1 - i;
+    ++i;
+  }
+  ti = i;
+  tj = i + 1 + t;
 }
 
 template <typename T>
