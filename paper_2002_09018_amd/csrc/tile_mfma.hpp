@@ -492,7 +492,7 @@ __device__ __forceinline__ void tile_mma(WaveAcc<T, WN>& acc, const Operand<SA>&
 // on the same XCD (workgroups are dealt round-robin over the 8 XCDs, each
 // with its own L2): XCD x receives the contiguous logical range
 // [x*q + min(x, r), ...) where nwg = 8q + r.
-__device__ __forceinline__ int xcd_remap(int b, int nwg) {
+__host__ __device__ __forceinline__ int xcd_remap(int b, int nwg) {
   const int q = nwg >> 3, r = nwg & 7;
   const int x = b & 7, s = b >> 3;
   return x * q + (x < r ? x : r) + s;
@@ -503,7 +503,7 @@ __device__ __forceinline__ int xcd_remap(int b, int nwg) {
 // xcd_remap), then its contiguous share of the second; -1 past both.  A
 // launch needs 8 (ceil((n1 + n2) / 8) + 1) workgroups, since the two
 // shares of one XCD round up separately.
-__device__ __forceinline__ int xcd_split_remap(int b, int n1, int n2) {
+__host__ __device__ __forceinline__ int xcd_split_remap(int b, int n1, int n2) {
   const int x = b & 7;
   int s = b >> 3;
   const int q1 = n1 >> 3, r1 = n1 & 7;
@@ -526,14 +526,14 @@ constexpr int kDealChunk = 8;
 // (symmetric problems of one size) xcd_split_remap with the diagonal tiles
 // last.
 enum { kMapXcd = 0, kMapDeal = 1, kMapDiagLast = 2 };
-__device__ __forceinline__ int deal_chunks(int b) {
+__host__ __device__ __forceinline__ int deal_chunks(int b) {
   const int x = b & 7, s = b >> 3;
   return ((s / kDealChunk) * 8 + x) * kDealChunk + (s % kDealChunk);
 }
 
 // Index t of the upper-triangular tile list of a T x T tile grid (row-major
 // over ti, tj >= ti) -> (ti, tj).
-__device__ __forceinline__ void unrank_upper(int t, int T, int& ti, int& tj) {
+__host__ __device__ __forceinline__ void unrank_upper(int t, int T, int& ti, int& tj) {
   int i = 0;
   while (t >= T - i) {
     t -= T - i;
@@ -545,7 +545,7 @@ __device__ __forceinline__ void unrank_upper(int t, int T, int& ti, int& tj) {
 
 // Index t of the strictly upper tile list of a T x T tile grid (row-major
 // over ti, tj > ti) -> (ti, tj).
-__device__ __forceinline__ void unrank_strict_upper(int t, int T, int& ti, int& tj) {
+__host__ __device__ __forceinline__ void unrank_strict_upper(int t, int T, int& ti, int& tj) {
   int i = 0;
   while (t >= T - 1 - i) {
     t -= T - 1 - i;

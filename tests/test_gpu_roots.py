@@ -362,6 +362,26 @@ def test_grouped_equals_singleton_and_deterministic(env):
         assert np.array_equal(Xg2[i], Xg[i])
 
 
+@pytest.mark.parametrize("n,count,pool", [(300, 24, 24), (520, 20, 20), (512, 264, 12)])
+def test_uniform_grouped_equals_singleton(env, n, count, pool):
+    """Uniform calls: up to 128 diagonal tiles per XCD (24 x 300, 20 x 520),
+    the product launches run each XCD's diagonal tiles last; past that
+    (264 x 512: 1056 diagonal tiles) they keep the row-major order.  Either
+    way every matrix's root equals its singleton call's bit for bit, with
+    the condition numbers spread so that matrices leave the iteration at
+    different times (the compact tile lists shrink between launches)."""
+    say("roots uniform grouped == singleton", n, count)
+    conds = np.logspace(1, 5, pool)
+    base = [spd(n, float(c), 700 + i) for i, c in enumerate(conds)]
+    As = [base[i % pool] for i in range(count)]
+    Xg, ig = roots(env, As, p=4, eps=1e-6)
+    assert len({i["iters"] for i in ig}) > 1
+    for i in sorted({0, 1, count // 2, count - 1} | set(range(0, count, max(1, count // 6)))):
+        Xs, is_ = roots(env, [As[i]], p=4, eps=1e-6)
+        assert np.array_equal(Xs[0], Xg[i]), i
+        assert is_[0]["iters"] == ig[i]["iters"] and is_[0]["status"] == ig[i]["status"], i
+
+
 def test_async_mode_matches_polling(env):
     say("roots poll=0")
     As = [spd(192, 1e3, 31), cfg.c3_matrix(0, n=128)[0]]

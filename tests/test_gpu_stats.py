@@ -133,6 +133,30 @@ def test_c4_two_layers_strided_blocks(env):
         assert abs(tl - g2) <= 1e-5 * g2 and abs(tr - g2) <= 1e-5 * g2
 
 
+@pytest.mark.parametrize("m,n,count", [(300, 2100, 20), (1024, 4096, 12), (256, 1024, 600)])
+def test_uniform_grouped_equals_single(env, m, n, count):
+    """Uniform grouped calls against one call per block, bit for bit (the
+    tiles' arithmetic does not depend on the launch).  The grouped launches
+    order their tiles differently: 300 x 2100 and 1024 x 4096 (contractions
+    of 2048 or more, or few diagonal tiles) run each XCD's diagonal tiles
+    last, 600 blocks of 256 x 1024 (L: 1200 diagonal tiles of a 1024-deep
+    contraction) keep the row-major order."""
+    torch, B, dev, h = env
+    say("stats uniform grouped == single", m, n, count)
+    g = torch.Generator(device=dev).manual_seed(41 + m)
+    Gs = [torch.randn(m, n, device=dev, generator=g) for _ in range(min(count, 24))]
+    Gs = [Gs[i % len(Gs)] for i in range(count)]
+    blocks = [B.Block(G=G, L=torch.zeros(m, m, device=dev), R=torch.zeros(n, n, device=dev)) for G in Gs]
+    B.shampoo_update_stats(h, blocks, beta2=1.0)
+    for i in sorted({0, 1, count // 2, count - 1} | set(range(0, count, max(1, count // 5)))):
+        one = B.Block(G=Gs[i], L=torch.zeros(m, m, device=dev), R=torch.zeros(n, n, device=dev))
+        B.shampoo_update_stats(h, [one], beta2=1.0)
+        torch.cuda.synchronize()
+        assert torch.equal(one.L, blocks[i].L) and torch.equal(one.R, blocks[i].R), i
+    Lo, Ro = O.stats_update(np.zeros((m, m)), np.zeros((n, n)), host(Gs[count - 1]).astype(np.float64))
+    assert rel(host(blocks[count - 1].L), Lo) <= TOL and rel(host(blocks[count - 1].R), Ro) <= TOL
+
+
 def test_empty_call_and_errors(env):
     torch, B, dev, h = env
     say("stats errors")
