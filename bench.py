@@ -302,14 +302,16 @@ def run_c4(args, torch, B):
         log(f"warm refresh: {warm['ms']:.1f} ms (cold {cold2_ms:.1f} ms), kept {warm['kept']}")
         del As2, X2
 
+    pblocks = B.PackedBlocks(h, blocks)   # checked and packed once for the repeated calls
+
     def step_fused():
-        B.shampoo_update_stats(h, blocks)
-        B.shampoo_precondition_graft(h, blocks, 6e-3)
+        B.shampoo_update_stats(h, pblocks)
+        B.shampoo_precondition_graft(h, pblocks, 6e-3)
 
     def step_split():
-        B.shampoo_update_stats(h, blocks)
-        B.shampoo_precondition(h, blocks)
-        B.shampoo_graft(h, blocks, 6e-3)
+        B.shampoo_update_stats(h, pblocks)
+        B.shampoo_precondition(h, pblocks)
+        B.shampoo_graft(h, pblocks, 6e-3)
 
     main_step = step_split if args.split_graft else step_fused
     for _ in range(args.warmup):
@@ -632,14 +634,16 @@ def run_c5(args, torch, B):
                            "alone_newton_tflops": sum((prods[j] + prods64[j]) * sym[j] for j in sel) / (ms_k * 1e-3) / 1e12}
         log(f"  class {k}: {len(sel)} roots alone in {ms_k:.2f} ms")
 
+    pblocks = B.PackedBlocks(h, blocks)   # checked and packed once for the repeated calls
+
     def step_fused():
-        B.shampoo_update_stats(h, blocks)
-        B.shampoo_precondition_graft(h, blocks, 1e-2)
+        B.shampoo_update_stats(h, pblocks)
+        B.shampoo_precondition_graft(h, pblocks, 1e-2)
 
     def step_split():
-        B.shampoo_update_stats(h, blocks)
-        B.shampoo_precondition(h, blocks)
-        B.shampoo_graft(h, blocks, 1e-2)
+        B.shampoo_update_stats(h, pblocks)
+        B.shampoo_precondition(h, pblocks)
+        B.shampoo_graft(h, pblocks, 1e-2)
 
     main_step = step_split if args.split_graft else step_fused
     for _ in range(args.warmup):
@@ -868,6 +872,10 @@ def run_c2(args, torch, B):
     infos = []
 
     restore_ev = []
+    # the step's block views and root jobs, checked and packed once (the
+    # calls repeat with the same tensors)
+    pblocks = B.PackedBlocks(h, blocks)
+    pjobs = B.PackedJobs(h, Ls, Lrs)
 
     def step(record, split=args.split_graft):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -876,15 +884,15 @@ def run_c2(args, torch, B):
         e1.record()
         if record:
             restore_ev.append((e0, e1))
-        B.shampoo_update_stats(h, blocks)
-        B.shampoo_inv_root_batched(h, Ls, Lrs, prm, ws, info)
+        B.shampoo_update_stats(h, pblocks)
+        B.shampoo_inv_root_batched(h, pjobs, None, prm, ws, info)
         if record:
             infos.append(info.clone())
         if split:
-            B.shampoo_precondition(h, blocks)
-            B.shampoo_graft(h, blocks, eta0)
+            B.shampoo_precondition(h, pblocks)
+            B.shampoo_graft(h, pblocks, eta0)
         else:  # graft pass 1 runs in the preconditioning GEMM's epilogue
-            B.shampoo_precondition_graft(h, blocks, eta0)
+            B.shampoo_precondition_graft(h, pblocks, eta0)
 
     for w in range(args.warmup):
         step(False)

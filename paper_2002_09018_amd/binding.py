@@ -309,8 +309,9 @@ def _check_jobs(handle, As, Xs, workspace, info, warm_out=None):
     raise ValueError("tensors of one call must all be on one GPU, the handle's")
 
 
-def _check_jobs_detailed(handle, As, Xs, workspace, info, warm_out=None):
-    As, Xs = list(As), list(Xs)
+def _job_list_tensors(As, Xs):
+    """Layout checks of the As / Xs of a root call (raise with the reason);
+    returns the tensors for the device check."""
     _need(len(As) == len(Xs), f"{len(As)} statistics but {len(Xs)} outputs")
     tensors = []
     for i, (a, x) in enumerate(zip(As, Xs)):
@@ -322,17 +323,29 @@ def _check_jobs_detailed(handle, As, Xs, workspace, info, warm_out=None):
             _contig(t, what)
             tensors.append((what, t))
         _need(a.data_ptr() != x.data_ptr() or n == 0, f"job {i}: A and X must be distinct buffers")
+    return tensors
+
+
+def _job_buffer_tensors(njobs, workspace, info, warm_out):
+    """Layout checks of the workspace / info / warm_out of a root call of
+    njobs jobs; returns the tensors for the device check."""
     _need(workspace is not None, "workspace is required")
     _contig(workspace, "workspace")
     _int32(info, "info")
     _contig(info, "info")
-    _min_numel(info, 8 * len(As), "info (8 int32 per job)")
-    tensors += [("workspace", workspace), ("info", info)]
+    _min_numel(info, 8 * njobs, "info (8 int32 per job)")
+    tensors = [("workspace", workspace), ("info", info)]
     if warm_out is not None:
         _int32(warm_out, "warm_out")
         _contig(warm_out, "warm_out")
-        _min_numel(warm_out, 2 * len(As), "warm_out (2 int32 per job)")
+        _min_numel(warm_out, 2 * njobs, "warm_out (2 int32 per job)")
         tensors.append(("warm_out", warm_out))
+    return tensors
+
+
+def _check_jobs_detailed(handle, As, Xs, workspace, info, warm_out=None):
+    As, Xs = list(As), list(Xs)
+    tensors = _job_list_tensors(As, Xs) + _job_buffer_tensors(len(As), workspace, info, warm_out)
     _devices(handle, tensors)
 
 
@@ -398,6 +411,75 @@ def _dtype_code(blocks):
     return SHAMPOO_BF16 if dt == torch.bfloat16 else SHAMPOO_F32
 
 
+class PackedBlocks:
+    """A block list checked and packed once, for calls that repeat with the
+    same views (a training loop passes the same blocks every step): every
+    entry point that takes a block list accepts it in its place and skips the
+    per-call checks and packing.  It records each tensor's pointer, size and
+    row stride as they are when packed and keeps the tensors alive; pack again
+    after any of them is reallocated, resized or replaced."""
+
+    def __init__(self, handle, blocks):
+        blocks = list(blocks)
+        _check_blocks(handle, blocks)
+        self.blocks = blocks
+        self._handle = getattr(handle, "value", handle)
+        self._arr = _blocks(blocks)
+        self._dtype = _dtype_code(blocks)
+        self._device = blocks[0].G.get_device() if blocks else None
+
+    def __len__(self):
+        return len(self.blocks)
+
+
+class PackedJobs:
+    """Inverse-root jobs (As, Xs) checked and packed once, as PackedBlocks:
+    accepted by shampoo_inv_root_batched and shampoo_inv_root_warm_batched in
+    place of As (Xs is then None).  Pack again after any tensor is
+    reallocated or replaced."""
+
+    def __init__(self, handle, As, Xs):
+        As, Xs = list(As), list(Xs)
+        _need(len(As) > 0, "PackedJobs: no jobs")
+        _devices(handle, _job_list_tensors(As, Xs))
+        self.As, self.Xs = As, Xs
+        self._handle = getattr(handle, "value", handle)
+        self._arr = _jobs(As, Xs)
+        self._device = As[0].get_device()
+
+    def __len__(self):
+        return len(self.As)
+
+
+def _block_args(handle, blocks, norms=None):
+    """(packed table, count, G dtype code) of a call's blocks: a PackedBlocks
+    as it was packed (only norms is checked), a list checked and packed now."""
+    if isinstance(blocks, PackedBlocks):
+        _need(blocks._handle == getattr(handle, "value", handle), "PackedBlocks was packed for another handle")
+        if norms is not None:
+            _check_norms(handle, norms, len(blocks))
+            _need(blocks._device is None or norms.get_device() == blocks._device,
+                  "norms: not on the blocks' device")
+        return blocks._arr, len(blocks), blocks._dtype
+    _check_blocks(handle, blocks, norms)
+    return _blocks(blocks), len(blocks), _dtype_code(blocks)
+
+
+def _job_args(handle, As, Xs, workspace, info, warm_out=None):
+    """(packed table, count) of a root call: a PackedJobs as it was packed (the
+    workspace, info and warm_out checked now), lists checked and packed now."""
+    if isinstance(As, PackedJobs):
+        _need(Xs is None, "with PackedJobs, Xs must be None (the outputs are packed)")
+        _need(As._handle == getattr(handle, "value", handle), "PackedJobs was packed for another handle")
+        tensors = _job_buffer_tensors(len(As), workspace, info, warm_out)
+        _devices(handle, tensors)
+        for what, t in tensors:
+            _need(t.get_device() == As._device, f"{what}: not on the jobs' device")
+        return As._arr, len(As)
+    _check_jobs(handle, As, Xs, workspace, info, warm_out)
+    return _jobs(As, Xs), len(As)
+
+
 # ------------------------------------------------------------------ entry points
 def shampoo_version():
     return _lib.shampoo_version().decode()
@@ -426,10 +508,9 @@ def shampoo_destroy(handle):
 
 
 def shampoo_update_stats(handle, blocks, beta2=1.0, stream=None):
-    _check_blocks(handle, blocks)
-    arr = _blocks(blocks)
-    _check(handle, _lib.shampoo_update_stats(handle, arr, len(blocks), _dtype_code(blocks), float(beta2),
-                                             _stream(stream)))
+    """blocks: a list of Block, or a PackedBlocks."""
+    arr, nb, dt = _block_args(handle, blocks)
+    _check(handle, _lib.shampoo_update_stats(handle, arr, nb, dt, float(beta2), _stream(stream)))
 
 
 def _jobs(As, Xs):
@@ -449,11 +530,11 @@ def shampoo_inv_root_workspace_bytes(ns, precision=PRECISION_AUTO):
 
 
 def shampoo_inv_root_batched(handle, As, Xs, params, workspace, info, stream=None):
-    """As, Xs: lists of contiguous n x n fp32 device tensors; workspace: a
-    uint8 device tensor; info: an int32 device tensor of 8 * len(As)."""
-    _check_jobs(handle, As, Xs, workspace, info)
-    arr = _jobs(As, Xs)
-    _check(handle, _lib.shampoo_inv_root_batched(handle, arr, len(As), C.byref(params), _ptr(workspace),
+    """As, Xs: lists of contiguous n x n fp32 device tensors (or As a
+    PackedJobs and Xs None); workspace: a uint8 device tensor; info: an int32
+    device tensor of 8 * len(As)."""
+    arr, nj = _job_args(handle, As, Xs, workspace, info)
+    _check(handle, _lib.shampoo_inv_root_batched(handle, arr, nj, C.byref(params), _ptr(workspace),
                                                  int(workspace.numel() * workspace.element_size()),
                                                  _ptr(info), _stream(stream)))
 
@@ -462,33 +543,29 @@ def shampoo_inv_root_warm_batched(handle, As, Xs, params, workspace, info, warm_
                                   stream=None):
     """As shampoo_inv_root_batched; Xs hold the warm starts X0 on entry.
     warm_out: None or an int32 device tensor of 2 * len(As)."""
-    _check_jobs(handle, As, Xs, workspace, info, warm_out)
-    arr = _jobs(As, Xs)
-    _check(handle, _lib.shampoo_inv_root_warm_batched(handle, arr, len(As), C.byref(params), float(comm_tol),
+    arr, nj = _job_args(handle, As, Xs, workspace, info, warm_out)
+    _check(handle, _lib.shampoo_inv_root_warm_batched(handle, arr, nj, C.byref(params), float(comm_tol),
                                                       _ptr(workspace),
                                                       int(workspace.numel() * workspace.element_size()),
                                                       _ptr(info), _ptr(warm_out), _stream(stream)))
 
 
 def shampoo_precondition(handle, blocks, stream=None):
-    _check_blocks(handle, blocks)
-    arr = _blocks(blocks)
-    _check(handle, _lib.shampoo_precondition(handle, arr, len(blocks), _dtype_code(blocks), _stream(stream)))
+    arr, nb, dt = _block_args(handle, blocks)
+    _check(handle, _lib.shampoo_precondition(handle, arr, nb, dt, _stream(stream)))
 
 
 def shampoo_graft(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
-    _check_blocks(handle, blocks, norms)
-    arr = _blocks(blocks)
-    _check(handle, _lib.shampoo_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0), float(beta1),
-                                      int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+    arr, nb, dt = _block_args(handle, blocks, norms)
+    _check(handle, _lib.shampoo_graft(handle, arr, nb, dt, float(eta0), float(beta1), int(bool(use_shampoo)),
+                                      _ptr(norms), _stream(stream)))
 
 
 def shampoo_graft_noalloc(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
     """shampoo_graft without any device allocation (fixed scratch; see the header for its limits)."""
-    _check_blocks(handle, blocks, norms)
-    arr = _blocks(blocks)
-    _check(handle, _lib.shampoo_graft_noalloc(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
-                                              float(beta1), int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+    arr, nb, dt = _block_args(handle, blocks, norms)
+    _check(handle, _lib.shampoo_graft_noalloc(handle, arr, nb, dt, float(eta0), float(beta1), int(bool(use_shampoo)),
+                                              _ptr(norms), _stream(stream)))
 
 
 def _nbytes(t):
@@ -586,17 +663,14 @@ def shampoo_embedding_graft(handle, rows, count, U, P, W, D, eta0, use_shampoo=T
 
 
 def shampoo_precondition_graft(handle, blocks, eta0, norms=None, stream=None):
-    _check_blocks(handle, blocks, norms)
-    arr = _blocks(blocks)
-    _check(handle, _lib.shampoo_precondition_graft(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
-                                                   _ptr(norms), _stream(stream)))
+    arr, nb, dt = _block_args(handle, blocks, norms)
+    _check(handle, _lib.shampoo_precondition_graft(handle, arr, nb, dt, float(eta0), _ptr(norms), _stream(stream)))
 
 
 def shampoo_graft_lamb(handle, blocks, eta0, beta1=0.0, use_shampoo=True, norms=None, stream=None):
-    _check_blocks(handle, blocks, norms)
-    arr = _blocks(blocks)
-    _check(handle, _lib.shampoo_graft_lamb(handle, arr, len(blocks), _dtype_code(blocks), float(eta0),
-                                           float(beta1), int(bool(use_shampoo)), _ptr(norms), _stream(stream)))
+    arr, nb, dt = _block_args(handle, blocks, norms)
+    _check(handle, _lib.shampoo_graft_lamb(handle, arr, nb, dt, float(eta0), float(beta1), int(bool(use_shampoo)),
+                                           _ptr(norms), _stream(stream)))
 
 
 def shampoo_timing_enable(handle, enable=True):

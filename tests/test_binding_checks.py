@@ -29,10 +29,12 @@ BLOCK_CALLS = [
     lambda blocks: B.shampoo_graft(None, blocks, 0.1),
     lambda blocks: B.shampoo_graft_lamb(None, blocks, 0.1),
     lambda blocks: B.shampoo_precondition_graft(None, blocks, 0.1),
+    lambda blocks: B.PackedBlocks(None, blocks),
 ]
 
 
-@pytest.mark.parametrize("call", BLOCK_CALLS, ids=["stats", "precondition", "graft", "graft_lamb", "precond_graft"])
+@pytest.mark.parametrize("call", BLOCK_CALLS,
+                         ids=["stats", "precondition", "graft", "graft_lamb", "precond_graft", "packed"])
 def test_block_checks(call):
     m, n = 6, 5
     # a well-formed block passes every layout check and fails only on the device
@@ -89,6 +91,17 @@ def test_root_job_checks(warm):
     if warm:
         _raises(call([A], [X], warm_out=torch.zeros(1, dtype=torch.int32)), "at least 2")
         _raises(call([A], [X], warm_out=torch.zeros(2, dtype=torch.float32)), "int32")
+
+
+def test_packed_job_checks():
+    """PackedJobs runs the job checks when it is made; a packed call passes
+    Xs as None."""
+    A, X = torch.zeros(8, 8), torch.zeros(8, 8)
+    _raises(lambda: B.PackedJobs(None, [A], [X]), "expected a GPU tensor")
+    _raises(lambda: B.PackedJobs(None, [A], [A]), "distinct")
+    _raises(lambda: B.PackedJobs(None, [torch.zeros(8, 9)], [X]), r"expected \(8, 8\)")
+    _raises(lambda: B.PackedJobs(None, [A], [X.double()]), "float32")
+    _raises(lambda: B.PackedJobs(None, [], []), "no jobs")
 
 
 def test_embedding_checks():
