@@ -430,7 +430,17 @@ struct NewtonJob {
   int tiles_n;      // ceil(n / 128)
   int up_begin;     // first logical upper-triangular tile
   int full_begin;   // first logical full-grid tile
+  int flat_begin;   // first flat chunk (kFlatChunk elements)
 };
+
+// Elementwise passes that need no transpose walk each matrix as one
+// contiguous array: a workgroup takes kFlatChunk consecutive elements of one
+// job (16-byte vectors when n % 4 == 0, which keeps every vector inside one
+// row).  A standalone copy of 96 matrices of 1024^2 streamed 6.2 TB/s this
+// way against 5.05 over 128 x 128 tiles (128 separate 512-byte row segments
+// per workgroup); in the library the output copy went from 144 to 134 us,
+// the first-iteration pass (three in, three out) stayed at about 465 us.
+constexpr int kFlatChunk = 4096;
 
 template <typename T>
 __device__ __forceinline__ int find_job_up(const NewtonJob<T>* jobs, int njobs, int t) {
@@ -438,6 +448,16 @@ __device__ __forceinline__ int find_job_up(const NewtonJob<T>* jobs, int njobs, 
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
     if (jobs[mid].up_begin <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+template <typename T>
+__device__ __forceinline__ int find_job_flat(const NewtonJob<T>* jobs, int njobs, int t) {
+  int lo = 0, hi = njobs - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (jobs[mid].flat_begin <= t) lo = mid; else hi = mid - 1;
   }
   return lo;
 }
@@ -1577,17 +1597,16 @@ __global__ __launch_bounds__(kThreads) void newton_poly0_kernel(const NewtonJob<
 // stored.  All outputs stay exactly symmetric.
 template <typename T>
 __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                                RootState* __restrict__ st, int total_full,
+                                                                RootState* __restrict__ st, int total_flat,
                                                                 double k1, double k2, double k3, double k4,
                                                                 double k5) {
   const int t = blockIdx.x;
-  if (t >= total_full) return;
-  const int j = find_job_full(jobs, njobs, t);
+  if (t >= total_flat) return;
+  const int j = find_job_flat(jobs, njobs, t);
   if (st[j].status != kActive) return;
   const NewtonJob<T>* J = jobs + j;
-  const int lt = t - J->full_begin;
-  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
   const int n = J->n;
+  const int e0 = (t - J->flat_begin) * kFlatChunk, e1 = min(e0 + kFlatChunk, n * n);
   const double cd = st[j].zc;
   const T c = (T)cd, c2 = (T)(cd * cd), c4 = (T)(cd * cd * cd * cd);
   const T K1 = (T)k1, K2 = (T)k2, K3c = (T)(k3 * cd), K4 = (T)k4, K5c = (T)(k5 * cd);
@@ -1597,7 +1616,6 @@ __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob
   T* S1 = J->S[1];
   T* X1 = J->X[1];
   const T* M = J->M[0];
-  const int r0 = ti * kTile, col0 = tj * kTile;
   float rmax = 0.f;
   auto one = [&](T mu, T s0, T s1, bool dg, T& e, T& r, T& x) {
     const T m = c * mu, m2 = c2 * s0, m4 = c4 * s1;
@@ -1608,10 +1626,9 @@ __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob
     if (!(d <= 3.0e38f)) d = INFINITY;
     rmax = rmax > d ? rmax : d;
   };
-  if (sizeof(T) == 4 && (n & 3) == 0 && r0 + kTile <= n && col0 + kTile <= n) {
-    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
-      const int r = r0 + (e >> 5), cc = col0 + 4 * (e & 31);
-      const int64_t i = (int64_t)r * n + cc;
+  if (sizeof(T) == 4 && (n & 3) == 0) {
+    for (int i = e0 + 4 * (int)threadIdx.x; i < e1; i += 4 * kThreads) {
+      const int r = i / n, col = i - r * n;  // the 4 elements share row r
       const f4v m = gload<f4v>(reinterpret_cast<const float*>(M) + i);
       const f4v s0 = gload<f4v>(reinterpret_cast<const float*>(S0) + i);
       const f4v s1 = gload<f4v>(reinterpret_cast<const float*>(S1) + i);
@@ -1619,7 +1636,7 @@ __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         T ee, rr, xx;
-        one((T)m[q], (T)s0[q], (T)s1[q], r == cc + q, ee, rr, xx);
+        one((T)m[q], (T)s0[q], (T)s1[q], r == col + q, ee, rr, xx);
         eo[q] = (float)ee;
         ro[q] = (float)rr;
         xo[q] = (float)xx;
@@ -1629,16 +1646,13 @@ __global__ __launch_bounds__(kThreads) void newton_first4_kernel(const NewtonJob
       gstore<f4v>(reinterpret_cast<float*>(X1) + i, xo);
     }
   } else {
-    for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-      const int r = r0 + (e >> 7), col = col0 + (e & 127);
-      if (r < n && col < n) {
-        const int64_t i = (int64_t)r * n + col;
-        T ee, rr, xx;
-        one(M[i], S0[i], S1[i], r == col, ee, rr, xx);
-        S0[i] = ee;
-        S1[i] = rr;
-        X1[i] = xx;
-      }
+    for (int i = e0 + (int)threadIdx.x; i < e1; i += kThreads) {
+      const int r = i / n, col = i - r * n;
+      T ee, rr, xx;
+      one(M[i], S0[i], S1[i], r == col, ee, rr, xx);
+      S0[i] = ee;
+      S1[i] = rr;
+      X1[i] = xx;
     }
   }
   rmax = wave_max(rmax);
@@ -1779,11 +1793,11 @@ __global__ __launch_bounds__(kThreads) void root_escalate_kernel(RootState* __re
 // selects the fp64 tail of AUTO).
 template <typename T>
 __global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T>* __restrict__ jobs, int njobs,
-                                                              const RootState* __restrict__ st, int total_full,
+                                                              const RootState* __restrict__ st, int total_flat,
                                                               int phase_is_tail, int p) {
   const int t = blockIdx.x;
-  if (t >= total_full) return;
-  const int j = find_job_full(jobs, njobs, t);
+  if (t >= total_flat) return;
+  const int j = find_job_flat(jobs, njobs, t);
   const RootState& s = st[j];
   if (phase_is_tail && !s.escalate) return;
   if (!phase_is_tail && s.escalate) return;
@@ -1796,21 +1810,16 @@ __global__ __launch_bounds__(kThreads) void root_output_kernel(const NewtonJob<T
   const T* src = J->X[s.parity];
   float* dst = J->Xout;
   const float x0 = (float)pow(s.z, 1.0 / p);
-  const int lt = t - J->full_begin;
-  const int ti = lt / J->tiles_n, tj = lt % J->tiles_n;
   const int n = J->n;
-  const int r0 = ti * kTile, c0 = tj * kTile;
-  if (!ident && sizeof(T) == 4 && (n & 3) == 0 && r0 + kTile <= n && c0 + kTile <= n) {
-    for (int e = threadIdx.x; e < kTile * kTile / 4; e += kThreads) {
-      const int r = r0 + (e >> 5), c = c0 + 4 * (e & 31);
-      gstore<f4v>(dst + (int64_t)r * n + c, gload<f4v>(reinterpret_cast<const float*>(src) + (int64_t)r * n + c));
-    }
+  const int e0 = (t - J->flat_begin) * kFlatChunk, e1 = min(e0 + kFlatChunk, n * n);
+  if (!ident && sizeof(T) == 4 && (n & 3) == 0) {
+    for (int i = e0 + 4 * (int)threadIdx.x; i < e1; i += 4 * kThreads)
+      gstore<f4v>(dst + i, gload<f4v>(reinterpret_cast<const float*>(src) + i));
     return;
   }
-  for (int e = threadIdx.x; e < kTile * kTile; e += kThreads) {
-    const int r = r0 + (e >> 7), c = c0 + (e & 127);
-    if (r < n && c < n)
-      dst[(int64_t)r * n + c] = ident ? (r == c ? x0 : 0.f) : (float)src[(int64_t)r * n + c];
+  for (int i = e0 + (int)threadIdx.x; i < e1; i += kThreads) {
+    const int r = i / n, c = i - r * n;
+    dst[i] = ident ? (r == c ? x0 : 0.f) : (float)src[i];
   }
 }
 

@@ -788,7 +788,8 @@ struct TileLists {
 // One precision phase of the coupled Newton iteration.
 template <typename T>
 shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileLists& tl, int njobs, RootState* st, int* dcount,
-                            int total_up, int total_full, const NewtonProgram& prog, int p, int scaling, float tol,
+                            int total_up, int total_full, int total_flat, const NewtonProgram& prog, int p,
+                            int scaling, float tol,
                             int cap, int poll, int cls, const float* esc_thr, int esc_n, hipStream_t s,
                             int* fails_out = nullptr) {
   // fails_out: set to the number of matrices stopped unaccepted (MAXITER,
@@ -834,8 +835,8 @@ shampoo_status newton_phase(Handle* h, const NewtonJob<T>* djobs, const TileList
       hipLaunchKernelGGL(frob_s1_kernel<T>, dim3(total_up), dim3(kThreads), 0, s, djobs, njobs, st, total_up);
       hipLaunchKernelGGL(root_rescale_kernel<T>, dim3(nb1), dim3(64), 0, s, djobs, njobs, st, p);
       if (first4)
-        hipLaunchKernelGGL(newton_first4_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st,
-                           total_full, a * a * a * a, 4.0 * a * a * a * b, 6.0 * a * a * b * b, 4.0 * a * b * b * b,
+        hipLaunchKernelGGL(newton_first4_kernel<T>, dim3(total_flat), dim3(kThreads), 0, s, djobs, njobs, st,
+                           total_flat, a * a * a * a, 4.0 * a * a * a * b, 6.0 * a * a * b * b, 4.0 * a * b * b * b,
                            b * b * b * b);
       else
         hipLaunchKernelGGL(root_scale_kernel<T>, dim3(total_full), dim3(kThreads), 0, s, djobs, njobs, st,
@@ -993,9 +994,9 @@ shampoo_status warm_phase(Handle* h, const NewtonJob<T>* djobs, const TileLists&
 
 template <typename T>
 std::vector<NewtonJob<T>> newton_table(const shampoo_root_job* jobs, int njobs, char* ws, const RootLayout& L,
-                                       int* total_up, int* total_full) {
+                                       int* total_up, int* total_full, int* total_flat) {
   std::vector<NewtonJob<T>> v(njobs);
-  int up = 0, full = 0;
+  int up = 0, full = 0, flat = 0;
   for (int j = 0; j < njobs; ++j) {
     const int n = jobs[j].n;
     const size_t nn = align256((size_t)n * n * sizeof(T));
@@ -1024,11 +1025,14 @@ std::vector<NewtonJob<T>> newton_table(const shampoo_root_job* jobs, int njobs, 
     J.tiles_n = cdiv(n, kTile);
     J.up_begin = up;
     J.full_begin = full;
+    J.flat_begin = flat;
     up += J.tiles_n * (J.tiles_n + 1) / 2;
     full += J.tiles_n * J.tiles_n;
+    flat += cdiv(n * n, kFlatChunk);
   }
   *total_up = up;
   *total_full = full;
+  *total_flat = flat;
   return v;
 }
 
@@ -1376,17 +1380,17 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
   char* ws = static_cast<char*>(workspace);
   RootState* st = reinterpret_cast<RootState*>(ws + L.state);
   int* dcount = reinterpret_cast<int*>(ws + L.counts);
-  int up = 0, full = 0;
+  int up = 0, full = 0, flat = 0;
   const NewtonJob<float>* j32 = nullptr;
   const NewtonJob<double>* j64 = nullptr;
   if (prec != SHAMPOO_PRECISION_FP64) {
-    auto t = newton_table<float>(jobs, njobs, ws, L, &up, &full);
+    auto t = newton_table<float>(jobs, njobs, ws, L, &up, &full, &flat);
     const void* d = nullptr;
     STATUS_TRY(upload_table(h, t.data(), t.size() * sizeof(t[0]), s, &d));
     j32 = static_cast<const NewtonJob<float>*>(d);
   }
   if (prec != SHAMPOO_PRECISION_FP32) {
-    auto t = newton_table<double>(jobs, njobs, ws, L, &up, &full);
+    auto t = newton_table<double>(jobs, njobs, ws, L, &up, &full, &flat);
     const void* d = nullptr;
     STATUS_TRY(upload_table(h, t.data(), t.size() * sizeof(t[0]), s, &d));
     j64 = static_cast<const NewtonJob<double>*>(d);
@@ -1532,7 +1536,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_escalate_kernel, dim3(1), dim3(kThreads), 0, s, st, njobs, dcount + 2 * kCountRing + 2);
       if (warm)  // results the warm phase accepted
-        hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 0, p);
+        hipLaunchKernelGGL(root_output_kernel<double>, dim3(flat), dim3(kThreads), 0, s, j64, njobs, st, flat, 0, p);
     }));
   }
   int run64 = tail_all && !(warm && warm_aborts == 0);
@@ -1560,7 +1564,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     if (warm && warm_aborts == 0)
       fails = 0;  // every warm result was accepted: no cold start
     else
-      STATUS_TRY(newton_phase<float>(h, j32, tl, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, cap,
+      STATUS_TRY(newton_phase<float>(h, j32, tl, njobs, st, dcount, up, full, flat, prog, p, prm->scaling, prm->tol, cap,
                                      prm->poll, SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       int* esc_count = dcount + 2 * kCountRing + 2;
@@ -1579,7 +1583,7 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
       }
     }
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(root_output_kernel<float>, dim3(full), dim3(kThreads), 0, s, j32, njobs, st, full, 0, p);
+      hipLaunchKernelGGL(root_output_kernel<float>, dim3(flat), dim3(kThreads), 0, s, j32, njobs, st, flat, 0, p);
     }));
   }
   if (run64) {
@@ -1588,10 +1592,10 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
         hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
       }));
     }
-    STATUS_TRY(newton_phase<double>(h, j64, tl, njobs, st, dcount, up, full, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
+    STATUS_TRY(newton_phase<double>(h, j64, tl, njobs, st, dcount, up, full, flat, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
                                     SHAMPOO_KCLASS_NEWTON_F64, nullptr, 0, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
-      hipLaunchKernelGGL(root_output_kernel<double>, dim3(full), dim3(kThreads), 0, s, j64, njobs, st, full, 1, p);
+      hipLaunchKernelGGL(root_output_kernel<double>, dim3(flat), dim3(kThreads), 0, s, j64, njobs, st, flat, 1, p);
     }));
   }
   STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
