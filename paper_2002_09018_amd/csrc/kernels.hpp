@@ -159,8 +159,10 @@ __global__ __launch_bounds__(kThreads, kMinWaves) void gemm_grouped_kernel(const
       ti = tj = l - n1 - pi * T;
     }
   } else {
-    // kMapDeal: problems of different sizes, tiles dealt in chunks
-    const int t = LIM ? (int)blockIdx.x : (map == kMapDeal ? deal_chunks(blockIdx.x) : xcd_remap(blockIdx.x, gridDim.x));
+    // kMapXcd: contiguous ranges per XCD; kMapDeal (problems of different
+    // sizes): chunks dealt over the XCDs; LIM: dispatch order
+    const int t =
+        LIM ? (int)blockIdx.x : (map == kMapDeal ? deal_chunks(blockIdx.x) : xcd_remap(blockIdx.x, gridDim.x));
     if (t >= total_tiles) return;
     pi = find_problem_gemm(probs, nprob, t);
     lt = t - probs[pi].tile_begin;

@@ -1564,8 +1564,8 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
     if (warm && warm_aborts == 0)
       fails = 0;  // every warm result was accepted: no cold start
     else
-      STATUS_TRY(newton_phase<float>(h, j32, tl, njobs, st, dcount, up, full, flat, prog, p, prm->scaling, prm->tol, cap,
-                                     prm->poll, SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
+      STATUS_TRY(newton_phase<float>(h, j32, tl, njobs, st, dcount, up, full, flat, prog, p, prm->scaling, prm->tol,
+                                     cap, prm->poll, SHAMPOO_KCLASS_NEWTON_F32, esc, esc_n, s, &fails));
     if (prec == SHAMPOO_PRECISION_AUTO) {
       int* esc_count = dcount + 2 * kCountRing + 2;
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
@@ -1592,8 +1592,8 @@ shampoo_status inv_root_impl(Handle* h, const shampoo_root_job* jobs, int njobs,
         hipLaunchKernelGGL(root_reset_kernel, dim3(nb1), dim3(64), 0, s, st, njobs, 1, 64);
       }));
     }
-    STATUS_TRY(newton_phase<double>(h, j64, tl, njobs, st, dcount, up, full, flat, prog, p, prm->scaling, prm->tol, prm->max_iters, prm->poll,
-                                    SHAMPOO_KCLASS_NEWTON_F64, nullptr, 0, s));
+    STATUS_TRY(newton_phase<double>(h, j64, tl, njobs, st, dcount, up, full, flat, prog, p, prm->scaling, prm->tol,
+                                    prm->max_iters, prm->poll, SHAMPOO_KCLASS_NEWTON_F64, nullptr, 0, s));
     STATUS_TRY(launch(h, SHAMPOO_KCLASS_ROOT_AUX, s, [&] {
       hipLaunchKernelGGL(root_output_kernel<double>, dim3(flat), dim3(kThreads), 0, s, j64, njobs, st, flat, 1, p);
     }));
