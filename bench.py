@@ -513,6 +513,7 @@ def run_c3(args, torch, B):
                                          "rel_err_vs_eigh": float(np.linalg.norm(Xh - Xo) / np.linalg.norm(Xo))}
             res[f"p{p}_eps{epsd:g}"] = r
             log(f"C3 p={p} eps_d={epsd:g}: {ms:.1f} ms, fp64 {r['newton_f64_tflops'] or 0:.1f} TFLOP/s")
+    warm = c3_warm(torch, B, h, As, ws)
     B.shampoo_destroy(h)
     main = res["p4_eps1e-06"]
     out = {"metric": "C3 ill-conditioned 2048^2 inverse roots (AUTO precision, fp64 tail)", "value": main["ms"],
@@ -520,7 +521,55 @@ def run_c3(args, torch, B):
            "dtype": "f32/f64", "data": "synthetic",
            "config": {"workload": "C3: 32 x 2048^2, lambda log-uniform [1e-6,1e2], eps_d * lambda_max with "
                                   "eps_d in {1e-6, 1e-8}, p in {2,4}"},
-           "roofline": main["roofline"], "results": res}
+           "roofline": main["roofline"], "results": res, "warm_start_drift": warm}
+    return out
+
+
+def c3_warm(torch, B, h, As, ws, drifts=(1e-8, 1e-6, 1e-4)):
+    """Warm start (coupled-Newton appendix) where it pays: the ill-conditioned
+    C3 matrices, whose cold roots take about 19 fp64 iterations.  Their
+    p = 4, eps_d = 1e-6 roots X0 seed the roots of the drifted statistics
+    A + s lambda_max u u^T (u a seeded unit vector per matrix, one drift size
+    s per case), rooted warm in fp64 and cold (AUTO, the C3 default, and
+    fp64) on the same matrices; the warm results are compared with the cold
+    fp64 roots (the same policy, so the same MaxSV and damping)."""
+    dev = As[0].device
+    nm, n = len(As), As[0].shape[0]
+    prm_auto = B.shampoo_root_params_default(p=4, eps=1e-6, eps_relative=1)
+    prm64 = B.shampoo_root_params_default(p=4, eps=1e-6, eps_relative=1, precision=B.PRECISION_FP64)
+    info = torch.zeros(8 * nm, dtype=torch.int32, device=dev)
+    X0 = [torch.zeros_like(a) for a in As]
+    B.shampoo_inv_root_batched(h, As, X0, prm_auto, ws, info)
+    torch.cuda.synchronize()
+    lam = [i["lambda_max"] for i in B.decode_root_info(info)]
+    g = torch.Generator(device=dev).manual_seed(33)
+    us = [torch.randn(n, device=dev, generator=g, dtype=torch.float64) for _ in range(nm)]
+    us = [u / torch.linalg.norm(u) for u in us]
+    out = {}
+
+    def cold(prm, A2):
+        X = [torch.zeros_like(a) for a in A2]
+        B.shampoo_inv_root_batched(h, A2, X, prm, ws, info)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        B.shampoo_inv_root_batched(h, A2, X, prm, ws, info)
+        torch.cuda.synchronize()
+        inf = B.decode_root_info(info)
+        return X, (time.perf_counter() - t0) * 1e3, float(np.mean([i["iters"] + i["iters_fp32"] * (
+            i["precision"] == 64) for i in inf]))
+
+    for sd in drifts:
+        A2 = [(a.double() + (sd * lm) * torch.outer(u, u)).float() for a, lm, u in zip(As, lam, us)]
+        Xa, cold_auto_ms, cold_auto_iters = cold(prm_auto, A2)
+        del Xa
+        Xc, cold64_ms, cold64_iters = cold(prm64, A2)
+        w = warm_measure(torch, B, h, A2, X0, prm64, ws, ref=Xc)
+        w.update({"cold_auto_ms": cold_auto_ms, "cold_auto_iters_mean": cold_auto_iters,
+                  "cold_fp64_ms": cold64_ms, "cold_fp64_iters_mean": cold64_iters})
+        out[f"drift{sd:g}"] = w
+        log(f"C3 warm, drift {sd:g}: {w['ms']:.1f} ms ({w['warm_iters_mean']:.1f} it, kept {w['kept']}) against "
+            f"cold {cold_auto_ms:.1f} ms AUTO / {cold64_ms:.1f} ms fp64")
+        del A2, Xc
     return out
 
 
