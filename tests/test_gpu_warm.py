@@ -78,6 +78,33 @@ def test_small_drift_keeps_the_warm_limit(env, prec, p):
         assert e < 0.2 * gap, (A.shape, e, gap)
 
 
+def test_ill_conditioned_tiny_drift_fp64(env):
+    """Where the warm start pays: damped condition ~1e6 (the cold fp64
+    iteration takes many steps) and a tiny drift.  The warm start is kept
+    after at most two iterations and equals the oracle's warm limit from the
+    same fp32 X0; the cold call on the same matrices takes at least ten."""
+    torch, B, dev, h = env
+    say("warm ill-conditioned tiny drift fp64")
+    p, tol = 4, 1e-10
+    cases = [drift_case(n, 1e6, 1e-9, p, 13 * n) for n in (200, 256)]
+    As, X0s = [a for a, _ in cases], [x for _, x in cases]
+    Xs, info, wout = warm_roots(env, As, X0s, p=p, eps=1e-6, tol=tol, precision=FP64)
+    prm = B.shampoo_root_params_default(p=p, eps=1e-6, tol=tol, precision=FP64)
+    dA = [to_dev(torch, a, dev) for a in As]
+    dX = [torch.zeros_like(a) for a in dA]
+    ws = torch.empty(B.shampoo_inv_root_workspace_bytes([a.shape[0] for a in As], FP64), dtype=torch.uint8,
+                     device=dev)
+    cinfo = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+    B.shampoo_inv_root_batched(h, dA, dX, prm, ws, cinfo)
+    torch.cuda.synchronize()
+    for (A, X0), X, inf, w, ci in zip(cases, Xs, info, wout, B.decode_root_info(cinfo)):
+        ref = O.coupled_newton_warm(A, p, X0, eps=1e-6, tol=tol)
+        assert not ref["warm_aborted"]
+        assert w[0] == 1 and 1 <= w[1] <= 2 and inf["status"] in (0, 1), (w, inf)
+        assert rel(X, ref["X"]) <= 1e-6, (A.shape, rel(X, ref["X"]))
+        assert ci["iters"] >= 10, ci
+
+
 @pytest.mark.parametrize("prec", [AUTO, FP64])
 def test_mixed_outcomes_in_one_call(env, prec):
     """One grouped call: kept warm starts, warm starts the commutator monitor
