@@ -2038,72 +2038,74 @@ __global__ __launch_bounds__(kThreads) void graft_pass2_kernel(const GraftBlock*
                                                               int use_shampoo, const double* __restrict__ partial,
                                                               float* __restrict__ norms) {
   __shared__ double red[kThreads / 64];
-  const int t = blockIdx.x;
-  if (t >= total_chunks) return;
-  const int bi = find_block_graft(blocks, nb, t);
-  const GraftBlock B = blocks[bi];
-  // the block's norms from its chunk partials, reduced cooperatively in a
-  // fixed order (every workgroup of the block gets the same bits)
-  double smg = 0.0, sps = 0.0;
-  for (int q = threadIdx.x; q < B.nparts; q += kThreads) {
-    smg += partial[2 * (B.part_begin + q) + 0];
-    sps += partial[2 * (B.part_begin + q) + 1];
-  }
-  smg = block_sum(smg, red);
-  sps = block_sum(sps, red);
-  const double nm = sqrt(smg), nps = sqrt(sps);
-  double eta;
-  if (use_shampoo || LAMB) eta = nps > 0.0 ? (double)eta0 * nm / nps : 0.0;
-  else eta = eta0;
-  const float etaf = (float)eta;
-  const int ch = t - B.chunk_begin;
-  if (ch == 0 && threadIdx.x == 0 && norms) {
-    norms[3 * bi + 0] = (float)nm;
-    norms[3 * bi + 1] = (float)nps;
-    norms[3 * bi + 2] = etaf;
-  }
-  if (etaf == 0.f) return;
-  const int r0 = ch * B.rows_per_chunk;
-  const int r1 = min(B.rows, r0 + B.rows_per_chunk);
-  const bool mom = beta1 > 0.f;
-  // direction: Ps (momentum) or P; before the roots Mg or (at beta1 = 0)
-  // D^{-1/2} o G, or G itself for LAMB
-  const float* dir = use_shampoo ? (mom ? B.Ps : B.P) : (mom ? B.Mg : nullptr);
-  // P is laid out like G; momentum buffers like W
-  const int64_t dir_w = use_shampoo && !mom ? 0 : 1;
-  for_chunk(B, r0, r1, [&](int64_t i, int64_t iw, int w) {
-    float step[4];
-    const int64_t id = dir_w ? iw : i;
-    if (dir) {
-      if (w == 4) {
-        const f4v v = gload<f4v>(dir + id);
-        step[0] = v[0]; step[1] = v[1]; step[2] = v[2]; step[3] = v[3];
-      } else {
-        step[0] = gload<float>(dir + id);
-      }
-    } else if (LAMB) {
-      if (w == 4) G4<SG>::load(B.G, i, step);
-      else step[0] = load_g<SG>(B.G, i);
-    } else {
-      float g[4];
-      if (w == 4) {
-        G4<SG>::load(B.G, i, g);
-        const f4v dv = gload<f4v>(B.D + iw);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) step[e] = ada_dir(g[e], dv[e]);
-      } else {
-        step[0] = ada_dir(load_g<SG>(B.G, i), gload<float>(B.D + iw));
-      }
+  // chunk t of the grid-stride walk (a launch of total_chunks workgroups
+  // takes one chunk each)
+  for (int t = blockIdx.x; t < total_chunks; t += gridDim.x) {
+    const int bi = find_block_graft(blocks, nb, t);
+    const GraftBlock B = blocks[bi];
+    // the block's norms from its chunk partials, reduced cooperatively in a
+    // fixed order (every workgroup of the block gets the same bits)
+    double smg = 0.0, sps = 0.0;
+    for (int q = threadIdx.x; q < B.nparts; q += kThreads) {
+      smg += partial[2 * (B.part_begin + q) + 0];
+      sps += partial[2 * (B.part_begin + q) + 1];
     }
-    if (w == 4) {
-      f4v wv = gload<f4v>(B.W + iw);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) wv[e] -= etaf * step[e];
-      gstore<f4v>(B.W + iw, wv);
-    } else {
-      gstore<float>(B.W + iw, gload<float>(B.W + iw) - etaf * step[0]);
+    smg = block_sum(smg, red);
+    sps = block_sum(sps, red);
+    const double nm = sqrt(smg), nps = sqrt(sps);
+    double eta;
+    if (use_shampoo || LAMB) eta = nps > 0.0 ? (double)eta0 * nm / nps : 0.0;
+    else eta = eta0;
+    const float etaf = (float)eta;
+    const int ch = t - B.chunk_begin;
+    if (ch == 0 && threadIdx.x == 0 && norms) {
+      norms[3 * bi + 0] = (float)nm;
+      norms[3 * bi + 1] = (float)nps;
+      norms[3 * bi + 2] = etaf;
     }
-  });
+    if (etaf == 0.f) continue;
+    const int r0 = ch * B.rows_per_chunk;
+    const int r1 = min(B.rows, r0 + B.rows_per_chunk);
+    const bool mom = beta1 > 0.f;
+    // direction: Ps (momentum) or P; before the roots Mg or (at beta1 = 0)
+    // D^{-1/2} o G, or G itself for LAMB
+    const float* dir = use_shampoo ? (mom ? B.Ps : B.P) : (mom ? B.Mg : nullptr);
+    // P is laid out like G; momentum buffers like W
+    const int64_t dir_w = use_shampoo && !mom ? 0 : 1;
+    for_chunk(B, r0, r1, [&](int64_t i, int64_t iw, int w) {
+      float step[4];
+      const int64_t id = dir_w ? iw : i;
+      if (dir) {
+        if (w == 4) {
+          const f4v v = gload<f4v>(dir + id);
+          step[0] = v[0]; step[1] = v[1]; step[2] = v[2]; step[3] = v[3];
+        } else {
+          step[0] = gload<float>(dir + id);
+        }
+      } else if (LAMB) {
+        if (w == 4) G4<SG>::load(B.G, i, step);
+        else step[0] = load_g<SG>(B.G, i);
+      } else {
+        float g[4];
+        if (w == 4) {
+          G4<SG>::load(B.G, i, g);
+          const f4v dv = gload<f4v>(B.D + iw);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) step[e] = ada_dir(g[e], dv[e]);
+        } else {
+          step[0] = ada_dir(load_g<SG>(B.G, i), gload<float>(B.D + iw));
+        }
+      }
+      if (w == 4) {
+        f4v wv = gload<f4v>(B.W + iw);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) wv[e] -= etaf * step[e];
+        gstore<f4v>(B.W + iw, wv);
+      } else {
+        gstore<float>(B.W + iw, gload<float>(B.W + iw) - etaf * step[0]);
+      }
+    });
+  }
 }
 
 // P = G (no root on either side), with up-cast.

@@ -396,6 +396,14 @@ std::vector<GraftBlock> graft_table(const shampoo_block* blocks, int nb, int* to
 // least 8 blocks and 2^24 elements: smaller calls have too short a graft
 // pass 2 to pay for the extra launches, and with blocks of mixed sizes every
 // group's launches end in a longer tail (measured: C5's step 0.5 ms slower).
+// Workgroups of a graft pass 2 that runs on the side stream beside the next
+// group's preconditioning GEMMs.  One per row chunk (about 6 000 for a
+// quarter of C2's blocks) takes compute units from those GEMMs.  Measured
+// on the C2 step (three runs each, same box):
+//   64 workgroups: 23.41 ms (the pass no longer finishes under the GEMMs);
+//   128: 22.34 ms; 256: 22.32 ms; one per chunk: 22.45 ms.
+constexpr int kPass2SideGrid = 256;
+
 std::vector<int> precond_groups(const shampoo_block* blocks, int nb) {
   constexpr int kGroups = 4;
   std::vector<double> w(nb);
@@ -552,8 +560,12 @@ shampoo_status precond_impl(Handle* h, const shampoo_block* blocks, int nb, hipS
         ps = h->side;
       }
       float* gn = norms ? norms + 3 * b0 : nullptr;
+      // beside the next group's GEMMs, a few workgroups walk the chunks
+      // (they leave the GEMMs their compute units); the last group's pass 2
+      // runs alone, on the whole GPU
+      const int grid = c + 1 < ngroups ? std::min(total, kPass2SideGrid) : total;
       STATUS_TRY(launch(h, SHAMPOO_KCLASS_GRAFT, ps, [&] {
-        hipLaunchKernelGGL((graft_pass2_kernel<SG, false>), dim3(total), dim3(kThreads), 0, ps, (const GraftBlock*)d,
+        hipLaunchKernelGGL((graft_pass2_kernel<SG, false>), dim3(grid), dim3(kThreads), 0, ps, (const GraftBlock*)d,
                            nbc, total, eta0, 0.f, 1, (const double*)gpart, gn);
       }));
     }
