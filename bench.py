@@ -891,9 +891,13 @@ def run_c2(args, torch, B):
     t0 = time.time()
     Ls, Gs, Ds, Ws = [], [], [], []
     sample = []
+    # the statistics are views into one allocation, so the restore before
+    # every step is one contiguous device copy
+    Lall = torch.empty(nb, n, n, device=dev)
     with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 4)) as ex:
         for i, (L, G, D, W) in enumerate(ex.map(lambda i: gen_block(i, n, k), range(nb))):
-            Ls.append(torch.from_numpy(L).to(dev))
+            Lall[i].copy_(torch.from_numpy(L))
+            Ls.append(Lall[i])
             Gs.append(torch.from_numpy(G).to(dev))
             Ds.append(torch.from_numpy(D).to(dev))
             Ws.append(torch.from_numpy(W).to(dev))
@@ -909,7 +913,7 @@ def run_c2(args, torch, B):
         torch.cuda.synchronize()
         log(f"calibration copy of {args.calib_copy_mb} MiB done")
         del src, dst
-    L0s = [L.clone() for L in Ls]          # pristine L_19, restored before every step
+    L0all = Lall.clone()                   # pristine L_19, restored before every step
     Lrs = [torch.zeros(n, n, device=dev) for _ in range(nb)]
     Ps = [torch.zeros(n, k, device=dev) for _ in range(nb)]
     blocks = [B.Block(G=Gs[i], W=Ws[i], D=Ds[i], P=Ps[i], L=Ls[i], Lr=Lrs[i]) for i in range(nb)]
@@ -929,7 +933,7 @@ def run_c2(args, torch, B):
     def step(record, split=args.split_graft):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record()
-        torch._foreach_copy_(Ls, L0s)
+        Lall.copy_(L0all)
         e1.record()
         if record:
             restore_ev.append((e0, e1))
