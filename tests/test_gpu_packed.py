@@ -64,6 +64,39 @@ def test_packed_equals_lists(dtype):
         B.shampoo_destroy(h)
 
 
+def test_packed_jobs_warm_equals_lists():
+    """The warm-started call with PackedJobs (Xs None) against the same call
+    with lists, bit for bit, outputs and warm outcomes."""
+    torch, B, dev = gpu_env()
+    say("packed jobs warm == lists")
+    h = B.shampoo_create(0)
+    try:
+        g = torch.Generator(device=dev).manual_seed(9)
+        ns = [200, 256, 77]
+        As = []
+        for n in ns:
+            a = torch.randn(n, n + 16, device=dev, generator=g)
+            As.append((a @ a.T / (n + 16)).contiguous())
+        prm = B.shampoo_root_params_default(p=4, eps=1e-6)
+        ws = torch.empty(B.shampoo_inv_root_workspace_bytes(ns, prm.precision), dtype=torch.uint8, device=dev)
+        info = torch.zeros(8 * len(As), dtype=torch.int32, device=dev)
+        X0 = [torch.zeros_like(a) for a in As]
+        B.shampoo_inv_root_batched(h, As, X0, prm, ws, info)
+        A2 = [(a + 1e-3 * torch.eye(a.shape[0], device=dev)).contiguous() for a in As]
+        X1, X2 = [x.clone() for x in X0], [x.clone() for x in X0]
+        w1 = torch.zeros(2 * len(As), dtype=torch.int32, device=dev)
+        w2 = torch.zeros_like(w1)
+        i1, i2 = torch.zeros_like(info), torch.zeros_like(info)
+        B.shampoo_inv_root_warm_batched(h, A2, X1, prm, ws, i1, w1)
+        B.shampoo_inv_root_warm_batched(h, B.PackedJobs(h, A2, X2), None, prm, ws, i2, w2)
+        torch.cuda.synchronize()
+        assert torch.equal(w1, w2) and torch.equal(i1, i2)
+        for a, b in zip(X1, X2):
+            assert torch.equal(a, b)
+    finally:
+        B.shampoo_destroy(h)
+
+
 def test_packed_other_handle_refused():
     torch, B, dev = gpu_env()
     say("packed other handle")
