@@ -416,13 +416,16 @@ class PackedBlocks:
     same views (a training loop passes the same blocks every step): every
     entry point that takes a block list accepts it in its place and skips the
     per-call checks and packing.  It records each tensor's pointer, size and
-    row stride as they are when packed and keeps the tensors alive; pack again
-    after any of them is reallocated, resized or replaced."""
+    row stride as they are when packed and keeps those tensors alive (a field
+    of a Block reassigned later still leaves the packed tensor valid, if
+    stale); pack again after any of them is reallocated, resized or
+    replaced."""
 
     def __init__(self, handle, blocks):
         blocks = list(blocks)
         _check_blocks(handle, blocks)
         self.blocks = blocks
+        self._tensors = [getattr(b, f) for b in blocks for f in _BLOCK_PTRS]
         self._handle = getattr(handle, "value", handle)
         self._arr = _blocks(blocks)
         self._dtype = _dtype_code(blocks)
@@ -442,7 +445,7 @@ class PackedJobs:
         As, Xs = list(As), list(Xs)
         _need(len(As) > 0, "PackedJobs: no jobs")
         _devices(handle, _job_list_tensors(As, Xs))
-        self.As, self.Xs = As, Xs
+        self.As, self.Xs = As, Xs  # the packed tensors stay alive with this object
         self._handle = getattr(handle, "value", handle)
         self._arr = _jobs(As, Xs)
         self._device = As[0].get_device()
